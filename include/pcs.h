@@ -1,0 +1,262 @@
+/*
+ * pcs.h -- C ABI of libpcs, the GPU byte layer under a Persistent
+ * Computational State (PCS) runtime for generative world models.
+ *
+ * The paper ("Persistent Computational State: A Session-Centric Runtime for
+ * Generative World Models") specifies PCS as a contract (Sec. 3, "The
+ * contract"): four operations over a session and opaque handles,
+ *     c = checkpoint(s),  s' = restore(c),  c' = fork(c),  delete(c),
+ * with four invariants: I1 round-trip, I2 durability (a checkpoint is an
+ * immutable snapshot, not a live alias), I3 fork independence and
+ * I4 snapshot completeness (|checkpoint| = |PCS|).  Which buffers belong to
+ * PCS is decided by derivability (Sec. 3, "The partition"): a buffer that
+ * re-running the compute does not reproduce must be snapshotted.  Sec. 4
+ * measures that by ablation; this library measures it with content
+ * fingerprints over K replays (pcs_fingerprint + pcs_classify).
+ *
+ * Fingerprint definition (the paper names no hash; this is the library's):
+ *   - a buffer's logical bytes are cut into 4096-byte chunks counted from its
+ *     first logical byte; the last chunk holds only the remaining bytes;
+ *   - each chunk's fingerprint is XXH64 with seed 0 of its bytes;
+ *   - a buffer's root is the binary Merkle root over its chunk fingerprints:
+ *     pairs (2j, 2j+1) of a level form node j of the next level as XXH64
+ *     (seed 0) of the 16 bytes left||right, each little-endian; an odd last
+ *     node is promoted unchanged; an empty buffer's root is XXH64 of the
+ *     empty input (0xEF46DB3751D8E999);
+ *   - a session root is the same Merkle tree over the buffer roots in plan
+ *     order.
+ *
+ * Conventions for every entry point:
+ *   - Pointers named d_* are device addresses (HIP device memory, or memory
+ *     the device can read and write); pointers named h_* are host memory.
+ *   - Every call is stream-ordered on the stream given to pcs_ctx_create:
+ *     device outputs are valid once that stream reaches the call's end;
+ *     handles are valid when the call returns.  Buffers a call reads must not
+ *     be modified, and buffers it writes must not be read, by other streams
+ *     until then (I2 durability is defined in stream order).
+ *   - Status: PCS_OK (0) or a negative PCS_E_* code.  On any error other
+ *     than PCS_E_HIP nothing has been enqueued and no handle was created;
+ *     pcs_last_error() describes the failure.  PCS_E_HIP means a HIP call
+ *     failed after some work may have been enqueued.
+ *   - A context is not thread-safe: use one context per host thread.
+ */
+#ifndef PCS_H
+#define PCS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PCS_OK 0
+#define PCS_E_INVAL (-1)   /* bad argument or descriptor                         */
+#define PCS_E_NOMEM (-2)   /* the arena cannot hold the request (no eviction)    */
+#define PCS_E_HANDLE (-3)  /* unknown or deleted snapshot handle                 */
+#define PCS_E_SHAPE (-4)   /* restore target layout differs from the snapshot's  */
+#define PCS_E_HIP (-5)     /* a HIP runtime call failed                          */
+
+#define PCS_CHUNK_BYTES 4096u
+
+/* Buffer kinds. */
+#define PCS_FLAT 0u  /* nbytes contiguous bytes at ptr                       */
+#define PCS_RING 1u  /* a ring-buffered window, see pcs_buf                  */
+
+/* Classification labels (derivability, Sec. 3 "The partition"). */
+#define PCS_RECOMPUTABLE 0u
+#define PCS_MUST_SNAPSHOT 1u
+
+/* Checkpoint flags. */
+#define PCS_CKPT_HASH 1u  /* also fingerprint while copying (one read of the state) */
+
+typedef struct pcs_ctx pcs_ctx;
+typedef uint64_t pcs_snap; /* opaque snapshot handle; 0 is never a valid handle */
+
+/*
+ * One candidate buffer of a session's runtime state.
+ *
+ * PCS_FLAT: `nbytes` bytes starting at `ptr`.  `ptr` must be 16-byte aligned;
+ *   nbytes may be any value, including 0.  Ring fields are ignored.
+ *
+ * PCS_RING: the windowed KV context of the paper's addressable-memory model
+ *   (Table 1; Sec. 7.11: a context capped by a local window and written at
+ *   contiguous positions).  `outer` independent rings (e.g. layers x {K,V});
+ *   ring o starts at ptr + o*outer_stride and holds `capacity` rows of
+ *   `row_bytes` (a row is one token: heads x head_dim x element size).  The
+ *   valid window is `window` rows; logical row t (0 <= t < window) of ring o
+ *   lives in physical row (head + t) mod capacity.  The buffer's logical
+ *   bytes are ring 0's window rows in order, then ring 1's, and so on:
+ *   nbytes = outer * window * row_bytes (pass that value or 0).
+ *   Requirements: ptr, row_bytes and outer_stride multiples of 16;
+ *   1 <= window <= capacity; head < capacity;
+ *   outer_stride >= capacity * row_bytes (rings do not overlap).
+ *
+ * Fingerprints and snapshots of a ring cover its logical window, so they do
+ * not depend on the head offset: a window restored at a different head
+ * fingerprints the same.
+ */
+typedef struct pcs_buf {
+    uint64_t ptr;          /* device address                                  */
+    uint64_t nbytes;       /* logical byte count (see above)                  */
+    uint32_t kind;         /* PCS_FLAT or PCS_RING                            */
+    uint32_t flags;        /* reserved, must be 0                             */
+    uint64_t row_bytes;    /* RING: bytes per row                             */
+    uint64_t capacity;     /* RING: rows per ring                             */
+    uint64_t head;         /* RING: physical row of logical row 0             */
+    uint64_t window;       /* RING: valid rows                                */
+    uint64_t outer;        /* RING: number of rings                           */
+    uint64_t outer_stride; /* RING: bytes from ring o to ring o+1             */
+} pcs_buf;
+
+typedef struct pcs_snap_info {
+    uint64_t state_bytes;   /* logical bytes a restore writes (I4: sum of plan sizes) */
+    uint64_t stored_bytes;  /* payload bytes this snapshot itself holds in the arena  */
+    uint64_t total_chunks;  /* chunks over all buffers                                */
+    uint64_t dirty_chunks;  /* incremental: chunks stored here; full: total_chunks    */
+    uint32_t nbufs;         /* buffers in the plan                                    */
+    uint32_t incremental;   /* 1 if taken against a parent                            */
+    uint32_t has_hashes;    /* 1 if chunk fingerprints are stored with it             */
+    uint32_t reserved;
+} pcs_snap_info;
+
+/*
+ * Creates a context over a caller-owned device arena.  All snapshot payloads,
+ * their stored fingerprints and manifests, and per-call scratch live inside
+ * [d_arena, d_arena + arena_bytes); the library never allocates device memory
+ * itself.  `hip_stream` is a hipStream_t (NULL = the null stream) on which
+ * every call of this context is enqueued.  The arena and the stream are
+ * borrowed: the caller keeps them alive until pcs_ctx_destroy returns.
+ * d_arena must be 4096-byte aligned.  Small pinned host buffers are
+ * allocated for descriptor uploads.
+ */
+int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ctx **out);
+
+/* Waits for the context's stream, then frees every handle and host resource. */
+int pcs_ctx_destroy(pcs_ctx *ctx);
+
+/* Text of the last failure on this context (never NULL; "" if none). */
+const char *pcs_last_error(const pcs_ctx *ctx);
+
+/* Host helper: number of 4096-byte chunks of each buffer (h_chunks[i]) and
+ * their sum (*total).  Either output may be NULL.  Validates descriptors. */
+int pcs_chunk_counts(const pcs_buf *h_bufs, uint32_t n, uint64_t *h_chunks, uint64_t *total);
+
+/*
+ * Fingerprints n buffers (chunked XXH64 + Merkle, definition above).
+ *   d_chunk_hashes: uint64[total chunks], buffer-major (buffer 0's chunks,
+ *                   then buffer 1's ...); may be NULL.
+ *   d_roots:        uint64[n], per-buffer Merkle roots; may be NULL.
+ *   d_session_root: uint64[1], root over the buffer roots; may be NULL.
+ */
+int pcs_fingerprint(pcs_ctx *ctx, const pcs_buf *h_bufs, uint32_t n, uint64_t *d_chunk_hashes,
+                    uint64_t *d_roots, uint64_t *d_session_root);
+
+/*
+ * Cross-replay classification (derivability, Sec. 3 "The partition"; the
+ * fingerprint stands in for the Sec. 4 ablation).
+ *   d_hashes:  uint64[K][total], replay-major; each replay is laid out like
+ *              pcs_fingerprint's d_chunk_hashes for the same plan.
+ *   h_chunks:  uint64[n], chunks per buffer (the same in every replay).
+ *   d_bitmap:  uint64[sum_b ceil(h_chunks[b]/64)]: each buffer starts on a
+ *              fresh word; chunk i of buffer b is bit (i mod 64) of its word
+ *              i/64 and is 1 iff its K fingerprints are not all equal.
+ *              Unused bits are 0.
+ *   d_labels:  uint8[n]: PCS_MUST_SNAPSHOT iff any chunk differs, else
+ *              PCS_RECOMPUTABLE.
+ * K >= 1 (K = 1 labels everything recomputable).
+ */
+int pcs_classify(pcs_ctx *ctx, const uint64_t *d_hashes, uint32_t K, const uint64_t *h_chunks,
+                 uint32_t n, uint64_t *d_bitmap, uint8_t *d_labels);
+
+/*
+ * checkpoint(s) -> c (Sec. 3 contract).  Copies the plan's logical bytes
+ * into a new immutable snapshot inside the arena and returns its handle.
+ *   parent == 0: full snapshot; component b starts 4096-aligned, in plan
+ *     order; padding bytes are zero.  With PCS_CKPT_HASH the chunk
+ *     fingerprints are computed from the same read and stored with the
+ *     snapshot (needed for it to serve as a parent).
+ *   parent != 0: incremental snapshot.  The plan must have the parent's
+ *     buffer count and the parent must hold fingerprints.  The plan is
+ *     fingerprinted; chunk i of buffer b is stored iff the parent had no
+ *     chunk i for b or its fingerprint changed; every other chunk is taken
+ *     from the parent chain at restore time.  Stored chunks use one 4096-byte
+ *     slot each, in increasing (buffer, chunk) order.  Fingerprints are
+ *     always stored (flags are ignored).
+ *   d_chunk_hashes, d_roots, d_session_root: optional copies of the
+ *     fingerprints, laid out as in pcs_fingerprint (need PCS_CKPT_HASH or a
+ *     parent; otherwise pass NULL).
+ * The snapshot shares no bytes with the plan buffers (I2): later writes to
+ * them do not change it.
+ */
+int pcs_checkpoint(pcs_ctx *ctx, const pcs_buf *h_plan, uint32_t n, pcs_snap parent, uint32_t flags,
+                   uint64_t *d_chunk_hashes, uint64_t *d_roots, uint64_t *d_session_root,
+                   pcs_snap *out);
+
+/*
+ * Full checkpoints of `sessions` sessions in one launch (batched suspend).
+ * Session s's plan is h_plans[off_s .. off_s + h_nbufs[s]) with
+ * off_s = sum of the earlier h_nbufs.  Output arrays concatenate the
+ * sessions in order (chunk hashes and roots as in pcs_fingerprint;
+ * d_session_roots is uint64[sessions]).  h_out receives one handle per
+ * session.  Either all snapshots are created or none.
+ */
+int pcs_checkpoint_batch(pcs_ctx *ctx, const pcs_buf *h_plans, const uint32_t *h_nbufs,
+                         uint32_t sessions, uint32_t flags, uint64_t *d_chunk_hashes,
+                         uint64_t *d_roots, uint64_t *d_session_roots, pcs_snap *h_out);
+
+/*
+ * restore(c) -> s' (Sec. 3 contract, I1).  Writes the snapshot's logical
+ * bytes into the n destination buffers.  dst[b] must have snapshot buffer
+ * b's logical size; a ring destination must have the same row_bytes, window
+ * and outer (its capacity, head and outer_stride may differ, so a window can
+ * be restored at a new head).  Only window rows are written.  Destinations
+ * must not overlap each other.  Returns PCS_E_SHAPE on a layout mismatch.
+ * Restores copy out of the snapshot, so two restores of one snapshot (or of
+ * a fork) are independent (I3).
+ */
+int pcs_restore(pcs_ctx *ctx, pcs_snap snap, const pcs_buf *h_dst, uint32_t n);
+
+/* Restores m snapshots in one launch; snapshot j goes to
+ * h_dsts[off_j .. off_j + h_nbufs[j]).  Validates everything first. */
+int pcs_restore_batch(pcs_ctx *ctx, const pcs_snap *h_snaps, uint32_t m, const pcs_buf *h_dsts,
+                      const uint32_t *h_nbufs);
+
+/* fork(c) -> c' (Sec. 3 contract, I3): a new handle on the same immutable
+ * snapshot.  No device work. */
+int pcs_fork(pcs_ctx *ctx, pcs_snap snap, pcs_snap *out);
+
+/* delete(c) (Sec. 3 contract): drops one handle.  Arena space is released
+ * when no handle and no incremental child needs it any more. */
+int pcs_delete(pcs_ctx *ctx, pcs_snap snap);
+
+/* Sizes and flags of a snapshot (I4 accounting).  May wait on the stream for
+ * an incremental snapshot's stored-chunk count. */
+int pcs_snapshot_info(pcs_ctx *ctx, pcs_snap snap, pcs_snap_info *out);
+
+/* Copies the payload this snapshot holds (stored_bytes of pcs_snap_info) to
+ * device memory d_dst of capacity `cap` bytes, stream-ordered. */
+int pcs_snapshot_payload(pcs_ctx *ctx, pcs_snap snap, void *d_dst, uint64_t cap);
+
+/* Copies the snapshot's stored chunk fingerprints (buffer-major) to d_dst,
+ * which holds `cap` uint64 values.  PCS_E_INVAL if it has none. */
+int pcs_snapshot_hashes(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_dst, uint64_t cap);
+
+/* Arena accounting: bytes in use, bytes free, largest free block, live handles. */
+int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t *largest_free,
+                    uint64_t *live_handles);
+
+/*
+ * Kernel timing.  While enabled, every kernel launch is bracketed by HIP
+ * events on the context stream.  pcs_kernel_time waits for the stream, then
+ * reports the number of launches and their summed duration in milliseconds
+ * for the kernel family `name` ("hash", "pack_hash", "copy", "merkle",
+ * "classify", "incremental", "map") since the last reset, and resets it.
+ */
+int pcs_set_timing(pcs_ctx *ctx, int enable);
+int pcs_kernel_time(pcs_ctx *ctx, const char *name, uint64_t *launches, double *total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PCS_H */

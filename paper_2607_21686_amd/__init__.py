@@ -1,0 +1,186 @@
+"""MI355X (gfx950) byte layer of a Persistent Computational State runtime.
+
+The paper ("Persistent Computational State: A Session-Centric Runtime for
+Generative World Models") specifies PCS as a contract (Sec. 3): checkpoint /
+restore / fork / delete over opaque handles, with invariants I1 round-trip,
+I2 durability, I3 fork independence and I4 snapshot completeness, and it
+decides which buffers are PCS by derivability.  This package is the GPU
+layer under that contract: chunked XXH64 fingerprints with a Merkle
+combine, cross-replay classification (must-snapshot vs recomputable),
+packed-gather checkpoints (flat buffers, growing banks with incremental
+checkpoints, ring-buffered KV windows) and scatter restore.
+
+All work runs in libpcs.so's HIP kernels behind the C ABI of
+``include/pcs.h``; this module only marshals torch tensors and streams.
+PyTorch is used for device memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from ._lib import (CHUNK_BYTES, CKPT_HASH, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_SHAPE, EXPORTS, FLAT,
+                   MUST_SNAPSHOT, RECOMPUTABLE, RING, PcsBuf, PcsError, PcsSnapInfo, lib)
+
+__all__ = ["Context", "PcsError", "flat", "ring", "chunk_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
+           "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "EXPORTS"]
+
+_L = lib()  # fails loudly if the HIP library is missing
+
+
+def chunk_count(nbytes: int) -> int:
+    return (nbytes + CHUNK_BYTES - 1) // CHUNK_BYTES
+
+
+def _dev_ptr(t) -> int:
+    if t is None:
+        return 0
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+        raise ValueError("expected a contiguous CUDA tensor")
+    return t.data_ptr()
+
+
+def flat(t: torch.Tensor, nbytes: int | None = None) -> PcsBuf:
+    """A PCS_FLAT descriptor over a contiguous device tensor (or its first nbytes)."""
+    size = t.numel() * t.element_size()
+    n = size if nbytes is None else nbytes
+    if n > size:
+        raise ValueError("nbytes exceeds the tensor")
+    return PcsBuf(ptr=_dev_ptr(t), nbytes=n, kind=FLAT)
+
+
+def ring(t: torch.Tensor, outer: int, capacity: int, row_bytes: int, head: int, window: int,
+         outer_stride: int | None = None) -> PcsBuf:
+    """A PCS_RING descriptor: `outer` rings of `capacity` rows inside tensor t."""
+    stride = capacity * row_bytes if outer_stride is None else outer_stride
+    need = (outer - 1) * stride + capacity * row_bytes if outer else 0
+    if need > t.numel() * t.element_size():
+        raise ValueError("ring geometry exceeds the tensor")
+    return PcsBuf(ptr=_dev_ptr(t), nbytes=0, kind=RING, row_bytes=row_bytes, capacity=capacity, head=head,
+                  window=window, outer=outer, outer_stride=stride)
+
+
+def _array(bufs):
+    arr = (PcsBuf * max(1, len(bufs)))()
+    for i, b in enumerate(bufs):
+        arr[i] = b
+    return arr
+
+
+def chunk_counts(bufs):
+    arr = _array(bufs)
+    out = (ctypes.c_uint64 * max(1, len(bufs)))()
+    total = ctypes.c_uint64()
+    st = _L.pcs_chunk_counts(arr, len(bufs), out, ctypes.byref(total))
+    if st:
+        raise PcsError(st, "invalid buffer descriptor")
+    return [int(out[i]) for i in range(len(bufs))], int(total.value)
+
+
+class Context:
+    """A libpcs context over a caller-owned uint8 device arena, bound to a stream."""
+
+    def __init__(self, arena: torch.Tensor, stream: torch.cuda.Stream | None = None):
+        if arena.dtype != torch.uint8:
+            raise ValueError("arena must be a uint8 tensor")
+        self._arena = arena
+        self.stream = stream if stream is not None else torch.cuda.current_stream(arena.device)
+        h = ctypes.c_void_p()
+        st = _L.pcs_ctx_create(ctypes.c_void_p(_dev_ptr(arena)), arena.numel(),
+                                 ctypes.c_void_p(self.stream.cuda_stream), ctypes.byref(h))
+        if st:
+            raise PcsError(st, "pcs_ctx_create failed")
+        self._h = h
+
+    def _check(self, st):
+        if st:
+            raise PcsError(st, _L.pcs_last_error(self._h).decode())
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _L.pcs_ctx_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # -- fingerprint / classify ------------------------------------------
+    def fingerprint(self, bufs, chunk_hashes=None, roots=None, session_root=None):
+        self._check(_L.pcs_fingerprint(self._h, _array(bufs), len(bufs), _dev_ptr(chunk_hashes),
+                                         _dev_ptr(roots), _dev_ptr(session_root)))
+
+    def classify(self, hashes, K: int, chunks_per_buf, bitmap, labels):
+        cpb = (ctypes.c_uint64 * max(1, len(chunks_per_buf)))(*[int(c) for c in chunks_per_buf])
+        self._check(_L.pcs_classify(self._h, _dev_ptr(hashes), K, cpb, len(chunks_per_buf),
+                                      _dev_ptr(bitmap), _dev_ptr(labels)))
+
+    # -- contract ----------------------------------------------------------
+    def checkpoint(self, plan, parent: int = 0, hash: bool = False, chunk_hashes=None, roots=None,
+                   session_root=None) -> int:
+        out = ctypes.c_uint64()
+        self._check(_L.pcs_checkpoint(self._h, _array(plan), len(plan), parent, CKPT_HASH if hash else 0,
+                                        _dev_ptr(chunk_hashes), _dev_ptr(roots), _dev_ptr(session_root),
+                                        ctypes.byref(out)))
+        return int(out.value)
+
+    def checkpoint_batch(self, plans, hash: bool = False, chunk_hashes=None, roots=None, session_roots=None):
+        flat_list = [b for p in plans for b in p]
+        nb = (ctypes.c_uint32 * max(1, len(plans)))(*[len(p) for p in plans])
+        out = (ctypes.c_uint64 * max(1, len(plans)))()
+        self._check(_L.pcs_checkpoint_batch(self._h, _array(flat_list), nb, len(plans),
+                                              CKPT_HASH if hash else 0, _dev_ptr(chunk_hashes),
+                                              _dev_ptr(roots), _dev_ptr(session_roots), out))
+        return [int(out[i]) for i in range(len(plans))]
+
+    def restore(self, snap: int, dsts):
+        self._check(_L.pcs_restore(self._h, snap, _array(dsts), len(dsts)))
+
+    def restore_batch(self, snaps, dsts_per_snap):
+        flat_list = [b for d in dsts_per_snap for b in d]
+        s = (ctypes.c_uint64 * max(1, len(snaps)))(*snaps)
+        nb = (ctypes.c_uint32 * max(1, len(snaps)))(*[len(d) for d in dsts_per_snap])
+        self._check(_L.pcs_restore_batch(self._h, s, len(snaps), _array(flat_list), nb))
+
+    def fork(self, snap: int) -> int:
+        out = ctypes.c_uint64()
+        self._check(_L.pcs_fork(self._h, snap, ctypes.byref(out)))
+        return int(out.value)
+
+    def delete(self, snap: int):
+        self._check(_L.pcs_delete(self._h, snap))
+
+    def info(self, snap: int) -> dict:
+        inf = PcsSnapInfo()
+        self._check(_L.pcs_snapshot_info(self._h, snap, ctypes.byref(inf)))
+        return {f: int(getattr(inf, f)) for f, _ in PcsSnapInfo._fields_ if f != "reserved"}
+
+    def payload(self, snap: int, out: torch.Tensor):
+        self._check(_L.pcs_snapshot_payload(self._h, snap, _dev_ptr(out), out.numel() * out.element_size()))
+
+    def stored_hashes(self, snap: int, out: torch.Tensor):
+        self._check(_L.pcs_snapshot_hashes(self._h, snap, _dev_ptr(out), out.numel()))
+
+    def arena_stats(self) -> dict:
+        v = [ctypes.c_uint64() for _ in range(4)]
+        self._check(_L.pcs_arena_stats(self._h, *[ctypes.byref(x) for x in v]))
+        return dict(zip(["used", "free", "largest_free", "live_handles"], [int(x.value) for x in v]))
+
+    # -- kernel timing -----------------------------------------------------
+    def set_timing(self, enable: bool):
+        self._check(_L.pcs_set_timing(self._h, 1 if enable else 0))
+
+    def kernel_time(self, name: str):
+        n = ctypes.c_uint64()
+        ms = ctypes.c_double()
+        self._check(_L.pcs_kernel_time(self._h, name.encode(), ctypes.byref(n), ctypes.byref(ms)))
+        return int(n.value), float(ms.value)

@@ -1,0 +1,95 @@
+"""ctypes binding of libpcs (include/pcs.h): argument marshalling only.
+
+Every step of the fingerprint / classify / checkpoint / restore path runs in
+the library's HIP kernels; this module turns torch tensors into device
+pointers and the current torch stream into the context's hipStream_t.  If
+libpcs.so is missing or fails to load, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpcs.so")
+
+OK = 0
+E_INVAL, E_NOMEM, E_HANDLE, E_SHAPE, E_HIP = -1, -2, -3, -4, -5
+CHUNK_BYTES = 4096
+FLAT, RING = 0, 1
+RECOMPUTABLE, MUST_SNAPSHOT = 0, 1
+CKPT_HASH = 1
+
+_ERRNAMES = {E_INVAL: "PCS_E_INVAL", E_NOMEM: "PCS_E_NOMEM", E_HANDLE: "PCS_E_HANDLE",
+             E_SHAPE: "PCS_E_SHAPE", E_HIP: "PCS_E_HIP"}
+
+# Every symbol include/pcs.h declares.
+EXPORTS = ("pcs_ctx_create", "pcs_ctx_destroy", "pcs_last_error", "pcs_chunk_counts", "pcs_fingerprint",
+           "pcs_classify", "pcs_checkpoint", "pcs_checkpoint_batch", "pcs_restore", "pcs_restore_batch",
+           "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload", "pcs_snapshot_hashes",
+           "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
+
+
+class PcsBuf(ctypes.Structure):
+    _fields_ = [("ptr", ctypes.c_uint64), ("nbytes", ctypes.c_uint64), ("kind", ctypes.c_uint32),
+                ("flags", ctypes.c_uint32), ("row_bytes", ctypes.c_uint64), ("capacity", ctypes.c_uint64),
+                ("head", ctypes.c_uint64), ("window", ctypes.c_uint64), ("outer", ctypes.c_uint64),
+                ("outer_stride", ctypes.c_uint64)]
+
+
+class PcsSnapInfo(ctypes.Structure):
+    _fields_ = [("state_bytes", ctypes.c_uint64), ("stored_bytes", ctypes.c_uint64),
+                ("total_chunks", ctypes.c_uint64), ("dirty_chunks", ctypes.c_uint64),
+                ("nbufs", ctypes.c_uint32), ("incremental", ctypes.c_uint32),
+                ("has_hashes", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
+class PcsError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("%s: %s" % (_ERRNAMES.get(code, code), msg))
+        self.code = code
+
+
+def load():
+    """Loads libpcs.so and declares every entry point's signature."""
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libpcs.so is not built (run __graft_entry__.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, U64, U32, I = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int
+    PU64 = ctypes.POINTER(ctypes.c_uint64)
+    PB = ctypes.POINTER(PcsBuf)
+    sig = {
+        "pcs_ctx_create": ([P, U64, P, ctypes.POINTER(P)], I),
+        "pcs_ctx_destroy": ([P], I),
+        "pcs_last_error": ([P], ctypes.c_char_p),
+        "pcs_chunk_counts": ([PB, U32, PU64, PU64], I),
+        "pcs_fingerprint": ([P, PB, U32, P, P, P], I),
+        "pcs_classify": ([P, P, U32, PU64, U32, P, P], I),
+        "pcs_checkpoint": ([P, PB, U32, U64, U32, P, P, P, PU64], I),
+        "pcs_checkpoint_batch": ([P, PB, ctypes.POINTER(U32), U32, U32, P, P, P, PU64], I),
+        "pcs_restore": ([P, U64, PB, U32], I),
+        "pcs_restore_batch": ([P, PU64, U32, PB, ctypes.POINTER(U32)], I),
+        "pcs_fork": ([P, U64, PU64], I),
+        "pcs_delete": ([P, U64], I),
+        "pcs_snapshot_info": ([P, U64, ctypes.POINTER(PcsSnapInfo)], I),
+        "pcs_snapshot_payload": ([P, U64, P, U64], I),
+        "pcs_snapshot_hashes": ([P, U64, P, U64], I),
+        "pcs_arena_stats": ([P, PU64, PU64, PU64, PU64], I),
+        "pcs_set_timing": ([P, I], I),
+        "pcs_kernel_time": ([P, ctypes.c_char_p, PU64, ctypes.POINTER(ctypes.c_double)], I),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    return lib
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        _lib = load()
+    return _lib

@@ -1,0 +1,1070 @@
+// pcs_runtime.cpp -- host runtime behind the C ABI in include/pcs.h.
+//
+// Owns: the arena sub-allocator (first fit over a caller-owned device
+// arena), the snapshot table (handle -> immutable snapshot record, shared by
+// forks, kept alive by incremental children), the descriptor builder (plan
+// buffers -> logical/physical runs and 64-chunk groups), pinned staging for
+// descriptor uploads, and stream ordering.  Every byte of state moves in the
+// kernels of pcs_kernels.hip; nothing here touches snapshot data on the host.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/pcs.h"
+#include "pcs_device.h"
+
+namespace pcs {
+namespace {
+
+constexpr uint64_t kAlign = 4096;
+constexpr uint64_t kMaxGroups = (1ULL << 32) / 256 - 1;  // grid limit of the 256-lane kernels
+constexpr uint32_t kStagingSlots = 8;
+constexpr uint32_t kCountSlots = 4096;
+
+uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+uint64_t div_up(uint64_t x, uint64_t a) { return (x + a - 1) / a; }
+
+// First-fit allocator over [0, size) in 4096-byte units.
+class Arena {
+  public:
+    void init(uint64_t size)
+    {
+        size_ = size;
+        used_ = 0;
+        free_.clear();
+        if (size) free_[0] = size;
+    }
+    bool alloc(uint64_t bytes, uint64_t *off)
+    {
+        bytes = std::max<uint64_t>(kAlign, round_up(bytes, kAlign));
+        for (auto it = free_.begin(); it != free_.end(); ++it) {
+            if (it->second < bytes) continue;
+            *off = it->first;
+            const uint64_t rest = it->second - bytes, noff = it->first + bytes;
+            free_.erase(it);
+            if (rest) free_[noff] = rest;
+            used_ += bytes;
+            return true;
+        }
+        return false;
+    }
+    void release(uint64_t off, uint64_t bytes)
+    {
+        bytes = std::max<uint64_t>(kAlign, round_up(bytes, kAlign));
+        used_ -= bytes;
+        auto it = free_.emplace(off, bytes).first;
+        auto nx = std::next(it);
+        if (nx != free_.end() && it->first + it->second == nx->first) {
+            it->second += nx->second;
+            free_.erase(nx);
+        }
+        if (it != free_.begin()) {
+            auto pv = std::prev(it);
+            if (pv->first + pv->second == it->first) {
+                pv->second += it->second;
+                free_.erase(it);
+            }
+        }
+    }
+    uint64_t used() const { return used_; }
+    uint64_t size() const { return size_; }
+    uint64_t largest() const
+    {
+        uint64_t m = 0;
+        for (auto &kv : free_) m = std::max(m, kv.second);
+        return m;
+    }
+
+  private:
+    uint64_t size_ = 0, used_ = 0;
+    std::map<uint64_t, uint64_t> free_;
+};
+
+// A plan buffer resolved into its logical byte stream.
+struct Layout {
+    uint32_t kind;
+    uint64_t nbytes, nchunks, ngroups;
+    uint64_t row_bytes, window, outer;  // RING shape (restore compatibility)
+};
+
+struct SnapNode;
+
+}  // namespace
+}  // namespace pcs
+
+struct pcs_ctx {
+    uint64_t arena_dev = 0;    // 4096-aligned device address of arena offset 0
+    hipStream_t stream = nullptr;
+    pcs::Arena arena;
+    std::unordered_map<uint64_t, std::shared_ptr<pcs::SnapNode>> handles;
+    uint64_t next_handle = 1;
+    std::string err;
+
+    struct Slot {
+        void *host = nullptr;
+        size_t cap = 0;
+        hipEvent_t ev = nullptr;
+        bool pending = false;
+    } staging[pcs::kStagingSlots];
+    uint32_t next_slot = 0;
+
+    uint64_t *counts = nullptr;              // pinned, one per pending incremental snapshot
+    std::vector<uint32_t> free_counts;
+    std::vector<std::weak_ptr<pcs::SnapNode>> pending;
+
+    bool timing = false;
+    std::map<std::string, std::vector<std::pair<hipEvent_t, hipEvent_t>>> timers;
+};
+
+namespace pcs {
+namespace {
+
+struct SnapNode {
+    pcs_ctx *ctx = nullptr;
+    uint64_t block_off = 0, block_bytes = 0;
+    uint32_t nbufs = 0;
+    bool incremental = false, has_hashes = false;
+    std::vector<Layout> bufs;
+    std::vector<uint64_t> chunk_begin;  // per buffer, in this snapshot's chunk order
+    std::vector<uint64_t> comp_off;     // full: component offset inside the payload
+    uint64_t total_chunks = 0, state_bytes = 0;
+    uint64_t hashes_off = 0, manifest_off = 0, roots_off = 0, payload_off = 0;  // arena offsets
+    uint64_t payload_bytes = 0;         // stored bytes (incremental: after settling)
+    uint64_t reserved_payload = 0;      // incremental: slots reserved before settling
+    bool settled = true;
+    int count_slot = -1;
+    hipEvent_t ev = nullptr;
+    std::shared_ptr<SnapNode> parent;   // chunks this snapshot's manifest points into
+
+    ~SnapNode()
+    {
+        if (ev) (void)hipEventDestroy(ev);
+        if (count_slot >= 0) ctx->free_counts.push_back((uint32_t)count_slot);
+        if (block_bytes) ctx->arena.release(block_off, block_bytes);
+    }
+};
+
+int fail(pcs_ctx *c, int code, const char *fmt, ...) __attribute__((format(printf, 3, 4)));
+int fail(pcs_ctx *c, int code, const char *fmt, ...)
+{
+    if (c) {
+        char buf[512];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof buf, fmt, ap);
+        va_end(ap);
+        c->err = buf;
+    }
+    return code;
+}
+
+int hip_fail(pcs_ctx *c, hipError_t e, const char *what)
+{
+    return fail(c, PCS_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(ctx, expr)                                              \
+    do {                                                                \
+        hipError_t e_ = (expr);                                         \
+        if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);        \
+    } while (0)
+
+bool mul_ok(uint64_t a, uint64_t b, uint64_t *out)
+{
+    return !__builtin_mul_overflow(a, b, out);
+}
+
+// Validates one descriptor and appends its runs (logical start, physical
+// address), merging physically adjacent pieces.
+int describe(pcs_ctx *c, const pcs_buf &b, uint32_t idx, Layout *lay, std::vector<Run> *runs)
+{
+    if (b.flags != 0) return fail(c, PCS_E_INVAL, "buffer %u: flags must be 0", idx);
+    Layout L{};
+    L.kind = b.kind;
+    std::vector<Run> rs;
+    if (b.kind == PCS_FLAT) {
+        if (b.nbytes && (b.ptr == 0 || b.ptr % 16))
+            return fail(c, PCS_E_INVAL, "buffer %u: flat ptr must be non-null and 16-byte aligned", idx);
+        L.nbytes = b.nbytes;
+        rs.push_back({0, b.ptr});
+    } else if (b.kind == PCS_RING) {
+        if (b.row_bytes == 0 || b.row_bytes % 16 || b.ptr % 16 || b.outer_stride % 16)
+            return fail(c, PCS_E_INVAL, "buffer %u: ring ptr, row_bytes and outer_stride must be multiples of 16", idx);
+        if (b.capacity == 0 || b.window > b.capacity || b.head >= b.capacity)
+            return fail(c, PCS_E_INVAL, "buffer %u: ring needs 0 <= window <= capacity and head < capacity", idx);
+        uint64_t ring_span, win_bytes, total;
+        if (!mul_ok(b.capacity, b.row_bytes, &ring_span) || !mul_ok(b.window, b.row_bytes, &win_bytes) ||
+            !mul_ok(win_bytes, b.outer, &total))
+            return fail(c, PCS_E_INVAL, "buffer %u: ring size overflows", idx);
+        if (b.outer > 1 && b.outer_stride < ring_span)
+            return fail(c, PCS_E_INVAL, "buffer %u: outer_stride < capacity*row_bytes (rings overlap)", idx);
+        if (b.nbytes != 0 && b.nbytes != total)
+            return fail(c, PCS_E_INVAL, "buffer %u: ring nbytes must be 0 or outer*window*row_bytes", idx);
+        if (total && b.ptr == 0) return fail(c, PCS_E_INVAL, "buffer %u: null ring pointer", idx);
+        if (b.outer > (1ULL << 30)) return fail(c, PCS_E_INVAL, "buffer %u: too many rings", idx);
+        L.nbytes = total;
+        L.row_bytes = b.row_bytes;
+        L.window = b.window;
+        L.outer = b.outer;
+        uint64_t lpos = 0;
+        auto add = [&](uint64_t addr, uint64_t len) {
+            if (len == 0) return;
+            if (!rs.empty()) {
+                const uint64_t prev_end_l = lpos;  // logical end so far
+                const Run &p = rs.back();
+                if (p.addr + (prev_end_l - p.lstart) == addr) {
+                    lpos += len;
+                    return;
+                }
+            }
+            rs.push_back({lpos, addr});
+            lpos += len;
+        };
+        for (uint64_t o = 0; o < b.outer && total; ++o) {
+            const uint64_t base = b.ptr + o * b.outer_stride;
+            const uint64_t first = std::min(b.window, b.capacity - b.head);
+            add(base + b.head * b.row_bytes, first * b.row_bytes);
+            add(base, (b.window - first) * b.row_bytes);
+        }
+        if (rs.empty()) rs.push_back({0, b.ptr});
+    } else {
+        return fail(c, PCS_E_INVAL, "buffer %u: unknown kind %u", idx, b.kind);
+    }
+    L.nchunks = div_up(L.nbytes, kChunk);
+    L.ngroups = div_up(L.nchunks, kGroupChunks);
+    *lay = L;
+    runs->insert(runs->end(), rs.begin(), rs.end());
+    return PCS_OK;
+}
+
+// A job under construction: buffer table, run table, and group totals.
+struct Job {
+    std::vector<JobBuf> bufs;
+    std::vector<Run> runs;
+    std::vector<Layout> lays;
+    uint64_t ngroups = 0, nchunks = 0;
+};
+
+int add_buffers(pcs_ctx *c, Job &job, const pcs_buf *bufs, uint32_t n, uint32_t idx0)
+{
+    for (uint32_t i = 0; i < n; ++i) {
+        Layout lay;
+        const size_t r0 = job.runs.size();
+        const int st = describe(c, bufs[i], idx0 + i, &lay, &job.runs);
+        if (st) return st;
+        if (job.runs.size() > (1ULL << 31)) return fail(c, PCS_E_INVAL, "too many runs");
+        JobBuf jb{};
+        jb.nbytes = lay.nbytes;
+        jb.nchunks = lay.nchunks;
+        jb.chunk_begin = job.nchunks;
+        jb.group_begin = job.ngroups;
+        jb.run_begin = (uint32_t)r0;
+        jb.run_count = (uint32_t)(job.runs.size() - r0);
+        job.nchunks += lay.nchunks;
+        job.ngroups += lay.ngroups;
+        if (job.ngroups > kMaxGroups) return fail(c, PCS_E_INVAL, "job too large (%llu groups)", (unsigned long long)job.ngroups);
+        job.bufs.push_back(jb);
+        job.lays.push_back(lay);
+    }
+    return PCS_OK;
+}
+
+// Per-call device scratch from the arena, released when the call returns.
+// Reuse is safe: later users are stream-ordered after this call's kernels.
+struct Temp {
+    pcs_ctx *c;
+    uint64_t off = 0, bytes = 0;
+    explicit Temp(pcs_ctx *ctx) : c(ctx) {}
+    ~Temp()
+    {
+        if (bytes) c->arena.release(off, bytes);
+    }
+    Temp(const Temp &) = delete;
+    Temp &operator=(const Temp &) = delete;
+};
+
+// Carves sub-buffers out of one temp block.
+struct Carver {
+    std::vector<std::pair<uint64_t *, uint64_t>> parts;  // (where to store offset, bytes)
+    uint64_t total = 0;
+    void add(uint64_t *off, uint64_t bytes)
+    {
+        *off = total;
+        total += round_up(std::max<uint64_t>(bytes, 8), 256);
+    }
+};
+
+int temp_alloc(pcs_ctx *c, Temp &t, uint64_t bytes)
+{
+    if (!c->arena.alloc(bytes, &t.off))
+        return fail(c, PCS_E_NOMEM, "arena cannot hold %llu bytes of scratch", (unsigned long long)bytes);
+    t.bytes = bytes;
+    return PCS_OK;
+}
+
+// Copies host bytes to device memory through a pinned staging slot.
+int upload(pcs_ctx *c, uint64_t dev, const void *src, size_t bytes)
+{
+    if (bytes == 0) return PCS_OK;
+    pcs_ctx::Slot &s = c->staging[c->next_slot];
+    c->next_slot = (c->next_slot + 1) % kStagingSlots;
+    if (s.pending) {
+        HIP_TRY(c, hipEventSynchronize(s.ev));
+        s.pending = false;
+    }
+    if (s.cap < bytes) {
+        if (s.host) HIP_TRY(c, hipHostFree(s.host));
+        s.host = nullptr;
+        const size_t cap = round_up(bytes, 1 << 20);
+        HIP_TRY(c, hipHostMalloc(&s.host, cap, hipHostMallocDefault));
+        s.cap = cap;
+    }
+    memcpy(s.host, src, bytes);
+    HIP_TRY(c, hipMemcpyAsync((void *)dev, s.host, bytes, hipMemcpyHostToDevice, c->stream));
+    HIP_TRY(c, hipEventRecord(s.ev, c->stream));
+    s.pending = true;
+    return PCS_OK;
+}
+
+template <class F>
+int launch(pcs_ctx *c, const char *name, F &&f)
+{
+    hipEvent_t a = nullptr, b = nullptr;
+    if (c->timing) {
+        HIP_TRY(c, hipEventCreate(&a));
+        HIP_TRY(c, hipEventCreate(&b));
+        HIP_TRY(c, hipEventRecord(a, c->stream));
+    }
+    const hipError_t e = f();
+    if (c->timing) {
+        HIP_TRY(c, hipEventRecord(b, c->stream));
+        c->timers[name].push_back({a, b});
+    }
+    if (e != hipSuccess) return hip_fail(c, e, name);
+    return PCS_OK;
+}
+
+// Incremental snapshots reserve worst-case payload space; once the stream
+// has produced the stored-chunk count, the unused tail goes back to the arena.
+void settle(pcs_ctx *c, bool wait)
+{
+    std::vector<std::weak_ptr<SnapNode>> keep;
+    for (auto &w : c->pending) {
+        auto n = w.lock();
+        if (!n || n->settled) continue;
+        hipError_t q = wait ? hipEventSynchronize(n->ev) : hipEventQuery(n->ev);
+        if (q != hipSuccess) {
+            keep.push_back(w);
+            continue;
+        }
+        const uint64_t dirty = c->counts[n->count_slot];
+        c->free_counts.push_back((uint32_t)n->count_slot);
+        n->count_slot = -1;
+        n->payload_bytes = dirty * kChunk;
+        const uint64_t keep_bytes = round_up(n->payload_off - n->block_off + n->payload_bytes, kAlign);
+        const uint64_t old = round_up(n->block_bytes, kAlign);
+        if (keep_bytes < old) {
+            c->arena.release(n->block_off + keep_bytes, old - keep_bytes);
+            n->block_bytes = keep_bytes;
+        }
+        n->settled = true;
+    }
+    c->pending.swap(keep);
+}
+
+// Allocates a snapshot block, first settling finished incremental
+// snapshots, then (if still short) waiting for all of them.
+bool alloc_block(pcs_ctx *c, uint64_t bytes, uint64_t *off)
+{
+    settle(c, false);
+    if (c->arena.alloc(bytes, off)) return true;
+    if (!c->pending.empty()) {
+        settle(c, true);
+        return c->arena.alloc(bytes, off);
+    }
+    return false;
+}
+
+std::shared_ptr<SnapNode> lookup(pcs_ctx *c, pcs_snap h)
+{
+    auto it = c->handles.find(h);
+    return it == c->handles.end() ? nullptr : it->second;
+}
+
+pcs_snap new_handle(pcs_ctx *c, std::shared_ptr<SnapNode> n)
+{
+    const pcs_snap h = c->next_handle++;
+    c->handles.emplace(h, std::move(n));
+    return h;
+}
+
+// Shared part of fingerprint / full checkpoint / batch checkpoint: a job over
+// `sessions` sessions whose buffers are already in `job`; fingerprints of
+// buffer b go to job.bufs[b].hash_dst, roots to root_dst[b][0..1], session
+// roots to sroot_dst[s][0..1].
+struct RootDst {
+    uint64_t d[2];
+};
+
+int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &sess_nbufs,
+                 const std::vector<RootDst> &root_dst, const std::vector<RootDst> &sroot_dst,
+                 bool want_roots)
+{
+    const uint32_t n = (uint32_t)job.bufs.size();
+    const uint32_t S = (uint32_t)sess_nbufs.size();
+    std::vector<MerkleList> lists;
+    if (want_roots) {
+        for (uint32_t b = 0; b < n; ++b)
+            lists.push_back({job.bufs[b].group_begin, job.lays[b].ngroups, {root_dst[b].d[0], root_dst[b].d[1]}});
+        uint64_t first = 0;
+        for (uint32_t s = 0; s < S; ++s) {
+            lists.push_back({first, sess_nbufs[s], {sroot_dst[s].d[0], sroot_dst[s].d[1]}});
+            first += sess_nbufs[s];
+        }
+    }
+    Carver cv;
+    uint64_t o_bufs, o_runs, o_lists, o_map, o_nodes, o_sa, o_sb, o_roots;
+    const uint64_t G = job.ngroups;
+    cv.add(&o_bufs, sizeof(JobBuf) * n);
+    cv.add(&o_runs, sizeof(Run) * job.runs.size());
+    cv.add(&o_lists, sizeof(MerkleList) * lists.size());
+    const uint64_t host_bytes = cv.total;
+    cv.add(&o_map, 4 * G);
+    cv.add(&o_nodes, 8 * G);
+    cv.add(&o_sa, 8 * std::max<uint64_t>(G, n));
+    cv.add(&o_sb, 8 * std::max<uint64_t>(G, n));
+    cv.add(&o_roots, 8 * n);
+    Temp t(c);
+    if (int st = temp_alloc(c, t, cv.total)) return st;
+    const uint64_t base = c->arena_dev + t.off;
+
+    std::vector<uint8_t> host(host_bytes, 0);
+    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+    if (!lists.empty()) memcpy(host.data() + o_lists, lists.data(), sizeof(MerkleList) * lists.size());
+    if (int st = upload(c, base, host.data(), host_bytes)) return st;
+
+    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
+    const Run *d_runs = (const Run *)(base + o_runs);
+    const MerkleList *d_lists = (const MerkleList *)(base + o_lists);
+    uint32_t *d_map = (uint32_t *)(base + o_map);
+    uint64_t *d_nodes = (uint64_t *)(base + o_nodes);
+    uint64_t *d_sa = (uint64_t *)(base + o_sa), *d_sb = (uint64_t *)(base + o_sb);
+    uint64_t *d_roots = (uint64_t *)(base + o_roots);
+    hipStream_t s = c->stream;
+
+    int st;
+    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, s); }))) return st;
+    if ((st = launch(c, copy ? "pack_hash" : "hash", [&] {
+             return launch_hash(d_bufs, d_runs, d_map, G, copy, false, d_nodes, nullptr, nullptr, s);
+         })))
+        return st;
+    if (want_roots) {
+        if ((st = launch(c, "merkle", [&] { return launch_merkle(d_lists, n, d_nodes, d_sa, d_sb, d_roots, s); })))
+            return st;
+        if ((st = launch(c, "merkle", [&] {
+                 return launch_merkle(d_lists + n, S, d_roots, d_sa, d_sb, nullptr, s);
+             })))
+            return st;
+    }
+    return PCS_OK;
+}
+
+struct FullPlan {
+    std::vector<uint64_t> comp_off;
+    uint64_t payload = 0, hashes_rel = 0, roots_rel = 0, payload_rel = 0, block = 0;
+};
+
+FullPlan full_plan(const Job &job, size_t b0, size_t nb, uint64_t nchunks, bool hashes)
+{
+    FullPlan p;
+    for (size_t b = b0; b < b0 + nb; ++b) {
+        p.comp_off.push_back(p.payload);
+        p.payload += job.lays[b].nchunks * kChunk;
+    }
+    uint64_t off = 0;
+    p.hashes_rel = off;
+    if (hashes) off += 8 * nchunks;
+    p.roots_rel = off;
+    off += 8 * (nb + 1);
+    p.payload_rel = round_up(off, kAlign);
+    p.block = p.payload_rel + p.payload;
+    return p;
+}
+
+std::shared_ptr<SnapNode> make_node(pcs_ctx *c, const Job &job, size_t b0, size_t nb, const FullPlan &p,
+                                    uint64_t block_off, bool hashes)
+{
+    auto node = std::make_shared<SnapNode>();
+    node->ctx = c;
+    node->block_off = block_off;
+    node->block_bytes = p.block;
+    node->nbufs = (uint32_t)nb;
+    node->has_hashes = hashes;
+    uint64_t cb = 0;
+    for (size_t b = b0; b < b0 + nb; ++b) {
+        node->bufs.push_back(job.lays[b]);
+        node->chunk_begin.push_back(cb);
+        cb += job.lays[b].nchunks;
+        node->state_bytes += job.lays[b].nbytes;
+    }
+    node->total_chunks = cb;
+    node->comp_off = p.comp_off;
+    node->hashes_off = block_off + p.hashes_rel;
+    node->roots_off = block_off + p.roots_rel;
+    node->payload_off = block_off + p.payload_rel;
+    node->payload_bytes = p.payload;
+    return node;
+}
+
+// Full checkpoints of several sessions in one launch.
+int checkpoint_full(pcs_ctx *c, const pcs_buf *plans, const uint32_t *nbufs, uint32_t sessions, uint32_t flags,
+                    uint64_t *d_hashes, uint64_t *d_roots, uint64_t *d_sroots, pcs_snap *out)
+{
+    const bool hash = (flags & PCS_CKPT_HASH) != 0;
+    if (!hash && (d_hashes || d_roots || d_sroots))
+        return fail(c, PCS_E_INVAL, "fingerprint outputs need PCS_CKPT_HASH");
+    Job job;
+    uint64_t nb_total = 0;
+    for (uint32_t s = 0; s < sessions; ++s) nb_total += nbufs[s];
+    if (nb_total > (1u << 24)) return fail(c, PCS_E_INVAL, "too many buffers");
+    if (int st = add_buffers(c, job, plans, (uint32_t)nb_total, 0)) return st;
+
+    // Reserve every snapshot block first (all or none).
+    std::vector<FullPlan> fps;
+    std::vector<uint64_t> offs;
+    size_t b0 = 0;
+    for (uint32_t s = 0; s < sessions; ++s) {
+        uint64_t nch = 0;
+        for (size_t b = b0; b < b0 + nbufs[s]; ++b) nch += job.lays[b].nchunks;
+        fps.push_back(full_plan(job, b0, nbufs[s], nch, hash));
+        uint64_t off;
+        if (!alloc_block(c, fps.back().block, &off)) {
+            for (size_t k = 0; k < offs.size(); ++k) c->arena.release(offs[k], fps[k].block);
+            return fail(c, PCS_E_NOMEM, "arena cannot hold snapshot %u (%llu bytes)", s,
+                        (unsigned long long)fps.back().block);
+        }
+        offs.push_back(off);
+        b0 += nbufs[s];
+    }
+    std::vector<std::shared_ptr<SnapNode>> nodes;
+    b0 = 0;
+    for (uint32_t s = 0; s < sessions; ++s) {
+        nodes.push_back(make_node(c, job, b0, nbufs[s], fps[s], offs[s], hash));
+        b0 += nbufs[s];
+    }
+
+    // Wire destinations.
+    std::vector<RootDst> rdst(nb_total), sdst(sessions);
+    b0 = 0;
+    uint64_t chunk0 = 0;
+    for (uint32_t s = 0; s < sessions; ++s) {
+        const auto &nd = nodes[s];
+        for (uint32_t k = 0; k < nbufs[s]; ++k) {
+            JobBuf &jb = job.bufs[b0 + k];
+            jb.payload = c->arena_dev + nd->payload_off + nd->comp_off[k];
+            if (hash) {
+                jb.hash_dst[0] = c->arena_dev + nd->hashes_off + 8 * nd->chunk_begin[k];
+                jb.hash_dst[1] = d_hashes ? (uint64_t)(d_hashes + jb.chunk_begin) : 0;
+                rdst[b0 + k].d[0] = c->arena_dev + nd->roots_off + 8 * k;
+                rdst[b0 + k].d[1] = d_roots ? (uint64_t)(d_roots + b0 + k) : 0;
+            }
+        }
+        sdst[s].d[0] = c->arena_dev + nd->roots_off + 8 * nbufs[s];
+        sdst[s].d[1] = d_sroots ? (uint64_t)(d_sroots + s) : 0;
+        b0 += nbufs[s];
+        chunk0 += nd->total_chunks;
+    }
+    (void)chunk0;
+
+    int st;
+    if (hash) {
+        std::vector<uint32_t> sn(nbufs, nbufs + sessions);
+        st = run_hash_job(c, job, true, sn, rdst, sdst, true);
+    } else {
+        Carver cv;
+        uint64_t o_bufs, o_runs, o_map;
+        cv.add(&o_bufs, sizeof(JobBuf) * job.bufs.size());
+        cv.add(&o_runs, sizeof(Run) * job.runs.size());
+        const uint64_t hb = cv.total;
+        cv.add(&o_map, 4 * job.ngroups);
+        Temp t(c);
+        st = temp_alloc(c, t, cv.total);
+        if (!st) {
+            const uint64_t base = c->arena_dev + t.off;
+            std::vector<uint8_t> host(hb, 0);
+            memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * job.bufs.size());
+            memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+            st = upload(c, base, host.data(), hb);
+            const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
+            const Run *d_runs = (const Run *)(base + o_runs);
+            uint32_t *d_map = (uint32_t *)(base + o_map);
+            const uint32_t n = (uint32_t)job.bufs.size();
+            const uint64_t G = job.ngroups;
+            if (!st) st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); });
+            if (!st) st = launch(c, "pack", [&] { return launch_pack(d_bufs, d_runs, d_map, G, c->stream); });
+        }
+    }
+    if (st) return st;  // nodes (and their blocks) are released here
+    for (uint32_t s = 0; s < sessions; ++s) out[s] = new_handle(c, nodes[s]);
+    return PCS_OK;
+}
+
+}  // namespace
+}  // namespace pcs
+
+using namespace pcs;
+
+extern "C" {
+
+int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ctx **out)
+{
+    if (!out) return PCS_E_INVAL;
+    *out = nullptr;
+    if (!d_arena || (uint64_t)d_arena % 16) return PCS_E_INVAL;
+    const uint64_t a = (uint64_t)d_arena;
+    const uint64_t aligned = round_up(a, kAlign);
+    if (arena_bytes < aligned - a + kAlign) return PCS_E_INVAL;
+    auto *c = new pcs_ctx();
+    c->arena_dev = aligned;
+    c->arena.init((arena_bytes - (aligned - a)) / kAlign * kAlign);
+    c->stream = (hipStream_t)hip_stream;
+    for (auto &s : c->staging) {
+        if (hipEventCreateWithFlags(&s.ev, hipEventDisableTiming) != hipSuccess) {
+            pcs_ctx_destroy(c);
+            return PCS_E_HIP;
+        }
+    }
+    if (hipHostMalloc((void **)&c->counts, 8 * kCountSlots, hipHostMallocDefault) != hipSuccess) {
+        pcs_ctx_destroy(c);
+        return PCS_E_HIP;
+    }
+    for (uint32_t i = 0; i < kCountSlots; ++i) c->free_counts.push_back(kCountSlots - 1 - i);
+    *out = c;
+    return PCS_OK;
+}
+
+int pcs_ctx_destroy(pcs_ctx *c)
+{
+    if (!c) return PCS_E_INVAL;
+    (void)hipStreamSynchronize(c->stream);
+    c->handles.clear();
+    c->pending.clear();
+    for (auto &kv : c->timers)
+        for (auto &ab : kv.second) {
+            (void)hipEventDestroy(ab.first);
+            (void)hipEventDestroy(ab.second);
+        }
+    for (auto &s : c->staging) {
+        if (s.ev) (void)hipEventDestroy(s.ev);
+        if (s.host) (void)hipHostFree(s.host);
+    }
+    if (c->counts) (void)hipHostFree(c->counts);
+    delete c;
+    return PCS_OK;
+}
+
+const char *pcs_last_error(const pcs_ctx *c) { return c ? c->err.c_str() : "null context"; }
+
+int pcs_chunk_counts(const pcs_buf *bufs, uint32_t n, uint64_t *chunks, uint64_t *total)
+{
+    if (n && !bufs) return PCS_E_INVAL;
+    uint64_t t = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        Layout lay;
+        std::vector<Run> rs;
+        if (int st = describe(nullptr, bufs[i], i, &lay, &rs)) return st;
+        if (chunks) chunks[i] = lay.nchunks;
+        t += lay.nchunks;
+    }
+    if (total) *total = t;
+    return PCS_OK;
+}
+
+int pcs_fingerprint(pcs_ctx *c, const pcs_buf *bufs, uint32_t n, uint64_t *d_hashes, uint64_t *d_roots,
+                    uint64_t *d_sroot)
+{
+    if (!c) return PCS_E_INVAL;
+    if (n && !bufs) return fail(c, PCS_E_INVAL, "null buffer array");
+    if (n > (1u << 24)) return fail(c, PCS_E_INVAL, "too many buffers");
+    Job job;
+    if (int st = add_buffers(c, job, bufs, n, 0)) return st;
+    std::vector<RootDst> rdst(n), sdst(1);
+    for (uint32_t b = 0; b < n; ++b) {
+        job.bufs[b].hash_dst[0] = d_hashes ? (uint64_t)(d_hashes + job.bufs[b].chunk_begin) : 0;
+        rdst[b].d[0] = d_roots ? (uint64_t)(d_roots + b) : 0;
+    }
+    sdst[0].d[0] = (uint64_t)d_sroot;
+    settle(c, false);
+    return run_hash_job(c, job, false, {n}, rdst, sdst, d_roots || d_sroot);
+}
+
+int pcs_classify(pcs_ctx *c, const uint64_t *d_hashes, uint32_t K, const uint64_t *h_chunks, uint32_t n,
+                 uint64_t *d_bitmap, uint8_t *d_labels)
+{
+    if (!c) return PCS_E_INVAL;
+    if (K == 0) return fail(c, PCS_E_INVAL, "K must be >= 1");
+    if (n && !h_chunks) return fail(c, PCS_E_INVAL, "null chunk counts");
+    if (n > (1u << 24)) return fail(c, PCS_E_INVAL, "too many buffers");
+    Job job;
+    for (uint32_t b = 0; b < n; ++b) {
+        JobBuf jb{};
+        jb.nchunks = h_chunks[b];
+        jb.chunk_begin = job.nchunks;
+        jb.group_begin = job.ngroups;
+        job.nchunks += h_chunks[b];
+        job.ngroups += div_up(h_chunks[b], kGroupChunks);
+        if (job.ngroups > kMaxGroups) return fail(c, PCS_E_INVAL, "too many chunks");
+        job.bufs.push_back(jb);
+    }
+    if (job.nchunks && !d_hashes) return fail(c, PCS_E_INVAL, "null hashes");
+    if (job.ngroups && !d_bitmap) return fail(c, PCS_E_INVAL, "null bitmap");
+    if (n && !d_labels) return fail(c, PCS_E_INVAL, "null labels");
+    if (n == 0) return PCS_OK;
+    Carver cv;
+    uint64_t o_bufs, o_map;
+    cv.add(&o_bufs, sizeof(JobBuf) * n);
+    const uint64_t hb = cv.total;
+    cv.add(&o_map, 4 * job.ngroups);
+    Temp t(c);
+    if (int st = temp_alloc(c, t, cv.total)) return st;
+    const uint64_t base = c->arena_dev + t.off;
+    std::vector<uint8_t> host(hb, 0);
+    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+    if (int st = upload(c, base, host.data(), hb)) return st;
+    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
+    uint32_t *d_map = (uint32_t *)(base + o_map);
+    const uint64_t G = job.ngroups, T = job.nchunks;
+    int st;
+    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
+    if ((st = launch(c, "classify", [&] { return launch_classify(d_bufs, d_map, G, d_hashes, K, T, d_bitmap, c->stream); })))
+        return st;
+    return launch(c, "classify", [&] { return launch_labels(d_bufs, n, d_bitmap, d_labels, c->stream); });
+}
+
+int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent, uint32_t flags,
+                   uint64_t *d_hashes, uint64_t *d_roots, uint64_t *d_sroot, pcs_snap *out)
+{
+    if (!c) return PCS_E_INVAL;
+    if (!out) return fail(c, PCS_E_INVAL, "null output handle");
+    if (n && !plan) return fail(c, PCS_E_INVAL, "null plan");
+    if (flags & ~PCS_CKPT_HASH) return fail(c, PCS_E_INVAL, "unknown flags");
+    if (parent == 0) {
+        const uint32_t nb[1] = {n};
+        return checkpoint_full(c, plan, nb, 1, flags, d_hashes, d_roots, d_sroot, out);
+    }
+
+    // Incremental checkpoint against `parent`.
+    auto par = lookup(c, parent);
+    if (!par) return fail(c, PCS_E_HANDLE, "unknown parent handle %llu", (unsigned long long)parent);
+    if (!par->has_hashes) return fail(c, PCS_E_INVAL, "parent snapshot holds no fingerprints");
+    if (par->nbufs != n) return fail(c, PCS_E_INVAL, "plan has %u buffers, parent %u", n, par->nbufs);
+    Job job;
+    if (int st = add_buffers(c, job, plan, n, 0)) return st;
+    const uint64_t T = job.nchunks, G = job.ngroups;
+
+    // Block: [hashes 8T][manifest 8T][roots 8(n+1)] [payload, T slots reserved].
+    const uint64_t hashes_rel = 0, manifest_rel = 8 * T, roots_rel = 16 * T;
+    const uint64_t payload_rel = round_up(roots_rel + 8 * (n + 1), kAlign);
+    const uint64_t block = payload_rel + T * kChunk;
+    if (c->free_counts.empty()) settle(c, true);
+    if (c->free_counts.empty()) return fail(c, PCS_E_NOMEM, "too many incremental snapshots in flight");
+    uint64_t boff;
+    if (!alloc_block(c, block, &boff))
+        return fail(c, PCS_E_NOMEM, "arena cannot hold incremental snapshot (%llu bytes reserved)",
+                    (unsigned long long)block);
+    auto node = std::make_shared<SnapNode>();
+    node->ctx = c;
+    node->block_off = boff;
+    node->block_bytes = block;
+    node->nbufs = n;
+    node->incremental = true;
+    node->has_hashes = true;
+    for (uint32_t b = 0; b < n; ++b) {
+        node->bufs.push_back(job.lays[b]);
+        node->chunk_begin.push_back(job.bufs[b].chunk_begin);
+        node->state_bytes += job.lays[b].nbytes;
+    }
+    node->total_chunks = T;
+    node->hashes_off = boff + hashes_rel;
+    node->manifest_off = boff + manifest_rel;
+    node->roots_off = boff + roots_rel;
+    node->payload_off = boff + payload_rel;
+    node->reserved_payload = T * kChunk;
+    node->parent = par;
+    if (hipEventCreateWithFlags(&node->ev, hipEventDisableTiming) != hipSuccess)
+        return fail(c, PCS_E_HIP, "hipEventCreate failed");
+
+    std::vector<MerkleList> lists;
+    for (uint32_t b = 0; b < n; ++b) {
+        JobBuf &jb = job.bufs[b];
+        jb.hash_dst[0] = c->arena_dev + node->hashes_off + 8 * jb.chunk_begin;
+        jb.hash_dst[1] = d_hashes ? (uint64_t)(d_hashes + jb.chunk_begin) : 0;
+        jb.manifest = c->arena_dev + node->manifest_off + 8 * jb.chunk_begin;
+        jb.parent_hash = c->arena_dev + par->hashes_off + 8 * par->chunk_begin[b];
+        jb.parent_chunks = par->bufs[b].nchunks;
+        if (par->incremental) {
+            jb.parent_manifest = c->arena_dev + par->manifest_off + 8 * par->chunk_begin[b];
+        } else {
+            jb.parent_slot0 = par->payload_off + par->comp_off[b];
+        }
+        lists.push_back({jb.group_begin, job.lays[b].ngroups,
+                         {c->arena_dev + node->roots_off + 8 * b, d_roots ? (uint64_t)(d_roots + b) : 0}});
+    }
+    lists.push_back({0, n, {c->arena_dev + node->roots_off + 8 * n, (uint64_t)d_sroot}});
+
+    Carver cv;
+    uint64_t o_bufs, o_runs, o_lists, o_map, o_nodes, o_sa, o_sb, o_roots, o_cnt, o_mask, o_offs, o_total, o_list;
+    cv.add(&o_bufs, sizeof(JobBuf) * n);
+    cv.add(&o_runs, sizeof(Run) * job.runs.size());
+    cv.add(&o_lists, sizeof(MerkleList) * lists.size());
+    const uint64_t hb = cv.total;
+    cv.add(&o_map, 4 * G);
+    cv.add(&o_nodes, 8 * G);
+    cv.add(&o_sa, 8 * std::max<uint64_t>(G, n));
+    cv.add(&o_sb, 8 * std::max<uint64_t>(G, n));
+    cv.add(&o_roots, 8 * n);
+    cv.add(&o_cnt, 4 * G);
+    cv.add(&o_mask, 8 * G);
+    cv.add(&o_offs, 8 * G);
+    cv.add(&o_total, 8);
+    cv.add(&o_list, 8 * T);
+    Temp t(c);
+    if (int st = temp_alloc(c, t, cv.total)) return st;
+    const uint64_t base = c->arena_dev + t.off;
+    std::vector<uint8_t> host(hb, 0);
+    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+    memcpy(host.data() + o_lists, lists.data(), sizeof(MerkleList) * lists.size());
+    if (int st = upload(c, base, host.data(), hb)) return st;
+
+    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
+    const Run *d_runs = (const Run *)(base + o_runs);
+    const MerkleList *d_lists = (const MerkleList *)(base + o_lists);
+    uint32_t *d_map = (uint32_t *)(base + o_map);
+    uint64_t *d_nodes = (uint64_t *)(base + o_nodes);
+    uint64_t *d_sa = (uint64_t *)(base + o_sa), *d_sb = (uint64_t *)(base + o_sb);
+    uint64_t *d_roots_tmp = (uint64_t *)(base + o_roots);
+    uint32_t *d_cnt = (uint32_t *)(base + o_cnt);
+    uint64_t *d_mask = (uint64_t *)(base + o_mask), *d_offs = (uint64_t *)(base + o_offs);
+    uint64_t *d_total = (uint64_t *)(base + o_total), *d_list = (uint64_t *)(base + o_list);
+    hipStream_t s = c->stream;
+    const uint64_t payload_dev = c->arena_dev + node->payload_off;
+    int st;
+    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, s); }))) return st;
+    if ((st = launch(c, "incremental", [&] {
+             return launch_hash(d_bufs, d_runs, d_map, G, false, true, d_nodes, d_cnt, d_mask, s);
+         })))
+        return st;
+    if ((st = launch(c, "merkle", [&] { return launch_merkle(d_lists, n, d_nodes, d_sa, d_sb, d_roots_tmp, s); })))
+        return st;
+    if ((st = launch(c, "merkle", [&] { return launch_merkle(d_lists + n, 1, d_roots_tmp, d_sa, d_sb, nullptr, s); })))
+        return st;
+    if ((st = launch(c, "incremental", [&] { return launch_scan(d_cnt, G, d_offs, d_total, s); }))) return st;
+    if ((st = launch(c, "incremental", [&] {
+             return launch_compact(d_bufs, d_map, G, d_mask, d_offs, node->payload_off, d_list, s);
+         })))
+        return st;
+    if ((st = launch(c, "incremental", [&] { return launch_pack_dirty(d_bufs, d_runs, d_list, d_total, T, payload_dev, s); })))
+        return st;
+    node->count_slot = (int)c->free_counts.back();
+    c->free_counts.pop_back();
+    HIP_TRY(c, hipMemcpyAsync(&c->counts[node->count_slot], d_total, 8, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipEventRecord(node->ev, s));
+    node->settled = false;
+    c->pending.push_back(node);
+    *out = new_handle(c, node);
+    return PCS_OK;
+}
+
+int pcs_checkpoint_batch(pcs_ctx *c, const pcs_buf *plans, const uint32_t *nbufs, uint32_t sessions, uint32_t flags,
+                         uint64_t *d_hashes, uint64_t *d_roots, uint64_t *d_sroots, pcs_snap *out)
+{
+    if (!c) return PCS_E_INVAL;
+    if (sessions && (!nbufs || !out)) return fail(c, PCS_E_INVAL, "null argument");
+    if (flags & ~PCS_CKPT_HASH) return fail(c, PCS_E_INVAL, "unknown flags");
+    uint64_t nb = 0;
+    for (uint32_t s = 0; s < sessions; ++s) nb += nbufs[s];
+    if (nb && !plans) return fail(c, PCS_E_INVAL, "null plans");
+    return checkpoint_full(c, plans, nbufs, sessions, flags, d_hashes, d_roots, d_sroots, out);
+}
+
+int pcs_restore_batch(pcs_ctx *c, const pcs_snap *snaps, uint32_t m, const pcs_buf *dsts, const uint32_t *nbufs)
+{
+    if (!c) return PCS_E_INVAL;
+    if (m && (!snaps || !nbufs)) return fail(c, PCS_E_INVAL, "null argument");
+    Job job;
+    uint64_t nb_total = 0;
+    std::vector<std::shared_ptr<SnapNode>> nodes;
+    for (uint32_t j = 0; j < m; ++j) {
+        auto nd = lookup(c, snaps[j]);
+        if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snaps[j]);
+        if (nbufs[j] != nd->nbufs)
+            return fail(c, PCS_E_SHAPE, "snapshot %u holds %u buffers, %u destinations given", j, nd->nbufs, nbufs[j]);
+        nodes.push_back(nd);
+        nb_total += nbufs[j];
+    }
+    if (nb_total && !dsts) return fail(c, PCS_E_INVAL, "null destinations");
+    if (nb_total > (1u << 24)) return fail(c, PCS_E_INVAL, "too many buffers");
+    if (int st = add_buffers(c, job, dsts, (uint32_t)nb_total, 0)) return st;
+    uint32_t b = 0;
+    for (uint32_t j = 0; j < m; ++j) {
+        const auto &nd = nodes[j];
+        for (uint32_t k = 0; k < nd->nbufs; ++k, ++b) {
+            const Layout &want = nd->bufs[k], &got = job.lays[b];
+            if (want.kind != got.kind || want.nbytes != got.nbytes ||
+                (want.kind == PCS_RING && (want.row_bytes != got.row_bytes || want.window != got.window ||
+                                           want.outer != got.outer)))
+                return fail(c, PCS_E_SHAPE, "restore %u buffer %u: destination layout differs from the snapshot", j, k);
+            JobBuf &jb = job.bufs[b];
+            if (nd->incremental)
+                jb.manifest = c->arena_dev + nd->manifest_off + 8 * nd->chunk_begin[k];
+            else
+                jb.payload = c->arena_dev + nd->payload_off + nd->comp_off[k];
+        }
+    }
+    const uint32_t n = (uint32_t)nb_total;
+    if (n == 0) return PCS_OK;
+    Carver cv;
+    uint64_t o_bufs, o_runs, o_map;
+    cv.add(&o_bufs, sizeof(JobBuf) * n);
+    cv.add(&o_runs, sizeof(Run) * job.runs.size());
+    const uint64_t hb = cv.total;
+    cv.add(&o_map, 4 * job.ngroups);
+    Temp t(c);
+    if (int st = temp_alloc(c, t, cv.total)) return st;
+    const uint64_t base = c->arena_dev + t.off;
+    std::vector<uint8_t> host(hb, 0);
+    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+    if (int st = upload(c, base, host.data(), hb)) return st;
+    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
+    const Run *d_runs = (const Run *)(base + o_runs);
+    uint32_t *d_map = (uint32_t *)(base + o_map);
+    const uint64_t G = job.ngroups;
+    int st;
+    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
+    return launch(c, "copy", [&] { return launch_restore(d_bufs, d_runs, d_map, G, c->arena_dev, c->stream); });
+}
+
+int pcs_restore(pcs_ctx *c, pcs_snap snap, const pcs_buf *dst, uint32_t n)
+{
+    return pcs_restore_batch(c, &snap, 1, dst, &n);
+}
+
+int pcs_fork(pcs_ctx *c, pcs_snap snap, pcs_snap *out)
+{
+    if (!c) return PCS_E_INVAL;
+    if (!out) return fail(c, PCS_E_INVAL, "null output handle");
+    auto nd = lookup(c, snap);
+    if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    *out = new_handle(c, nd);
+    return PCS_OK;
+}
+
+int pcs_delete(pcs_ctx *c, pcs_snap snap)
+{
+    if (!c) return PCS_E_INVAL;
+    auto it = c->handles.find(snap);
+    if (it == c->handles.end()) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    c->handles.erase(it);
+    return PCS_OK;
+}
+
+int pcs_snapshot_info(pcs_ctx *c, pcs_snap snap, pcs_snap_info *out)
+{
+    if (!c) return PCS_E_INVAL;
+    if (!out) return fail(c, PCS_E_INVAL, "null output");
+    auto nd = lookup(c, snap);
+    if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    if (!nd->settled) settle(c, true);
+    memset(out, 0, sizeof *out);
+    out->state_bytes = nd->state_bytes;
+    out->stored_bytes = nd->payload_bytes;
+    out->total_chunks = nd->total_chunks;
+    out->dirty_chunks = nd->incremental ? nd->payload_bytes / kChunk : nd->total_chunks;
+    out->nbufs = nd->nbufs;
+    out->incremental = nd->incremental;
+    out->has_hashes = nd->has_hashes;
+    return PCS_OK;
+}
+
+int pcs_snapshot_payload(pcs_ctx *c, pcs_snap snap, void *d_dst, uint64_t cap)
+{
+    if (!c) return PCS_E_INVAL;
+    auto nd = lookup(c, snap);
+    if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    if (!nd->settled) settle(c, true);
+    if (cap < nd->payload_bytes) return fail(c, PCS_E_INVAL, "destination holds %llu bytes, payload is %llu",
+                                             (unsigned long long)cap, (unsigned long long)nd->payload_bytes);
+    if (nd->payload_bytes == 0) return PCS_OK;
+    if (!d_dst) return fail(c, PCS_E_INVAL, "null destination");
+    HIP_TRY(c, hipMemcpyAsync(d_dst, (void *)(c->arena_dev + nd->payload_off), nd->payload_bytes,
+                              hipMemcpyDeviceToDevice, c->stream));
+    return PCS_OK;
+}
+
+int pcs_snapshot_hashes(pcs_ctx *c, pcs_snap snap, uint64_t *d_dst, uint64_t cap)
+{
+    if (!c) return PCS_E_INVAL;
+    auto nd = lookup(c, snap);
+    if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    if (!nd->has_hashes) return fail(c, PCS_E_INVAL, "snapshot holds no fingerprints");
+    if (cap < nd->total_chunks) return fail(c, PCS_E_INVAL, "destination too small");
+    if (nd->total_chunks == 0) return PCS_OK;
+    if (!d_dst) return fail(c, PCS_E_INVAL, "null destination");
+    HIP_TRY(c, hipMemcpyAsync(d_dst, (void *)(c->arena_dev + nd->hashes_off), 8 * nd->total_chunks,
+                              hipMemcpyDeviceToDevice, c->stream));
+    return PCS_OK;
+}
+
+int pcs_arena_stats(pcs_ctx *c, uint64_t *used, uint64_t *free_bytes, uint64_t *largest, uint64_t *live)
+{
+    if (!c) return PCS_E_INVAL;
+    settle(c, false);
+    if (used) *used = c->arena.used();
+    if (free_bytes) *free_bytes = c->arena.size() - c->arena.used();
+    if (largest) *largest = c->arena.largest();
+    if (live) *live = c->handles.size();
+    return PCS_OK;
+}
+
+int pcs_set_timing(pcs_ctx *c, int enable)
+{
+    if (!c) return PCS_E_INVAL;
+    c->timing = enable != 0;
+    return PCS_OK;
+}
+
+int pcs_kernel_time(pcs_ctx *c, const char *name, uint64_t *launches, double *total_ms)
+{
+    if (!c || !name) return PCS_E_INVAL;
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    double ms = 0;
+    uint64_t k = 0;
+    auto it = c->timers.find(name);
+    if (it != c->timers.end()) {
+        for (auto &ab : it->second) {
+            float t = 0;
+            HIP_TRY(c, hipEventElapsedTime(&t, ab.first, ab.second));
+            ms += t;
+            ++k;
+            (void)hipEventDestroy(ab.first);
+            (void)hipEventDestroy(ab.second);
+        }
+        c->timers.erase(it);
+    }
+    if (launches) *launches = k;
+    if (total_ms) *total_ms = ms;
+    return PCS_OK;
+}
+
+}  // extern "C"

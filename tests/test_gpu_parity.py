@@ -1,0 +1,364 @@
+"""GPU parity: libpcs (HIP, through the C ABI) against the CPU oracle,
+element by element, on seeded inputs that span several 64-chunk groups,
+ragged tails, empty buffers and wrapped ring windows.  Bit-exact throughout
+(everything is integer and byte work)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from tests.gpu_util import arena, dev, host, log, u64, zeros_u64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def pcs():
+    import paper_2607_21686_amd as P
+    return P
+
+
+@pytest.fixture()
+def ctx(pcs):
+    c = pcs.Context(arena(256 << 20))
+    yield c
+    c.close()
+
+
+FLAT_SIZES = [0, 1, 7, 15, 16, 17, 31, 32, 33, 63, 100, 4095, 4096, 4097, 8191, 12288 + 24,
+              64 * 4096, 64 * 4096 + 1, 65 * 4096 - 5, 130 * 4096 + 8, 200 * 4096 + 4000]
+
+
+def oracle_fp(bufs):
+    h, r, s = oracle.fingerprint(bufs)
+    return h, r, s
+
+
+def gpu_fp(ctx, pcs, descs, total_chunks):
+    ch = zeros_u64(total_chunks)
+    rt = zeros_u64(len(descs))
+    sr = zeros_u64(1)
+    ctx.fingerprint(descs, ch, rt, sr)
+    return u64(ch)[:total_chunks], u64(rt)[:len(descs)], int(u64(sr)[0])
+
+
+def test_fingerprint_flat_sizes(ctx, pcs):
+    rng = np.random.default_rng(10)
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in FLAT_SIZES]
+    log("fingerprint flat sizes", FLAT_SIZES)
+    d = [dev(b) for b in bufs]
+    descs = [pcs.flat(t, b.size) for t, b in zip(d, bufs)]
+    h, r, s = oracle_fp(bufs)
+    gh, gr, gs = gpu_fp(ctx, pcs, descs, h.size)
+    assert np.array_equal(gh, h)
+    assert np.array_equal(gr, r)
+    assert gs == s
+
+
+def test_fingerprint_each_size_alone(ctx, pcs):
+    rng = np.random.default_rng(11)
+    for n in FLAT_SIZES + [1 << 20, (1 << 20) + 3]:
+        b = rng.integers(0, 256, size=n, dtype=np.uint8)
+        log("fingerprint single", n)
+        h, r, s = oracle_fp([b])
+        gh, gr, gs = gpu_fp(ctx, pcs, [pcs.flat(dev(b), n)], h.size)
+        assert np.array_equal(gh, h) and np.array_equal(gr, r) and gs == s, n
+
+
+def test_fingerprint_no_buffers(ctx, pcs):
+    log("fingerprint of zero buffers")
+    gh, gr, gs = gpu_fp(ctx, pcs, [], 0)
+    assert gs == oracle.merkle_root([])
+
+
+RING_CASES = [
+    # outer, capacity, row_bytes, window, head, pad
+    (1, 8, 16, 8, 0, 0),
+    (1, 8, 16, 5, 6, 0),
+    (3, 10, 32, 7, 9, 48),
+    (4, 64, 2048, 40, 60, 0),
+    (2, 16, 48, 1, 15, 16),
+    (2, 16, 48, 16, 3, 0),
+    (5, 7, 4096, 6, 4, 4096),
+    (2, 300, 2048, 257, 299, 0),     # odd head: chunks straddle the wrap
+    (6, 1000, 16, 999, 1, 32),       # tiny rows: many rows per chunk
+    (64, 96, 2048, 64, 95, 0),       # many rings, wrap at the last slot
+]
+
+
+@pytest.mark.parametrize("case", RING_CASES)
+def test_fingerprint_ring(ctx, pcs, case):
+    outer, cap, row, win, head, pad = case
+    g = W.Ring(outer, cap, row, win, head, cap * row + pad)
+    log("fingerprint ring", case)
+    data = np.random.default_rng(cap + row).integers(0, 256, size=g.ring_bytes, dtype=np.uint8)
+    logical = oracle.ring_window(data, g.outer, g.outer_stride, g.capacity, g.row_bytes, g.head, g.window)
+    h, r, s = oracle_fp([logical])
+    d = dev(data)
+    gh, gr, gs = gpu_fp(ctx, pcs, [pcs.ring(d, outer, cap, row, head, win, g.outer_stride)], h.size)
+    assert np.array_equal(gh, h) and np.array_equal(gr, r) and gs == s
+
+
+def test_classify_matches_oracle(ctx, pcs):
+    rng = np.random.default_rng(12)
+    for trial in range(6):
+        K = int(rng.integers(1, 6))
+        sizes = [int(rng.integers(0, 150 * 4096)) for _ in range(int(rng.integers(1, 9)))]
+        base = [rng.integers(0, 256, size=s, dtype=np.uint8) for s in sizes]
+        reps = [base]
+        for _ in range(K - 1):
+            rep = []
+            for a in base:
+                a = a.copy()
+                if a.size and rng.random() < 0.6:
+                    for _ in range(int(rng.integers(1, 6))):
+                        a[int(rng.integers(0, a.size))] ^= np.uint8(1 << int(rng.integers(0, 8)))
+                rep.append(a)
+            reps.append(rep)
+        log("classify trial", trial, "K", K, "sizes", sizes)
+        oh = np.stack([oracle.fingerprint(rep)[0] for rep in reps])
+        cpb = [oracle.chunk_count(s) for s in sizes]
+        obm, olab = oracle.classify(oh, cpb)
+        total = sum(cpb)
+        gh = zeros_u64(K * total)
+        for k, rep in enumerate(reps):
+            descs = [pcs.flat(dev(a), a.size) for a in rep]
+            ch = zeros_u64(total)
+            ctx.fingerprint(descs, ch)
+            gh[k * total:(k + 1) * total] = ch[:total]
+        nw = oracle.bitmap_words(cpb)
+        bm = zeros_u64(nw)
+        lab = torch.zeros(max(1, len(sizes)), dtype=torch.uint8, device="cuda")
+        ctx.classify(gh, K, cpb, bm, lab)
+        assert np.array_equal(u64(gh).reshape(K, total) if total else oh, oh)
+        assert np.array_equal(u64(bm)[:nw], obm)
+        assert np.array_equal(host(lab)[:len(sizes)], olab)
+
+
+def test_checkpoint_restore_flat(ctx, pcs):
+    rng = np.random.default_rng(13)
+    sizes = [0, 16, 100, 4096, 4097, 70 * 4096 + 9, 3]
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    st = oracle.Store()
+    oh = st.checkpoint(bufs)
+    d = [dev(b) for b in bufs]
+    for hashed in (False, True):
+        log("checkpoint/restore flat, hash =", hashed)
+        kw = {}
+        if hashed:
+            ch, rt, sr = zeros_u64(sum(oracle.chunk_count(n) for n in sizes)), zeros_u64(len(sizes)), zeros_u64(1)
+            kw = dict(chunk_hashes=ch, roots=rt, session_root=sr)
+        snap = ctx.checkpoint([pcs.flat(t, n) for t, n in zip(d, sizes)], hash=hashed, **kw)
+        inf = ctx.info(snap)
+        assert inf["state_bytes"] == sum(sizes) == st.state_bytes(oh)
+        assert inf["stored_bytes"] == st.payload(oh).size
+        pay = torch.empty(inf["stored_bytes"], dtype=torch.uint8, device="cuda")
+        ctx.payload(snap, pay)
+        assert np.array_equal(host(pay), st.payload(oh))
+        if hashed:
+            h, r, s = oracle.fingerprint(bufs)
+            assert np.array_equal(u64(ch)[:h.size], h) and np.array_equal(u64(rt)[:len(sizes)], r)
+            assert int(u64(sr)[0]) == s
+            sh = zeros_u64(h.size)
+            ctx.stored_hashes(snap, sh)
+            assert np.array_equal(u64(sh)[:h.size], h)
+        outs = [torch.full((max(n, 1),), 0xEE, dtype=torch.uint8, device="cuda") for n in sizes]
+        ctx.restore(snap, [pcs.flat(o, n) for o, n in zip(outs, sizes)])
+        for o, b in zip(outs, bufs):
+            got = host(o)
+            assert np.array_equal(got[:b.size], b)
+            assert np.all(got[b.size:] == 0xEE)  # nothing written past the buffer
+        ctx.delete(snap)
+
+
+def test_durability_and_fork_independence(ctx, pcs):
+    rng = np.random.default_rng(14)
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in (9000, 123457)]
+    d = [dev(b) for b in bufs]
+    log("durability + fork")
+    snap = ctx.checkpoint([pcs.flat(t) for t in d], hash=True)
+    for t in d:                      # mutate the sources, stream-ordered after the checkpoint
+        t.random_(0, 256)
+    f = ctx.fork(snap)
+    a = [torch.empty_like(t) for t in d]
+    b = [torch.empty_like(t) for t in d]
+    ctx.restore(snap, [pcs.flat(t) for t in a])
+    ctx.restore(f, [pcs.flat(t) for t in b])
+    for t in a:                      # mutate one restore; the other and the snapshot are unaffected
+        t.zero_()
+    ctx.delete(snap)
+    c = [torch.empty_like(t) for t in d]
+    ctx.restore(f, [pcs.flat(t) for t in c])
+    for x, y, z in zip(b, c, bufs):
+        assert np.array_equal(host(x), z) and np.array_equal(host(y), z)
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.restore(snap, [pcs.flat(t) for t in c])
+    assert e.value.code == pcs.E_HANDLE
+    ctx.delete(f)
+    assert ctx.arena_stats()["live_handles"] == 0
+
+
+@pytest.mark.parametrize("case", RING_CASES)
+def test_ring_checkpoint_restore_new_head(ctx, pcs, case):
+    outer, cap, row, win, head, pad = case
+    g = W.Ring(outer, cap, row, win, head, cap * row + pad)
+    log("ring checkpoint/restore", case)
+    rng = np.random.default_rng(cap * 7 + row)
+    data = rng.integers(0, 256, size=g.ring_bytes, dtype=np.uint8)
+    logical = oracle.ring_window(data, g.outer, g.outer_stride, g.capacity, g.row_bytes, g.head, g.window)
+    d = dev(data)
+    snap = ctx.checkpoint([pcs.ring(d, outer, cap, row, head, win, g.outer_stride)], hash=True)
+    pay = torch.empty(ctx.info(snap)["stored_bytes"], dtype=torch.uint8, device="cuda")
+    ctx.payload(snap, pay)
+    assert np.array_equal(host(pay), oracle.pack([logical]))
+    for new_head in sorted({0, cap - 1, (head + 1) % cap, int(rng.integers(0, cap))}):
+        dst_np = np.full(g.ring_bytes, 0x5A, dtype=np.uint8)
+        dst = dev(dst_np)
+        ctx.restore(snap, [pcs.ring(dst, outer, cap, row, new_head, win, g.outer_stride)])
+        want = dst_np.copy()
+        oracle.ring_place(logical, want, g.outer, g.outer_stride, g.capacity, g.row_bytes, new_head, g.window)
+        assert np.array_equal(host(dst), want), new_head   # window placed, everything else untouched
+    # A different capacity and stride is a compatible destination too.
+    g2 = W.Ring(outer, cap + 3, row, win, 2, (cap + 3) * row + 16)
+    dst2 = dev(np.zeros(g2.ring_bytes, dtype=np.uint8))
+    ctx.restore(snap, [pcs.ring(dst2, outer, cap + 3, row, 2, win, g2.outer_stride)])
+    back = oracle.ring_window(host(dst2), g2.outer, g2.outer_stride, g2.capacity, g2.row_bytes, 2, g2.window)
+    assert np.array_equal(back, logical)
+    ctx.delete(snap)
+
+
+def test_incremental_chain_small(ctx, pcs):
+    bank = W.config2(1, capacity=96, latent_shape=(4, 6, 10), pose_dim=7, step_entries=4)
+    lat, pos = dev(bank.latents), dev(bank.poses)
+    st = oracle.Store()
+    gh, oh = [], []
+    parent_g, parent_o = 0, 0
+    for j in range(0, 25):
+        e = 4 * j
+        plan = [pcs.flat(lat, e * bank.latent_entry_bytes), pcs.flat(pos, e * bank.pose_entry_bytes)]
+        log("incremental step", j, "entries", e)
+        if parent_g == 0:
+            s = ctx.checkpoint(plan, hash=True)
+            o = st.checkpoint(bank.prefix(e))
+        else:
+            s = ctx.checkpoint(plan, parent=parent_g)
+            o = st.checkpoint(bank.prefix(e), parent_o)
+        inf = ctx.info(s)
+        pay = torch.empty(max(1, inf["stored_bytes"]), dtype=torch.uint8, device="cuda")
+        ctx.payload(s, pay)
+        assert inf["stored_bytes"] == st.payload(o).size
+        assert np.array_equal(host(pay)[:inf["stored_bytes"]], st.payload(o))
+        gh.append(s)
+        oh.append(o)
+        parent_g, parent_o = s, o
+    order = np.random.default_rng(15).permutation(len(gh))
+    for j in order:
+        e = 4 * int(j)
+        want = bank.prefix(e)
+        outs = [torch.empty(max(1, w.size), dtype=torch.uint8, device="cuda") for w in want]
+        ctx.restore(gh[j], [pcs.flat(o, w.size) for o, w in zip(outs, want)])
+        for o, w in zip(outs, want):
+            assert np.array_equal(host(o)[:w.size], w), j
+    # Deleting every handle but the last keeps the chain restorable.
+    for s in gh[:-1]:
+        ctx.delete(s)
+    want = bank.prefix(4 * (len(gh) - 1))
+    outs = [torch.empty(w.size, dtype=torch.uint8, device="cuda") for w in want]
+    ctx.restore(gh[-1], [pcs.flat(o, w.size) for o, w in zip(outs, want)])
+    assert all(np.array_equal(host(o), w) for o, w in zip(outs, want))
+
+
+def test_incremental_changes_and_shrink(ctx, pcs):
+    rng = np.random.default_rng(16)
+    base = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in (20 * 4096 + 7, 3 * 4096, 100, 2 * 4096 + 9, 70 * 4096)]
+    new = [b.copy() for b in base]
+    new[0][5 * 4096 + 3] ^= 1
+    new[1] = np.concatenate([new[1], rng.integers(0, 256, size=5000, dtype=np.uint8)])
+    new[2] = new[2][:60]
+    new[4][[0, 64 * 4096 + 1, 69 * 4096 + 17]] ^= 0xFF
+    log("incremental with changes, growth and shrink")
+    st = oracle.Store()
+    po = st.checkpoint(base)
+    co = st.checkpoint(new, po)
+    p = ctx.checkpoint([pcs.flat(dev(b)) for b in base], hash=True)
+    c = ctx.checkpoint([pcs.flat(dev(b)) for b in new], parent=p)
+    inf = ctx.info(c)
+    assert inf["incremental"] == 1 and inf["dirty_chunks"] * 4096 == st.payload(co).size
+    pay = torch.empty(max(1, inf["stored_bytes"]), dtype=torch.uint8, device="cuda")
+    ctx.payload(c, pay)
+    assert np.array_equal(host(pay)[:inf["stored_bytes"]], st.payload(co))
+    outs = [torch.empty(b.size, dtype=torch.uint8, device="cuda") for b in new]
+    ctx.restore(c, [pcs.flat(o) for o in outs])
+    assert all(np.array_equal(host(o), b) for o, b in zip(outs, new))
+
+
+def test_batch_checkpoint_restore(ctx, pcs):
+    plan = W.config5_plan(4, sessions=6, layers=1, window=24, capacity=40, heads=2, head_dim=8,
+                          obs_shape=(5, 7, 3), restore_fraction=0.5)
+    g = plan.ring
+    rng = np.random.default_rng(17)
+    rings = [rng.integers(0, 256, size=g.ring_bytes, dtype=np.uint8) for _ in range(plan.sessions)]
+    obs = [rng.integers(0, 256, size=plan.obs_bytes, dtype=np.uint8) for _ in range(plan.sessions)]
+    rs = [rng.integers(0, 256, size=16, dtype=np.uint8) for _ in range(plan.sessions)]
+    dr, do, dg = [dev(x) for x in rings], [dev(x) for x in obs], [dev(x) for x in rs]
+    plans = [[pcs.ring(dr[s], g.outer, g.capacity, g.row_bytes, plan.heads[s], g.window), pcs.flat(do[s]),
+              pcs.flat(dg[s])] for s in range(plan.sessions)]
+    logical = [[oracle.ring_window(rings[s], g.outer, g.outer_stride, g.capacity, g.row_bytes, plan.heads[s],
+                                   g.window), obs[s], rs[s]] for s in range(plan.sessions)]
+    log("batch checkpoint", plan.sessions, "sessions")
+    total = sum(oracle.chunk_count(b.size) for L in logical for b in L)
+    ch, rt, sr = zeros_u64(total), zeros_u64(3 * plan.sessions), zeros_u64(plan.sessions)
+    snaps = ctx.checkpoint_batch(plans, hash=True, chunk_hashes=ch, roots=rt, session_roots=sr)
+    oh = np.concatenate([oracle.fingerprint(L)[0] for L in logical])
+    orr = np.concatenate([oracle.fingerprint(L)[1] for L in logical])
+    osr = np.array([oracle.fingerprint(L)[2] for L in logical], dtype=np.uint64)
+    assert np.array_equal(u64(ch)[:total], oh)
+    assert np.array_equal(u64(rt)[:3 * plan.sessions], orr)
+    assert np.array_equal(u64(sr)[:plan.sessions], osr)
+    # Restore a permuted subset at new heads, in one launch.
+    order, heads = plan.restore_order, plan.restore_heads
+    dst_r = [dev(np.zeros(g.ring_bytes, dtype=np.uint8)) for _ in order]
+    dst_o = [torch.empty(plan.obs_bytes, dtype=torch.uint8, device="cuda") for _ in order]
+    dst_g = [torch.empty(16, dtype=torch.uint8, device="cuda") for _ in order]
+    dsts = [[pcs.ring(dst_r[k], g.outer, g.capacity, g.row_bytes, heads[k], g.window), pcs.flat(dst_o[k]),
+             pcs.flat(dst_g[k])] for k in range(len(order))]
+    ctx.restore_batch([snaps[s] for s in order], dsts)
+    for k, s in enumerate(order):
+        win = oracle.ring_window(host(dst_r[k]), g.outer, g.outer_stride, g.capacity, g.row_bytes, heads[k], g.window)
+        assert np.array_equal(win, logical[s][0])
+        assert np.array_equal(host(dst_o[k]), obs[s]) and np.array_equal(host(dst_g[k]), rs[s])
+
+
+def test_errors_enqueue_nothing(ctx, pcs):
+    t = torch.zeros(4096 * 3, dtype=torch.uint8, device="cuda")
+    log("error paths")
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.fingerprint([pcs.PcsBuf(ptr=t.data_ptr() + 3, nbytes=10, kind=pcs.FLAT)])
+    assert e.value.code == pcs.E_INVAL
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.fingerprint([pcs.ring(t, 1, 8, 16, 8, 4)])          # head >= capacity
+    assert e.value.code == pcs.E_INVAL
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.fingerprint([pcs.PcsBuf(ptr=t.data_ptr(), nbytes=10, kind=7)])
+    assert e.value.code == pcs.E_INVAL
+    s = ctx.checkpoint([pcs.flat(t, 5000)])
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.restore(s, [pcs.flat(t, 4999)])
+    assert e.value.code == pcs.E_SHAPE
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.restore(s, [pcs.flat(t, 5000), pcs.flat(t, 1)])
+    assert e.value.code == pcs.E_SHAPE
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.checkpoint([pcs.flat(t, 5000)], parent=s)         # parent without fingerprints
+    assert e.value.code == pcs.E_INVAL
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.fork(12345)
+    assert e.value.code == pcs.E_HANDLE
+    big = torch.zeros(300 << 20, dtype=torch.uint8, device="cuda")
+    before = ctx.arena_stats()
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.checkpoint([pcs.flat(big)])                       # arena is 256 MiB
+    assert e.value.code == pcs.E_NOMEM
+    assert ctx.arena_stats() == before
+    ctx.delete(s)
