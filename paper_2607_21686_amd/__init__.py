@@ -47,7 +47,9 @@ def flat(t: torch.Tensor, nbytes: int | None = None) -> PcsBuf:
     n = size if nbytes is None else nbytes
     if n > size:
         raise ValueError("nbytes exceeds the tensor")
-    return PcsBuf(ptr=_dev_ptr(t), nbytes=n, kind=FLAT)
+    b = PcsBuf(ptr=_dev_ptr(t), nbytes=n, kind=FLAT)
+    b._tensor = t  # the descriptor keeps its memory alive until the call has been enqueued
+    return b
 
 
 def ring(t: torch.Tensor, outer: int, capacity: int, row_bytes: int, head: int, window: int,
@@ -57,8 +59,10 @@ def ring(t: torch.Tensor, outer: int, capacity: int, row_bytes: int, head: int, 
     need = (outer - 1) * stride + capacity * row_bytes if outer else 0
     if need > t.numel() * t.element_size():
         raise ValueError("ring geometry exceeds the tensor")
-    return PcsBuf(ptr=_dev_ptr(t), nbytes=0, kind=RING, row_bytes=row_bytes, capacity=capacity, head=head,
-                  window=window, outer=outer, outer_stride=stride)
+    b = PcsBuf(ptr=_dev_ptr(t), nbytes=0, kind=RING, row_bytes=row_bytes, capacity=capacity, head=head,
+               window=window, outer=outer, outer_stride=stride)
+    b._tensor = t
+    return b
 
 
 def _array(bufs):
