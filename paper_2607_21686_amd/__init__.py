@@ -23,7 +23,7 @@ import torch
 from ._lib import (CHUNK_BYTES, CKPT_HASH, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_SHAPE, EXPORTS, FLAT,
                    MUST_SNAPSHOT, RECOMPUTABLE, RING, PcsBuf, PcsError, PcsSnapInfo, lib)
 
-__all__ = ["Context", "PcsError", "flat", "ring", "chunk_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
+__all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
            "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "EXPORTS"]
 
 _L = lib()  # fails loudly if the HIP library is missing
@@ -65,11 +65,29 @@ def ring(t: torch.Tensor, outer: int, capacity: int, row_bytes: int, head: int, 
     return b
 
 
+class BufArray:
+    """A prebuilt descriptor array (reuse it across calls to skip marshalling)."""
+
+    def __init__(self, bufs):
+        self.bufs = list(bufs)  # keeps the descriptors' tensors alive
+        self.arr = (PcsBuf * max(1, len(self.bufs)))()
+        for i, b in enumerate(self.bufs):
+            self.arr[i] = b
+
+    def __len__(self):
+        return len(self.bufs)
+
+
 def _array(bufs):
-    arr = (PcsBuf * max(1, len(bufs)))()
-    for i, b in enumerate(bufs):
-        arr[i] = b
-    return arr
+    if isinstance(bufs, BufArray):
+        return bufs.arr
+    return BufArray(bufs).arr
+
+
+def u64_array(values):
+    """A prebuilt ctypes uint64 array (e.g. chunks per buffer for classify)."""
+    values = list(values)
+    return (ctypes.c_uint64 * max(1, len(values)))(*[int(v) for v in values])
 
 
 def chunk_counts(bufs):
@@ -124,9 +142,9 @@ class Context:
                                          _dev_ptr(roots), _dev_ptr(session_root)))
 
     def classify(self, hashes, K: int, chunks_per_buf, bitmap, labels):
-        cpb = (ctypes.c_uint64 * max(1, len(chunks_per_buf)))(*[int(c) for c in chunks_per_buf])
-        self._check(_L.pcs_classify(self._h, _dev_ptr(hashes), K, cpb, len(chunks_per_buf),
-                                      _dev_ptr(bitmap), _dev_ptr(labels)))
+        n = len(chunks_per_buf)
+        cpb = chunks_per_buf if isinstance(chunks_per_buf, ctypes.Array) else u64_array(chunks_per_buf)
+        self._check(_L.pcs_classify(self._h, _dev_ptr(hashes), K, cpb, n, _dev_ptr(bitmap), _dev_ptr(labels)))
 
     # -- contract ----------------------------------------------------------
     def checkpoint(self, plan, parent: int = 0, hash: bool = False, chunk_hashes=None, roots=None,
@@ -137,23 +155,34 @@ class Context:
                                         ctypes.byref(out)))
         return int(out.value)
 
-    def checkpoint_batch(self, plans, hash: bool = False, chunk_hashes=None, roots=None, session_roots=None):
-        flat_list = [b for p in plans for b in p]
-        nb = (ctypes.c_uint32 * max(1, len(plans)))(*[len(p) for p in plans])
-        out = (ctypes.c_uint64 * max(1, len(plans)))()
-        self._check(_L.pcs_checkpoint_batch(self._h, _array(flat_list), nb, len(plans),
+    def checkpoint_batch(self, plans, hash: bool = False, chunk_hashes=None, roots=None, session_roots=None,
+                         nbufs=None):
+        """plans: list of per-session descriptor lists, or a BufArray of all
+        sessions' descriptors together with `nbufs` (buffers per session)."""
+        if isinstance(plans, BufArray):
+            arr, counts = plans.arr, list(nbufs)
+        else:
+            arr, counts = _array([b for p in plans for b in p]), [len(p) for p in plans]
+        nb = (ctypes.c_uint32 * max(1, len(counts)))(*counts)
+        out = (ctypes.c_uint64 * max(1, len(counts)))()
+        self._check(_L.pcs_checkpoint_batch(self._h, arr, nb, len(counts),
                                               CKPT_HASH if hash else 0, _dev_ptr(chunk_hashes),
                                               _dev_ptr(roots), _dev_ptr(session_roots), out))
-        return [int(out[i]) for i in range(len(plans))]
+        return [int(out[i]) for i in range(len(counts))]
 
     def restore(self, snap: int, dsts):
         self._check(_L.pcs_restore(self._h, snap, _array(dsts), len(dsts)))
 
-    def restore_batch(self, snaps, dsts_per_snap):
-        flat_list = [b for d in dsts_per_snap for b in d]
+    def restore_batch(self, snaps, dsts_per_snap, nbufs=None):
+        """dsts_per_snap: list of per-snapshot descriptor lists, or a BufArray
+        with `nbufs` (destinations per snapshot)."""
+        if isinstance(dsts_per_snap, BufArray):
+            arr, counts = dsts_per_snap.arr, list(nbufs)
+        else:
+            arr, counts = _array([b for d in dsts_per_snap for b in d]), [len(d) for d in dsts_per_snap]
         s = (ctypes.c_uint64 * max(1, len(snaps)))(*snaps)
-        nb = (ctypes.c_uint32 * max(1, len(snaps)))(*[len(d) for d in dsts_per_snap])
-        self._check(_L.pcs_restore_batch(self._h, s, len(snaps), _array(flat_list), nb))
+        nb = (ctypes.c_uint32 * max(1, len(counts)))(*counts)
+        self._check(_L.pcs_restore_batch(self._h, s, len(snaps), arr, nb))
 
     def fork(self, snap: int) -> int:
         out = ctypes.c_uint64()
