@@ -163,6 +163,18 @@ __device__ __forceinline__ void store16(uint64_t a, uint4 v)
     *(g_v4u32 *)a = w;
 }
 
+// Streaming (nontemporal) forms for bulk state that is touched once per call.
+__device__ __forceinline__ uint4 load16_nt(uint64_t a)
+{
+    const v4u32 v = __builtin_nontemporal_load((const g_v4u32 *)a);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void store16_nt(uint64_t a, uint4 v)
+{
+    const v4u32 w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, (g_v4u32 *)a);
+}
+
 // Bytes [0, n) of a granule from `a` (n < 16), zero above: in-bounds reads only.
 __device__ uint4 load_partial(uint64_t a, uint32_t n)
 {
@@ -196,81 +208,153 @@ __global__ void k_group_map(const JobBuf *__restrict__ bufs, uint32_t nbuf, uint
 
 // ---------------------------------------------------------------- fingerprint
 
-// One workgroup = one 64-chunk group; two lanes per chunk.  Lane p of a pair
-// owns XXH64 accumulators 2p and 2p+1, which read exactly the 16 bytes at
-// offset 16p of every 32-byte stripe, so each lane's data arrives in one
-// 16-byte load per stripe and no lane exchange is needed until the final
-// convergence.  COPY also writes every loaded granule to the chunk's
-// snapshot slot (zero-padding a partial last chunk): one read of the state
-// both packs and fingerprints it.  DIFF marks chunks that are new or changed
-// against the parent's fingerprints and counts them per group.
-constexpr int kHashBatch = 8;
-
-template <bool COPY, bool DIFF>
-__global__ __launch_bounds__(128) void k_hash(const JobBuf *__restrict__ bufs,
-                                              const Run *__restrict__ runs,
-                                              const uint32_t *__restrict__ map,
-                                              uint64_t *__restrict__ nodes,
-                                              uint32_t *__restrict__ dirty_count,
-                                              uint64_t *__restrict__ dirty_mask)
+// Physical address of logical offset L of a buffer (binary search of its
+// runs): the path for the few chunks that straddle a ring wrap.
+__device__ uint64_t phys_addr(const Run *runs, uint32_t begin, uint32_t count, uint64_t L)
 {
+    uint32_t lo = begin, hi = begin + count;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (runs[mid].lstart <= L) lo = mid; else hi = mid;
+    }
+    return runs[lo].addr + (L - runs[lo].lstart);
+}
+
+// Per-chunk setup shared by the tile kernels: lane c < 64 of the first
+// wavefront finds chunk c's length and, when the whole chunk lies in one
+// physical run, its physical start address (0 otherwise).
+__device__ __forceinline__ void chunk_table(const JobBuf &jb, const Run *runs, uint64_t c0, uint32_t nv,
+                                            uint64_t *caddr, uint32_t *clen)
+{
+    const uint32_t t = threadIdx.x;
+    if (t < kGroupChunks) {
+        uint64_t a = 0;
+        uint32_t len = 0;
+        if (t < nv) {
+            const uint64_t cb = (c0 + t) * kChunk;
+            len = (uint32_t)umin(kChunk, jb.nbytes - cb);
+            const Cursor cur = cursor_seek(runs, jb.run_begin, jb.run_count, jb.nbytes, cb);
+            if (cb + len <= cur.run_end) a = cb + cur.delta;
+        }
+        caddr[t] = a;
+        clen[t] = len;
+    }
+}
+
+constexpr uint32_t kSlice = 1024;                 // bytes of each chunk moved per step
+constexpr uint32_t kSteps = kChunk / kSlice;      // steps per chunk
+constexpr uint32_t kRow = kSlice + 32;            // padded LDS row: lane pairs of 8 chunks hit distinct banks
+
+// Selects word i (0..3) of a 32-byte tail held in registers.
+__device__ __forceinline__ uint64_t sel4(uint64_t a, uint64_t b, uint64_t c, uint64_t d, uint32_t i)
+{
+    return i == 0 ? a : i == 1 ? b : i == 2 ? c : d;
+}
+
+// Fingerprint tile kernel.  One workgroup = one 64-chunk group of one
+// buffer.  Step k moves the k-th 1 KiB slice of every chunk of the group:
+// all T lanes load it with coalesced 16-byte loads (64 lanes per chunk
+// slice), COPY stores it to the chunk's snapshot slot (zero-padding a partial
+// last chunk), and every lane writes it to an LDS tile; then lane pairs of
+// the first two wavefronts hash the tile while the next slice's loads are in
+// flight.  Lane p of a pair owns XXH64 accumulators 2p and 2p+1, which read
+// exactly bytes [16p, 16p+16) of each 32-byte stripe.  DIFF marks chunks that
+// are new or changed against the parent's fingerprints and counts them.
+template <bool COPY, bool DIFF, int T>
+__global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs,
+                                            const uint32_t *__restrict__ map, uint64_t *__restrict__ nodes,
+                                            uint32_t *__restrict__ dirty_count,
+                                            uint64_t *__restrict__ dirty_mask)
+{
+    constexpr int U = kGroupChunks * kSlice / 16 / T;  // granules per lane per step
+    __shared__ __attribute__((aligned(16))) uint8_t tile[kGroupChunks * kRow];
+    __shared__ uint64_t caddr[kGroupChunks];
+    __shared__ uint32_t clen[kGroupChunks];
     __shared__ uint64_t leaves[kGroupChunks];
     __shared__ uint32_t dflag[kGroupChunks];
 
     const uint64_t G = blockIdx.x;
     const JobBuf &jb = bufs[map[G]];
-    const uint32_t t = threadIdx.x, ci = t >> 1, p = t & 1;
-    const uint64_t gl = G - jb.group_begin;
-    const uint64_t nchunks = jb.nchunks, nbytes = jb.nbytes;
-    const uint32_t nv = (uint32_t)umin(kGroupChunks, nchunks - gl * kGroupChunks);
-    const uint64_t i = gl * kGroupChunks + ci;
+    const uint32_t t = threadIdx.x;
+    const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
+    const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
+    const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
+    chunk_table(jb, runs, c0, nv, caddr, clen);
+    __syncthreads();
 
-    if (ci < nv) {
-        const uint64_t cbase = i * kChunk;
-        const uint32_t len = (uint32_t)umin(kChunk, nbytes - cbase);
-        const uint32_t nst = len >> 5;
-        const uint64_t L0 = cbase + 16 * p;
-        Cursor cur = cursor_seek(runs, jb.run_begin, jb.run_count, nbytes, L0);
-        const uint64_t dst = COPY ? jb.payload + cbase : 0;
+    // This lane's granules: chunk (k*T + t) / 64, slot t % 64 of each slice.
+    const uint32_t slot = (t & 63) * 16;
+    uint64_t ga[U];
+    uint32_t gl[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+        const uint32_t c = (k * T + t) >> 6;
+        ga[k] = c < nv ? caddr[c] : 0;
+        gl[k] = c < nv ? clen[c] : 0;
+    }
+    auto load_granule = [&](int k, uint32_t x) -> uint4 {
+        const uint32_t c = (k * T + t) >> 6;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (x < gl[k]) {
+            const uint64_t a = ga[k] ? ga[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
+            v = x + 16 <= gl[k] ? load16_nt(a) : load_partial(a, gl[k] - x);
+        }
+        return v;
+    };
 
-        uint64_t va = p ? 0 : P1 + P2;   // accumulator 2p   (seed 0)
-        uint64_t vb = p ? 0 - P1 : P2;   // accumulator 2p+1
-        if (len == kChunk && L0 + kChunk - 16 <= cur.run_end) {
-            // Whole chunk in one physical run: batches of kHashBatch stripes,
-            // the next batch's loads in flight while this one is hashed.
-            const uint64_t a0 = L0 + cur.delta;
-            const uint64_t d0 = dst + 16 * p;
-            uint4 d[kHashBatch], n[kHashBatch];
+    uint4 r[U];
 #pragma unroll
-            for (int u = 0; u < kHashBatch; ++u) d[u] = load16(a0 + 32 * u);
-            for (uint32_t s = 0; s < kChunk / 32; s += kHashBatch) {
-                if (s + kHashBatch < kChunk / 32) {
+    for (int k = 0; k < U; ++k) r[k] = load_granule(k, slot);
+
+    const uint32_t ci = t >> 1, p = t & 1;
+    const bool hasher = t < 2 * kGroupChunks && ci < nv;
+    const uint32_t len = hasher ? clen[ci] : 0;
+    const uint32_t nst = len >> 5;
+    uint64_t va = p ? 0 : P1 + P2;   // accumulator 2p   (seed 0)
+    uint64_t vb = p ? 0 - P1 : P2;   // accumulator 2p+1
+    uint64_t tw0 = 0, tw1 = 0, tw2 = 0, tw3 = 0;  // the chunk's tail (< 32 bytes), zero padded
+
+    for (uint32_t step = 0; step < kSteps; ++step) {
 #pragma unroll
-                    for (int u = 0; u < kHashBatch; ++u) n[u] = load16(a0 + 32 * (uint64_t)(s + kHashBatch + u));
-                }
-#pragma unroll
-                for (int u = 0; u < kHashBatch; ++u) {
-                    if (COPY) store16(d0 + 32 * (uint64_t)(s + u), d[u]);
-                    va = xround(va, ((uint64_t)d[u].y << 32) | d[u].x);
-                    vb = xround(vb, ((uint64_t)d[u].w << 32) | d[u].z);
-                }
-#pragma unroll
-                for (int u = 0; u < kHashBatch; ++u) d[u] = n[u];
+        for (int k = 0; k < U; ++k) {
+            const uint32_t c = (k * T + t) >> 6;
+            if (c < nv) {
+                if (COPY) store16_nt(jb.payload + (c0 + c) * kChunk + step * kSlice + slot, r[k]);
+                *reinterpret_cast<uint4 *>(tile + c * kRow + slot) = r[k];
             }
-        } else {
-            for (uint32_t s = 0; s < nst; ++s) {
-                const uint64_t L = L0 + 32 * (uint64_t)s;
-                const uint4 d = load16(cursor_addr(cur, L));
-                if (COPY) store16(dst + 32 * (uint64_t)s + 16 * p, d);
+        }
+        __syncthreads();
+        if (step + 1 < kSteps) {
+#pragma unroll
+            for (int k = 0; k < U; ++k) r[k] = load_granule(k, (step + 1) * kSlice + slot);
+        }
+        if (hasher) {
+            const uint8_t *row = tile + ci * kRow;
+            const uint32_t s0 = step * (kSlice / 32);
+            const uint32_t ns = nst > s0 ? umin(kSlice / 32, nst - s0) : 0;
+#pragma unroll 8
+            for (uint32_t s = 0; s < ns; ++s) {
+                const uint4 d = *reinterpret_cast<const uint4 *>(row + 32 * s + 16 * p);
                 va = xround(va, ((uint64_t)d.y << 32) | d.x);
                 vb = xround(vb, ((uint64_t)d.w << 32) | d.z);
             }
+            const uint32_t tp = nst * 32;  // tail start, 32-aligned, inside this slice if here
+            if (p == 0 && tp < len && tp >= step * kSlice && tp < (step + 1) * kSlice) {
+                const uint4 x = *reinterpret_cast<const uint4 *>(row + tp - step * kSlice);
+                const uint4 y = *reinterpret_cast<const uint4 *>(row + tp - step * kSlice + 16);
+                tw0 = ((uint64_t)x.y << 32) | x.x;
+                tw1 = ((uint64_t)x.w << 32) | x.z;
+                tw2 = ((uint64_t)y.y << 32) | y.x;
+                tw3 = ((uint64_t)y.w << 32) | y.z;
+            }
         }
+        __syncthreads();
+    }
+
+    if (t < 2 * kGroupChunks) {
         const uint64_t oa = shfl64(va, (int)(t ^ 1) & 63);
         const uint64_t ob = shfl64(vb, (int)(t ^ 1) & 63);
-
-        uint64_t h = 0;
-        if (p == 0) {
+        if (hasher && p == 0) {
             uint64_t acc;
             if (len >= 32) {
                 acc = rotl(va, 1) + rotl(vb, 7) + rotl(oa, 12) + rotl(ob, 18);
@@ -282,49 +366,31 @@ __global__ __launch_bounds__(128) void k_hash(const JobBuf *__restrict__ bufs,
                 acc = P5;
             }
             acc += len;
-            uint32_t pos = nst * 32;
-            if (pos < len) {
-                // The tail lies in one run: runs are 16-byte granular and
-                // only a flat buffer (a single run) has a tail that is not a
-                // whole granule.  Naturally aligned, in-bounds loads only.
-                uint64_t tp = cursor_addr(cur, cbase + pos);
-                for (; len - pos >= 8; pos += 8, tp += 8) {
-                    acc ^= xround(0, *(const g_u64 *)tp);
-                    acc = rotl(acc, 27) * P1 + P4;
-                }
-                if (len - pos >= 4) {
-                    acc ^= (uint64_t)(*(const g_u32 *)tp) * P1;
-                    acc = rotl(acc, 23) * P2 + P3;
-                    pos += 4;
-                    tp += 4;
-                }
-                for (; pos < len; ++pos, ++tp) {
-                    acc ^= (uint64_t)(*(const g_u8 *)tp) * P5;
-                    acc = rotl(acc, 11) * P1;
-                }
+            // Tail: 8-byte lanes, one 4-byte lane, single bytes (offsets
+            // relative to the tail start).
+            uint32_t o = 0;
+            const uint32_t rem = len - nst * 32;
+            for (; rem - o >= 8; o += 8) {
+                acc ^= xround(0, sel4(tw0, tw1, tw2, tw3, o >> 3));
+                acc = rotl(acc, 27) * P1 + P4;
             }
-            h = avalanche(acc);
-        }
-
-        if (COPY && len < kChunk) {
-            // Tail and zero padding of the last chunk's slot, granule by
-            // granule (after the hash tail, so the cursor only moves forward).
-            for (uint32_t q = 2 * nst + p; q < kChunk / 16; q += 2) {
-                const uint32_t lo = 16 * q;
-                uint4 v = make_uint4(0, 0, 0, 0);
-                if (lo + 16 <= len) v = load16(cursor_addr(cur, cbase + lo));
-                else if (lo < len) v = load_partial(cursor_addr(cur, cbase + lo), len - lo);
-                store16(dst + lo, v);
+            if (rem - o >= 4) {
+                acc ^= (uint64_t)(uint32_t)sel4(tw0, tw1, tw2, tw3, o >> 3) * P1;
+                acc = rotl(acc, 23) * P2 + P3;
+                o += 4;
             }
-        }
-
-        if (p == 0) {
+            for (; o < rem; ++o) {
+                const uint64_t byte = (sel4(tw0, tw1, tw2, tw3, o >> 3) >> (8 * (o & 7))) & 0xFF;
+                acc ^= byte * P5;
+                acc = rotl(acc, 11) * P1;
+            }
+            const uint64_t h = avalanche(acc);
+            const uint64_t i = c0 + ci;
             if (jb.hash_dst[0]) ((g_u64 *)jb.hash_dst[0])[i] = h;
             if (jb.hash_dst[1]) ((g_u64 *)jb.hash_dst[1])[i] = h;
             leaves[ci] = h;
             if (DIFF) {
-                const bool d = i >= jb.parent_chunks ||
-                               ((const g_u64 *)jb.parent_hash)[i] != h;
+                const bool d = i >= jb.parent_chunks || ((const g_u64 *)jb.parent_hash)[i] != h;
                 dflag[ci] = d ? 1u : 0u;
             }
         }
@@ -332,8 +398,8 @@ __global__ __launch_bounds__(128) void k_hash(const JobBuf *__restrict__ bufs,
     __syncthreads();
     if (t < 64) {
         const uint64_t v = t < nv ? leaves[t] : 0;
-        const uint64_t r = wave_merkle(v, nv);
-        if (t == 0) nodes[G] = r;
+        const uint64_t root = wave_merkle(v, nv);
+        if (t == 0) nodes[G] = root;
         if (DIFF) {
             const uint64_t mask = __ballot(t < nv && dflag[t] != 0);
             if (t == 0) {
@@ -408,73 +474,63 @@ __global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ l
 
 // ---------------------------------------------------------------- copies
 
-constexpr int kCopyUnroll = 4;
-
-// Pack: one workgroup copies its group's chunks, 256 lanes x 16 bytes = one
-// whole 4096-byte chunk per step (fully coalesced on both sides), from the
-// buffer's runs into the snapshot slots; a partial last chunk is
-// zero-padded to the end of its slot.
-__global__ __launch_bounds__(256) void k_pack(const JobBuf *__restrict__ bufs,
-                                              const Run *__restrict__ runs,
-                                              const uint32_t *__restrict__ map)
+// Copy tile kernel: one workgroup moves one 64-chunk group, 1 KiB of every
+// chunk per step, with coalesced 16-byte loads and stores (the shape of the
+// fused kernel without the hash).
+//   PACK:    the buffer's runs -> the chunk slots of the snapshot; a partial
+//            last chunk is zero-padded to the end of its slot.
+//   !PACK:   the chunk slots (contiguous, or per chunk through a manifest of
+//            arena offsets) -> the destination buffer's runs; only logical
+//            bytes are written.
+template <bool PACK, int T>
+__global__ __launch_bounds__(T) void k_copy(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs,
+                                            const uint32_t *__restrict__ map, uint64_t arena_base)
 {
+    constexpr int U = kGroupChunks * kSlice / 16 / T;
+    __shared__ uint64_t caddr[kGroupChunks];  // runs side: chunk start if in one run, else 0
+    __shared__ uint32_t clen[kGroupChunks];
     const uint64_t G = blockIdx.x;
     const JobBuf &jb = bufs[map[G]];
-    const uint64_t gl = G - jb.group_begin;
-    const uint64_t c0 = gl * kGroupChunks, nbytes = jb.nbytes;
+    const uint32_t t = threadIdx.x;
+    const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
     const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
-    const uint32_t x = threadIdx.x * 16;
-    Cursor cur = cursor_seek(runs, jb.run_begin, jb.run_count, nbytes, c0 * kChunk + x);
-    for (uint32_t k = 0; k < nv; k += kCopyUnroll) {
-        uint4 v[kCopyUnroll];
-#pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u) {
-            const uint64_t cb = (c0 + k + u) * kChunk;
-            v[u] = make_uint4(0, 0, 0, 0);
-            if (k + u < nv) {
-                if (cb + x + 16 <= nbytes) v[u] = load16(cursor_addr(cur, cb + x));
-                else if (cb + x < nbytes) v[u] = load_partial(cursor_addr(cur, cb + x), (uint32_t)(nbytes - cb - x));
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u)
-            if (k + u < nv) store16(jb.payload + (c0 + k + u) * kChunk + x, v[u]);
-    }
-}
-
-// Restore: snapshot slots (contiguous, or per-chunk through a manifest of
-// arena offsets) back into the destination buffer's runs.  Only logical
-// bytes are written.
-__global__ __launch_bounds__(256) void k_restore(const JobBuf *__restrict__ bufs,
-                                                 const Run *__restrict__ runs,
-                                                 const uint32_t *__restrict__ map,
-                                                 uint64_t arena_base)
-{
-    const uint64_t G = blockIdx.x;
-    const JobBuf &jb = bufs[map[G]];
-    const uint64_t gl = G - jb.group_begin;
-    const uint64_t c0 = gl * kGroupChunks, nbytes = jb.nbytes;
-    const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
-    const uint32_t x = threadIdx.x * 16;
+    const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
     const g_u64 *man = (const g_u64 *)jb.manifest;
-    Cursor cur = cursor_seek(runs, jb.run_begin, jb.run_count, nbytes, c0 * kChunk + x);
-    for (uint32_t k = 0; k < nv; k += kCopyUnroll) {
-        uint4 v[kCopyUnroll];
+    chunk_table(jb, runs, c0, nv, caddr, clen);
+    __syncthreads();
+
+    const uint32_t slot = (t & 63) * 16;
+    uint64_t ra[U], sa[U];
+    uint32_t gl[U];
 #pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u) {
-            const uint64_t c = c0 + k + u;
-            v[u] = make_uint4(0, 0, 0, 0);
-            if (k + u < nv && c * kChunk + x < nbytes) {
-                const uint64_t src = man ? arena_base + man[c] : jb.payload + c * kChunk;
-                v[u] = load16(src + x);  // slots are whole 4096-byte granules
+    for (int k = 0; k < U; ++k) {
+        const uint32_t c = (k * T + t) >> 6;
+        ra[k] = c < nv ? caddr[c] : 0;
+        gl[k] = c < nv ? clen[c] : 0;
+        sa[k] = c < nv ? (PACK || !man ? jb.payload + (c0 + c) * kChunk : arena_base + man[c0 + c]) : 0;
+    }
+    auto runs_addr = [&](int k, uint32_t x) -> uint64_t {
+        const uint32_t c = (k * T + t) >> 6;
+        return ra[k] ? ra[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
+    };
+    for (uint32_t step = 0; step < kSteps; ++step) {
+        const uint32_t x = step * kSlice + slot;
+        uint4 v[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            v[k] = make_uint4(0, 0, 0, 0);
+            if (x < gl[k]) {
+                if (PACK) v[k] = x + 16 <= gl[k] ? load16_nt(runs_addr(k, x)) : load_partial(runs_addr(k, x), gl[k] - x);
+                else v[k] = load16_nt(sa[k] + x);  // slots are whole 4096-byte granules
             }
         }
 #pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u) {
-            const uint64_t cb = (c0 + k + u) * kChunk;
-            if (k + u < nv) {
-                if (cb + x + 16 <= nbytes) store16(cursor_addr(cur, cb + x), v[u]);
-                else if (cb + x < nbytes) store_partial(cursor_addr(cur, cb + x), v[u], (uint32_t)(nbytes - cb - x));
+        for (int k = 0; k < U; ++k) {
+            if (PACK) {
+                if (sa[k]) store16_nt(sa[k] + x, v[k]);
+            } else if (x < gl[k]) {
+                if (x + 16 <= gl[k]) store16_nt(runs_addr(k, x), v[k]);
+                else store_partial(runs_addr(k, x), v[k], gl[k] - x);
             }
         }
     }
@@ -604,6 +660,11 @@ __global__ void k_labels(const JobBuf *__restrict__ bufs, uint32_t nbuf,
     labels[b] = any ? 1 : 0;
 }
 
+// Workgroup sizes (lanes) of the tile kernels, from measurement on MI355X.
+constexpr int kPackLanes = 1024;
+constexpr int kHashLanes = 512;
+constexpr int kCopyLanes = 1024;
+
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
@@ -622,14 +683,17 @@ hipError_t launch_hash(const JobBuf *bufs, const Run *runs, const uint32_t *map,
                        uint64_t *dirty_mask, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    const dim3 grid((uint32_t)ngroups), block(128);
+    const dim3 grid((uint32_t)ngroups);
     if (copy && diff) return hipErrorInvalidValue;
     if (copy)
-        hipLaunchKernelGGL((k_hash<true, false>), grid, block, 0, s, bufs, runs, map, nodes, dirty_count, dirty_mask);
+        hipLaunchKernelGGL((k_hash<true, false, kPackLanes>), grid, dim3(kPackLanes), 0, s, bufs, runs, map, nodes,
+                           dirty_count, dirty_mask);
     else if (diff)
-        hipLaunchKernelGGL((k_hash<false, true>), grid, block, 0, s, bufs, runs, map, nodes, dirty_count, dirty_mask);
+        hipLaunchKernelGGL((k_hash<false, true, kHashLanes>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
+                           dirty_count, dirty_mask);
     else
-        hipLaunchKernelGGL((k_hash<false, false>), grid, block, 0, s, bufs, runs, map, nodes, dirty_count, dirty_mask);
+        hipLaunchKernelGGL((k_hash<false, false, kHashLanes>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
+                           dirty_count, dirty_mask);
     return hipGetLastError();
 }
 
@@ -646,7 +710,8 @@ hipError_t launch_pack(const JobBuf *bufs, const Run *runs, const uint32_t *map,
                        hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_pack, dim3((uint32_t)ngroups), dim3(256), 0, s, bufs, runs, map);
+    hipLaunchKernelGGL((k_copy<true, kCopyLanes>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs, map,
+                       (uint64_t)0);
     return hipGetLastError();
 }
 
@@ -654,7 +719,8 @@ hipError_t launch_restore(const JobBuf *bufs, const Run *runs, const uint32_t *m
                           uint64_t ngroups, uint64_t arena_base, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_restore, dim3((uint32_t)ngroups), dim3(256), 0, s, bufs, runs, map, arena_base);
+    hipLaunchKernelGGL((k_copy<false, kCopyLanes>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs,
+                       map, arena_base);
     return hipGetLastError();
 }
 
