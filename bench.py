@@ -51,11 +51,68 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (for HBM counter scaling)")
+    ap.add_argument("--summarize", nargs="+", metavar="DB",
+                    help="no GPU: print kernel statistics from rocprofv3 databases (trace or --pmc runs)")
     return ap.parse_args()
+
+
+def summarize(dbs):
+    """Kernel statistics from rocprofv3 (rocpd) databases: durations from a
+    kernel-trace run, per-dispatch counter values from --pmc runs.  Counter
+    values are printed as rocprofv3 reports them (FETCH_SIZE / WRITE_SIZE in
+    KiB per dispatch), together with the largest __amd_rocclr_copyBuffer
+    dispatch, which is the plain 1 GiB calibration copy of --calibrate-copy."""
+    import sqlite3
+
+    def short(name):
+        name = name.replace("pcs::(anonymous namespace)::", "").replace("(anonymous namespace)::", "")
+        return name.split("(")[0][:60] if "pcs::" in name or name.startswith(("void k_", "k_", "void pcs")) \
+            else name.split("(")[0][:60]
+
+    for db in dbs:
+        con = sqlite3.connect(db)
+        cur = con.cursor()
+        print("## %s" % db)
+        has_pmc = cur.execute("select count(*) from counters_collection").fetchone()[0] > 0
+        if has_pmc:
+            print("| kernel | counter | dispatches | mean | min | max |")
+            print("|---|---|---|---|---|---|")
+            q = ("select kernel_name, counter_name, count(*), avg(value), min(value), max(value) "
+                 "from counters_collection group by kernel_name, counter_name order by avg(value) desc")
+            for name, cn, n, avg, mn, mx in cur.execute(q):
+                if "pcs::" in name or "rocclr_copyBuffer" in name:
+                    print("| %s | %s | %d | %.1f | %.1f | %.1f |" % (short(name), cn, n, avg, mn, mx))
+        else:
+            print("| kernel | calls | avg us | min us | max us | total ms |")
+            print("|---|---|---|---|---|---|")
+            q = ("select name, count(*), avg(duration), min(duration), max(duration), sum(duration) "
+                 "from kernels group by name order by sum(duration) desc")
+            for name, n, avg, mn, mx, tot in cur.execute(q):
+                if "pcs::" in name or "rocclr_copyBuffer" in name:
+                    print("| %s | %d | %.1f | %.1f | %.1f | %.3f |" % (short(name), n, avg / 1e3, mn / 1e3,
+                                                                        mx / 1e3, tot / 1e6))
+        print()
+
+
+def traffic_record():
+    """Scaled HBM traffic of the fused pack+fingerprint kernel, measured with
+    rocprofv3 counters, if the kernel source is unchanged since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_hash_copy_batch1024_traffic.json")
+    src = os.path.join(ROOT, "paper_2607_21686_amd", "csrc", "pcs_kernels.hip")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    return rec if rec.get("kernel_source_sha256") == sha else None
 
 
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args.summarize)
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU: this build has no multi-GPU path (sessions shard across GPUs "
               "with no exchange; see the design notes).", file=sys.stderr)
@@ -174,6 +231,9 @@ def main():
     avg_cp = ms_cp / max(1, n_cp)
     achieved_restore = 2 * rest_state / (avg_cp * 1e-3) / 1e9
 
+    rec = traffic_record()
+    traffic = rec["traffic_bytes_per_launch"] if rec and rec.get("sessions") == S else None
+
     out = {
         "metric": "checkpoint+restore GB/s and fingerprint GB/s at 1 MI355X; % of HBM peak",
         "value": round(value, 2),
@@ -192,7 +252,7 @@ def main():
                                "classify vs previous step, fork+restore %d permuted" % (S, R),
                    "sessions": S, "restored": R, "state_bytes_per_session": state_per_session},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "kernel": "k_hash<copy> (fused pack + fingerprint)",
                      "avg_ms": round(avg_ph, 4), "algorithmic_bytes": alg_ph},
         "breakdown": {
