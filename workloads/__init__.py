@@ -277,3 +277,53 @@ def config5_plan(seed: int = 4, sessions: int = 1024, layers: int = 4, window: i
     order = [int(x) for x in rng.permutation(sessions)[: int(sessions * restore_fraction)]]
     rh = [int(x) for x in rng.integers(0, capacity, size=len(order))]
     return Batch(sessions, ring, hs, int(np.prod(obs_shape)), 16, order, rh)
+
+
+# ---------------------------------------------------------------- device-side full-size inputs
+
+def config3_device(seed: int = 2, layers: int = 32, capacity: int = 8192, window: int = 4096, heads: int = 8,
+                   head_dim: int = 128, device="cuda"):
+    """The windowed KV ring [layers][2][capacity][heads][head_dim] bf16 N(0,1) on the GPU.
+
+    Returns (uint8 view of the ring, Ring geometry with a wrapping head, a different head)."""
+    g, h2 = kv_ring_geometry(layers, capacity, window, heads, head_dim, seed)
+    ring = device_bf16_normal(g.ring_bytes // 2, seed, device).view(__import__("torch").uint8)
+    return ring, g, h2
+
+
+def config4_device(plan: SweepPlan, seed: int = 3, device="cuda"):
+    """Replays of the sweep on the GPU: reps[k-1][b] is a uint8 tensor; replays
+    share the base tensor for every buffer they leave untouched."""
+    import torch
+    base = []
+    for b, (n, dt) in enumerate(zip(plan.sizes, plan.dtypes)):
+        if dt in ("float16", "bfloat16", "float32"):
+            tdt = {"float16": torch.float16, "bfloat16": torch.bfloat16, "float32": torch.float32}[dt]
+            g = torch.Generator(device=device)
+            g.manual_seed(seed * 100003 + b)
+            t = torch.empty(n // ITEMSIZE[dt], dtype=tdt, device=device).normal_(0.0, 1.0, generator=g)
+            base.append(t.view(torch.uint8))
+        else:
+            base.append(device_bytes(n, seed * 100003 + b, device))
+    reps = [base]
+    for k in range(2, plan.replays + 1):
+        cur = list(base)
+        for b in plan.designated:
+            a = base[b].clone()
+            fresh = device_bytes(len(plan.rewritten[(k, b)]) * 4096, seed * 7919 + k * 131 + b, device)
+            for j, c in enumerate(plan.rewritten[(k, b)]):
+                s, e = 4096 * c, min(4096 * (c + 1), a.numel())
+                a[s:e] = fresh[4096 * j:4096 * j + (e - s)]
+            cur[b] = a
+        reps.append(cur)
+    return reps
+
+
+def config5_device(plan: Batch, seed: int = 4, device="cuda"):
+    """Per-session rings, observations and RNG states on the GPU, as [S, bytes] uint8 tensors."""
+    import torch
+    S, g = plan.sessions, plan.ring
+    rings = device_bf16_normal(S * g.ring_bytes // 2, seed * 10 + 0, device).view(torch.uint8).view(S, g.ring_bytes)
+    obs = device_bytes(S * plan.obs_bytes, seed * 10 + 1, device).view(S, plan.obs_bytes)
+    rngs = device_bytes(S * plan.rng_bytes, seed * 10 + 2, device).view(S, plan.rng_bytes)
+    return rings, obs, rngs
