@@ -241,9 +241,6 @@ __device__ __forceinline__ void chunk_table(const JobBuf &jb, const Run *runs, u
     }
 }
 
-constexpr uint32_t kSlice = 1024;                 // bytes of each chunk moved per step
-constexpr uint32_t kSteps = kChunk / kSlice;      // steps per chunk
-constexpr uint32_t kRow = kSlice + 32;            // padded LDS row: lane pairs of 8 chunks hit distinct banks
 
 // Selects word i (0..3) of a 32-byte tail held in registers.
 __device__ __forceinline__ uint64_t sel4(uint64_t a, uint64_t b, uint64_t c, uint64_t d, uint32_t i)
@@ -260,13 +257,17 @@ __device__ __forceinline__ uint64_t sel4(uint64_t a, uint64_t b, uint64_t c, uin
 // flight.  Lane p of a pair owns XXH64 accumulators 2p and 2p+1, which read
 // exactly bytes [16p, 16p+16) of each 32-byte stripe.  DIFF marks chunks that
 // are new or changed against the parent's fingerprints and counts them.
-template <bool COPY, bool DIFF, int T>
+template <bool COPY, bool DIFF, int T, int SL>
 __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs,
                                             const uint32_t *__restrict__ map, uint64_t *__restrict__ nodes,
                                             uint32_t *__restrict__ dirty_count,
                                             uint64_t *__restrict__ dirty_mask)
 {
-    constexpr int U = kGroupChunks * kSlice / 16 / T;  // granules per lane per step
+    constexpr uint32_t kSlice = SL, kSteps = kChunk / SL;
+    constexpr uint32_t kRow = SL + 32;                  // padded LDS row: lane pairs of 8 chunks hit distinct banks
+    constexpr uint32_t LPS = SL / 16;                   // lanes per chunk slice
+    constexpr int U = kGroupChunks * SL / 16 / T;       // granules per lane per step
+    static_assert(U >= 1 && T % LPS == 0, "tile shape");
     __shared__ __attribute__((aligned(16))) uint8_t tile[kGroupChunks * kRow];
     __shared__ uint64_t caddr[kGroupChunks];
     __shared__ uint32_t clen[kGroupChunks];
@@ -282,18 +283,18 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
     chunk_table(jb, runs, c0, nv, caddr, clen);
     __syncthreads();
 
-    // This lane's granules: chunk (k*T + t) / 64, slot t % 64 of each slice.
-    const uint32_t slot = (t & 63) * 16;
+    // This lane's granules: chunk (k*T + t) / LPS, slot t % LPS of each slice.
+    const uint32_t slot = (t % LPS) * 16;
     uint64_t ga[U];
     uint32_t gl[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-        const uint32_t c = (k * T + t) >> 6;
+        const uint32_t c = (k * T + t) / LPS;
         ga[k] = c < nv ? caddr[c] : 0;
         gl[k] = c < nv ? clen[c] : 0;
     }
     auto load_granule = [&](int k, uint32_t x) -> uint4 {
-        const uint32_t c = (k * T + t) >> 6;
+        const uint32_t c = (k * T + t) / LPS;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (x < gl[k]) {
             const uint64_t a = ga[k] ? ga[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
@@ -317,7 +318,7 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
     for (uint32_t step = 0; step < kSteps; ++step) {
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-            const uint32_t c = (k * T + t) >> 6;
+            const uint32_t c = (k * T + t) / LPS;
             if (c < nv) {
                 if (COPY) store16_nt(jb.payload + (c0 + c) * kChunk + step * kSlice + slot, r[k]);
                 *reinterpret_cast<uint4 *>(tile + c * kRow + slot) = r[k];
@@ -482,11 +483,13 @@ __global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ l
 //   !PACK:   the chunk slots (contiguous, or per chunk through a manifest of
 //            arena offsets) -> the destination buffer's runs; only logical
 //            bytes are written.
-template <bool PACK, int T>
+template <bool PACK, int T, int SL>
 __global__ __launch_bounds__(T) void k_copy(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs,
                                             const uint32_t *__restrict__ map, uint64_t arena_base)
 {
-    constexpr int U = kGroupChunks * kSlice / 16 / T;
+    constexpr uint32_t kSteps = kChunk / SL, LPS = SL / 16;
+    constexpr int U = kGroupChunks * SL / 16 / T;
+    static_assert(U >= 1 && T % LPS == 0, "tile shape");
     __shared__ uint64_t caddr[kGroupChunks];  // runs side: chunk start if in one run, else 0
     __shared__ uint32_t clen[kGroupChunks];
     const uint64_t G = blockIdx.x;
@@ -499,30 +502,39 @@ __global__ __launch_bounds__(T) void k_copy(const JobBuf *__restrict__ bufs, con
     chunk_table(jb, runs, c0, nv, caddr, clen);
     __syncthreads();
 
-    const uint32_t slot = (t & 63) * 16;
+    const uint32_t slot = (t % LPS) * 16;
     uint64_t ra[U], sa[U];
     uint32_t gl[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-        const uint32_t c = (k * T + t) >> 6;
+        const uint32_t c = (k * T + t) / LPS;
         ra[k] = c < nv ? caddr[c] : 0;
         gl[k] = c < nv ? clen[c] : 0;
         sa[k] = c < nv ? (PACK || !man ? jb.payload + (c0 + c) * kChunk : arena_base + man[c0 + c]) : 0;
     }
     auto runs_addr = [&](int k, uint32_t x) -> uint64_t {
-        const uint32_t c = (k * T + t) >> 6;
+        const uint32_t c = (k * T + t) / LPS;
         return ra[k] ? ra[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
     };
-    for (uint32_t step = 0; step < kSteps; ++step) {
-        const uint32_t x = step * kSlice + slot;
-        uint4 v[U];
+    auto load = [&](int k, uint32_t x) -> uint4 {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (x < gl[k]) {
+            if (PACK) v = x + 16 <= gl[k] ? load16_nt(runs_addr(k, x)) : load_partial(runs_addr(k, x), gl[k] - x);
+            else v = load16_nt(sa[k] + x);  // slots are whole 4096-byte granules
+        }
+        return v;
+    };
+    // All lanes move the same slice of the group's chunks in lockstep (a
+    // barrier per step); the next slice's loads are issued before this
+    // slice's stores.
+    uint4 v[U], n[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-            v[k] = make_uint4(0, 0, 0, 0);
-            if (x < gl[k]) {
-                if (PACK) v[k] = x + 16 <= gl[k] ? load16_nt(runs_addr(k, x)) : load_partial(runs_addr(k, x), gl[k] - x);
-                else v[k] = load16_nt(sa[k] + x);  // slots are whole 4096-byte granules
-            }
+    for (int k = 0; k < U; ++k) v[k] = load(k, slot);
+    for (uint32_t step = 0; step < kSteps; ++step) {
+        const uint32_t x = step * SL + slot;
+        if (step + 1 < kSteps) {
+#pragma unroll
+            for (int k = 0; k < U; ++k) n[k] = load(k, x + SL);
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
@@ -533,6 +545,9 @@ __global__ __launch_bounds__(T) void k_copy(const JobBuf *__restrict__ bufs, con
                 else store_partial(runs_addr(k, x), v[k], gl[k] - x);
             }
         }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < U; ++k) v[k] = n[k];
     }
 }
 
@@ -661,9 +676,9 @@ __global__ void k_labels(const JobBuf *__restrict__ bufs, uint32_t nbuf,
 }
 
 // Workgroup sizes (lanes) of the tile kernels, from measurement on MI355X.
-constexpr int kPackLanes = 1024;
-constexpr int kHashLanes = 512;
-constexpr int kCopyLanes = 1024;
+constexpr int kPackLanes = 1024, kPackSlice = 512;
+constexpr int kHashLanes = 256, kHashSlice = 512;
+constexpr int kCopyLanes = 1024, kCopySlice = 1024;
 
 }  // namespace
 
@@ -686,13 +701,13 @@ hipError_t launch_hash(const JobBuf *bufs, const Run *runs, const uint32_t *map,
     const dim3 grid((uint32_t)ngroups);
     if (copy && diff) return hipErrorInvalidValue;
     if (copy)
-        hipLaunchKernelGGL((k_hash<true, false, kPackLanes>), grid, dim3(kPackLanes), 0, s, bufs, runs, map, nodes,
+        hipLaunchKernelGGL((k_hash<true, false, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, bufs, runs, map, nodes,
                            dirty_count, dirty_mask);
     else if (diff)
-        hipLaunchKernelGGL((k_hash<false, true, kHashLanes>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
+        hipLaunchKernelGGL((k_hash<false, true, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
                            dirty_count, dirty_mask);
     else
-        hipLaunchKernelGGL((k_hash<false, false, kHashLanes>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
+        hipLaunchKernelGGL((k_hash<false, false, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
                            dirty_count, dirty_mask);
     return hipGetLastError();
 }
@@ -710,7 +725,7 @@ hipError_t launch_pack(const JobBuf *bufs, const Run *runs, const uint32_t *map,
                        hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_copy<true, kCopyLanes>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs, map,
+    hipLaunchKernelGGL((k_copy<true, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs, map,
                        (uint64_t)0);
     return hipGetLastError();
 }
@@ -719,7 +734,7 @@ hipError_t launch_restore(const JobBuf *bufs, const Run *runs, const uint32_t *m
                           uint64_t ngroups, uint64_t arena_base, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_copy<false, kCopyLanes>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs,
+    hipLaunchKernelGGL((k_copy<false, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs,
                        map, arena_base);
     return hipGetLastError();
 }
