@@ -181,7 +181,12 @@ int pcs_classify(pcs_ctx *ctx, const uint64_t *d_hashes, uint32_t K, const uint6
  *     chunk i for b or its fingerprint changed; every other chunk is taken
  *     from the parent chain at restore time.  Stored chunks use one 4096-byte
  *     slot each, in increasing (buffer, chunk) order.  Fingerprints are
- *     always stored (flags are ignored).
+ *     always stored (flags are ignored).  The call normally reserves one slot
+ *     per chunk and returns the unused part to the arena once the stream has
+ *     produced the stored-chunk count; if the arena cannot hold that
+ *     reservation it waits for the stream and allocates exactly, and if even
+ *     that fails it returns PCS_E_NOMEM after its fingerprint outputs were
+ *     written.
  *   d_chunk_hashes, d_roots, d_session_root: optional copies of the
  *     fingerprints, laid out as in pcs_fingerprint (need PCS_CKPT_HASH or a
  *     parent; otherwise pass NULL).
@@ -234,7 +239,10 @@ int pcs_delete(pcs_ctx *ctx, pcs_snap snap);
 int pcs_snapshot_info(pcs_ctx *ctx, pcs_snap snap, pcs_snap_info *out);
 
 /* Copies the payload this snapshot holds (stored_bytes of pcs_snap_info) to
- * device memory d_dst of capacity `cap` bytes, stream-ordered. */
+ * device memory d_dst of capacity `cap` bytes, stream-ordered: a full
+ * snapshot in its canonical layout, an incremental one as its stored 4096-byte
+ * slots in increasing (buffer, chunk) order.  For an incremental snapshot
+ * d_dst must be 16-byte aligned. */
 int pcs_snapshot_payload(pcs_ctx *ctx, pcs_snap snap, void *d_dst, uint64_t cap);
 
 /* Copies the snapshot's stored chunk fingerprints (buffer-major) to d_dst,

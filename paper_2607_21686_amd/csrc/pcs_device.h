@@ -68,10 +68,11 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, ui
                        hipStream_t s);
 hipError_t launch_compact(const JobBuf *bufs, const uint32_t *map, uint64_t ngroups,
                           const uint64_t *dirty_mask, const uint64_t *offsets,
-                          uint64_t payload_arena_off, uint64_t *list, hipStream_t s);
+                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s);
 hipError_t launch_pack_dirty(const JobBuf *bufs, const Run *runs, const uint64_t *list,
-                             const uint64_t *total, uint64_t max_slots, uint64_t payload,
+                             const uint64_t *total, uint64_t max_slots, uint64_t payload_top,
                              hipStream_t s);
+hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
 hipError_t launch_classify(const JobBuf *bufs, const uint32_t *map, uint64_t ngroups,
                            const uint64_t *hashes, uint32_t K, uint64_t total, uint64_t *bitmap,
                            hipStream_t s);

@@ -101,8 +101,8 @@ __device__ uint64_t wave_merkle(uint64_t v, uint32_t m)
     return v;
 }
 
-// Logical-to-physical cursor over one buffer's runs.  Logical offsets fed to
-// cursor_addr must not decrease.
+// The run of a buffer that holds a logical offset, with the physical
+// displacement of that run and where it ends.
 struct Cursor {
     const Run *runs;
     uint32_t idx, last;  // current run, last run of the buffer
@@ -133,15 +133,6 @@ __device__ __forceinline__ Cursor cursor_seek(const Run *runs, uint32_t begin, u
     c.idx = lo;
     cursor_load(c);
     return c;
-}
-
-__device__ __forceinline__ uint64_t cursor_addr(Cursor &c, uint64_t L)
-{
-    while (L >= c.run_end && c.idx < c.last) {
-        ++c.idx;
-        cursor_load(c);
-    }
-    return L + c.delta;
 }
 
 // Device addresses arrive as integers; casting them to the global address
@@ -584,12 +575,14 @@ __global__ __launch_bounds__(1024) void k_scan(const uint32_t *__restrict__ coun
 
 // Assigns slots to dirty chunks in (buffer, chunk) order, lists them, and
 // writes the new snapshot's manifest: a dirty chunk points at its slot, a
-// clean one at wherever the parent holds it.
+// clean one at wherever the parent holds it.  Slot s is the 4096 bytes
+// ending s*4096 below the top of the snapshot's payload reservation (slots
+// grow downwards, so the unused part of the reservation is its low end).
 __global__ __launch_bounds__(64) void k_compact(const JobBuf *__restrict__ bufs,
                                                 const uint32_t *__restrict__ map,
                                                 const uint64_t *__restrict__ dirty_mask,
                                                 const uint64_t *__restrict__ offsets,
-                                                uint64_t payload_arena_off,
+                                                uint64_t payload_arena_top,
                                                 uint64_t *__restrict__ list)
 {
     const uint64_t G = blockIdx.x;
@@ -605,38 +598,52 @@ __global__ __launch_bounds__(64) void k_compact(const JobBuf *__restrict__ bufs,
         const uint64_t below = lane ? (mask & ((1ULL << lane) - 1)) : 0;
         const uint64_t slot = offsets[G] + (uint64_t)__popcll(below);
         list[slot] = ((uint64_t)b << 40) | i;
-        man[i] = payload_arena_off + slot * kChunk;
+        man[i] = payload_arena_top - (slot + 1) * kChunk;
     } else {
         man[i] = jb.parent_manifest ? ((const g_u64 *)jb.parent_manifest)[i]
                                     : jb.parent_slot0 + i * kChunk;
     }
 }
 
-// Copies listed dirty chunks into consecutive slots (64 slots per
-// workgroup, one whole chunk per step), zero-padding partial chunks.
+// Copies listed dirty chunks into their slots (slot s ends s*4096 below
+// `payload_top`): one wavefront per slot, each lane moving 64 bytes with
+// four 16-byte loads in flight, zero-padding partial chunks.
 __global__ __launch_bounds__(256) void k_pack_dirty(const JobBuf *__restrict__ bufs,
                                                     const Run *__restrict__ runs,
                                                     const uint64_t *__restrict__ list,
                                                     const uint64_t *__restrict__ total_ptr,
-                                                    uint64_t payload)
+                                                    uint64_t payload_top)
 {
-    const uint64_t total = *total_ptr;
-    const uint64_t s0 = (uint64_t)blockIdx.x * kGroupChunks;
-    if (s0 >= total) return;
-    const uint32_t ns = (uint32_t)umin(kGroupChunks, total - s0);
-    const uint32_t x = threadIdx.x * 16;
-    for (uint32_t k = 0; k < ns; ++k) {
-        const uint64_t e = list[s0 + k];
-        const JobBuf &jb = bufs[e >> 40];
-        const uint64_t cb = (e & ((1ULL << 40) - 1)) * kChunk;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (cb + x < jb.nbytes) {
-            Cursor cur = cursor_seek(runs, jb.run_begin, jb.run_count, jb.nbytes, cb + x);
-            if (cb + x + 16 <= jb.nbytes) v = load16(cursor_addr(cur, cb + x));
-            else v = load_partial(cursor_addr(cur, cb + x), (uint32_t)(jb.nbytes - cb - x));
+    const uint64_t slot = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (slot >= *total_ptr) return;
+    const uint32_t lane = threadIdx.x & 63;
+    const uint64_t e = list[slot];
+    const JobBuf &jb = bufs[e >> 40];
+    const uint64_t cb = (e & ((1ULL << 40) - 1)) * kChunk;
+    const uint64_t len = umin(kChunk, jb.nbytes - cb);
+    const uint64_t dst = payload_top - (slot + 1) * kChunk;
+    uint4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t x = (k * 64 + lane) * 16;
+        v[k] = make_uint4(0, 0, 0, 0);
+        if (x < len) {
+            const uint64_t a = phys_addr(runs, jb.run_begin, jb.run_count, cb + x);
+            v[k] = x + 16 <= len ? load16(a) : load_partial(a, (uint32_t)(len - x));
         }
-        store16(payload + (s0 + k) * kChunk + x, v);
     }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) store16(dst + (k * 64 + lane) * 16, v[k]);
+}
+
+// Copies n slots stored downwards from `top` into increasing order at dst
+// (slot s -> dst + s*4096): the readable form of an incremental payload.
+__global__ __launch_bounds__(256) void k_reverse_slots(uint64_t top, uint64_t dst, uint64_t n)
+{
+    const uint64_t s = blockIdx.x;
+    if (s >= n) return;
+    const uint32_t x = threadIdx.x * 16;
+    store16(dst + s * kChunk + x, load16(top - (s + 1) * kChunk + x));
 }
 
 // ---------------------------------------------------------------- classify
@@ -748,21 +755,28 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, ui
 
 hipError_t launch_compact(const JobBuf *bufs, const uint32_t *map, uint64_t ngroups,
                           const uint64_t *dirty_mask, const uint64_t *offsets,
-                          uint64_t payload_arena_off, uint64_t *list, hipStream_t s)
+                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
     hipLaunchKernelGGL(k_compact, dim3((uint32_t)ngroups), dim3(64), 0, s, bufs, map, dirty_mask, offsets,
-                       payload_arena_off, list);
+                       payload_arena_top, list);
     return hipGetLastError();
 }
 
 hipError_t launch_pack_dirty(const JobBuf *bufs, const Run *runs, const uint64_t *list,
-                             const uint64_t *total, uint64_t max_slots, uint64_t payload,
+                             const uint64_t *total, uint64_t max_slots, uint64_t payload_top,
                              hipStream_t s)
 {
     if (max_slots == 0) return hipSuccess;
-    const uint32_t blocks = (uint32_t)((max_slots + kGroupChunks - 1) / kGroupChunks);
-    hipLaunchKernelGGL(k_pack_dirty, dim3(blocks), dim3(256), 0, s, bufs, runs, list, total, payload);
+    const uint32_t blocks = (uint32_t)((max_slots + 3) / 4);
+    hipLaunchKernelGGL(k_pack_dirty, dim3(blocks), dim3(256), 0, s, bufs, runs, list, total, payload_top);
+    return hipGetLastError();
+}
+
+hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_reverse_slots, dim3((uint32_t)n), dim3(256), 0, s, top, dst, n);
     return hipGetLastError();
 }
 

@@ -56,6 +56,23 @@ class Arena {
         }
         return false;
     }
+    // Highest-address fit: [end - bytes, end) of the highest free range that
+    // holds it.  Incremental payload reservations come from the top, so the
+    // part a reservation gives back (its low end) merges with free space.
+    bool alloc_top(uint64_t bytes, uint64_t *off)
+    {
+        bytes = std::max<uint64_t>(kAlign, round_up(bytes, kAlign));
+        for (auto it = free_.rbegin(); it != free_.rend(); ++it) {
+            if (it->second < bytes) continue;
+            const uint64_t start = it->first, size = it->second;
+            *off = start + size - bytes;
+            if (size == bytes) free_.erase(start);
+            else free_[start] = size - bytes;
+            used_ += bytes;
+            return true;
+        }
+        return false;
+    }
     void release(uint64_t off, uint64_t bytes)
     {
         bytes = std::max<uint64_t>(kAlign, round_up(bytes, kAlign));
@@ -138,7 +155,8 @@ struct SnapNode {
     uint64_t total_chunks = 0, state_bytes = 0;
     uint64_t hashes_off = 0, manifest_off = 0, roots_off = 0, payload_off = 0;  // arena offsets
     uint64_t payload_bytes = 0;         // stored bytes (incremental: after settling)
-    uint64_t reserved_payload = 0;      // incremental: slots reserved before settling
+    uint64_t pay_off = 0, pay_bytes = 0;  // incremental: payload block (slots grow down from its top)
+    uint64_t pay_top = 0;               // incremental: arena offset of the top of the payload block
     bool settled = true;
     int count_slot = -1;
     hipEvent_t ev = nullptr;
@@ -149,6 +167,7 @@ struct SnapNode {
         if (ev) (void)hipEventDestroy(ev);
         if (count_slot >= 0) ctx->free_counts.push_back((uint32_t)count_slot);
         if (block_bytes) ctx->arena.release(block_off, block_bytes);
+        if (pay_bytes) ctx->arena.release(pay_off, pay_bytes);
     }
 };
 
@@ -369,11 +388,12 @@ void settle(pcs_ctx *c, bool wait)
         c->free_counts.push_back((uint32_t)n->count_slot);
         n->count_slot = -1;
         n->payload_bytes = dirty * kChunk;
-        const uint64_t keep_bytes = round_up(n->payload_off - n->block_off + n->payload_bytes, kAlign);
-        const uint64_t old = round_up(n->block_bytes, kAlign);
-        if (keep_bytes < old) {
-            c->arena.release(n->block_off + keep_bytes, old - keep_bytes);
-            n->block_bytes = keep_bytes;
+        n->payload_off = n->pay_top - n->payload_bytes;
+        if (n->payload_bytes < n->pay_bytes) {
+            const uint64_t give = n->pay_bytes - n->payload_bytes;  // the low, unused end
+            c->arena.release(n->pay_off, give);
+            n->pay_off += give;
+            n->pay_bytes -= give;
         }
         n->settled = true;
     }
@@ -389,6 +409,17 @@ bool alloc_block(pcs_ctx *c, uint64_t bytes, uint64_t *off)
     if (!c->pending.empty()) {
         settle(c, true);
         return c->arena.alloc(bytes, off);
+    }
+    return false;
+}
+
+bool alloc_block_top(pcs_ctx *c, uint64_t bytes, uint64_t *off)
+{
+    settle(c, false);
+    if (c->arena.alloc_top(bytes, off)) return true;
+    if (!c->pending.empty()) {
+        settle(c, true);
+        return c->arena.alloc_top(bytes, off);
     }
     return false;
 }
@@ -771,20 +802,28 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     if (int st = add_buffers(c, job, plan, n, 0)) return st;
     const uint64_t T = job.nchunks, G = job.ngroups;
 
-    // Block: [hashes 8T][manifest 8T][roots 8(n+1)] [payload, T slots reserved].
+    // Metadata block [hashes 8T][manifest 8T][roots 8(n+1)] from the bottom;
+    // payload reservation (one slot per chunk, trimmed once the stored count
+    // is known) from the top.
     const uint64_t hashes_rel = 0, manifest_rel = 8 * T, roots_rel = 16 * T;
-    const uint64_t payload_rel = round_up(roots_rel + 8 * (n + 1), kAlign);
-    const uint64_t block = payload_rel + T * kChunk;
+    const uint64_t meta = roots_rel + 8 * (n + 1);
     if (c->free_counts.empty()) settle(c, true);
     if (c->free_counts.empty()) return fail(c, PCS_E_NOMEM, "too many incremental snapshots in flight");
-    uint64_t boff;
-    if (!alloc_block(c, block, &boff))
-        return fail(c, PCS_E_NOMEM, "arena cannot hold incremental snapshot (%llu bytes reserved)",
-                    (unsigned long long)block);
+    uint64_t boff, poff = 0;
+    if (!alloc_block(c, meta, &boff))
+        return fail(c, PCS_E_NOMEM, "arena cannot hold incremental snapshot metadata (%llu bytes)",
+                    (unsigned long long)meta);
+    // Pipelined path: reserve one slot per chunk now and trim later.  When
+    // that does not fit (even after every pending trim), take the exact path:
+    // wait for the stored-chunk count, then allocate exactly that many slots.
+    const bool exact = T && !alloc_block_top(c, T * kChunk, &poff);
     auto node = std::make_shared<SnapNode>();
     node->ctx = c;
     node->block_off = boff;
-    node->block_bytes = block;
+    node->block_bytes = meta;
+    node->pay_off = poff;
+    node->pay_bytes = exact ? 0 : T * kChunk;
+    node->pay_top = poff + node->pay_bytes;
     node->nbufs = n;
     node->incremental = true;
     node->has_hashes = true;
@@ -797,8 +836,7 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     node->hashes_off = boff + hashes_rel;
     node->manifest_off = boff + manifest_rel;
     node->roots_off = boff + roots_rel;
-    node->payload_off = boff + payload_rel;
-    node->reserved_payload = T * kChunk;
+    node->payload_off = node->pay_top;
     node->parent = par;
     if (hipEventCreateWithFlags(&node->ev, hipEventDisableTiming) != hipSuccess)
         return fail(c, PCS_E_HIP, "hipEventCreate failed");
@@ -857,7 +895,7 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     uint64_t *d_mask = (uint64_t *)(base + o_mask), *d_offs = (uint64_t *)(base + o_offs);
     uint64_t *d_total = (uint64_t *)(base + o_total), *d_list = (uint64_t *)(base + o_list);
     hipStream_t s = c->stream;
-    const uint64_t payload_dev = c->arena_dev + node->payload_off;
+    uint64_t payload_top_dev = c->arena_dev + node->pay_top;
     int st;
     if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, s); }))) return st;
     if ((st = launch(c, "incremental", [&] {
@@ -869,12 +907,31 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     if ((st = launch(c, "merkle", [&] { return launch_merkle(d_lists + n, 1, d_roots_tmp, d_sa, d_sb, nullptr, s); })))
         return st;
     if ((st = launch(c, "incremental", [&] { return launch_scan(d_cnt, G, d_offs, d_total, s); }))) return st;
+    if (exact) {
+        HIP_TRY(c, hipMemcpyAsync(&c->counts[c->free_counts.back()], d_total, 8, hipMemcpyDeviceToHost, s));
+        HIP_TRY(c, hipEventRecord(node->ev, s));
+        HIP_TRY(c, hipEventSynchronize(node->ev));
+        const uint64_t dirty = c->counts[c->free_counts.back()];
+        if (dirty && !alloc_block_top(c, dirty * kChunk, &poff))
+            return fail(c, PCS_E_NOMEM, "arena cannot hold %llu stored chunks of an incremental snapshot "
+                        "(its fingerprint outputs were written)", (unsigned long long)dirty);
+        node->pay_off = poff;
+        node->pay_bytes = dirty * kChunk;
+        node->pay_top = poff + node->pay_bytes;
+        node->payload_bytes = node->pay_bytes;
+        node->payload_off = poff;
+        payload_top_dev = c->arena_dev + node->pay_top;
+    }
     if ((st = launch(c, "incremental", [&] {
-             return launch_compact(d_bufs, d_map, G, d_mask, d_offs, node->payload_off, d_list, s);
+             return launch_compact(d_bufs, d_map, G, d_mask, d_offs, node->pay_top, d_list, s);
          })))
         return st;
-    if ((st = launch(c, "incremental", [&] { return launch_pack_dirty(d_bufs, d_runs, d_list, d_total, T, payload_dev, s); })))
+    if ((st = launch(c, "incremental", [&] { return launch_pack_dirty(d_bufs, d_runs, d_list, d_total, T, payload_top_dev, s); })))
         return st;
+    if (exact) {
+        *out = new_handle(c, node);
+        return PCS_OK;
+    }
     node->count_slot = (int)c->free_counts.back();
     c->free_counts.pop_back();
     HIP_TRY(c, hipMemcpyAsync(&c->counts[node->count_slot], d_total, 8, hipMemcpyDeviceToHost, s));
@@ -1007,6 +1064,15 @@ int pcs_snapshot_payload(pcs_ctx *c, pcs_snap snap, void *d_dst, uint64_t cap)
                                              (unsigned long long)cap, (unsigned long long)nd->payload_bytes);
     if (nd->payload_bytes == 0) return PCS_OK;
     if (!d_dst) return fail(c, PCS_E_INVAL, "null destination");
+    if (nd->incremental) {
+        // Stored slots grow downwards from the top of the reservation; hand
+        // them out in increasing slot order.
+        if ((uint64_t)d_dst % 16) return fail(c, PCS_E_INVAL, "destination must be 16-byte aligned");
+        return launch(c, "copy", [&] {
+            return launch_reverse_slots(c->arena_dev + nd->pay_top, (uint64_t)d_dst, nd->payload_bytes / kChunk,
+                                        c->stream);
+        });
+    }
     HIP_TRY(c, hipMemcpyAsync(d_dst, (void *)(c->arena_dev + nd->payload_off), nd->payload_bytes,
                               hipMemcpyDeviceToDevice, c->stream));
     return PCS_OK;

@@ -362,3 +362,33 @@ def test_errors_enqueue_nothing(ctx, pcs):
     assert e.value.code == pcs.E_NOMEM
     assert ctx.arena_stats() == before
     ctx.delete(s)
+
+
+def test_incremental_chain_in_tight_arena(pcs):
+    # 64 growing incremental checkpoints whose final state is ~6.4 MiB must fit
+    # in a 16 MiB arena: worst-case reservations are given back without
+    # leaving holes the next (larger) reservation cannot use.
+    bank = W.config2(1, capacity=512, latent_shape=(4, 15, 26), pose_dim=7, step_entries=8)
+    lat, pos = dev(bank.latents), dev(bank.poses)
+    final = 512 * (bank.latent_entry_bytes + bank.pose_entry_bytes)
+    log("tight arena: final state", final)
+    c = pcs.Context(arena(16 << 20))
+    handles, parent = [], 0
+    for j in range(1, 65):
+        e = 8 * j
+        plan = [pcs.flat(lat, e * bank.latent_entry_bytes), pcs.flat(pos, e * bank.pose_entry_bytes)]
+        h = c.checkpoint(plan, parent=parent, hash=parent == 0)
+        handles.append(h)
+        parent = h
+    stats = c.arena_stats()
+    assert stats["used"] < 2 * final + (1 << 20), stats
+    for j in (0, 31, 63):
+        e = 8 * (j + 1)
+        want = bank.prefix(e)
+        outs = [torch.empty(w.size, dtype=torch.uint8, device="cuda") for w in want]
+        c.restore(handles[j], [pcs.flat(o) for o in outs])
+        assert all(np.array_equal(host(o), w) for o, w in zip(outs, want)), j
+    for h in handles:
+        c.delete(h)
+    assert c.arena_stats()["used"] == 0
+    c.close()
