@@ -221,6 +221,21 @@ int pcs_checkpoint_batch(pcs_ctx *ctx, const pcs_buf *h_plans, const uint32_t *h
  */
 int pcs_restore(pcs_ctx *ctx, pcs_snap snap, const pcs_buf *h_dst, uint32_t n);
 
+/*
+ * Verified restore: restore(c) as above, fingerprinting every restored chunk
+ * from the same read and comparing it with the fingerprint stored at
+ * checkpoint time (the snapshot must hold fingerprints).  Detects a snapshot
+ * whose bytes changed after it was taken (I2: a snapshot is immutable).
+ *   d_bad_bitmap: uint64 words laid out like pcs_classify's bitmap (each
+ *                 buffer on fresh words, chunk i = bit i mod 64 of word i/64):
+ *                 1 = the restored chunk's fingerprint differs.  Required
+ *                 unless the snapshot has no chunks.
+ *   d_bad_labels: optional uint8[n]: 1 iff any chunk of that buffer differs.
+ * The bytes are restored whether or not they verify.
+ */
+int pcs_restore_verify(pcs_ctx *ctx, pcs_snap snap, const pcs_buf *h_dst, uint32_t n, uint64_t *d_bad_bitmap,
+                       uint8_t *d_bad_labels);
+
 /* Restores m snapshots in one launch; snapshot j goes to
  * h_dsts[off_j .. off_j + h_nbufs[j]).  Validates everything first. */
 int pcs_restore_batch(pcs_ctx *ctx, const pcs_snap *h_snaps, uint32_t m, const pcs_buf *h_dsts,
@@ -245,6 +260,14 @@ int pcs_snapshot_info(pcs_ctx *ctx, pcs_snap snap, pcs_snap_info *out);
  * d_dst must be 16-byte aligned. */
 int pcs_snapshot_payload(pcs_ctx *ctx, pcs_snap snap, void *d_dst, uint64_t cap);
 
+/* Read-only view of the payload a snapshot holds: its device address and
+ * size (stored_bytes), e.g. to stream it to storage without a copy.  A full
+ * snapshot is in its canonical layout; an incremental one stores its slots
+ * in decreasing address order (slot 0 highest).  The memory belongs to the
+ * library, must not be written (snapshots are immutable, I2) and stays valid
+ * until the snapshot's last handle is deleted. */
+int pcs_snapshot_view(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_payload, uint64_t *bytes);
+
 /* Copies the snapshot's stored chunk fingerprints (buffer-major) to d_dst,
  * which holds `cap` uint64 values.  PCS_E_INVAL if it has none. */
 int pcs_snapshot_hashes(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_dst, uint64_t cap);
@@ -257,8 +280,8 @@ int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t
  * Kernel timing.  While enabled, every kernel launch is bracketed by HIP
  * events on the context stream.  pcs_kernel_time waits for the stream, then
  * reports the number of launches and their summed duration in milliseconds
- * for the kernel family `name` ("hash", "pack_hash", "copy", "merkle",
- * "classify", "incremental", "map") since the last reset, and resets it.
+ * for the kernel family `name` ("hash", "pack_hash", "pack", "copy",
+ * "verify", "merkle", "classify", "incremental", "map") since the last reset, and resets it.
  */
 int pcs_set_timing(pcs_ctx *ctx, int enable);
 int pcs_kernel_time(pcs_ctx *ctx, const char *name, uint64_t *launches, double *total_ms);

@@ -184,6 +184,16 @@ class Context:
         nb = (ctypes.c_uint32 * max(1, len(counts)))(*counts)
         self._check(_L.pcs_restore_batch(self._h, s, len(snaps), arr, nb))
 
+    def restore_verify(self, snap: int, dsts, bad_bitmap, bad_labels=None):
+        self._check(_L.pcs_restore_verify(self._h, snap, _array(dsts), len(dsts), _dev_ptr(bad_bitmap),
+                                          _dev_ptr(bad_labels)))
+
+    def view(self, snap: int):
+        """(device address, bytes) of the payload the snapshot holds; read-only."""
+        a, n = ctypes.c_uint64(), ctypes.c_uint64()
+        self._check(_L.pcs_snapshot_view(self._h, snap, ctypes.byref(a), ctypes.byref(n)))
+        return int(a.value), int(n.value)
+
     def fork(self, snap: int) -> int:
         out = ctypes.c_uint64()
         self._check(_L.pcs_fork(self._h, snap, ctypes.byref(out)))

@@ -26,7 +26,8 @@ _ERRNAMES = {E_INVAL: "PCS_E_INVAL", E_NOMEM: "PCS_E_NOMEM", E_HANDLE: "PCS_E_HA
 # Every symbol include/pcs.h declares.
 EXPORTS = ("pcs_ctx_create", "pcs_ctx_destroy", "pcs_last_error", "pcs_chunk_counts", "pcs_fingerprint",
            "pcs_classify", "pcs_checkpoint", "pcs_checkpoint_batch", "pcs_restore", "pcs_restore_batch",
-           "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload", "pcs_snapshot_hashes",
+           "pcs_restore_verify", "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload",
+           "pcs_snapshot_view", "pcs_snapshot_hashes",
            "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
 
 
@@ -69,6 +70,8 @@ def load():
         "pcs_checkpoint_batch": ([P, PB, ctypes.POINTER(U32), U32, U32, P, P, P, PU64], I),
         "pcs_restore": ([P, U64, PB, U32], I),
         "pcs_restore_batch": ([P, PU64, U32, PB, ctypes.POINTER(U32)], I),
+        "pcs_restore_verify": ([P, U64, PB, U32, P, P], I),
+        "pcs_snapshot_view": ([P, U64, PU64, PU64], I),
         "pcs_fork": ([P, U64, PU64], I),
         "pcs_delete": ([P, U64], I),
         "pcs_snapshot_info": ([P, U64, ctypes.POINTER(PcsSnapInfo)], I),

@@ -33,7 +33,8 @@ struct JobBuf {
                               // incremental pack: where this buffer's new manifest entries go
     uint64_t hash_dst[2];     // device addresses of chunk 0's fingerprint outputs (0 = none)
     uint64_t root_dst[2];     // device addresses of the root outputs (0 = none)
-    uint64_t parent_hash;     // incremental: device address of the parent's chunk-0 fingerprint
+    uint64_t parent_hash;     // incremental: device address of the parent's chunk-0 fingerprint;
+                              // verified restore: of the snapshot's stored chunk-0 fingerprint
     uint64_t parent_chunks;   // incremental: chunks the parent held for this buffer
     uint64_t parent_manifest; // incremental: parent's manifest entries (0 if the parent is full)
     uint64_t parent_slot0;    // incremental, full parent: arena offset of the parent's chunk-0 slot
@@ -57,6 +58,8 @@ hipError_t launch_group_map(const JobBuf *bufs, uint32_t nbuf, uint64_t ngroups,
 hipError_t launch_hash(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
                        bool copy, bool diff, uint64_t *nodes, uint32_t *dirty_count,
                        uint64_t *dirty_mask, hipStream_t s);
+hipError_t launch_restore_verify(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
+                                 uint64_t arena_base, uint64_t *bad_bitmap, hipStream_t s);
 hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_t *in,
                          uint64_t *scratch_a, uint64_t *scratch_b, uint64_t *roots_out,
                          hipStream_t s);

@@ -239,25 +239,37 @@ __device__ __forceinline__ uint64_t sel4(uint64_t a, uint64_t b, uint64_t c, uin
     return i == 0 ? a : i == 1 ? b : i == 2 ? c : d;
 }
 
+// What a tile-kernel launch does besides fingerprinting every chunk.
+enum TileMode : int {
+    kModeHash = 0,    // fingerprint the buffer's runs
+    kModePack = 1,    // ... and store every chunk to its snapshot slot (checkpoint)
+    kModeDiff = 2,    // ... and mark chunks new or changed against the parent (incremental)
+    kModeVerify = 3,  // copy snapshot slots to the buffer's runs (restore), fingerprint
+                      // the restored bytes and mark chunks whose fingerprint differs
+                      // from the one stored at checkpoint time
+};
+
 // Fingerprint tile kernel.  One workgroup = one 64-chunk group of one
-// buffer.  Step k moves the k-th 1 KiB slice of every chunk of the group:
-// all T lanes load it with coalesced 16-byte loads (64 lanes per chunk
-// slice), COPY stores it to the chunk's snapshot slot (zero-padding a partial
-// last chunk), and every lane writes it to an LDS tile; then lane pairs of
-// the first two wavefronts hash the tile while the next slice's loads are in
-// flight.  Lane p of a pair owns XXH64 accumulators 2p and 2p+1, which read
-// exactly bytes [16p, 16p+16) of each 32-byte stripe.  DIFF marks chunks that
-// are new or changed against the parent's fingerprints and counts them.
-template <bool COPY, bool DIFF, int T, int SL>
+// buffer.  Step k moves the k-th SL-byte slice of every chunk of the group:
+// all T lanes load it with coalesced 16-byte loads (SL/16 lanes per chunk
+// slice), kModePack stores it to the chunk's snapshot slot (zero-padding a
+// partial last chunk) and kModeVerify to the buffer's runs, and every lane
+// writes it to an LDS tile; then lane pairs of the first two wavefronts hash
+// the tile while the next slice's loads are in flight.  Lane p of a pair owns
+// XXH64 accumulators 2p and 2p+1, which read exactly bytes [16p, 16p+16) of
+// each 32-byte stripe.  kModeDiff / kModeVerify ballot one flag per chunk into
+// a per-group mask (the group is one bitmap word).
+template <int MODE, int T, int SL>
 __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs,
                                             const uint32_t *__restrict__ map, uint64_t *__restrict__ nodes,
-                                            uint32_t *__restrict__ dirty_count,
-                                            uint64_t *__restrict__ dirty_mask)
+                                            uint32_t *__restrict__ flag_count, uint64_t *__restrict__ flag_mask,
+                                            uint64_t arena_base)
 {
-    constexpr uint32_t kSlice = SL, kSteps = kChunk / SL;
+    constexpr uint32_t kSteps = kChunk / SL;
     constexpr uint32_t kRow = SL + 32;                  // padded LDS row: lane pairs of 8 chunks hit distinct banks
     constexpr uint32_t LPS = SL / 16;                   // lanes per chunk slice
     constexpr int U = kGroupChunks * SL / 16 / T;       // granules per lane per step
+    constexpr bool kFromSlots = MODE == kModeVerify;    // source is the snapshot, destination the runs
     static_assert(U >= 1 && T % LPS == 0, "tile shape");
     __shared__ __attribute__((aligned(16))) uint8_t tile[kGroupChunks * kRow];
     __shared__ uint64_t caddr[kGroupChunks];
@@ -271,25 +283,37 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
     const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
     const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
     const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
+    const g_u64 *man = (const g_u64 *)jb.manifest;
     chunk_table(jb, runs, c0, nv, caddr, clen);
     __syncthreads();
 
     // This lane's granules: chunk (k*T + t) / LPS, slot t % LPS of each slice.
     const uint32_t slot = (t % LPS) * 16;
-    uint64_t ga[U];
+    uint64_t ga[U];   // runs side: chunk start when the chunk lies in one run, else 0
+    uint64_t sa[U];   // slots side: the chunk's 4096-byte slot (0 if the group has no such chunk)
     uint32_t gl[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
         const uint32_t c = (k * T + t) / LPS;
         ga[k] = c < nv ? caddr[c] : 0;
         gl[k] = c < nv ? clen[c] : 0;
+        sa[k] = 0;
+        if (c < nv && (MODE == kModePack || kFromSlots))
+            sa[k] = (kFromSlots && man) ? arena_base + man[c0 + c] : jb.payload + (c0 + c) * kChunk;
     }
-    auto load_granule = [&](int k, uint32_t x) -> uint4 {
+    auto runs_addr = [&](int k, uint32_t x) -> uint64_t {
         const uint32_t c = (k * T + t) / LPS;
+        return ga[k] ? ga[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
+    };
+    auto load_granule = [&](int k, uint32_t x) -> uint4 {
         uint4 v = make_uint4(0, 0, 0, 0);
         if (x < gl[k]) {
-            const uint64_t a = ga[k] ? ga[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
-            v = x + 16 <= gl[k] ? load16_nt(a) : load_partial(a, gl[k] - x);
+            if (kFromSlots) {
+                v = load16_nt(sa[k] + x);  // slots are whole 4096-byte granules, zero padded
+            } else {
+                const uint64_t a = runs_addr(k, x);
+                v = x + 16 <= gl[k] ? load16_nt(a) : load_partial(a, gl[k] - x);
+            }
         }
         return v;
     };
@@ -311,19 +335,24 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
         for (int k = 0; k < U; ++k) {
             const uint32_t c = (k * T + t) / LPS;
             if (c < nv) {
-                if (COPY) store16_nt(jb.payload + (c0 + c) * kChunk + step * kSlice + slot, r[k]);
+                const uint32_t x = step * SL + slot;
+                if (MODE == kModePack) store16_nt(sa[k] + x, r[k]);
+                if (kFromSlots && x < gl[k]) {
+                    if (x + 16 <= gl[k]) store16_nt(runs_addr(k, x), r[k]);
+                    else store_partial(runs_addr(k, x), r[k], gl[k] - x);
+                }
                 *reinterpret_cast<uint4 *>(tile + c * kRow + slot) = r[k];
             }
         }
         __syncthreads();
         if (step + 1 < kSteps) {
 #pragma unroll
-            for (int k = 0; k < U; ++k) r[k] = load_granule(k, (step + 1) * kSlice + slot);
+            for (int k = 0; k < U; ++k) r[k] = load_granule(k, (step + 1) * SL + slot);
         }
         if (hasher) {
             const uint8_t *row = tile + ci * kRow;
-            const uint32_t s0 = step * (kSlice / 32);
-            const uint32_t ns = nst > s0 ? umin(kSlice / 32, nst - s0) : 0;
+            const uint32_t s0 = step * (SL / 32);
+            const uint32_t ns = nst > s0 ? umin(SL / 32, nst - s0) : 0;
 #pragma unroll 8
             for (uint32_t s = 0; s < ns; ++s) {
                 const uint4 d = *reinterpret_cast<const uint4 *>(row + 32 * s + 16 * p);
@@ -331,9 +360,9 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
                 vb = xround(vb, ((uint64_t)d.w << 32) | d.z);
             }
             const uint32_t tp = nst * 32;  // tail start, 32-aligned, inside this slice if here
-            if (p == 0 && tp < len && tp >= step * kSlice && tp < (step + 1) * kSlice) {
-                const uint4 x = *reinterpret_cast<const uint4 *>(row + tp - step * kSlice);
-                const uint4 y = *reinterpret_cast<const uint4 *>(row + tp - step * kSlice + 16);
+            if (p == 0 && tp < len && tp >= step * SL && tp < (step + 1) * SL) {
+                const uint4 x = *reinterpret_cast<const uint4 *>(row + tp - step * SL);
+                const uint4 y = *reinterpret_cast<const uint4 *>(row + tp - step * SL + 16);
                 tw0 = ((uint64_t)x.y << 32) | x.x;
                 tw1 = ((uint64_t)x.w << 32) | x.z;
                 tw2 = ((uint64_t)y.y << 32) | y.x;
@@ -381,22 +410,23 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
             if (jb.hash_dst[0]) ((g_u64 *)jb.hash_dst[0])[i] = h;
             if (jb.hash_dst[1]) ((g_u64 *)jb.hash_dst[1])[i] = h;
             leaves[ci] = h;
-            if (DIFF) {
+            if (MODE == kModeDiff) {
                 const bool d = i >= jb.parent_chunks || ((const g_u64 *)jb.parent_hash)[i] != h;
                 dflag[ci] = d ? 1u : 0u;
             }
+            if (MODE == kModeVerify) dflag[ci] = ((const g_u64 *)jb.parent_hash)[i] != h ? 1u : 0u;
         }
     }
     __syncthreads();
     if (t < 64) {
         const uint64_t v = t < nv ? leaves[t] : 0;
         const uint64_t root = wave_merkle(v, nv);
-        if (t == 0) nodes[G] = root;
-        if (DIFF) {
+        if (t == 0 && nodes) nodes[G] = root;
+        if (MODE == kModeDiff || MODE == kModeVerify) {
             const uint64_t mask = __ballot(t < nv && dflag[t] != 0);
             if (t == 0) {
-                dirty_mask[G] = mask;
-                dirty_count[G] = (uint32_t)__popcll(mask);
+                if (flag_mask) flag_mask[G] = mask;
+                if (flag_count) flag_count[G] = (uint32_t)__popcll(mask);
             }
         }
     }
@@ -708,14 +738,23 @@ hipError_t launch_hash(const JobBuf *bufs, const Run *runs, const uint32_t *map,
     const dim3 grid((uint32_t)ngroups);
     if (copy && diff) return hipErrorInvalidValue;
     if (copy)
-        hipLaunchKernelGGL((k_hash<true, false, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, bufs, runs, map, nodes,
-                           dirty_count, dirty_mask);
+        hipLaunchKernelGGL((k_hash<kModePack, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, bufs, runs, map,
+                           nodes, dirty_count, dirty_mask, (uint64_t)0);
     else if (diff)
-        hipLaunchKernelGGL((k_hash<false, true, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
-                           dirty_count, dirty_mask);
+        hipLaunchKernelGGL((k_hash<kModeDiff, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map,
+                           nodes, dirty_count, dirty_mask, (uint64_t)0);
     else
-        hipLaunchKernelGGL((k_hash<false, false, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map, nodes,
-                           dirty_count, dirty_mask);
+        hipLaunchKernelGGL((k_hash<kModeHash, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map,
+                           nodes, dirty_count, dirty_mask, (uint64_t)0);
+    return hipGetLastError();
+}
+
+hipError_t launch_restore_verify(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
+                                 uint64_t arena_base, uint64_t *bad_bitmap, hipStream_t s)
+{
+    if (ngroups == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_hash<kModeVerify, kPackLanes, kPackSlice>), dim3((uint32_t)ngroups), dim3(kPackLanes), 0, s,
+                       bufs, runs, map, (uint64_t *)nullptr, (uint32_t *)nullptr, bad_bitmap, arena_base);
     return hipGetLastError();
 }
 

@@ -1012,6 +1012,71 @@ int pcs_restore_batch(pcs_ctx *c, const pcs_snap *snaps, uint32_t m, const pcs_b
     return launch(c, "copy", [&] { return launch_restore(d_bufs, d_runs, d_map, G, c->arena_dev, c->stream); });
 }
 
+int pcs_restore_verify(pcs_ctx *c, pcs_snap snap, const pcs_buf *dst, uint32_t n, uint64_t *d_bad_bitmap,
+                       uint8_t *d_bad_labels)
+{
+    if (!c) return PCS_E_INVAL;
+    auto nd = lookup(c, snap);
+    if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    if (!nd->has_hashes) return fail(c, PCS_E_INVAL, "snapshot holds no fingerprints to verify against");
+    if (n != nd->nbufs) return fail(c, PCS_E_SHAPE, "snapshot holds %u buffers, %u destinations given", nd->nbufs, n);
+    if (n && !dst) return fail(c, PCS_E_INVAL, "null destinations");
+    Job job;
+    if (int st = add_buffers(c, job, dst, n, 0)) return st;
+    if (job.ngroups && !d_bad_bitmap) return fail(c, PCS_E_INVAL, "null mismatch bitmap");
+    for (uint32_t k = 0; k < n; ++k) {
+        const Layout &want = nd->bufs[k], &got = job.lays[k];
+        if (want.kind != got.kind || want.nbytes != got.nbytes ||
+            (want.kind == PCS_RING && (want.row_bytes != got.row_bytes || want.window != got.window ||
+                                       want.outer != got.outer)))
+            return fail(c, PCS_E_SHAPE, "buffer %u: destination layout differs from the snapshot", k);
+        JobBuf &jb = job.bufs[k];
+        if (nd->incremental)
+            jb.manifest = c->arena_dev + nd->manifest_off + 8 * nd->chunk_begin[k];
+        else
+            jb.payload = c->arena_dev + nd->payload_off + nd->comp_off[k];
+        jb.parent_hash = c->arena_dev + nd->hashes_off + 8 * nd->chunk_begin[k];
+    }
+    if (n == 0) return PCS_OK;
+    Carver cv;
+    uint64_t o_bufs, o_runs, o_map;
+    cv.add(&o_bufs, sizeof(JobBuf) * n);
+    cv.add(&o_runs, sizeof(Run) * job.runs.size());
+    const uint64_t hb = cv.total;
+    cv.add(&o_map, 4 * job.ngroups);
+    Temp t(c);
+    if (int st = temp_alloc(c, t, cv.total)) return st;
+    const uint64_t base = c->arena_dev + t.off;
+    std::vector<uint8_t> host(hb, 0);
+    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+    if (int st = upload(c, base, host.data(), hb)) return st;
+    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
+    const Run *d_runs = (const Run *)(base + o_runs);
+    uint32_t *d_map = (uint32_t *)(base + o_map);
+    const uint64_t G = job.ngroups;
+    int st;
+    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
+    if ((st = launch(c, "verify", [&] {
+             return launch_restore_verify(d_bufs, d_runs, d_map, G, c->arena_dev, d_bad_bitmap, c->stream);
+         })))
+        return st;
+    if (d_bad_labels)
+        return launch(c, "verify", [&] { return launch_labels(d_bufs, n, d_bad_bitmap, d_bad_labels, c->stream); });
+    return PCS_OK;
+}
+
+int pcs_snapshot_view(pcs_ctx *c, pcs_snap snap, uint64_t *d_payload, uint64_t *bytes)
+{
+    if (!c) return PCS_E_INVAL;
+    auto nd = lookup(c, snap);
+    if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    if (!nd->settled) settle(c, true);
+    if (d_payload) *d_payload = c->arena_dev + nd->payload_off;
+    if (bytes) *bytes = nd->payload_bytes;
+    return PCS_OK;
+}
+
 int pcs_restore(pcs_ctx *c, pcs_snap snap, const pcs_buf *dst, uint32_t n)
 {
     return pcs_restore_batch(c, &snap, 1, dst, &n);
