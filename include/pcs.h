@@ -55,6 +55,7 @@ extern "C" {
 #define PCS_E_HANDLE (-3)  /* unknown or deleted snapshot handle                 */
 #define PCS_E_SHAPE (-4)   /* restore target layout differs from the snapshot's  */
 #define PCS_E_HIP (-5)     /* a HIP runtime call failed                          */
+#define PCS_E_CORRUPT (-6) /* an imported image does not match its fingerprints  */
 
 #define PCS_CHUNK_BYTES 4096u
 
@@ -271,6 +272,30 @@ int pcs_snapshot_view(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_payload, uint64_t
 /* Copies the snapshot's stored chunk fingerprints (buffer-major) to d_dst,
  * which holds `cap` uint64 values.  PCS_E_INVAL if it has none. */
 int pcs_snapshot_hashes(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_dst, uint64_t cap);
+
+/*
+ * Durable snapshots across a process boundary (I2 in its strong form: a
+ * session survives the death of the process that created it; Sec. 7.2
+ * "Across a process boundary").
+ *
+ * pcs_export writes a self-contained image of the snapshot to host memory
+ * h_dst (capacity `cap`) and waits for it: a header (layout of every buffer,
+ * Merkle roots, chunk fingerprints) and the full logical state in the
+ * canonical layout, whether the snapshot is full or incremental.  With
+ * h_dst == NULL it only reports the size in *written.  Layout (little-endian):
+ *   "PCSIMG01"; u32 version 1; u32 nbufs n; u64 chunks T; u64 state bytes;
+ *   u64 payload bytes; u64 flags 0; n x {u32 kind, u32 0, u64 nbytes,
+ *   u64 row_bytes, u64 window, u64 outer, u64 0}; n buffer roots and the
+ *   session root; T chunk fingerprints; zero padding to a 4096-byte boundary;
+ *   the payload (components 4096-aligned, zero padded).
+ *
+ * pcs_import rebuilds a full snapshot (with fingerprints) from such an image
+ * in this context, fingerprints the imported bytes on the device and returns
+ * PCS_E_CORRUPT, creating no handle, if any chunk or root differs from the
+ * image.  It waits for the stream.
+ */
+int pcs_export(pcs_ctx *ctx, pcs_snap snap, void *h_dst, uint64_t cap, uint64_t *written);
+int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
 
 /* Arena accounting: bytes in use, bytes free, largest free block, live handles. */
 int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t *largest_free,

@@ -298,3 +298,33 @@ class Store:
     def state_bytes(self, handle: int) -> int:
         """Logical bytes the snapshot restores (I4: the sum of its buffer sizes)."""
         return int(sum(self._snaps[handle].nbytes))
+
+
+# ----------------------------------------- durable images (Sec. 7.2, I2)
+
+IMAGE_MAGIC = b"PCSIMG01"
+
+
+def export_image(buffers, layouts=None) -> bytes:
+    """Self-contained image of a snapshot of logical byte strings.
+
+    layouts[b] = (kind, row_bytes, window, outer) with kind 0 (flat, ring
+    fields 0) or 1 (ring); default flat.  Layout, little-endian: magic, u32
+    version 1, u32 n, u64 chunks, u64 state bytes, u64 payload bytes, u64
+    flags 0; per buffer u32 kind, u32 0, u64 nbytes, u64 row_bytes, u64
+    window, u64 outer, u64 0; n buffer roots, session root; all chunk
+    fingerprints; zero padding to 4096; the canonical payload.
+    """
+    import struct
+    bufs = [_bytes(b) for b in buffers]
+    n = len(bufs)
+    layouts = layouts or [(0, 0, 0, 0)] * n
+    hashes, roots, sroot = fingerprint(bufs)
+    payload = pack(bufs)
+    head = IMAGE_MAGIC + struct.pack("<IIQQQQ", 1, n, hashes.size, sum(b.size for b in bufs), payload.size, 0)
+    for b, (kind, row, win, outer) in zip(bufs, layouts):
+        head += struct.pack("<IIQQQQQ", kind, 0, b.size, row, win, outer, 0)
+    head += struct.pack("<%dQ" % (n + 1), *([int(r) for r in roots] + [sroot]))
+    head += hashes.astype("<u8").tobytes()
+    pad = (-len(head)) % CHUNK
+    return head + b"\0" * pad + payload.tobytes()

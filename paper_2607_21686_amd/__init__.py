@@ -20,11 +20,12 @@ import ctypes
 
 import torch
 
-from ._lib import (CHUNK_BYTES, CKPT_HASH, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_SHAPE, EXPORTS, FLAT,
+from ._lib import (CHUNK_BYTES, CKPT_HASH, E_CORRUPT, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_SHAPE, EXPORTS, FLAT,
                    MUST_SNAPSHOT, RECOMPUTABLE, RING, PcsBuf, PcsError, PcsSnapInfo, lib)
 
 __all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
-           "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "EXPORTS"]
+           "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "E_CORRUPT",
+           "EXPORTS"]
 
 _L = lib()  # fails loudly if the HIP library is missing
 
@@ -193,6 +194,23 @@ class Context:
         a, n = ctypes.c_uint64(), ctypes.c_uint64()
         self._check(_L.pcs_snapshot_view(self._h, snap, ctypes.byref(a), ctypes.byref(n)))
         return int(a.value), int(n.value)
+
+    def export(self, snap: int):
+        """The snapshot's self-contained host image (numpy uint8)."""
+        import numpy as np
+        size = ctypes.c_uint64()
+        self._check(_L.pcs_export(self._h, snap, None, 0, ctypes.byref(size)))
+        img = np.empty(size.value, dtype=np.uint8)
+        self._check(_L.pcs_export(self._h, snap, img.ctypes.data_as(ctypes.c_void_p), img.size, ctypes.byref(size)))
+        return img
+
+    def import_image(self, img) -> int:
+        """A new full snapshot from an image written by export (verified)."""
+        import numpy as np
+        a = np.ascontiguousarray(img, dtype=np.uint8)
+        out = ctypes.c_uint64()
+        self._check(_L.pcs_import(self._h, a.ctypes.data_as(ctypes.c_void_p), a.size, ctypes.byref(out)))
+        return int(out.value)
 
     def fork(self, snap: int) -> int:
         out = ctypes.c_uint64()

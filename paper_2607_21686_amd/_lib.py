@@ -14,21 +14,21 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libpcs.so")
 
 OK = 0
-E_INVAL, E_NOMEM, E_HANDLE, E_SHAPE, E_HIP = -1, -2, -3, -4, -5
+E_INVAL, E_NOMEM, E_HANDLE, E_SHAPE, E_HIP, E_CORRUPT = -1, -2, -3, -4, -5, -6
 CHUNK_BYTES = 4096
 FLAT, RING = 0, 1
 RECOMPUTABLE, MUST_SNAPSHOT = 0, 1
 CKPT_HASH = 1
 
 _ERRNAMES = {E_INVAL: "PCS_E_INVAL", E_NOMEM: "PCS_E_NOMEM", E_HANDLE: "PCS_E_HANDLE",
-             E_SHAPE: "PCS_E_SHAPE", E_HIP: "PCS_E_HIP"}
+             E_SHAPE: "PCS_E_SHAPE", E_HIP: "PCS_E_HIP", E_CORRUPT: "PCS_E_CORRUPT"}
 
 # Every symbol include/pcs.h declares.
 EXPORTS = ("pcs_ctx_create", "pcs_ctx_destroy", "pcs_last_error", "pcs_chunk_counts", "pcs_fingerprint",
            "pcs_classify", "pcs_checkpoint", "pcs_checkpoint_batch", "pcs_restore", "pcs_restore_batch",
            "pcs_restore_verify", "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload",
            "pcs_snapshot_view", "pcs_snapshot_hashes",
-           "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
+           "pcs_export", "pcs_import", "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
 
 
 class PcsBuf(ctypes.Structure):
@@ -77,6 +77,8 @@ def load():
         "pcs_snapshot_info": ([P, U64, ctypes.POINTER(PcsSnapInfo)], I),
         "pcs_snapshot_payload": ([P, U64, P, U64], I),
         "pcs_snapshot_hashes": ([P, U64, P, U64], I),
+        "pcs_export": ([P, U64, P, U64, PU64], I),
+        "pcs_import": ([P, P, U64, PU64], I),
         "pcs_arena_stats": ([P, PU64, PU64, PU64, PU64], I),
         "pcs_set_timing": ([P, I], I),
         "pcs_kernel_time": ([P, ctypes.c_char_p, PU64, ctypes.POINTER(ctypes.c_double)], I),

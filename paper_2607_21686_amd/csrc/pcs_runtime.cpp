@@ -649,6 +649,136 @@ int checkpoint_full(pcs_ctx *c, const pcs_buf *plans, const uint32_t *nbufs, uin
     return PCS_OK;
 }
 
+// strict: a destination must have the snapshot buffer's kind and ring shape;
+// otherwise only its logical size must match (used to lay a snapshot out
+// flat, e.g. for export).
+int restore_impl(pcs_ctx *c, const pcs_snap *snaps, uint32_t m, const pcs_buf *dsts, const uint32_t *nbufs,
+                 bool strict)
+{
+    if (!c) return PCS_E_INVAL;
+    if (m && (!snaps || !nbufs)) return fail(c, PCS_E_INVAL, "null argument");
+    Job job;
+    uint64_t nb_total = 0;
+    std::vector<std::shared_ptr<SnapNode>> nodes;
+    for (uint32_t j = 0; j < m; ++j) {
+        auto nd = lookup(c, snaps[j]);
+        if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snaps[j]);
+        if (nbufs[j] != nd->nbufs)
+            return fail(c, PCS_E_SHAPE, "snapshot %u holds %u buffers, %u destinations given", j, nd->nbufs, nbufs[j]);
+        nodes.push_back(nd);
+        nb_total += nbufs[j];
+    }
+    if (nb_total && !dsts) return fail(c, PCS_E_INVAL, "null destinations");
+    if (nb_total > (1u << 24)) return fail(c, PCS_E_INVAL, "too many buffers");
+    if (int st = add_buffers(c, job, dsts, (uint32_t)nb_total, 0)) return st;
+    uint32_t b = 0;
+    for (uint32_t j = 0; j < m; ++j) {
+        const auto &nd = nodes[j];
+        for (uint32_t k = 0; k < nd->nbufs; ++k, ++b) {
+            const Layout &want = nd->bufs[k], &got = job.lays[b];
+            if (want.nbytes != got.nbytes ||
+                (strict && (want.kind != got.kind ||
+                            (want.kind == PCS_RING && (want.row_bytes != got.row_bytes ||
+                                                       want.window != got.window || want.outer != got.outer)))))
+                return fail(c, PCS_E_SHAPE, "restore %u buffer %u: destination layout differs from the snapshot", j, k);
+            JobBuf &jb = job.bufs[b];
+            if (nd->incremental)
+                jb.manifest = c->arena_dev + nd->manifest_off + 8 * nd->chunk_begin[k];
+            else
+                jb.payload = c->arena_dev + nd->payload_off + nd->comp_off[k];
+        }
+    }
+    const uint32_t n = (uint32_t)nb_total;
+    if (n == 0) return PCS_OK;
+    Carver cv;
+    uint64_t o_bufs, o_runs, o_map;
+    cv.add(&o_bufs, sizeof(JobBuf) * n);
+    cv.add(&o_runs, sizeof(Run) * job.runs.size());
+    const uint64_t hb = cv.total;
+    cv.add(&o_map, 4 * job.ngroups);
+    Temp t(c);
+    if (int st = temp_alloc(c, t, cv.total)) return st;
+    const uint64_t base = c->arena_dev + t.off;
+    std::vector<uint8_t> host(hb, 0);
+    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+    if (int st = upload(c, base, host.data(), hb)) return st;
+    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
+    const Run *d_runs = (const Run *)(base + o_runs);
+    uint32_t *d_map = (uint32_t *)(base + o_map);
+    const uint64_t G = job.ngroups;
+    int st;
+    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
+    return launch(c, "copy", [&] { return launch_restore(d_bufs, d_runs, d_map, G, c->arena_dev, c->stream); });
+}
+
+
+// ---------------------------------------------------------------- snapshot images
+//
+// A self-contained host image of a snapshot (little-endian):
+//   [0, 8)    magic "PCSIMG01"
+//   [8, 12)   u32 version (1)         [12, 16)  u32 nbufs n
+//   [16, 24)  u64 total chunks T      [24, 32)  u64 state bytes
+//   [32, 40)  u64 payload bytes       [40, 48)  u64 flags (0)
+//   n x 48 B  per buffer: u32 kind, u32 0, u64 nbytes, u64 row_bytes,
+//             u64 window, u64 outer, u64 0   (ring fields 0 for flat buffers)
+//   (n+1) x 8 buffer roots, then the session root
+//   T x 8     chunk fingerprints, buffer-major
+//   zero padding to a 4096-byte boundary, then the payload in the canonical
+//   full-snapshot layout (components 4096-aligned, zero padded).
+constexpr char kImageMagic[8] = {'P', 'C', 'S', 'I', 'M', 'G', '0', '1'};
+constexpr uint64_t kImageHead = 48, kImageDesc = 48;
+
+struct ImageLayout {
+    uint64_t roots_off, hashes_off, data_off, size, payload;
+    std::vector<uint64_t> comp_off;
+};
+
+ImageLayout image_layout(const std::vector<Layout> &bufs, uint64_t T)
+{
+    ImageLayout L;
+    const uint64_t n = bufs.size();
+    L.roots_off = kImageHead + kImageDesc * n;
+    L.hashes_off = L.roots_off + 8 * (n + 1);
+    L.data_off = round_up(L.hashes_off + 8 * T, kAlign);
+    L.payload = 0;
+    for (auto &b : bufs) {
+        L.comp_off.push_back(L.payload);
+        L.payload += b.nchunks * kChunk;
+    }
+    L.size = L.data_off + L.payload;
+    return L;
+}
+
+void put32(uint8_t *p, uint32_t v) { memcpy(p, &v, 4); }
+void put64(uint8_t *p, uint64_t v) { memcpy(p, &v, 8); }
+uint32_t get32(const uint8_t *p) { uint32_t v; memcpy(&v, p, 4); return v; }
+uint64_t get64(const uint8_t *p) { uint64_t v; memcpy(&v, p, 8); return v; }
+
+// Fingerprints flat device regions (e.g. payload components) into device
+// arrays: chunk hashes (buffer-major), buffer roots, session root.
+int fingerprint_regions(pcs_ctx *c, const std::vector<uint64_t> &addr, const std::vector<uint64_t> &nbytes,
+                        uint64_t *d_hashes, uint64_t *d_roots, uint64_t *d_sroot)
+{
+    const uint32_t n = (uint32_t)addr.size();
+    std::vector<pcs_buf> bufs(n);
+    for (uint32_t b = 0; b < n; ++b) {
+        memset(&bufs[b], 0, sizeof(pcs_buf));
+        bufs[b].ptr = addr[b];
+        bufs[b].nbytes = nbytes[b];
+        bufs[b].kind = PCS_FLAT;
+    }
+    Job job;
+    if (int st = add_buffers(c, job, bufs.data(), n, 0)) return st;
+    std::vector<RootDst> rdst(n), sdst(1);
+    for (uint32_t b = 0; b < n; ++b) {
+        job.bufs[b].hash_dst[0] = (uint64_t)(d_hashes + job.bufs[b].chunk_begin);
+        rdst[b].d[0] = (uint64_t)(d_roots + b);
+    }
+    sdst[0].d[0] = (uint64_t)d_sroot;
+    return run_hash_job(c, job, false, {n}, rdst, sdst, true);
+}
+
 }  // namespace
 }  // namespace pcs
 
@@ -956,60 +1086,7 @@ int pcs_checkpoint_batch(pcs_ctx *c, const pcs_buf *plans, const uint32_t *nbufs
 
 int pcs_restore_batch(pcs_ctx *c, const pcs_snap *snaps, uint32_t m, const pcs_buf *dsts, const uint32_t *nbufs)
 {
-    if (!c) return PCS_E_INVAL;
-    if (m && (!snaps || !nbufs)) return fail(c, PCS_E_INVAL, "null argument");
-    Job job;
-    uint64_t nb_total = 0;
-    std::vector<std::shared_ptr<SnapNode>> nodes;
-    for (uint32_t j = 0; j < m; ++j) {
-        auto nd = lookup(c, snaps[j]);
-        if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snaps[j]);
-        if (nbufs[j] != nd->nbufs)
-            return fail(c, PCS_E_SHAPE, "snapshot %u holds %u buffers, %u destinations given", j, nd->nbufs, nbufs[j]);
-        nodes.push_back(nd);
-        nb_total += nbufs[j];
-    }
-    if (nb_total && !dsts) return fail(c, PCS_E_INVAL, "null destinations");
-    if (nb_total > (1u << 24)) return fail(c, PCS_E_INVAL, "too many buffers");
-    if (int st = add_buffers(c, job, dsts, (uint32_t)nb_total, 0)) return st;
-    uint32_t b = 0;
-    for (uint32_t j = 0; j < m; ++j) {
-        const auto &nd = nodes[j];
-        for (uint32_t k = 0; k < nd->nbufs; ++k, ++b) {
-            const Layout &want = nd->bufs[k], &got = job.lays[b];
-            if (want.kind != got.kind || want.nbytes != got.nbytes ||
-                (want.kind == PCS_RING && (want.row_bytes != got.row_bytes || want.window != got.window ||
-                                           want.outer != got.outer)))
-                return fail(c, PCS_E_SHAPE, "restore %u buffer %u: destination layout differs from the snapshot", j, k);
-            JobBuf &jb = job.bufs[b];
-            if (nd->incremental)
-                jb.manifest = c->arena_dev + nd->manifest_off + 8 * nd->chunk_begin[k];
-            else
-                jb.payload = c->arena_dev + nd->payload_off + nd->comp_off[k];
-        }
-    }
-    const uint32_t n = (uint32_t)nb_total;
-    if (n == 0) return PCS_OK;
-    Carver cv;
-    uint64_t o_bufs, o_runs, o_map;
-    cv.add(&o_bufs, sizeof(JobBuf) * n);
-    cv.add(&o_runs, sizeof(Run) * job.runs.size());
-    const uint64_t hb = cv.total;
-    cv.add(&o_map, 4 * job.ngroups);
-    Temp t(c);
-    if (int st = temp_alloc(c, t, cv.total)) return st;
-    const uint64_t base = c->arena_dev + t.off;
-    std::vector<uint8_t> host(hb, 0);
-    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
-    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
-    if (int st = upload(c, base, host.data(), hb)) return st;
-    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
-    const Run *d_runs = (const Run *)(base + o_runs);
-    uint32_t *d_map = (uint32_t *)(base + o_map);
-    const uint64_t G = job.ngroups;
-    int st;
-    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
-    return launch(c, "copy", [&] { return launch_restore(d_bufs, d_runs, d_map, G, c->arena_dev, c->stream); });
+    return restore_impl(c, snaps, m, dsts, nbufs, true);
 }
 
 int pcs_restore_verify(pcs_ctx *c, pcs_snap snap, const pcs_buf *dst, uint32_t n, uint64_t *d_bad_bitmap,
@@ -1195,6 +1272,157 @@ int pcs_kernel_time(pcs_ctx *c, const char *name, uint64_t *launches, double *to
     }
     if (launches) *launches = k;
     if (total_ms) *total_ms = ms;
+    return PCS_OK;
+}
+
+int pcs_export(pcs_ctx *c, pcs_snap snap, void *h_dst, uint64_t cap, uint64_t *written)
+{
+    if (!c) return PCS_E_INVAL;
+    auto nd = lookup(c, snap);
+    if (!nd) return fail(c, PCS_E_HANDLE, "unknown handle %llu", (unsigned long long)snap);
+    if (!nd->settled) settle(c, true);
+    const uint32_t n = nd->nbufs;
+    const uint64_t T = nd->total_chunks;
+    const ImageLayout L = image_layout(nd->bufs, T);
+    if (written) *written = L.size;
+    if (!h_dst) return PCS_OK;
+    if (cap < L.size) return fail(c, PCS_E_INVAL, "image needs %llu bytes", (unsigned long long)L.size);
+    uint8_t *img = (uint8_t *)h_dst;
+    memset(img, 0, L.data_off);
+    memcpy(img, kImageMagic, 8);
+    put32(img + 8, 1);
+    put32(img + 12, n);
+    put64(img + 16, T);
+    put64(img + 24, nd->state_bytes);
+    put64(img + 32, L.payload);
+    for (uint32_t b = 0; b < n; ++b) {
+        uint8_t *d = img + kImageHead + kImageDesc * b;
+        const Layout &y = nd->bufs[b];
+        put32(d, y.kind);
+        put64(d + 8, y.nbytes);
+        put64(d + 16, y.kind == PCS_RING ? y.row_bytes : 0);
+        put64(d + 24, y.kind == PCS_RING ? y.window : 0);
+        put64(d + 32, y.kind == PCS_RING ? y.outer : 0);
+    }
+    hipStream_t s = c->stream;
+    // Canonical payload: a full snapshot already is one; an incremental one is
+    // laid out flat through its manifest into scratch first.
+    Temp t(c);
+    uint64_t payload_dev = c->arena_dev + nd->payload_off;
+    if (nd->incremental && L.payload) {
+        if (int st = temp_alloc(c, t, L.payload)) return st;
+        payload_dev = c->arena_dev + t.off;
+        HIP_TRY(c, hipMemsetAsync((void *)payload_dev, 0, L.payload, s));
+        std::vector<pcs_buf> flat(n);
+        for (uint32_t b = 0; b < n; ++b) {
+            memset(&flat[b], 0, sizeof(pcs_buf));
+            flat[b].ptr = payload_dev + L.comp_off[b];
+            flat[b].nbytes = nd->bufs[b].nbytes;
+            flat[b].kind = PCS_FLAT;
+        }
+        if (int st = restore_impl(c, &snap, 1, flat.data(), &n, false)) return st;
+    }
+    // Fingerprints: stored ones, or computed from the payload.
+    Temp th(c);
+    uint64_t hashes_dev = c->arena_dev + nd->hashes_off, roots_dev = c->arena_dev + nd->roots_off;
+    if (!nd->has_hashes) {
+        if (int st = temp_alloc(c, th, 8 * T + 8 * (n + 1))) return st;
+        hashes_dev = c->arena_dev + th.off;
+        roots_dev = hashes_dev + 8 * T;
+        std::vector<uint64_t> addr(n), nb(n);
+        for (uint32_t b = 0; b < n; ++b) {
+            addr[b] = payload_dev + L.comp_off[b];
+            nb[b] = nd->bufs[b].nbytes;
+        }
+        if (int st = fingerprint_regions(c, addr, nb, (uint64_t *)hashes_dev, (uint64_t *)roots_dev,
+                                         (uint64_t *)(roots_dev + 8 * n)))
+            return st;
+    }
+    HIP_TRY(c, hipMemcpyAsync(img + L.roots_off, (void *)roots_dev, 8 * (n + 1), hipMemcpyDeviceToHost, s));
+    if (T) HIP_TRY(c, hipMemcpyAsync(img + L.hashes_off, (void *)hashes_dev, 8 * T, hipMemcpyDeviceToHost, s));
+    if (L.payload)
+        HIP_TRY(c, hipMemcpyAsync(img + L.data_off, (void *)payload_dev, L.payload, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipStreamSynchronize(s));
+    return PCS_OK;
+}
+
+int pcs_import(pcs_ctx *c, const void *h_src, uint64_t size, pcs_snap *out)
+{
+    if (!c) return PCS_E_INVAL;
+    if (!out || !h_src) return fail(c, PCS_E_INVAL, "null argument");
+    const uint8_t *img = (const uint8_t *)h_src;
+    if (size < kImageHead || memcmp(img, kImageMagic, 8) != 0) return fail(c, PCS_E_CORRUPT, "not a snapshot image");
+    if (get32(img + 8) != 1) return fail(c, PCS_E_CORRUPT, "unknown image version %u", get32(img + 8));
+    const uint32_t n = get32(img + 12);
+    const uint64_t T = get64(img + 16), state = get64(img + 24), payload = get64(img + 32);
+    if (n > (1u << 24) || size < kImageHead + kImageDesc * (uint64_t)n)
+        return fail(c, PCS_E_CORRUPT, "truncated image header");
+    std::vector<Layout> lays(n);
+    uint64_t sum_chunks = 0, sum_bytes = 0;
+    for (uint32_t b = 0; b < n; ++b) {
+        const uint8_t *d = img + kImageHead + kImageDesc * b;
+        Layout y{};
+        y.kind = get32(d);
+        y.nbytes = get64(d + 8);
+        y.row_bytes = get64(d + 16);
+        y.window = get64(d + 24);
+        y.outer = get64(d + 32);
+        if (y.kind != PCS_FLAT && y.kind != PCS_RING) return fail(c, PCS_E_CORRUPT, "buffer %u: bad kind", b);
+        y.nchunks = div_up(y.nbytes, kChunk);
+        y.ngroups = div_up(y.nchunks, kGroupChunks);
+        sum_chunks += y.nchunks;
+        sum_bytes += y.nbytes;
+        lays[b] = y;
+    }
+    const ImageLayout L = image_layout(lays, sum_chunks);
+    if (sum_chunks != T || sum_bytes != state || L.payload != payload || L.size != size)
+        return fail(c, PCS_E_CORRUPT, "image header is inconsistent with its size");
+
+    // A full snapshot with fingerprints, filled from the image.
+    Job job;
+    job.lays = lays;
+    uint64_t cb = 0;
+    for (auto &y : lays) {
+        JobBuf jb{};
+        jb.nbytes = y.nbytes;
+        jb.nchunks = y.nchunks;
+        jb.chunk_begin = cb;
+        cb += y.nchunks;
+        job.bufs.push_back(jb);
+    }
+    const FullPlan fp = full_plan(job, 0, n, T, true);
+    uint64_t boff;
+    if (!alloc_block(c, fp.block, &boff))
+        return fail(c, PCS_E_NOMEM, "arena cannot hold the imported snapshot (%llu bytes)", (unsigned long long)fp.block);
+    auto node = make_node(c, job, 0, n, fp, boff, true);
+    hipStream_t s = c->stream;
+    HIP_TRY(c, hipMemcpyAsync((void *)(c->arena_dev + node->roots_off), img + L.roots_off, 8 * (n + 1),
+                              hipMemcpyHostToDevice, s));
+    if (T) HIP_TRY(c, hipMemcpyAsync((void *)(c->arena_dev + node->hashes_off), img + L.hashes_off, 8 * T,
+                                     hipMemcpyHostToDevice, s));
+    if (payload) HIP_TRY(c, hipMemcpyAsync((void *)(c->arena_dev + node->payload_off), img + L.data_off, payload,
+                                           hipMemcpyHostToDevice, s));
+    // Verify: fingerprint the imported payload and compare with the image.
+    Temp t(c);
+    if (int st = temp_alloc(c, t, 8 * T + 8 * (n + 1))) return st;
+    const uint64_t h_dev = c->arena_dev + t.off, r_dev = h_dev + 8 * T;
+    std::vector<uint64_t> addr(n), nb(n);
+    for (uint32_t b = 0; b < n; ++b) {
+        addr[b] = c->arena_dev + node->payload_off + node->comp_off[b];
+        nb[b] = lays[b].nbytes;
+    }
+    if (int st = fingerprint_regions(c, addr, nb, (uint64_t *)h_dev, (uint64_t *)r_dev, (uint64_t *)(r_dev + 8 * n)))
+        return st;
+    std::vector<uint64_t> got(T + n + 1);
+    HIP_TRY(c, hipMemcpyAsync(got.data(), (void *)h_dev, 8 * (T + n + 1), hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipStreamSynchronize(s));
+    for (uint64_t i = 0; i < T; ++i)
+        if (got[i] != get64(img + L.hashes_off + 8 * i))
+            return fail(c, PCS_E_CORRUPT, "chunk %llu does not match its fingerprint", (unsigned long long)i);
+    for (uint32_t b = 0; b <= n; ++b)
+        if (got[T + b] != get64(img + L.roots_off + 8 * b))
+            return fail(c, PCS_E_CORRUPT, "root %u does not match", b);
+    *out = new_handle(c, node);
     return PCS_OK;
 }
 

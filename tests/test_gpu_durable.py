@@ -1,0 +1,159 @@
+"""Durable snapshots across a process boundary (I2 in its strong form, the
+paper's checkpoint-then-die protocol of Sec. 7.2): export to a host image,
+import in another context or process, restore byte-identically; a corrupted
+image is refused.  Images are compared byte for byte with the oracle's
+writer of the same format."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from tests.gpu_util import arena, dev, host, log
+
+pytestmark = pytest.mark.gpu
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def pcs():
+    import paper_2607_21686_amd as P
+    return P
+
+
+def state(seed=5):
+    """A Markovian-style state plus a small wrapped KV ring (seeded)."""
+    c = W.config1(seed)
+    g = W.Ring(4, 48, 2048, 40, 45)
+    ring = W.host_kv_ring(g, seed)
+    return c.obs.reshape(-1), c.rng_state, g, ring
+
+
+def plan_of(pcs, obs_t, rng_t, ring_t, g):
+    return [pcs.flat(obs_t), pcs.flat(rng_t), pcs.ring(ring_t, g.outer, g.capacity, g.row_bytes, g.head, g.window)]
+
+
+def test_export_matches_oracle_image_and_imports(pcs):
+    obs, rs, g, ring = state()
+    logical = [obs, rs, oracle.ring_window(ring, g.outer, g.outer_stride, g.capacity, g.row_bytes, g.head, g.window)]
+    layouts = [(0, 0, 0, 0), (0, 0, 0, 0), (1, g.row_bytes, g.window, g.outer)]
+    want = np.frombuffer(oracle.export_image(logical, layouts), dtype=np.uint8)
+    ctx = pcs.Context(arena(64 << 20))
+    d = [dev(obs), dev(rs), dev(ring)]
+    for hashed in (True, False):
+        log("export, hash =", hashed)
+        s = ctx.checkpoint(plan_of(pcs, d[0], d[1], d[2], g), hash=hashed)
+        img = ctx.export(s)
+        assert np.array_equal(img, want)
+        ctx.delete(s)
+    before = ctx.arena_stats()
+    s2 = ctx.import_image(want)
+    info = ctx.info(s2)
+    assert info["state_bytes"] == sum(b.size for b in logical) and info["has_hashes"] == 1
+    outs = [torch.empty_like(d[0]), torch.empty_like(d[1]), dev(np.zeros(g.ring_bytes, dtype=np.uint8))]
+    ctx.restore(s2, [pcs.flat(outs[0]), pcs.flat(outs[1]),
+                     pcs.ring(outs[2], g.outer, g.capacity, g.row_bytes, 7, g.window)])
+    assert np.array_equal(host(outs[0]), obs) and np.array_equal(host(outs[1]), rs)
+    assert np.array_equal(oracle.ring_window(host(outs[2]), g.outer, g.outer_stride, g.capacity, g.row_bytes, 7,
+                                             g.window), logical[2])
+    ctx.delete(s2)
+    assert ctx.arena_stats() == before
+    ctx.close()
+
+
+def test_export_of_incremental_chain(pcs):
+    bank = W.config2(1, capacity=48, latent_shape=(4, 15, 26), pose_dim=7, step_entries=8)
+    lat, pos = dev(bank.latents), dev(bank.poses)
+    ctx = pcs.Context(arena(32 << 20))
+    parent = 0
+    for j in range(1, 6):
+        e = 8 * j
+        parent = ctx.checkpoint([pcs.flat(lat, e * bank.latent_entry_bytes), pcs.flat(pos, e * bank.pose_entry_bytes)],
+                                parent=parent, hash=parent == 0)
+    log("export of an incremental snapshot")
+    img = ctx.export(parent)
+    want = np.frombuffer(oracle.export_image(bank.prefix(40)), dtype=np.uint8)
+    assert np.array_equal(img, want)
+    ctx.close()
+
+
+def test_import_refuses_corruption(pcs):
+    obs, rs, g, ring = state(6)
+    logical = [obs, rs]
+    img = np.frombuffer(oracle.export_image(logical), dtype=np.uint8).copy()
+    ctx = pcs.Context(arena(16 << 20))
+    before = ctx.arena_stats()
+    data_off = len(img) - oracle.pack(logical).size
+    cases = {
+        "payload byte": lambda a: a.__setitem__(data_off + 1000, a[data_off + 1000] ^ 1),
+        "rng byte": lambda a: a.__setitem__(data_off + 196608 + 3, a[data_off + 196608 + 3] ^ 0x80),
+        "fingerprint": lambda a: a.__setitem__(48 + 96 + 24 + 5, a[48 + 96 + 24 + 5] ^ 1),
+        "root": lambda a: a.__setitem__(48 + 96 + 8, a[48 + 96 + 8] ^ 1),
+        "magic": lambda a: a.__setitem__(0, 0),
+        "size field": lambda a: a.__setitem__(24, a[24] ^ 1),
+    }
+    for name, mutate in cases.items():
+        log("import of a corrupted image:", name)
+        bad = img.copy()
+        mutate(bad)
+        with pytest.raises(pcs.PcsError) as e:
+            ctx.import_image(bad)
+        assert e.value.code == pcs.E_CORRUPT, name
+        assert ctx.arena_stats() == before, name
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.import_image(img[:-1])
+    assert e.value.code == pcs.E_CORRUPT
+    s = ctx.import_image(img)      # the intact image still imports
+    ctx.delete(s)
+    ctx.close()
+
+
+CHILD = r"""
+import os, sys
+sys.path.insert(0, {root!r})
+import numpy as np, torch
+import paper_2607_21686_amd as P
+from tests.test_gpu_durable import state
+obs, rs, g, ring = state(7)
+d = [torch.from_numpy(x.copy()).cuda() for x in (obs, rs, ring)]
+ctx = P.Context(torch.empty(64 << 20, dtype=torch.uint8, device="cuda"))
+s = ctx.checkpoint([P.flat(d[0]), P.flat(d[1]), P.ring(d[2], g.outer, g.capacity, g.row_bytes, g.head, g.window)],
+                   hash=True)
+img = ctx.export(s)
+with open({path!r}, "wb") as f:
+    f.write(img.tobytes())
+    f.flush()
+    os.fsync(f.fileno())
+print("exported", img.size, flush=True)
+os._exit(0)   # the process dies without any cleanup
+"""
+
+
+def test_checkpoint_then_die_then_resume(pcs, tmp_path):
+    path = str(tmp_path / "session.pcs")
+    log("child process: checkpoint, export, die")
+    r = subprocess.run([sys.executable, "-c", CHILD.format(root=ROOT, path=path)], cwd=ROOT, capture_output=True,
+                       text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert "exported" in r.stdout
+    img = np.fromfile(path, dtype=np.uint8)
+    obs, rs, g, ring = state(7)
+    logical = [obs, rs, oracle.ring_window(ring, g.outer, g.outer_stride, g.capacity, g.row_bytes, g.head, g.window)]
+    assert np.array_equal(img, np.frombuffer(oracle.export_image(logical, [(0, 0, 0, 0), (0, 0, 0, 0),
+                                                                           (1, g.row_bytes, g.window, g.outer)]),
+                                             dtype=np.uint8))
+    log("this process: import, restore at a new head")
+    ctx = pcs.Context(arena(64 << 20))
+    s = ctx.import_image(img)
+    outs = [torch.empty(obs.size, dtype=torch.uint8, device="cuda"), torch.empty(16, dtype=torch.uint8, device="cuda"),
+            dev(np.zeros(g.ring_bytes, dtype=np.uint8))]
+    ctx.restore(s, [pcs.flat(outs[0]), pcs.flat(outs[1]), pcs.ring(outs[2], g.outer, g.capacity, g.row_bytes, 3,
+                                                                    g.window)])
+    assert np.array_equal(host(outs[0]), obs) and np.array_equal(host(outs[1]), rs)
+    assert np.array_equal(oracle.ring_window(host(outs[2]), g.outer, g.outer_stride, g.capacity, g.row_bytes, 3,
+                                             g.window), logical[2])
+    ctx.close()
