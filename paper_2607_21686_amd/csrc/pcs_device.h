@@ -52,34 +52,73 @@ struct MerkleList {
     uint64_t dst[2];
 };
 
+// Where a launch finds its buffer and run tables.
+//   DevTables: in device memory (uploaded per call), with a group -> buffer
+//              map written by k_group_map; any job size.
+//   ArgTables: carried in the kernel arguments themselves (no upload, no map
+//              kernel: a workgroup finds its buffer with a short search); jobs
+//              of at most kArgBufs buffers and kArgRuns runs.
+constexpr uint32_t kArgBufs = 8, kArgRuns = 64;
+struct DevTables {
+    const JobBuf *bufs;
+    const Run *runs;
+    const uint32_t *map;
+    uint32_t nbuf;
+    uint32_t pad;
+};
+struct ArgTables {
+    uint32_t nbuf;
+    uint32_t pad;
+    JobBuf bufs[kArgBufs];
+    Run runs[kArgRuns];
+};
+// Merkle lists carried in the kernel arguments: the first nbuf_lists reduce
+// group nodes to buffer roots, the rest reduce those roots to session roots
+// (their begin/count index the buffer lists).
+struct ArgLists {
+    uint32_t nbuf_lists;
+    uint32_t nlists;
+    MerkleList lists[kArgBufs + 1];
+};
+
 // Kernel launchers (pcs_kernels.hip).  All are asynchronous on `s`.
+enum TileMode : int {
+    kModeHash = 0,    // fingerprint the buffer's runs
+    kModePack = 1,    // ... and store every chunk to its snapshot slot (checkpoint)
+    kModeDiff = 2,    // ... and mark chunks new or changed against the parent (incremental)
+    kModeVerify = 3,  // copy snapshot slots to the buffer's runs (restore), fingerprint
+                      // the restored bytes and mark chunks whose fingerprint differs
+                      // from the one stored at checkpoint time
+};
 hipError_t launch_group_map(const JobBuf *bufs, uint32_t nbuf, uint64_t ngroups, uint32_t *map,
                             hipStream_t s);
-hipError_t launch_hash(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
-                       bool copy, bool diff, uint64_t *nodes, uint32_t *dirty_count,
-                       uint64_t *dirty_mask, hipStream_t s);
-hipError_t launch_restore_verify(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
-                                 uint64_t arena_base, uint64_t *bad_bitmap, hipStream_t s);
+template <class Tab>
+hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint32_t *flag_count,
+                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s);
+template <class Tab>
+hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s);
+template <class Tab>
+hipError_t launch_compact(const Tab &tab, uint64_t ngroups, const uint64_t *dirty_mask, const uint64_t *offsets,
+                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s);
+template <class Tab>
+hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_t *total, uint64_t max_slots,
+                             uint64_t payload_top, hipStream_t s);
+template <class Tab>
+hipError_t launch_classify(const Tab &tab, uint64_t ngroups, const uint64_t *hashes, uint32_t K, uint64_t total,
+                           uint64_t *bitmap, hipStream_t s);
+template <class Tab>
+hipError_t launch_labels(const Tab &tab, const uint64_t *bitmap, uint8_t *labels, hipStream_t s);
 hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_t *in,
                          uint64_t *scratch_a, uint64_t *scratch_b, uint64_t *roots_out,
                          hipStream_t s);
-hipError_t launch_pack(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
-                       hipStream_t s);
-hipError_t launch_restore(const JobBuf *bufs, const Run *runs, const uint32_t *map,
-                          uint64_t ngroups, uint64_t arena_base, hipStream_t s);
+hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64_t *scratch_a,
+                               uint64_t *scratch_b, hipStream_t s);
 hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total,
                        hipStream_t s);
-hipError_t launch_compact(const JobBuf *bufs, const uint32_t *map, uint64_t ngroups,
-                          const uint64_t *dirty_mask, const uint64_t *offsets,
-                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s);
-hipError_t launch_pack_dirty(const JobBuf *bufs, const Run *runs, const uint64_t *list,
-                             const uint64_t *total, uint64_t max_slots, uint64_t payload_top,
-                             hipStream_t s);
+constexpr uint64_t kScanCompactMaxGroups = 4096;
+hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint32_t *counts,
+                                     const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
+                                     uint64_t *total, uint64_t *total_host, hipStream_t s);
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
-hipError_t launch_classify(const JobBuf *bufs, const uint32_t *map, uint64_t ngroups,
-                           const uint64_t *hashes, uint32_t K, uint64_t total, uint64_t *bitmap,
-                           hipStream_t s);
-hipError_t launch_labels(const JobBuf *bufs, uint32_t nbuf, const uint64_t *bitmap,
-                         uint8_t *labels, hipStream_t s);
 
 }  // namespace pcs

@@ -4,8 +4,10 @@
 //
 // Work decomposition shared by every kernel: a job is a table of buffers,
 // each cut into 4096-byte chunks, and the chunks of one buffer into aligned
-// groups of 64.  One workgroup handles one group; a group-to-buffer map
-// (k_group_map) replaces any per-block search.  Groups never straddle
+// groups of 64.  One workgroup handles one group; it finds its buffer through
+// a group-to-buffer map (k_group_map) when the tables live in device memory,
+// or by a short search when a small job carries its tables in the kernel
+// arguments (no upload and no map launch).  Groups never straddle
 // buffers, so a group's 64 chunk fingerprints reduce to one Merkle node
 // inside the workgroup (a promote-odd tree over n leaves splits into aligned
 // 64-leaf subtrees), and a group is exactly one word of the classification
@@ -239,15 +241,18 @@ __device__ __forceinline__ uint64_t sel4(uint64_t a, uint64_t b, uint64_t c, uin
     return i == 0 ? a : i == 1 ? b : i == 2 ? c : d;
 }
 
-// What a tile-kernel launch does besides fingerprinting every chunk.
-enum TileMode : int {
-    kModeHash = 0,    // fingerprint the buffer's runs
-    kModePack = 1,    // ... and store every chunk to its snapshot slot (checkpoint)
-    kModeDiff = 2,    // ... and mark chunks new or changed against the parent (incremental)
-    kModeVerify = 3,  // copy snapshot slots to the buffer's runs (restore), fingerprint
-                      // the restored bytes and mark chunks whose fingerprint differs
-                      // from the one stored at checkpoint time
-};
+// A workgroup's buffer: through the map, or by searching a table of at most
+// kArgBufs buffers (largest b with group_begin <= G; empty buffers lose ties).
+__device__ __forceinline__ uint32_t buf_index(const DevTables &t, uint64_t G) { return t.map[G]; }
+__device__ __forceinline__ uint32_t buf_index(const ArgTables &t, uint64_t G)
+{
+    uint32_t lo = 0, hi = t.nbuf;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (t.bufs[mid].group_begin <= G) lo = mid; else hi = mid;
+    }
+    return lo;
+}
 
 // Fingerprint tile kernel.  One workgroup = one 64-chunk group of one
 // buffer.  Step k moves the k-th SL-byte slice of every chunk of the group:
@@ -259,9 +264,8 @@ enum TileMode : int {
 // XXH64 accumulators 2p and 2p+1, which read exactly bytes [16p, 16p+16) of
 // each 32-byte stripe.  kModeDiff / kModeVerify ballot one flag per chunk into
 // a per-group mask (the group is one bitmap word).
-template <int MODE, int T, int SL>
-__global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs,
-                                            const uint32_t *__restrict__ map, uint64_t *__restrict__ nodes,
+template <class Tab, int MODE, int T, int SL>
+__global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
                                             uint32_t *__restrict__ flag_count, uint64_t *__restrict__ flag_mask,
                                             uint64_t arena_base)
 {
@@ -278,7 +282,8 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
     __shared__ uint32_t dflag[kGroupChunks];
 
     const uint64_t G = blockIdx.x;
-    const JobBuf &jb = bufs[map[G]];
+    const JobBuf &jb = tab.bufs[buf_index(tab, G)];
+    const Run *runs = tab.runs;
     const uint32_t t = threadIdx.x;
     const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
     const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
@@ -434,27 +439,21 @@ __global__ __launch_bounds__(T) void k_hash(const JobBuf *__restrict__ bufs, con
 
 // ---------------------------------------------------------------- Merkle lists
 
-// One workgroup per list: promote-odd Merkle root of in[begin, begin+count).
-// Aligned 64-value blocks reduce independently (one wavefront each); up to
-// two passes through global scratch bring a list to <= 4096 values, then
-// the rest happens in LDS.  Each scratch array is read only after it is
-// fully written in this launch.
-__global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ lists,
-                                                const uint64_t *__restrict__ in,
-                                                uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
-                                                uint64_t *__restrict__ roots_out)
+// Promote-odd Merkle root of src[0, m), computed by the whole workgroup
+// (256 lanes); the result is valid in thread 0.  Aligned 64-value blocks
+// reduce independently (one wavefront each); up to two passes through global
+// scratch sa/sb (each read only after it is fully written) bring the list to
+// <= 4096 values, then the rest happens in LDS.  Ends with a barrier so the
+// LDS buffers can be reused.
+__device__ uint64_t reduce_list(const uint64_t *src, uint64_t m, uint64_t *sa, uint64_t *sb, uint64_t *lds,
+                                uint64_t *lds2)
 {
-    __shared__ uint64_t lds[4096];
-    __shared__ uint64_t lds2[64];
-    const MerkleList Lst = lists[blockIdx.x];
     const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
-    uint64_t m = Lst.count;
     uint64_t root = 0;
     if (m == 0) {
         root = empty_hash();
     } else {
-        const uint64_t *src = in + Lst.begin;
-        uint64_t *scratch[2] = {sa + Lst.begin, sb + Lst.begin};
+        uint64_t *scratch[2] = {sa, sb};
         for (int k = 0; k < 2 && m > 4096; ++k) {
             const uint64_t nb = (m + 63) / 64;
             for (uint64_t blk = wave; blk < nb; blk += 4) {
@@ -487,16 +486,63 @@ __global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ l
             root = wave_merkle(v, (uint32_t)m);
         }
     }
-    if (t == 0) {
+    __syncthreads();
+    return root;
+}
+
+// One workgroup per list (device-memory list table).
+__global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ lists,
+                                                const uint64_t *__restrict__ in,
+                                                uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
+                                                uint64_t *__restrict__ roots_out)
+{
+    __shared__ uint64_t lds[4096];
+    __shared__ uint64_t lds2[64];
+    const MerkleList Lst = lists[blockIdx.x];
+    const uint64_t root = reduce_list(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
+    if (threadIdx.x == 0) {
         if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
         if (Lst.dst[1]) *(g_u64 *)Lst.dst[1] = root;
         if (roots_out) roots_out[blockIdx.x] = root;
     }
 }
 
+// One workgroup for a small job: every buffer list, then every session list
+// over the buffer roots just computed (kept in LDS).
+__global__ __launch_bounds__(256) void k_merkle_small(const ArgLists L, const uint64_t *__restrict__ in,
+                                                      uint64_t *__restrict__ sa, uint64_t *__restrict__ sb)
+{
+    __shared__ uint64_t lds[4096];
+    __shared__ uint64_t lds2[64];
+    __shared__ uint64_t roots[kArgBufs];
+    for (uint32_t j = 0; j < L.nbuf_lists; ++j) {
+        const MerkleList &Lst = L.lists[j];
+        const uint64_t root = reduce_list(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
+        if (threadIdx.x == 0) {
+            roots[j] = root;
+            if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
+            if (Lst.dst[1]) *(g_u64 *)Lst.dst[1] = root;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const uint32_t lane = threadIdx.x;
+        for (uint32_t j = L.nbuf_lists; j < L.nlists; ++j) {
+            const MerkleList &Lst = L.lists[j];
+            const uint32_t cnt = (uint32_t)Lst.count;
+            const uint64_t v = lane < cnt ? roots[Lst.begin + lane] : 0;
+            const uint64_t root = cnt ? wave_merkle(v, cnt) : empty_hash();
+            if (lane == 0) {
+                if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
+                if (Lst.dst[1]) *(g_u64 *)Lst.dst[1] = root;
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- copies
 
-// Copy tile kernel: one workgroup moves one 64-chunk group, 1 KiB of every
+// Copy tile kernel: one workgroup moves one 64-chunk group, SL bytes of every
 // chunk per step, with coalesced 16-byte loads and stores (the shape of the
 // fused kernel without the hash).
 //   PACK:    the buffer's runs -> the chunk slots of the snapshot; a partial
@@ -504,9 +550,8 @@ __global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ l
 //   !PACK:   the chunk slots (contiguous, or per chunk through a manifest of
 //            arena offsets) -> the destination buffer's runs; only logical
 //            bytes are written.
-template <bool PACK, int T, int SL>
-__global__ __launch_bounds__(T) void k_copy(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs,
-                                            const uint32_t *__restrict__ map, uint64_t arena_base)
+template <class Tab, bool PACK, int T, int SL>
+__global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
 {
     constexpr uint32_t kSteps = kChunk / SL, LPS = SL / 16;
     constexpr int U = kGroupChunks * SL / 16 / T;
@@ -514,7 +559,8 @@ __global__ __launch_bounds__(T) void k_copy(const JobBuf *__restrict__ bufs, con
     __shared__ uint64_t caddr[kGroupChunks];  // runs side: chunk start if in one run, else 0
     __shared__ uint32_t clen[kGroupChunks];
     const uint64_t G = blockIdx.x;
-    const JobBuf &jb = bufs[map[G]];
+    const JobBuf &jb = tab.bufs[buf_index(tab, G)];
+    const Run *runs = tab.runs;
     const uint32_t t = threadIdx.x;
     const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
     const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
@@ -575,12 +621,11 @@ __global__ __launch_bounds__(T) void k_copy(const JobBuf *__restrict__ bufs, con
 // ---------------------------------------------------------------- incremental
 
 // Exclusive scan of per-group dirty counts (one workgroup; Hillis-Steele
-// over 1024 per-thread partial sums).
-__global__ __launch_bounds__(1024) void k_scan(const uint32_t *__restrict__ counts, uint64_t n,
-                                               uint64_t *__restrict__ offsets,
-                                               uint64_t *__restrict__ total)
+// over 1024 per-thread partial sums).  Writes offsets[] and *total; returns
+// nothing else.  `offsets` may be LDS or global memory.
+__device__ void scan_counts(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total,
+                            uint64_t (*sums)[1024])
 {
-    __shared__ uint64_t sums[2][1024];
     const uint32_t t = threadIdx.x;
     const uint64_t per = (n + 1023) / 1024;
     const uint64_t s0 = umin(n, t * per), s1 = umin(n, s0 + per);
@@ -601,54 +646,88 @@ __global__ __launch_bounds__(1024) void k_scan(const uint32_t *__restrict__ coun
         run += counts[j];
     }
     if (t == 1023) *total = sums[cur][t];
+    __syncthreads();
 }
 
-// Assigns slots to dirty chunks in (buffer, chunk) order, lists them, and
-// writes the new snapshot's manifest: a dirty chunk points at its slot, a
-// clean one at wherever the parent holds it.  Slot s is the 4096 bytes
-// ending s*4096 below the top of the snapshot's payload reservation (slots
-// grow downwards, so the unused part of the reservation is its low end).
-__global__ __launch_bounds__(64) void k_compact(const JobBuf *__restrict__ bufs,
-                                                const uint32_t *__restrict__ map,
-                                                const uint64_t *__restrict__ dirty_mask,
-                                                const uint64_t *__restrict__ offsets,
-                                                uint64_t payload_arena_top,
-                                                uint64_t *__restrict__ list)
+__global__ __launch_bounds__(1024) void k_scan(const uint32_t *__restrict__ counts, uint64_t n,
+                                               uint64_t *__restrict__ offsets, uint64_t *__restrict__ total)
 {
-    const uint64_t G = blockIdx.x;
-    const uint32_t b = map[G];
-    const JobBuf &jb = bufs[b];
-    const uint32_t lane = threadIdx.x;
-    const uint64_t gl = G - jb.group_begin;
-    const uint64_t i = gl * kGroupChunks + lane;
-    if (i >= jb.nchunks) return;
-    const uint64_t mask = dirty_mask[G];
+    __shared__ uint64_t sums[2][1024];
+    scan_counts(counts, n, offsets, total, sums);
+}
+
+// Slot assignment for one chunk: dirty chunks get slots in (buffer, chunk)
+// order and are listed; the new manifest points a dirty chunk at its slot
+// (slot s is the 4096 bytes ending s*4096 below the top of the snapshot's
+// payload reservation: slots grow downwards, so the unused part of the
+// reservation is its low end) and a clean one at wherever the parent holds it.
+__device__ __forceinline__ void compact_chunk(const JobBuf &jb, uint32_t b, uint64_t i, uint32_t lane, uint64_t mask,
+                                              uint64_t off, uint64_t payload_arena_top, uint64_t *list)
+{
     g_u64 *man = (g_u64 *)jb.manifest;
     if ((mask >> lane) & 1) {
         const uint64_t below = lane ? (mask & ((1ULL << lane) - 1)) : 0;
-        const uint64_t slot = offsets[G] + (uint64_t)__popcll(below);
+        const uint64_t slot = off + (uint64_t)__popcll(below);
         list[slot] = ((uint64_t)b << 40) | i;
         man[i] = payload_arena_top - (slot + 1) * kChunk;
     } else {
-        man[i] = jb.parent_manifest ? ((const g_u64 *)jb.parent_manifest)[i]
-                                    : jb.parent_slot0 + i * kChunk;
+        man[i] = jb.parent_manifest ? ((const g_u64 *)jb.parent_manifest)[i] : jb.parent_slot0 + i * kChunk;
+    }
+}
+
+template <class Tab>
+__global__ __launch_bounds__(64) void k_compact(const Tab tab, const uint64_t *__restrict__ dirty_mask,
+                                                const uint64_t *__restrict__ offsets, uint64_t payload_arena_top,
+                                                uint64_t *__restrict__ list)
+{
+    const uint64_t G = blockIdx.x;
+    const uint32_t b = buf_index(tab, G);
+    const JobBuf &jb = tab.bufs[b];
+    const uint32_t lane = threadIdx.x;
+    const uint64_t i = (G - jb.group_begin) * kGroupChunks + lane;
+    if (i >= jb.nchunks) return;
+    compact_chunk(jb, b, i, lane, dirty_mask[G], offsets[G], payload_arena_top, list);
+}
+
+// Small incremental jobs: the scan and the slot assignment in one
+// workgroup (offsets in LDS), and the stored-chunk count written both to
+// device memory and to the caller's pinned host word.
+__global__ __launch_bounds__(1024) void k_scan_compact_small(const ArgTables tab, uint64_t ngroups,
+                                                             const uint32_t *__restrict__ counts,
+                                                             const uint64_t *__restrict__ dirty_mask,
+                                                             uint64_t payload_arena_top, uint64_t *__restrict__ list,
+                                                             uint64_t *__restrict__ total, uint64_t *total_host)
+{
+    __shared__ uint64_t sums[2][1024];
+    __shared__ uint64_t offs[kScanCompactMaxGroups];
+    scan_counts(counts, ngroups, offs, total, sums);
+    for (uint64_t g = threadIdx.x; g < ngroups; g += 1024) {
+        const uint32_t b = buf_index(tab, g);
+        const JobBuf &jb = tab.bufs[b];
+        const uint64_t c0 = (g - jb.group_begin) * kGroupChunks;
+        const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
+        const uint64_t mask = dirty_mask[g];
+        for (uint32_t lane = 0; lane < nv; ++lane)
+            compact_chunk(jb, b, c0 + lane, lane, mask, offs[g], payload_arena_top, list);
+    }
+    if (threadIdx.x == 1023 && total_host) {
+        *(volatile uint64_t *)total_host = *total;
+        __threadfence_system();
     }
 }
 
 // Copies listed dirty chunks into their slots (slot s ends s*4096 below
 // `payload_top`): one wavefront per slot, each lane moving 64 bytes with
 // four 16-byte loads in flight, zero-padding partial chunks.
-__global__ __launch_bounds__(256) void k_pack_dirty(const JobBuf *__restrict__ bufs,
-                                                    const Run *__restrict__ runs,
-                                                    const uint64_t *__restrict__ list,
-                                                    const uint64_t *__restrict__ total_ptr,
-                                                    uint64_t payload_top)
+template <class Tab>
+__global__ __launch_bounds__(256) void k_pack_dirty(const Tab tab, const uint64_t *__restrict__ list,
+                                                    const uint64_t *__restrict__ total_ptr, uint64_t payload_top)
 {
     const uint64_t slot = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (slot >= *total_ptr) return;
     const uint32_t lane = threadIdx.x & 63;
     const uint64_t e = list[slot];
-    const JobBuf &jb = bufs[e >> 40];
+    const JobBuf &jb = tab.bufs[e >> 40];
     const uint64_t cb = (e & ((1ULL << 40) - 1)) * kChunk;
     const uint64_t len = umin(kChunk, jb.nbytes - cb);
     const uint64_t dst = payload_top - (slot + 1) * kChunk;
@@ -658,7 +737,7 @@ __global__ __launch_bounds__(256) void k_pack_dirty(const JobBuf *__restrict__ b
         const uint32_t x = (k * 64 + lane) * 16;
         v[k] = make_uint4(0, 0, 0, 0);
         if (x < len) {
-            const uint64_t a = phys_addr(runs, jb.run_begin, jb.run_count, cb + x);
+            const uint64_t a = phys_addr(tab.runs, jb.run_begin, jb.run_count, cb + x);
             v[k] = x + 16 <= len ? load16(a) : load_partial(a, (uint32_t)(len - x));
         }
     }
@@ -681,13 +760,12 @@ __global__ __launch_bounds__(256) void k_reverse_slots(uint64_t top, uint64_t ds
 // One wavefront per bitmap word (= one 64-chunk group of one buffer): chunk
 // i differs iff its K replay fingerprints are not all equal; the wave's
 // ballot is the word.
-__global__ __launch_bounds__(64) void k_classify(const JobBuf *__restrict__ bufs,
-                                                 const uint32_t *__restrict__ map,
-                                                 const uint64_t *__restrict__ hashes, uint32_t K,
+template <class Tab>
+__global__ __launch_bounds__(64) void k_classify(const Tab tab, const uint64_t *__restrict__ hashes, uint32_t K,
                                                  uint64_t total, uint64_t *__restrict__ bitmap)
 {
     const uint64_t G = blockIdx.x;
-    const JobBuf &jb = bufs[map[G]];
+    const JobBuf &jb = tab.bufs[buf_index(tab, G)];
     const uint32_t lane = threadIdx.x;
     const uint64_t i = (G - jb.group_begin) * kGroupChunks + lane;
     bool differs = false;
@@ -700,19 +778,23 @@ __global__ __launch_bounds__(64) void k_classify(const JobBuf *__restrict__ bufs
     if (lane == 0) bitmap[G] = word;
 }
 
-__global__ void k_labels(const JobBuf *__restrict__ bufs, uint32_t nbuf,
-                         const uint64_t *__restrict__ bitmap, uint8_t *__restrict__ labels)
+// Per buffer: 1 iff any of its bitmap words is non-zero (one wavefront per
+// buffer, lanes striding over the words).
+template <class Tab>
+__global__ __launch_bounds__(64) void k_labels(const Tab tab, const uint64_t *__restrict__ bitmap,
+                                               uint8_t *__restrict__ labels)
 {
-    const uint32_t b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= nbuf) return;
-    const JobBuf &jb = bufs[b];
+    const uint32_t b = blockIdx.x;
+    const JobBuf &jb = tab.bufs[b];
     const uint64_t nw = (jb.nchunks + kGroupChunks - 1) / kGroupChunks;
     uint64_t any = 0;
-    for (uint64_t w = 0; w < nw; ++w) any |= bitmap[jb.group_begin + w];
-    labels[b] = any ? 1 : 0;
+    for (uint64_t w = threadIdx.x; w < nw; w += 64) any |= bitmap[jb.group_begin + w];
+    const bool set = __ballot(any != 0) != 0;
+    if (threadIdx.x == 0) labels[b] = set ? 1 : 0;
 }
 
-// Workgroup sizes (lanes) of the tile kernels, from measurement on MI355X.
+// Workgroup sizes (lanes) and slice bytes of the tile kernels, from
+// measurement on MI355X.
 constexpr int kPackLanes = 1024, kPackSlice = 512;
 constexpr int kHashLanes = 256, kHashSlice = 512;
 constexpr int kCopyLanes = 1024, kCopySlice = 1024;
@@ -730,31 +812,82 @@ hipError_t launch_group_map(const JobBuf *bufs, uint32_t nbuf, uint64_t ngroups,
     return hipGetLastError();
 }
 
-hipError_t launch_hash(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
-                       bool copy, bool diff, uint64_t *nodes, uint32_t *dirty_count,
-                       uint64_t *dirty_mask, hipStream_t s)
+template <class Tab>
+hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint32_t *flag_count,
+                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
     const dim3 grid((uint32_t)ngroups);
-    if (copy && diff) return hipErrorInvalidValue;
-    if (copy)
-        hipLaunchKernelGGL((k_hash<kModePack, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, bufs, runs, map,
-                           nodes, dirty_count, dirty_mask, (uint64_t)0);
-    else if (diff)
-        hipLaunchKernelGGL((k_hash<kModeDiff, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map,
-                           nodes, dirty_count, dirty_mask, (uint64_t)0);
-    else
-        hipLaunchKernelGGL((k_hash<kModeHash, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, bufs, runs, map,
-                           nodes, dirty_count, dirty_mask, (uint64_t)0);
+    switch (mode) {
+    case kModeHash:
+        hipLaunchKernelGGL((k_hash<Tab, kModeHash, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, tab, nodes,
+                           flag_count, flag_mask, arena_base);
+        break;
+    case kModePack:
+        hipLaunchKernelGGL((k_hash<Tab, kModePack, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, tab, nodes,
+                           flag_count, flag_mask, arena_base);
+        break;
+    case kModeDiff:
+        hipLaunchKernelGGL((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, tab, nodes,
+                           flag_count, flag_mask, arena_base);
+        break;
+    case kModeVerify:
+        hipLaunchKernelGGL((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, tab,
+                           nodes, flag_count, flag_mask, arena_base);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_restore_verify(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
-                                 uint64_t arena_base, uint64_t *bad_bitmap, hipStream_t s)
+template <class Tab>
+hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_hash<kModeVerify, kPackLanes, kPackSlice>), dim3((uint32_t)ngroups), dim3(kPackLanes), 0, s,
-                       bufs, runs, map, (uint64_t *)nullptr, (uint32_t *)nullptr, bad_bitmap, arena_base);
+    if (pack)
+        hipLaunchKernelGGL((k_copy<Tab, true, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0,
+                           s, tab, arena_base);
+    else
+        hipLaunchKernelGGL((k_copy<Tab, false, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0,
+                           s, tab, arena_base);
+    return hipGetLastError();
+}
+
+template <class Tab>
+hipError_t launch_compact(const Tab &tab, uint64_t ngroups, const uint64_t *dirty_mask, const uint64_t *offsets,
+                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s)
+{
+    if (ngroups == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_compact<Tab>), dim3((uint32_t)ngroups), dim3(64), 0, s, tab, dirty_mask, offsets,
+                       payload_arena_top, list);
+    return hipGetLastError();
+}
+
+template <class Tab>
+hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_t *total, uint64_t max_slots,
+                             uint64_t payload_top, hipStream_t s)
+{
+    if (max_slots == 0) return hipSuccess;
+    const uint32_t blocks = (uint32_t)((max_slots + 3) / 4);
+    hipLaunchKernelGGL((k_pack_dirty<Tab>), dim3(blocks), dim3(256), 0, s, tab, list, total, payload_top);
+    return hipGetLastError();
+}
+
+template <class Tab>
+hipError_t launch_classify(const Tab &tab, uint64_t ngroups, const uint64_t *hashes, uint32_t K, uint64_t total,
+                           uint64_t *bitmap, hipStream_t s)
+{
+    if (ngroups == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_classify<Tab>), dim3((uint32_t)ngroups), dim3(64), 0, s, tab, hashes, K, total, bitmap);
+    return hipGetLastError();
+}
+
+template <class Tab>
+hipError_t launch_labels(const Tab &tab, const uint64_t *bitmap, uint8_t *labels, hipStream_t s)
+{
+    if (tab.nbuf == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_labels<Tab>), dim3(tab.nbuf), dim3(64), 0, s, tab, bitmap, labels);
     return hipGetLastError();
 }
 
@@ -767,21 +900,11 @@ hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_
     return hipGetLastError();
 }
 
-hipError_t launch_pack(const JobBuf *bufs, const Run *runs, const uint32_t *map, uint64_t ngroups,
-                       hipStream_t s)
+hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64_t *scratch_a,
+                               uint64_t *scratch_b, hipStream_t s)
 {
-    if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_copy<true, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs, map,
-                       (uint64_t)0);
-    return hipGetLastError();
-}
-
-hipError_t launch_restore(const JobBuf *bufs, const Run *runs, const uint32_t *map,
-                          uint64_t ngroups, uint64_t arena_base, hipStream_t s)
-{
-    if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_copy<false, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0, s, bufs, runs,
-                       map, arena_base);
+    if (lists.nlists == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_merkle_small, dim3(1), dim3(256), 0, s, lists, in, scratch_a, scratch_b);
     return hipGetLastError();
 }
 
@@ -792,23 +915,13 @@ hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, ui
     return hipGetLastError();
 }
 
-hipError_t launch_compact(const JobBuf *bufs, const uint32_t *map, uint64_t ngroups,
-                          const uint64_t *dirty_mask, const uint64_t *offsets,
-                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s)
+hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint32_t *counts,
+                                     const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
+                                     uint64_t *total, uint64_t *total_host, hipStream_t s)
 {
-    if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_compact, dim3((uint32_t)ngroups), dim3(64), 0, s, bufs, map, dirty_mask, offsets,
-                       payload_arena_top, list);
-    return hipGetLastError();
-}
-
-hipError_t launch_pack_dirty(const JobBuf *bufs, const Run *runs, const uint64_t *list,
-                             const uint64_t *total, uint64_t max_slots, uint64_t payload_top,
-                             hipStream_t s)
-{
-    if (max_slots == 0) return hipSuccess;
-    const uint32_t blocks = (uint32_t)((max_slots + 3) / 4);
-    hipLaunchKernelGGL(k_pack_dirty, dim3(blocks), dim3(256), 0, s, bufs, runs, list, total, payload_top);
+    if (ngroups > kScanCompactMaxGroups) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_scan_compact_small, dim3(1), dim3(1024), 0, s, tab, ngroups, counts, dirty_mask,
+                       payload_arena_top, list, total, total_host);
     return hipGetLastError();
 }
 
@@ -819,21 +932,19 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
     return hipGetLastError();
 }
 
-hipError_t launch_classify(const JobBuf *bufs, const uint32_t *map, uint64_t ngroups,
-                           const uint64_t *hashes, uint32_t K, uint64_t total, uint64_t *bitmap,
-                           hipStream_t s)
-{
-    if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_classify, dim3((uint32_t)ngroups), dim3(64), 0, s, bufs, map, hashes, K, total, bitmap);
-    return hipGetLastError();
-}
-
-hipError_t launch_labels(const JobBuf *bufs, uint32_t nbuf, const uint64_t *bitmap,
-                         uint8_t *labels, hipStream_t s)
-{
-    if (nbuf == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_labels, dim3((nbuf + 255) / 256), dim3(256), 0, s, bufs, nbuf, bitmap, labels);
-    return hipGetLastError();
-}
+#define PCS_INSTANTIATE(Tab)                                                                                        \
+    template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint32_t *, uint64_t *, uint64_t, \
+                                         hipStream_t);                                                            \
+    template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t);                     \
+    template hipError_t launch_compact<Tab>(const Tab &, uint64_t, const uint64_t *, const uint64_t *, uint64_t,   \
+                                            uint64_t *, hipStream_t);                                             \
+    template hipError_t launch_pack_dirty<Tab>(const Tab &, const uint64_t *, const uint64_t *, uint64_t,         \
+                                               uint64_t, hipStream_t);                                            \
+    template hipError_t launch_classify<Tab>(const Tab &, uint64_t, const uint64_t *, uint32_t, uint64_t,         \
+                                             uint64_t *, hipStream_t);                                            \
+    template hipError_t launch_labels<Tab>(const Tab &, const uint64_t *, uint8_t *, hipStream_t);
+PCS_INSTANTIATE(DevTables)
+PCS_INSTANTIATE(ArgTables)
+#undef PCS_INSTANTIATE
 
 }  // namespace pcs

@@ -134,6 +134,7 @@ struct pcs_ctx {
     uint32_t next_slot = 0;
 
     uint64_t *counts = nullptr;              // pinned, one per pending incremental snapshot
+    uint64_t *counts_dev = nullptr;          // the same words as the device addresses them
     std::vector<uint32_t> free_counts;
     std::vector<std::weak_ptr<pcs::SnapNode>> pending;
 
@@ -445,12 +446,113 @@ struct RootDst {
     uint64_t d[2];
 };
 
+bool is_small(const Job &job) { return job.bufs.size() <= kArgBufs && job.runs.size() <= kArgRuns; }
+
+// The descriptor tables of a job as the kernels see them: in the kernel
+// arguments for a small job, else uploaded into per-call scratch with a
+// group -> buffer map.
+struct Staged {
+    bool small = false;
+    ArgTables arg;
+    DevTables dev;
+};
+
+// Lays out per-call scratch as [tables (big jobs)][extra host bytes] (one
+// upload) then [group map (big jobs)][dev_bytes of device-only scratch],
+// uploads, and launches the group map for a big job.
+int stage(pcs_ctx *c, const Job &job, bool small, Temp &t, const std::vector<uint8_t> &extra, uint64_t dev_bytes,
+          Staged &sg, uint64_t &extra_dev, uint64_t &scratch_dev)
+{
+    const uint32_t n = (uint32_t)job.bufs.size();
+    const uint64_t G = job.ngroups;
+    Carver cv;
+    uint64_t o_bufs = 0, o_runs = 0, o_extra = 0, o_map = 0, o_scr = 0;
+    if (!small) {
+        cv.add(&o_bufs, sizeof(JobBuf) * n);
+        cv.add(&o_runs, sizeof(Run) * job.runs.size());
+    }
+    if (!extra.empty()) cv.add(&o_extra, extra.size());
+    const uint64_t hb = cv.total;
+    if (!small) cv.add(&o_map, 4 * G);
+    cv.add(&o_scr, dev_bytes);
+    if (int e = temp_alloc(c, t, cv.total)) return e;
+    const uint64_t base = c->arena_dev + t.off;
+    extra_dev = base + o_extra;
+    scratch_dev = base + o_scr;
+    sg.small = small;
+    if (small) {
+        memset(&sg.arg, 0, sizeof sg.arg);
+        sg.arg.nbuf = n;
+        if (n) memcpy(sg.arg.bufs, job.bufs.data(), sizeof(JobBuf) * n);
+        if (!job.runs.empty()) memcpy(sg.arg.runs, job.runs.data(), sizeof(Run) * job.runs.size());
+    } else {
+        sg.dev = DevTables{(const JobBuf *)(base + o_bufs), (const Run *)(base + o_runs),
+                           (const uint32_t *)(base + o_map), n, 0};
+    }
+    if (hb) {
+        std::vector<uint8_t> host(hb, 0);
+        if (!small) {
+            if (n) memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+            if (!job.runs.empty()) memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+        }
+        if (!extra.empty()) memcpy(host.data() + o_extra, extra.data(), extra.size());
+        if (int e = upload(c, base, host.data(), hb)) return e;
+    }
+    if (!small && G)
+        return launch(c, "map", [&] {
+            return launch_group_map(sg.dev.bufs, n, G, (uint32_t *)sg.dev.map, c->stream);
+        });
+    return PCS_OK;
+}
+
+template <class F>
+int with_tables(const Staged &sg, F &&f)
+{
+    return sg.small ? f(sg.arg) : f(sg.dev);
+}
+
+std::vector<uint8_t> bytes_of(const std::vector<MerkleList> &lists)
+{
+    std::vector<uint8_t> v(sizeof(MerkleList) * lists.size());
+    if (!lists.empty()) memcpy(v.data(), lists.data(), v.size());
+    return v;
+}
+
+ArgLists arg_lists(const std::vector<MerkleList> &lists, uint32_t nbuf_lists)
+{
+    ArgLists al;
+    memset(&al, 0, sizeof al);
+    al.nbuf_lists = nbuf_lists;
+    al.nlists = (uint32_t)lists.size();
+    for (size_t j = 0; j < lists.size(); ++j) al.lists[j] = lists[j];
+    return al;
+}
+
+// Buffer roots then session roots: one single-workgroup launch for a small
+// job, else one workgroup per list in two launches.
+int run_merkle(pcs_ctx *c, bool small, const std::vector<MerkleList> &lists, uint32_t nbuf_lists,
+               uint64_t lists_dev, uint64_t *d_nodes, uint64_t *d_sa, uint64_t *d_sb, uint64_t *d_roots)
+{
+    hipStream_t s = c->stream;
+    if (small) {
+        const ArgLists al = arg_lists(lists, nbuf_lists);
+        return launch(c, "merkle", [&] { return launch_merkle_small(al, d_nodes, d_sa, d_sb, s); });
+    }
+    const MerkleList *d_lists = (const MerkleList *)lists_dev;
+    const uint32_t nsess = (uint32_t)lists.size() - nbuf_lists;
+    if (int st = launch(c, "merkle", [&] { return launch_merkle(d_lists, nbuf_lists, d_nodes, d_sa, d_sb, d_roots, s); }))
+        return st;
+    return launch(c, "merkle", [&] { return launch_merkle(d_lists + nbuf_lists, nsess, d_roots, d_sa, d_sb, nullptr, s); });
+}
+
 int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &sess_nbufs,
                  const std::vector<RootDst> &root_dst, const std::vector<RootDst> &sroot_dst,
                  bool want_roots)
 {
     const uint32_t n = (uint32_t)job.bufs.size();
     const uint32_t S = (uint32_t)sess_nbufs.size();
+    const uint64_t G = job.ngroups;
+    const bool small = is_small(job) && S <= 1;
     std::vector<MerkleList> lists;
     if (want_roots) {
         for (uint32_t b = 0; b < n; ++b)
@@ -462,51 +564,27 @@ int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &s
         }
     }
     Carver cv;
-    uint64_t o_bufs, o_runs, o_lists, o_map, o_nodes, o_sa, o_sb, o_roots;
-    const uint64_t G = job.ngroups;
-    cv.add(&o_bufs, sizeof(JobBuf) * n);
-    cv.add(&o_runs, sizeof(Run) * job.runs.size());
-    cv.add(&o_lists, sizeof(MerkleList) * lists.size());
-    const uint64_t host_bytes = cv.total;
-    cv.add(&o_map, 4 * G);
+    uint64_t o_nodes, o_sa, o_sb, o_roots;
     cv.add(&o_nodes, 8 * G);
     cv.add(&o_sa, 8 * std::max<uint64_t>(G, n));
     cv.add(&o_sb, 8 * std::max<uint64_t>(G, n));
     cv.add(&o_roots, 8 * n);
     Temp t(c);
-    if (int st = temp_alloc(c, t, cv.total)) return st;
-    const uint64_t base = c->arena_dev + t.off;
-
-    std::vector<uint8_t> host(host_bytes, 0);
-    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
-    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
-    if (!lists.empty()) memcpy(host.data() + o_lists, lists.data(), sizeof(MerkleList) * lists.size());
-    if (int st = upload(c, base, host.data(), host_bytes)) return st;
-
-    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
-    const Run *d_runs = (const Run *)(base + o_runs);
-    const MerkleList *d_lists = (const MerkleList *)(base + o_lists);
-    uint32_t *d_map = (uint32_t *)(base + o_map);
-    uint64_t *d_nodes = (uint64_t *)(base + o_nodes);
-    uint64_t *d_sa = (uint64_t *)(base + o_sa), *d_sb = (uint64_t *)(base + o_sb);
-    uint64_t *d_roots = (uint64_t *)(base + o_roots);
-    hipStream_t s = c->stream;
-
-    int st;
-    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, s); }))) return st;
-    if ((st = launch(c, copy ? "pack_hash" : "hash", [&] {
-             return launch_hash(d_bufs, d_runs, d_map, G, copy, false, d_nodes, nullptr, nullptr, s);
-         })))
+    Staged sg;
+    uint64_t lists_dev, scr;
+    if (int st = stage(c, job, small, t, small ? std::vector<uint8_t>() : bytes_of(lists), cv.total, sg, lists_dev, scr))
         return st;
-    if (want_roots) {
-        if ((st = launch(c, "merkle", [&] { return launch_merkle(d_lists, n, d_nodes, d_sa, d_sb, d_roots, s); })))
-            return st;
-        if ((st = launch(c, "merkle", [&] {
-                 return launch_merkle(d_lists + n, S, d_roots, d_sa, d_sb, nullptr, s);
-             })))
-            return st;
-    }
-    return PCS_OK;
+    uint64_t *d_nodes = (uint64_t *)(scr + o_nodes);
+    uint64_t *d_sa = (uint64_t *)(scr + o_sa), *d_sb = (uint64_t *)(scr + o_sb);
+    uint64_t *d_roots = (uint64_t *)(scr + o_roots);
+    hipStream_t s = c->stream;
+    int st = with_tables(sg, [&](const auto &tab) {
+        return launch(c, copy ? "pack_hash" : "hash", [&] {
+            return launch_tile(tab, G, copy ? kModePack : kModeHash, d_nodes, nullptr, nullptr, 0, s);
+        });
+    });
+    if (st || !want_roots) return st;
+    return run_merkle(c, small, lists, n, lists_dev, d_nodes, d_sa, d_sb, d_roots);
 }
 
 struct FullPlan {
@@ -621,28 +699,15 @@ int checkpoint_full(pcs_ctx *c, const pcs_buf *plans, const uint32_t *nbufs, uin
         std::vector<uint32_t> sn(nbufs, nbufs + sessions);
         st = run_hash_job(c, job, true, sn, rdst, sdst, true);
     } else {
-        Carver cv;
-        uint64_t o_bufs, o_runs, o_map;
-        cv.add(&o_bufs, sizeof(JobBuf) * job.bufs.size());
-        cv.add(&o_runs, sizeof(Run) * job.runs.size());
-        const uint64_t hb = cv.total;
-        cv.add(&o_map, 4 * job.ngroups);
         Temp t(c);
-        st = temp_alloc(c, t, cv.total);
-        if (!st) {
-            const uint64_t base = c->arena_dev + t.off;
-            std::vector<uint8_t> host(hb, 0);
-            memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * job.bufs.size());
-            memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
-            st = upload(c, base, host.data(), hb);
-            const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
-            const Run *d_runs = (const Run *)(base + o_runs);
-            uint32_t *d_map = (uint32_t *)(base + o_map);
-            const uint32_t n = (uint32_t)job.bufs.size();
-            const uint64_t G = job.ngroups;
-            if (!st) st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); });
-            if (!st) st = launch(c, "pack", [&] { return launch_pack(d_bufs, d_runs, d_map, G, c->stream); });
-        }
+        Staged sg;
+        uint64_t xd, scr;
+        st = stage(c, job, is_small(job), t, {}, 0, sg, xd, scr);
+        const uint64_t G = job.ngroups;
+        if (!st)
+            st = with_tables(sg, [&](const auto &tab) {
+                return launch(c, "pack", [&] { return launch_copy(tab, G, true, 0, c->stream); });
+            });
     }
     if (st) return st;  // nodes (and their blocks) are released here
     for (uint32_t s = 0; s < sessions; ++s) out[s] = new_handle(c, nodes[s]);
@@ -690,26 +755,14 @@ int restore_impl(pcs_ctx *c, const pcs_snap *snaps, uint32_t m, const pcs_buf *d
     }
     const uint32_t n = (uint32_t)nb_total;
     if (n == 0) return PCS_OK;
-    Carver cv;
-    uint64_t o_bufs, o_runs, o_map;
-    cv.add(&o_bufs, sizeof(JobBuf) * n);
-    cv.add(&o_runs, sizeof(Run) * job.runs.size());
-    const uint64_t hb = cv.total;
-    cv.add(&o_map, 4 * job.ngroups);
     Temp t(c);
-    if (int st = temp_alloc(c, t, cv.total)) return st;
-    const uint64_t base = c->arena_dev + t.off;
-    std::vector<uint8_t> host(hb, 0);
-    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
-    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
-    if (int st = upload(c, base, host.data(), hb)) return st;
-    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
-    const Run *d_runs = (const Run *)(base + o_runs);
-    uint32_t *d_map = (uint32_t *)(base + o_map);
+    Staged sg;
+    uint64_t xd, scr;
+    if (int st = stage(c, job, is_small(job), t, {}, 0, sg, xd, scr)) return st;
     const uint64_t G = job.ngroups;
-    int st;
-    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
-    return launch(c, "copy", [&] { return launch_restore(d_bufs, d_runs, d_map, G, c->arena_dev, c->stream); });
+    return with_tables(sg, [&](const auto &tab) {
+        return launch(c, "copy", [&] { return launch_copy(tab, G, false, c->arena_dev, c->stream); });
+    });
 }
 
 
@@ -804,7 +857,8 @@ int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ct
             return PCS_E_HIP;
         }
     }
-    if (hipHostMalloc((void **)&c->counts, 8 * kCountSlots, hipHostMallocDefault) != hipSuccess) {
+    if (hipHostMalloc((void **)&c->counts, 8 * kCountSlots, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
+        hipHostGetDevicePointer((void **)&c->counts_dev, c->counts, 0) != hipSuccess) {
         pcs_ctx_destroy(c);
         return PCS_E_HIP;
     }
@@ -890,25 +944,18 @@ int pcs_classify(pcs_ctx *c, const uint64_t *d_hashes, uint32_t K, const uint64_
     if (job.ngroups && !d_bitmap) return fail(c, PCS_E_INVAL, "null bitmap");
     if (n && !d_labels) return fail(c, PCS_E_INVAL, "null labels");
     if (n == 0) return PCS_OK;
-    Carver cv;
-    uint64_t o_bufs, o_map;
-    cv.add(&o_bufs, sizeof(JobBuf) * n);
-    const uint64_t hb = cv.total;
-    cv.add(&o_map, 4 * job.ngroups);
     Temp t(c);
-    if (int st = temp_alloc(c, t, cv.total)) return st;
-    const uint64_t base = c->arena_dev + t.off;
-    std::vector<uint8_t> host(hb, 0);
-    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
-    if (int st = upload(c, base, host.data(), hb)) return st;
-    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
-    uint32_t *d_map = (uint32_t *)(base + o_map);
+    Staged sg;
+    uint64_t xd, scr;
+    if (int st = stage(c, job, is_small(job), t, {}, 0, sg, xd, scr)) return st;
     const uint64_t G = job.ngroups, T = job.nchunks;
-    int st;
-    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
-    if ((st = launch(c, "classify", [&] { return launch_classify(d_bufs, d_map, G, d_hashes, K, T, d_bitmap, c->stream); })))
-        return st;
-    return launch(c, "classify", [&] { return launch_labels(d_bufs, n, d_bitmap, d_labels, c->stream); });
+    return with_tables(sg, [&](const auto &tab) {
+        if (int st = launch(c, "classify", [&] {
+                return launch_classify(tab, G, d_hashes, K, T, d_bitmap, c->stream);
+            }))
+            return st;
+        return launch(c, "classify", [&] { return launch_labels(tab, d_bitmap, d_labels, c->stream); });
+    });
 }
 
 int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent, uint32_t flags,
@@ -989,13 +1036,12 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     }
     lists.push_back({0, n, {c->arena_dev + node->roots_off + 8 * n, (uint64_t)d_sroot}});
 
+    // A small job (tables in kernel arguments) that took the pipelined
+    // reservation runs as: fingerprint+diff, Merkle, scan+compact (which also
+    // writes the stored-chunk count to pinned host memory), dirty copy.
+    const bool small = is_small(job) && !exact && G <= kScanCompactMaxGroups;
     Carver cv;
-    uint64_t o_bufs, o_runs, o_lists, o_map, o_nodes, o_sa, o_sb, o_roots, o_cnt, o_mask, o_offs, o_total, o_list;
-    cv.add(&o_bufs, sizeof(JobBuf) * n);
-    cv.add(&o_runs, sizeof(Run) * job.runs.size());
-    cv.add(&o_lists, sizeof(MerkleList) * lists.size());
-    const uint64_t hb = cv.total;
-    cv.add(&o_map, 4 * G);
+    uint64_t o_nodes, o_sa, o_sb, o_roots, o_cnt, o_mask, o_offs, o_total, o_list;
     cv.add(&o_nodes, 8 * G);
     cv.add(&o_sa, 8 * std::max<uint64_t>(G, n));
     cv.add(&o_sb, 8 * std::max<uint64_t>(G, n));
@@ -1006,36 +1052,44 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     cv.add(&o_total, 8);
     cv.add(&o_list, 8 * T);
     Temp t(c);
-    if (int st = temp_alloc(c, t, cv.total)) return st;
-    const uint64_t base = c->arena_dev + t.off;
-    std::vector<uint8_t> host(hb, 0);
-    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
-    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
-    memcpy(host.data() + o_lists, lists.data(), sizeof(MerkleList) * lists.size());
-    if (int st = upload(c, base, host.data(), hb)) return st;
-
-    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
-    const Run *d_runs = (const Run *)(base + o_runs);
-    const MerkleList *d_lists = (const MerkleList *)(base + o_lists);
-    uint32_t *d_map = (uint32_t *)(base + o_map);
-    uint64_t *d_nodes = (uint64_t *)(base + o_nodes);
-    uint64_t *d_sa = (uint64_t *)(base + o_sa), *d_sb = (uint64_t *)(base + o_sb);
-    uint64_t *d_roots_tmp = (uint64_t *)(base + o_roots);
-    uint32_t *d_cnt = (uint32_t *)(base + o_cnt);
-    uint64_t *d_mask = (uint64_t *)(base + o_mask), *d_offs = (uint64_t *)(base + o_offs);
-    uint64_t *d_total = (uint64_t *)(base + o_total), *d_list = (uint64_t *)(base + o_list);
+    Staged sg;
+    uint64_t lists_dev, scr;
+    if (int st = stage(c, job, small, t, small ? std::vector<uint8_t>() : bytes_of(lists), cv.total, sg, lists_dev, scr))
+        return st;
+    uint64_t *d_nodes = (uint64_t *)(scr + o_nodes);
+    uint64_t *d_sa = (uint64_t *)(scr + o_sa), *d_sb = (uint64_t *)(scr + o_sb);
+    uint64_t *d_roots_tmp = (uint64_t *)(scr + o_roots);
+    uint32_t *d_cnt = (uint32_t *)(scr + o_cnt);
+    uint64_t *d_mask = (uint64_t *)(scr + o_mask), *d_offs = (uint64_t *)(scr + o_offs);
+    uint64_t *d_total = (uint64_t *)(scr + o_total), *d_list = (uint64_t *)(scr + o_list);
     hipStream_t s = c->stream;
     uint64_t payload_top_dev = c->arena_dev + node->pay_top;
-    int st;
-    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, s); }))) return st;
-    if ((st = launch(c, "incremental", [&] {
-             return launch_hash(d_bufs, d_runs, d_map, G, false, true, d_nodes, d_cnt, d_mask, s);
-         })))
-        return st;
-    if ((st = launch(c, "merkle", [&] { return launch_merkle(d_lists, n, d_nodes, d_sa, d_sb, d_roots_tmp, s); })))
-        return st;
-    if ((st = launch(c, "merkle", [&] { return launch_merkle(d_lists + n, 1, d_roots_tmp, d_sa, d_sb, nullptr, s); })))
-        return st;
+    int st = with_tables(sg, [&](const auto &tab) {
+        return launch(c, "incremental", [&] {
+            return launch_tile(tab, G, kModeDiff, d_nodes, d_cnt, d_mask, 0, s);
+        });
+    });
+    if (st) return st;
+    if ((st = run_merkle(c, small, lists, n, lists_dev, d_nodes, d_sa, d_sb, d_roots_tmp))) return st;
+    if (small) {
+        node->count_slot = (int)c->free_counts.back();
+        c->free_counts.pop_back();
+        uint64_t *host_word = &c->counts_dev[node->count_slot];
+        const uint64_t top = node->pay_top;
+        if ((st = launch(c, "incremental", [&] {
+                 return launch_scan_compact_small(sg.arg, G, d_cnt, d_mask, top, d_list, d_total, host_word, s);
+             })))
+            return st;
+        if ((st = launch(c, "incremental", [&] {
+                 return launch_pack_dirty(sg.arg, d_list, d_total, T, payload_top_dev, s);
+             })))
+            return st;
+        HIP_TRY(c, hipEventRecord(node->ev, s));
+        node->settled = false;
+        c->pending.push_back(node);
+        *out = new_handle(c, node);
+        return PCS_OK;
+    }
     if ((st = launch(c, "incremental", [&] { return launch_scan(d_cnt, G, d_offs, d_total, s); }))) return st;
     if (exact) {
         HIP_TRY(c, hipMemcpyAsync(&c->counts[c->free_counts.back()], d_total, 8, hipMemcpyDeviceToHost, s));
@@ -1052,12 +1106,16 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         node->payload_off = poff;
         payload_top_dev = c->arena_dev + node->pay_top;
     }
-    if ((st = launch(c, "incremental", [&] {
-             return launch_compact(d_bufs, d_map, G, d_mask, d_offs, node->pay_top, d_list, s);
-         })))
-        return st;
-    if ((st = launch(c, "incremental", [&] { return launch_pack_dirty(d_bufs, d_runs, d_list, d_total, T, payload_top_dev, s); })))
-        return st;
+    st = with_tables(sg, [&](const auto &tab) {
+        if (int e = launch(c, "incremental", [&] {
+                return launch_compact(tab, G, d_mask, d_offs, node->pay_top, d_list, s);
+            }))
+            return e;
+        return launch(c, "incremental", [&] {
+            return launch_pack_dirty(tab, d_list, d_total, T, payload_top_dev, s);
+        });
+    });
+    if (st) return st;
     if (exact) {
         *out = new_handle(c, node);
         return PCS_OK;
@@ -1115,32 +1173,19 @@ int pcs_restore_verify(pcs_ctx *c, pcs_snap snap, const pcs_buf *dst, uint32_t n
         jb.parent_hash = c->arena_dev + nd->hashes_off + 8 * nd->chunk_begin[k];
     }
     if (n == 0) return PCS_OK;
-    Carver cv;
-    uint64_t o_bufs, o_runs, o_map;
-    cv.add(&o_bufs, sizeof(JobBuf) * n);
-    cv.add(&o_runs, sizeof(Run) * job.runs.size());
-    const uint64_t hb = cv.total;
-    cv.add(&o_map, 4 * job.ngroups);
     Temp t(c);
-    if (int st = temp_alloc(c, t, cv.total)) return st;
-    const uint64_t base = c->arena_dev + t.off;
-    std::vector<uint8_t> host(hb, 0);
-    memcpy(host.data() + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
-    memcpy(host.data() + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
-    if (int st = upload(c, base, host.data(), hb)) return st;
-    const JobBuf *d_bufs = (const JobBuf *)(base + o_bufs);
-    const Run *d_runs = (const Run *)(base + o_runs);
-    uint32_t *d_map = (uint32_t *)(base + o_map);
+    Staged sg;
+    uint64_t xd, scr;
+    if (int st = stage(c, job, is_small(job), t, {}, 0, sg, xd, scr)) return st;
     const uint64_t G = job.ngroups;
-    int st;
-    if ((st = launch(c, "map", [&] { return launch_group_map(d_bufs, n, G, d_map, c->stream); }))) return st;
-    if ((st = launch(c, "verify", [&] {
-             return launch_restore_verify(d_bufs, d_runs, d_map, G, c->arena_dev, d_bad_bitmap, c->stream);
-         })))
-        return st;
-    if (d_bad_labels)
-        return launch(c, "verify", [&] { return launch_labels(d_bufs, n, d_bad_bitmap, d_bad_labels, c->stream); });
-    return PCS_OK;
+    return with_tables(sg, [&](const auto &tab) {
+        if (int st = launch(c, "verify", [&] {
+                return launch_tile(tab, G, kModeVerify, nullptr, nullptr, d_bad_bitmap, c->arena_dev, c->stream);
+            }))
+            return st;
+        if (!d_bad_labels) return (int)PCS_OK;
+        return launch(c, "verify", [&] { return launch_labels(tab, d_bad_bitmap, d_bad_labels, c->stream); });
+    });
 }
 
 int pcs_snapshot_view(pcs_ctx *c, pcs_snap snap, uint64_t *d_payload, uint64_t *bytes)
