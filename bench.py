@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (for HBM counter scaling)")
+    ap.add_argument("--traffic", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
+                    help="no GPU: write the scaled HBM traffic record of the fused pack+fingerprint and restore "
+                         "kernels from a FETCH_SIZE and a WRITE_SIZE run of this bench with --calibrate-copy")
     ap.add_argument("--summarize", nargs="+", metavar="DB",
                     help="no GPU: print kernel statistics from rocprofv3 databases (trace or --pmc runs)")
     return ap.parse_args()
@@ -96,24 +99,88 @@ def summarize(dbs):
         print()
 
 
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "k_hash_copy_batch1024_traffic.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_21686_amd", "csrc", f) for f in ("pcs_kernels.hip", "pcs_device.h")]
+
+
+def kernel_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
 def traffic_record():
     """Scaled HBM traffic of the fused pack+fingerprint kernel, measured with
-    rocprofv3 counters, if the kernel source is unchanged since."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "k_hash_copy_batch1024_traffic.json")
-    src = os.path.join(ROOT, "paper_2607_21686_amd", "csrc", "pcs_kernels.hip")
+    rocprofv3 counters, if the kernel sources are unchanged since."""
     try:
-        rec = json.load(open(path))
+        rec = json.load(open(TRAFFIC_JSON))
     except (OSError, ValueError):
         return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    return rec if rec.get("kernel_source_sha256") == sha else None
+    return rec if rec.get("kernel_source_sha256") == kernel_source_sha() else None
+
+
+def traffic(fetch_db, write_db, sessions=1024, restored=512):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB, as rocprofv3 reports them)
+    of the fused pack+fingerprint kernel and the restore copy kernel, each
+    scaled by what the same counter reads for the plain 1 GiB calibration copy
+    (true traffic 1 GiB read + 1 GiB written), against the algorithmic bytes of
+    one launch (state read once and written once)."""
+    import sqlite3
+    import workloads as W
+
+    def per_kernel(db, counter):
+        cur = sqlite3.connect(db).cursor()
+        q = "select kernel_name, value from counters_collection where counter_name = ?"
+        rows = cur.execute(q, (counter,)).fetchall()
+        pick = lambda pat: [v for n, v in rows if pat in n]
+        calib = max(pick("rocclr_copyBuffer"))
+        return {"pack": pick("k_hash<pcs::DevTables, 1,"), "copy": pick("k_copy<pcs::DevTables, false,"),
+                "calib": calib}
+
+    f, w = per_kernel(fetch_db, "FETCH_SIZE"), per_kernel(write_db, "WRITE_SIZE")
+    gib_kib = (1 << 30) / 1024
+    fs, ws = gib_kib / f["calib"], gib_kib / w["calib"]
+    plan = W.config5_plan(1, sessions=1)
+    state = plan.ring.window_bytes + plan.obs_bytes + plan.rng_bytes
+    mean = lambda xs: sum(xs) / len(xs)
+
+    def one(kind, n_sessions):
+        fk, wk = mean(f[kind]), mean(w[kind])
+        t = int(round((fk * fs + wk * ws) * 1024))
+        alg = 2 * state * n_sessions
+        return {"fetch_KiB_per_dispatch": round(fk, 1), "write_KiB_per_dispatch": round(wk, 1),
+                "dispatches": [len(f[kind]), len(w[kind])], "traffic_bytes_per_launch": t,
+                "algorithmic_bytes_per_launch": alg, "traffic_over_algorithmic": round(t / alg, 5)}
+
+    rec = {"kernel": "k_hash<DevTables, pack> (fused pack + fingerprint)",
+           "workload": "batched suspend/resume, %d sessions x %d B of state" % (sessions, state),
+           "sessions": sessions,
+           "calibration_copy_bytes": 1 << 30, "calibration_fetch_KiB": round(f["calib"], 1),
+           "calibration_write_KiB": round(w["calib"], 1), "fetch_scale": round(fs, 6), "write_scale": round(ws, 6)}
+    rec.update(one("pack", sessions))
+    rec["restore_kernel"] = dict(kernel="k_copy<DevTables, unpack> (%d sessions)" % restored, **one("copy", restored))
+    rec["kernel_source_sha256"] = kernel_source_sha()
+    rec["commands"] = [
+        "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/prof_fetch -o fetch -- python3 bench.py --steps 2 --warmup 1 "
+        "--no-cpu-baseline --calibrate-copy",
+        "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/prof_write -o write -- python3 bench.py --steps 2 --warmup 1 "
+        "--no-cpu-baseline --calibrate-copy",
+        "python3 bench.py --traffic gpurun_out/prof_fetch/fetch_results.db gpurun_out/prof_write/write_results.db"]
+    with open(TRAFFIC_JSON, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec, indent=1))
 
 
 def main():
     args = parse()
     if args.summarize:
         summarize(args.summarize)
+        return
+    if args.traffic:
+        traffic(*args.traffic)
         return
     if args.gpus != 1:
         print("bench.py runs on one GPU: this build has no multi-GPU path (sessions shard across GPUs "
