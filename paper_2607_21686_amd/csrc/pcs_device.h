@@ -53,16 +53,21 @@ struct MerkleList {
 };
 
 // Where a launch finds its buffer and run tables.
-//   DevTables: in device memory (uploaded per call), with a group -> buffer
-//              map written by k_group_map; any job size.
+//   DevTables: in device memory (uploaded per call), with a group map
+//              written by k_group_map that gives each group its buffer and
+//              the run holding its first byte; any job size.
 //   ArgTables: carried in the kernel arguments themselves (no upload, no map
-//              kernel: a workgroup finds its buffer with a short search); jobs
-//              of at most kArgBufs buffers and kArgRuns runs.
+//              kernel: a workgroup finds its buffer and first run with short
+//              searches); jobs of at most kArgBufs buffers and kArgRuns runs.
 constexpr uint32_t kArgBufs = 8, kArgRuns = 64;
+struct GroupRef {
+    uint32_t buf;
+    uint32_t run;
+};
 struct DevTables {
     const JobBuf *bufs;
     const Run *runs;
-    const uint32_t *map;
+    const GroupRef *map;
     uint32_t nbuf;
     uint32_t pad;
 };
@@ -90,7 +95,7 @@ enum TileMode : int {
                       // the restored bytes and mark chunks whose fingerprint differs
                       // from the one stored at checkpoint time
 };
-hipError_t launch_group_map(const JobBuf *bufs, uint32_t nbuf, uint64_t ngroups, uint32_t *map,
+hipError_t launch_group_map(const JobBuf *bufs, const Run *runs, uint32_t nbuf, uint64_t ngroups, GroupRef *map,
                             hipStream_t s);
 template <class Tab>
 hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint32_t *flag_count,

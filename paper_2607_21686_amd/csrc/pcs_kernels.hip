@@ -120,6 +120,18 @@ __device__ __forceinline__ void cursor_load(Cursor &c)
     c.run_end = c.idx < c.last ? c.runs[c.idx + 1].lstart : c.nbytes;
 }
 
+// The run of [begin, begin + count) that holds logical offset L: the largest
+// index whose lstart <= L (runs are sorted by lstart, the first at 0).
+__device__ __forceinline__ uint32_t find_run(const Run *runs, uint32_t begin, uint32_t count, uint64_t L)
+{
+    uint32_t lo = begin, hi = begin + count;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (runs[mid].lstart <= L) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
 __device__ __forceinline__ Cursor cursor_seek(const Run *runs, uint32_t begin, uint32_t count,
                                               uint64_t nbytes, uint64_t L)
 {
@@ -127,12 +139,7 @@ __device__ __forceinline__ Cursor cursor_seek(const Run *runs, uint32_t begin, u
     c.runs = runs;
     c.last = begin + count - 1;
     c.nbytes = nbytes;
-    uint32_t lo = begin, hi = begin + count;  // largest idx with lstart <= L
-    while (hi - lo > 1) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (runs[mid].lstart <= L) lo = mid; else hi = mid;
-    }
-    c.idx = lo;
+    c.idx = find_run(runs, begin, count, L);
     cursor_load(c);
     return c;
 }
@@ -186,17 +193,22 @@ __device__ void store_partial(uint64_t a, uint4 v, uint32_t n)
 
 // ---------------------------------------------------------------- group map
 
-__global__ void k_group_map(const JobBuf *__restrict__ bufs, uint32_t nbuf, uint64_t ngroups,
-                            uint32_t *__restrict__ map)
+// One lane per group: its buffer (the largest b with group_begin <= g; empty
+// buffers own no group and lose ties) and the run holding its first byte, so
+// that the tile kernels start without searching.
+__global__ void k_group_map(const JobBuf *__restrict__ bufs, const Run *__restrict__ runs, uint32_t nbuf,
+                            uint64_t ngroups, GroupRef *__restrict__ map)
 {
     const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (g >= ngroups) return;
-    uint32_t lo = 0, hi = nbuf;  // largest b with group_begin <= g (empty buffers lose ties)
+    uint32_t lo = 0, hi = nbuf;
     while (hi - lo > 1) {
         const uint32_t mid = (lo + hi) >> 1;
         if (bufs[mid].group_begin <= g) lo = mid; else hi = mid;
     }
-    map[g] = lo;
+    const JobBuf &jb = bufs[lo];
+    const uint64_t x0 = (g - jb.group_begin) * kGroupChunks * kChunk;
+    map[g] = GroupRef{lo, find_run(runs, jb.run_begin, jb.run_count, x0)};
 }
 
 // ---------------------------------------------------------------- fingerprint
@@ -205,35 +217,65 @@ __global__ void k_group_map(const JobBuf *__restrict__ bufs, uint32_t nbuf, uint
 // runs): the path for the few chunks that straddle a ring wrap.
 __device__ uint64_t phys_addr(const Run *runs, uint32_t begin, uint32_t count, uint64_t L)
 {
-    uint32_t lo = begin, hi = begin + count;
-    while (hi - lo > 1) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (runs[mid].lstart <= L) lo = mid; else hi = mid;
-    }
-    return runs[lo].addr + (L - runs[lo].lstart);
+    const Run r = runs[find_run(runs, begin, count, L)];
+    return r.addr + (L - r.lstart);
 }
 
+// Where one chunk's bytes lie: byte x (x < len) is at (x < split ? a1 : a2)
+// + x when the chunk spans at most two physical runs (it straddles a ring's
+// wrap, or the end of one ring row set and the start of the next, when that
+// boundary falls inside it); a1 = 0 marks a chunk spanning more runs (rows
+// shorter than a chunk), whose addresses are searched per access.  Run
+// boundaries are 16-byte aligned, so no 16-byte granule crosses one.
+struct ChunkLoc {
+    uint64_t a1, a2;
+    uint32_t split, len;
+};
+
 // Per-chunk setup shared by the tile kernels: lane c < 64 of the first
-// wavefront finds chunk c's length and, when the whole chunk lies in one
-// physical run, its physical start address (0 otherwise).
-__device__ __forceinline__ void chunk_table(const JobBuf &jb, const Run *runs, uint64_t c0, uint32_t nv,
-                                            uint64_t *caddr, uint32_t *clen)
+// wavefront describes chunk c of the group.  r0 is the run holding the
+// group's first byte; a chunk's run is found by stepping forward from there
+// (a group usually lies in one or two runs), with a search for groups that
+// span many short runs.
+__device__ __forceinline__ void chunk_table(const JobBuf &jb, const Run *runs, uint32_t r0, uint64_t c0,
+                                            uint32_t nv, ChunkLoc *loc)
 {
     const uint32_t t = threadIdx.x;
     if (t < kGroupChunks) {
-        uint64_t a = 0;
-        uint32_t len = 0;
+        ChunkLoc l{0, 0, 0, 0};
         if (t < nv) {
             const uint64_t cb = (c0 + t) * kChunk;
-            len = (uint32_t)umin(kChunk, jb.nbytes - cb);
-            const Cursor cur = cursor_seek(runs, jb.run_begin, jb.run_count, jb.nbytes, cb);
-            if (cb + len <= cur.run_end) a = cb + cur.delta;
+            l.len = (uint32_t)umin(kChunk, jb.nbytes - cb);
+            const uint32_t last = jb.run_begin + jb.run_count - 1;
+            uint32_t idx = r0;
+            Run r = runs[idx];
+            uint64_t end = idx < last ? runs[idx + 1].lstart : jb.nbytes;
+            for (int k = 0; end <= cb; ++k) {  // cb < nbytes: ends at the last run at the latest
+                if (k == 2) {
+                    idx = find_run(runs, idx + 1, last - idx, cb);
+                } else {
+                    ++idx;
+                }
+                r = runs[idx];
+                end = idx < last ? runs[idx + 1].lstart : jb.nbytes;
+            }
+            const uint64_t a1 = r.addr + (cb - r.lstart);
+            if (cb + l.len <= end) {
+                l.a1 = l.a2 = a1;
+                l.split = l.len;
+            } else {  // idx < last here, since the last run ends at nbytes
+                const Run r2 = runs[idx + 1];
+                const uint64_t end2 = idx + 1 < last ? runs[idx + 2].lstart : jb.nbytes;
+                if (cb + l.len <= end2) {
+                    l.a1 = a1;
+                    l.split = (uint32_t)(end - cb);
+                    l.a2 = r2.addr - l.split;  // byte `split` of the chunk is r2's first byte
+                }
+            }
         }
-        caddr[t] = a;
-        clen[t] = len;
+        loc[t] = l;
     }
 }
-
 
 // Selects word i (0..3) of a 32-byte tail held in registers.
 __device__ __forceinline__ uint64_t sel4(uint64_t a, uint64_t b, uint64_t c, uint64_t d, uint32_t i)
@@ -243,7 +285,7 @@ __device__ __forceinline__ uint64_t sel4(uint64_t a, uint64_t b, uint64_t c, uin
 
 // A workgroup's buffer: through the map, or by searching a table of at most
 // kArgBufs buffers (largest b with group_begin <= G; empty buffers lose ties).
-__device__ __forceinline__ uint32_t buf_index(const DevTables &t, uint64_t G) { return t.map[G]; }
+__device__ __forceinline__ uint32_t buf_index(const DevTables &t, uint64_t G) { return t.map[G].buf; }
 __device__ __forceinline__ uint32_t buf_index(const ArgTables &t, uint64_t G)
 {
     uint32_t lo = 0, hi = t.nbuf;
@@ -252,6 +294,15 @@ __device__ __forceinline__ uint32_t buf_index(const ArgTables &t, uint64_t G)
         if (t.bufs[mid].group_begin <= G) lo = mid; else hi = mid;
     }
     return lo;
+}
+
+// A workgroup's buffer and the run holding its group's first byte.
+__device__ __forceinline__ GroupRef group_ref(const DevTables &t, uint64_t G) { return t.map[G]; }
+__device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
+{
+    const uint32_t b = buf_index(t, G);
+    const JobBuf &jb = t.bufs[b];
+    return GroupRef{b, find_run(t.runs, jb.run_begin, jb.run_count, (G - jb.group_begin) * kGroupChunks * kChunk)};
 }
 
 // Fingerprint tile kernel.  One workgroup = one 64-chunk group of one
@@ -276,39 +327,42 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     constexpr bool kFromSlots = MODE == kModeVerify;    // source is the snapshot, destination the runs
     static_assert(U >= 1 && T % LPS == 0, "tile shape");
     __shared__ __attribute__((aligned(16))) uint8_t tile[kGroupChunks * kRow];
-    __shared__ uint64_t caddr[kGroupChunks];
-    __shared__ uint32_t clen[kGroupChunks];
+    __shared__ ChunkLoc cloc[kGroupChunks];
     __shared__ uint64_t leaves[kGroupChunks];
     __shared__ uint32_t dflag[kGroupChunks];
 
     const uint64_t G = blockIdx.x;
-    const JobBuf &jb = tab.bufs[buf_index(tab, G)];
+    const GroupRef gr = group_ref(tab, G);
+    const JobBuf &jb = tab.bufs[gr.buf];
     const Run *runs = tab.runs;
     const uint32_t t = threadIdx.x;
     const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
     const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
     const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
     const g_u64 *man = (const g_u64 *)jb.manifest;
-    chunk_table(jb, runs, c0, nv, caddr, clen);
+    chunk_table(jb, runs, gr.run, c0, nv, cloc);
     __syncthreads();
 
     // This lane's granules: chunk (k*T + t) / LPS, slot t % LPS of each slice.
     const uint32_t slot = (t % LPS) * 16;
-    uint64_t ga[U];   // runs side: chunk start when the chunk lies in one run, else 0
-    uint64_t sa[U];   // slots side: the chunk's 4096-byte slot (0 if the group has no such chunk)
-    uint32_t gl[U];
+    uint64_t ga[U], gb[U];  // runs side: where the chunk's bytes lie (ChunkLoc)
+    uint64_t sa[U];         // slots side: the chunk's 4096-byte slot (0 if the group has no such chunk)
+    uint32_t gs[U], gl[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
         const uint32_t c = (k * T + t) / LPS;
-        ga[k] = c < nv ? caddr[c] : 0;
-        gl[k] = c < nv ? clen[c] : 0;
+        const ChunkLoc l = c < nv ? cloc[c] : ChunkLoc{0, 0, 0, 0};
+        ga[k] = l.a1;
+        gb[k] = l.a2;
+        gs[k] = l.split;
+        gl[k] = l.len;
         sa[k] = 0;
         if (c < nv && (MODE == kModePack || kFromSlots))
             sa[k] = (kFromSlots && man) ? arena_base + man[c0 + c] : jb.payload + (c0 + c) * kChunk;
     }
     auto runs_addr = [&](int k, uint32_t x) -> uint64_t {
         const uint32_t c = (k * T + t) / LPS;
-        return ga[k] ? ga[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
+        return ga[k] ? (x < gs[k] ? ga[k] : gb[k]) + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
     };
     auto load_granule = [&](int k, uint32_t x) -> uint4 {
         uint4 v = make_uint4(0, 0, 0, 0);
@@ -329,7 +383,7 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
 
     const uint32_t ci = t >> 1, p = t & 1;
     const bool hasher = t < 2 * kGroupChunks && ci < nv;
-    const uint32_t len = hasher ? clen[ci] : 0;
+    const uint32_t len = hasher ? cloc[ci].len : 0;
     const uint32_t nst = len >> 5;
     uint64_t va = p ? 0 : P1 + P2;   // accumulator 2p   (seed 0)
     uint64_t vb = p ? 0 - P1 : P2;   // accumulator 2p+1
@@ -556,32 +610,35 @@ __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
     constexpr uint32_t kSteps = kChunk / SL, LPS = SL / 16;
     constexpr int U = kGroupChunks * SL / 16 / T;
     static_assert(U >= 1 && T % LPS == 0, "tile shape");
-    __shared__ uint64_t caddr[kGroupChunks];  // runs side: chunk start if in one run, else 0
-    __shared__ uint32_t clen[kGroupChunks];
+    __shared__ ChunkLoc cloc[kGroupChunks];
     const uint64_t G = blockIdx.x;
-    const JobBuf &jb = tab.bufs[buf_index(tab, G)];
+    const GroupRef gr = group_ref(tab, G);
+    const JobBuf &jb = tab.bufs[gr.buf];
     const Run *runs = tab.runs;
     const uint32_t t = threadIdx.x;
     const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
     const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
     const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
     const g_u64 *man = (const g_u64 *)jb.manifest;
-    chunk_table(jb, runs, c0, nv, caddr, clen);
+    chunk_table(jb, runs, gr.run, c0, nv, cloc);
     __syncthreads();
 
     const uint32_t slot = (t % LPS) * 16;
-    uint64_t ra[U], sa[U];
-    uint32_t gl[U];
+    uint64_t ra[U], rb[U], sa[U];
+    uint32_t rs[U], gl[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
         const uint32_t c = (k * T + t) / LPS;
-        ra[k] = c < nv ? caddr[c] : 0;
-        gl[k] = c < nv ? clen[c] : 0;
+        const ChunkLoc l = c < nv ? cloc[c] : ChunkLoc{0, 0, 0, 0};
+        ra[k] = l.a1;
+        rb[k] = l.a2;
+        rs[k] = l.split;
+        gl[k] = l.len;
         sa[k] = c < nv ? (PACK || !man ? jb.payload + (c0 + c) * kChunk : arena_base + man[c0 + c]) : 0;
     }
     auto runs_addr = [&](int k, uint32_t x) -> uint64_t {
         const uint32_t c = (k * T + t) / LPS;
-        return ra[k] ? ra[k] + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
+        return ra[k] ? (x < rs[k] ? ra[k] : rb[k]) + x : phys_addr(runs, run_begin, run_count, (c0 + c) * kChunk + x);
     };
     auto load = [&](int k, uint32_t x) -> uint4 {
         uint4 v = make_uint4(0, 0, 0, 0);
@@ -803,12 +860,12 @@ constexpr int kCopyLanes = 1024, kCopySlice = 1024;
 
 // ---------------------------------------------------------------- launchers
 
-hipError_t launch_group_map(const JobBuf *bufs, uint32_t nbuf, uint64_t ngroups, uint32_t *map,
+hipError_t launch_group_map(const JobBuf *bufs, const Run *runs, uint32_t nbuf, uint64_t ngroups, GroupRef *map,
                             hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
     const uint32_t blocks = (uint32_t)((ngroups + 255) / 256);
-    hipLaunchKernelGGL(k_group_map, dim3(blocks), dim3(256), 0, s, bufs, nbuf, ngroups, map);
+    hipLaunchKernelGGL(k_group_map, dim3(blocks), dim3(256), 0, s, bufs, runs, nbuf, ngroups, map);
     return hipGetLastError();
 }
 

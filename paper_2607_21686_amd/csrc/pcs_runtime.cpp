@@ -473,7 +473,7 @@ int stage(pcs_ctx *c, const Job &job, bool small, Temp &t, const std::vector<uin
     }
     if (!extra.empty()) cv.add(&o_extra, extra.size());
     const uint64_t hb = cv.total;
-    if (!small) cv.add(&o_map, 4 * G);
+    if (!small) cv.add(&o_map, sizeof(GroupRef) * G);
     cv.add(&o_scr, dev_bytes);
     if (int e = temp_alloc(c, t, cv.total)) return e;
     const uint64_t base = c->arena_dev + t.off;
@@ -487,7 +487,7 @@ int stage(pcs_ctx *c, const Job &job, bool small, Temp &t, const std::vector<uin
         if (!job.runs.empty()) memcpy(sg.arg.runs, job.runs.data(), sizeof(Run) * job.runs.size());
     } else {
         sg.dev = DevTables{(const JobBuf *)(base + o_bufs), (const Run *)(base + o_runs),
-                           (const uint32_t *)(base + o_map), n, 0};
+                           (const GroupRef *)(base + o_map), n, 0};
     }
     if (hb) {
         std::vector<uint8_t> host(hb, 0);
@@ -500,7 +500,7 @@ int stage(pcs_ctx *c, const Job &job, bool small, Temp &t, const std::vector<uin
     }
     if (!small && G)
         return launch(c, "map", [&] {
-            return launch_group_map(sg.dev.bufs, n, G, (uint32_t *)sg.dev.map, c->stream);
+            return launch_group_map(sg.dev.bufs, sg.dev.runs, n, G, (GroupRef *)sg.dev.map, c->stream);
         });
     return PCS_OK;
 }

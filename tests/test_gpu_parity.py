@@ -84,6 +84,8 @@ RING_CASES = [
     (2, 300, 2048, 257, 299, 0),     # odd head: chunks straddle the wrap
     (6, 1000, 16, 999, 1, 32),       # tiny rows: many rows per chunk
     (64, 96, 2048, 64, 95, 0),       # many rings, wrap at the last slot
+    (40, 9, 2048, 7, 5, 0),          # 80 runs (device tables); a group spans ~36 runs
+    (200, 4, 16, 3, 2, 0),           # 400 runs of 16-48 bytes; every chunk spans ~170 runs
 ]
 
 
