@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import warnings
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libpcs.so")
@@ -52,9 +53,14 @@ class PcsError(RuntimeError):
 
 
 def load():
-    """Loads libpcs.so and declares every entry point's signature."""
+    """Loads libpcs.so and declares every entry point's signature.  Warns when
+    the library is older than one of its sources (a stale build)."""
     if not os.path.exists(LIB_PATH):
         raise ImportError("libpcs.so is not built (run __graft_entry__.build())")
+    from . import build
+    if build.stale():
+        warnings.warn("libpcs.so is older than its sources; rebuild with __graft_entry__.build()", RuntimeWarning,
+                      stacklevel=2)
     lib = ctypes.CDLL(LIB_PATH)
     P, U64, U32, I = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int
     PU64 = ctypes.POINTER(ctypes.c_uint64)
