@@ -297,6 +297,43 @@ int pcs_snapshot_hashes(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_dst, uint64_t c
 int pcs_export(pcs_ctx *ctx, pcs_snap snap, void *h_dst, uint64_t cap, uint64_t *written);
 int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
 
+/*
+ * Relevance-keyed bank shrink (Sec. 5, "The two semantic decisions the
+ * runtime owns": what to evict is decided by relevance to the return, not by
+ * recency; Sec. 7.5 and Tables 5-6: every policy prunes a session's bank to
+ * the same retained fraction and differs only in which entries it ranks as
+ * worth keeping).
+ *
+ * A bank is n_entries entries held as nparts component arrays (struct of
+ * arrays, e.g. latents and poses); part p's entry i is entry_bytes bytes at
+ * src + i * entry_bytes.  d_scores holds n_entries float32 relevance scores
+ * on the device, supplied by the caller (e.g. pose distance to the anchor);
+ * LOWER is more relevant.  Scores are ordered totally by their bit pattern:
+ * -inf < ... < -0.0 < +0.0 < ... < +inf < every NaN; equal scores rank the
+ * lower index first.  The call keeps the `keep` best-ranked entries and
+ * writes them, in increasing original index order (a stable compaction), to
+ * dst + j * entry_bytes, j = 0..keep-1, for every part.  dst == src shrinks
+ * in place (through arena scratch); otherwise the keep * entry_bytes bytes
+ * at dst must not overlap the n_entries * entry_bytes bytes at src.  If
+ * d_kept is not NULL it receives the kept indices (keep uint32 values,
+ * increasing).  Asynchronous on the context stream; a following incremental
+ * checkpoint of the shrunk bank (parent = the bank's last snapshot) stores
+ * only the chunks the shrink changed.
+ *
+ * Limits and errors: n_entries <= 65536 and keep <= n_entries, else
+ * PCS_E_INVAL; nparts <= 64; entry_bytes > 0; PCS_E_NOMEM if the arena
+ * cannot hold the scratch (4 * 4 + 8 bytes per entry, plus the largest
+ * in-place part's keep * entry_bytes).
+ */
+typedef struct pcs_bank_part {
+    uint64_t src;          /* device address of entry 0 */
+    uint64_t dst;          /* device address for kept entry 0 (== src: in place) */
+    uint64_t entry_bytes;  /* bytes per entry of this part */
+} pcs_bank_part;
+
+int pcs_bank_shrink(pcs_ctx *ctx, const pcs_bank_part *h_parts, uint32_t nparts, uint64_t n_entries,
+                    const float *d_scores, uint64_t keep, uint32_t *d_kept);
+
 /* Arena accounting: bytes in use, bytes free, largest free block, live handles. */
 int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t *largest_free,
                     uint64_t *live_handles);
@@ -306,7 +343,7 @@ int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t
  * events on the context stream.  pcs_kernel_time waits for the stream, then
  * reports the number of launches and their summed duration in milliseconds
  * for the kernel family `name` ("hash", "pack_hash", "pack", "copy",
- * "verify", "merkle", "classify", "incremental", "map") since the last reset, and resets it.
+ * "verify", "merkle", "classify", "incremental", "map", "shrink") since the last reset, and resets it.
  */
 int pcs_set_timing(pcs_ctx *ctx, int enable);
 int pcs_kernel_time(pcs_ctx *ctx, const char *name, uint64_t *launches, double *total_ms);

@@ -69,6 +69,8 @@ def _L():
         lib.orc_payload_layout.restype = u64
         lib.orc_dirty.argtypes = [p, p, p, p, u32, p]
         lib.orc_dirty.restype = u64
+        lib.orc_bank_select.argtypes = [p, u32, u32, p]
+        lib.orc_bank_select.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -328,3 +330,38 @@ def export_image(buffers, layouts=None) -> bytes:
     head += hashes.astype("<u8").tobytes()
     pad = (-len(head)) % CHUNK
     return head + b"\0" * pad + payload.tobytes()
+
+
+# ---------------------------------------------------------------- bank shrink
+
+def keep_count(fraction, n_entries: int) -> int:
+    """Entries a shrink to `fraction` keeps: the exact product fraction x n
+    rounded half to even, at least 1 for a non-empty bank, at most n."""
+    from fractions import Fraction
+    if n_entries <= 0:
+        return 0
+    return min(n_entries, max(1, round(Fraction(fraction) * n_entries)))
+
+
+def bank_select(scores, keep: int) -> np.ndarray:
+    """The `keep` best-ranked entries (lower score first; -0.0 before +0.0;
+    NaN last; ties by lower index), in increasing index order (Sec. 5,
+    Sec. 7.5, Tables 5-6)."""
+    s = np.ascontiguousarray(scores, dtype=np.float32)
+    out = np.zeros(max(1, keep), dtype=np.uint32)
+    if _L().orc_bank_select(s.ctypes.data, s.size, keep, out.ctypes.data) != 0:
+        raise ValueError("keep exceeds the number of entries")
+    return out[:keep]
+
+
+def bank_shrink(parts, scores, keep: int):
+    """Shrinks a struct-of-arrays bank: parts = [(bytes of n entries, entry
+    bytes), ...]; returns (kept indices, [the kept entries of each part, in
+    index order, as one byte string each])."""
+    n = np.asarray(scores).size
+    kept = bank_select(scores, keep)
+    out = []
+    for data, eb in parts:
+        a = _bytes(data)[:n * eb].reshape(n, eb) if n else np.zeros((0, eb), dtype=np.uint8)
+        out.append(a[kept.astype(np.int64)].reshape(-1).copy())
+    return kept, out

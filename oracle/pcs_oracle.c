@@ -33,10 +33,15 @@
  * recursive largest-power-of-two split; the ring window against numpy.roll;
  * classification against direct byte comparison; pack/unpack, incremental
  * chains and fork against brute-force round trips; snapshot sizes against
- * the byte counts the paper prints in Table 1 and Sec. 7.2.
+ * the byte counts the paper prints in Table 1 and Sec. 7.2; the bank
+ * shrink's selection against Python's sort with a key built from float
+ * semantics and against a rank-counting definition on small inputs, and the
+ * keep count against the frames Table 6 lists per retained fraction.
  */
+#include <math.h>
 #include <stdint.h>
 #include <stddef.h>
+#include <stdlib.h>
 #include <string.h>
 
 /* ------------------------------------------------------------------ */
@@ -328,4 +333,65 @@ uint64_t orc_dirty(const uint64_t *hashes, const uint64_t *counts,
         pbase += parent_counts[b];
     }
     return ndirty;
+}
+
+/* ------------------------------------------------------------------ */
+/* Relevance-keyed bank shrink (Sec. 5: what to evict is decided by   */
+/* relevance to the return, not recency; Sec. 7.5 and Tables 5-6: a   */
+/* shrink keeps a fixed fraction of a session's bank entries and the  */
+/* policies differ only in which entries they rank as worth keeping). */
+/* ------------------------------------------------------------------ */
+
+/* The library's ranking of caller-supplied scores (lower = more relevant):
+ * numeric order, -0.0 before +0.0, every NaN after +inf, and among equal
+ * scores the lower index first.  Returns 1 iff entry (a, ia) ranks before
+ * entry (b, ib). */
+static int ranks_before(float a, uint32_t ia, float b, uint32_t ib)
+{
+    const int na = isnan(a) != 0, nb = isnan(b) != 0;
+    if (na || nb) {
+        if (na && nb) return ia < ib;
+        return nb;  /* a is a number, b is NaN */
+    }
+    if (a < b) return 1;
+    if (a > b) return 0;
+    {
+        const int sa = signbit(a) != 0, sb = signbit(b) != 0;
+        if (sa != sb) return sa;  /* -0.0 before +0.0 */
+    }
+    return ia < ib;
+}
+
+static const float *g_rank_scores; /* qsort has no context argument */
+
+static int cmp_rank(const void *x, const void *y)
+{
+    const uint32_t i = *(const uint32_t *)x, j = *(const uint32_t *)y;
+    if (i == j) return 0;
+    return ranks_before(g_rank_scores[i], i, g_rank_scores[j], j) ? -1 : 1;
+}
+
+static int cmp_index(const void *x, const void *y)
+{
+    const uint32_t i = *(const uint32_t *)x, j = *(const uint32_t *)y;
+    return (i > j) - (i < j);
+}
+
+/* kept[0..keep) = the `keep` best-ranked of n entries, in increasing index
+ * order (the order the shrunk bank holds them in).  Returns 0, or -1 if
+ * keep > n or memory runs out. */
+int orc_bank_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept)
+{
+    uint32_t *order;
+    if (keep > n) return -1;
+    if (n == 0) return 0;
+    order = (uint32_t *)malloc(sizeof(uint32_t) * n);
+    if (!order) return -1;
+    for (uint32_t i = 0; i < n; ++i) order[i] = i;
+    g_rank_scores = scores;
+    qsort(order, n, sizeof(uint32_t), cmp_rank);
+    memcpy(kept, order, sizeof(uint32_t) * keep);
+    qsort(kept, keep, sizeof(uint32_t), cmp_index);
+    free(order);
+    return 0;
 }

@@ -21,9 +21,9 @@ import ctypes
 import torch
 
 from ._lib import (CHUNK_BYTES, CKPT_HASH, E_CORRUPT, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_SHAPE, EXPORTS, FLAT,
-                   MUST_SNAPSHOT, RECOMPUTABLE, RING, PcsBuf, PcsError, PcsSnapInfo, lib)
+                   MUST_SNAPSHOT, RECOMPUTABLE, RING, PcsBankPart, PcsBuf, PcsError, PcsSnapInfo, lib)
 
-__all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
+__all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_count", "keep_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
            "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "E_CORRUPT",
            "EXPORTS"]
 
@@ -32,6 +32,15 @@ _L = lib()  # fails loudly if the HIP library is missing
 
 def chunk_count(nbytes: int) -> int:
     return (nbytes + CHUNK_BYTES - 1) // CHUNK_BYTES
+
+
+def keep_count(fraction: float, n_entries: int) -> int:
+    """Entries a shrink to `fraction` of a bank keeps: fraction x n rounded to
+    the nearest integer (halves to even), at least one entry of a non-empty
+    bank (Table 6 lists the frames a fraction keeps of a bank of about 21)."""
+    if n_entries <= 0:
+        return 0
+    return min(n_entries, max(1, round(fraction * n_entries)))
 
 
 def _dev_ptr(t) -> int:
@@ -211,6 +220,27 @@ class Context:
         out = ctypes.c_uint64()
         self._check(_L.pcs_import(self._h, a.ctypes.data_as(ctypes.c_void_p), a.size, ctypes.byref(out)))
         return int(out.value)
+
+    def bank_shrink(self, parts, scores, keep: int, kept=None):
+        """Relevance-keyed bank shrink (pcs_bank_shrink): keeps the `keep`
+        entries with the lowest scores (ties: lower index first; NaN last) in
+        their original order.  parts: sequence of (src, dst, entry_bytes) with
+        device tensors; dst None (or src itself) shrinks in place.  scores:
+        float32 device tensor, one score per entry.  kept: optional int32
+        device tensor receiving the kept indices."""
+        if not isinstance(scores, torch.Tensor) or scores.dtype != torch.float32:
+            raise TypeError("scores must be a float32 device tensor")
+        n = scores.numel()
+        arr = (PcsBankPart * max(1, len(parts)))()
+        for i, (src, dst, eb) in enumerate(parts):
+            dst = src if dst is None else dst
+            if src.numel() * src.element_size() < n * eb or dst.numel() * dst.element_size() < keep * eb:
+                raise ValueError("bank part %d is smaller than its entries" % i)
+            arr[i] = PcsBankPart(_dev_ptr(src), _dev_ptr(dst), eb)
+        if kept is not None and (kept.dtype != torch.int32 or kept.numel() < keep):
+            raise ValueError("kept must be an int32 device tensor of at least keep values")
+        self._check(_L.pcs_bank_shrink(self._h, arr, len(parts), n, _dev_ptr(scores) if n else None, keep,
+                                       _dev_ptr(kept) if kept is not None else None))
 
     def fork(self, snap: int) -> int:
         out = ctypes.c_uint64()

@@ -29,7 +29,7 @@ EXPORTS = ("pcs_ctx_create", "pcs_ctx_destroy", "pcs_last_error", "pcs_chunk_cou
            "pcs_classify", "pcs_checkpoint", "pcs_checkpoint_batch", "pcs_restore", "pcs_restore_batch",
            "pcs_restore_verify", "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload",
            "pcs_snapshot_view", "pcs_snapshot_hashes",
-           "pcs_export", "pcs_import", "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
+           "pcs_export", "pcs_import", "pcs_bank_shrink", "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
 
 
 class PcsBuf(ctypes.Structure):
@@ -44,6 +44,10 @@ class PcsSnapInfo(ctypes.Structure):
                 ("total_chunks", ctypes.c_uint64), ("dirty_chunks", ctypes.c_uint64),
                 ("nbufs", ctypes.c_uint32), ("incremental", ctypes.c_uint32),
                 ("has_hashes", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
+class PcsBankPart(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_uint64), ("dst", ctypes.c_uint64), ("entry_bytes", ctypes.c_uint64)]
 
 
 class PcsError(RuntimeError):
@@ -85,6 +89,7 @@ def load():
         "pcs_snapshot_hashes": ([P, U64, P, U64], I),
         "pcs_export": ([P, U64, P, U64, PU64], I),
         "pcs_import": ([P, P, U64, PU64], I),
+        "pcs_bank_shrink": ([P, ctypes.POINTER(PcsBankPart), U32, U64, P, U64, P], I),
         "pcs_arena_stats": ([P, PU64, PU64, PU64, PU64], I),
         "pcs_set_timing": ([P, I], I),
         "pcs_kernel_time": ([P, ctypes.c_char_p, PU64, ctypes.POINTER(ctypes.c_double)], I),

@@ -125,5 +125,14 @@ hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, con
                                      const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
                                      uint64_t *total, uint64_t *total_host, hipStream_t s);
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
+// Bank shrink: flags[i] = entry i is among the `keep` best-ranked (score
+// order of pcs_bank_shrink), offsets = exclusive scan of flags, kept = the
+// kept indices in increasing order.
+hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *flags, uint64_t *offsets,
+                                uint64_t *total, uint32_t *kept, hipStream_t s);
+// dst entry j <- src entry kept[j] (entry j when kept is null), count entries
+// of entry_bytes bytes.
+hipError_t launch_gather_entries(uint64_t src, uint64_t dst, uint64_t entry_bytes, const uint32_t *kept,
+                                 uint64_t count, hipStream_t s);
 
 }  // namespace pcs

@@ -856,6 +856,77 @@ constexpr int kPackLanes = 1024, kPackSlice = 512;
 constexpr int kHashLanes = 256, kHashSlice = 512;
 constexpr int kCopyLanes = 1024, kCopySlice = 1024;
 
+// ---------------------------------------------------------------- bank shrink
+
+// Total order on float32 relevance scores as unsigned keys: negative values
+// reversed below the positive ones (-0.0 just below +0.0), every NaN above
+// +inf.
+__device__ __forceinline__ uint32_t score_key(uint32_t bits)
+{
+    if ((bits & 0x7F800000u) == 0x7F800000u && (bits & 0x007FFFFFu)) return 0xFFFFFFFFu;
+    return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+}
+
+// Entry i is kept iff fewer than `keep` entries rank before it (a smaller
+// key, or an equal key at a lower index).  One lane per entry counts over
+// all keys, staged through LDS in tiles that every lane reads in the same
+// order (broadcast reads).
+__global__ __launch_bounds__(256) void k_shrink_rank(const uint32_t *__restrict__ scores, uint32_t n, uint32_t keep,
+                                                     uint32_t *__restrict__ flags)
+{
+    __shared__ uint32_t tile[2048];
+    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+    const uint32_t ki = i < n ? score_key(scores[i]) : 0;
+    uint32_t rank = 0;
+    for (uint32_t base = 0; base < n; base += 2048) {
+        const uint32_t m = n - base < 2048 ? n - base : 2048;
+        for (uint32_t j = threadIdx.x; j < m; j += 256) tile[j] = score_key(scores[base + j]);
+        __syncthreads();
+        for (uint32_t j = 0; j < m; ++j) {
+            const uint32_t kj = tile[j];
+            rank += (kj < ki || (kj == ki && base + j < i)) ? 1u : 0u;
+        }
+        __syncthreads();
+    }
+    if (i < n) flags[i] = rank < keep ? 1u : 0u;
+}
+
+// Kept entry i goes to position offsets[i] (exclusive scan of the flags), so
+// the kept list is in increasing index order.
+__global__ __launch_bounds__(256) void k_shrink_place(const uint32_t *__restrict__ flags,
+                                                      const uint64_t *__restrict__ offsets, uint32_t n,
+                                                      uint32_t *__restrict__ kept)
+{
+    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+    if (i < n && flags[i]) kept[offsets[i]] = i;
+}
+
+// Moves kept entries of one bank part: destination entry j <- source entry
+// kept[j] (entry j itself when kept is null), eb bytes each, in G-byte
+// granules (eb and both bases are multiples of G).  Work item w is slice
+// w % spe of entry w / spe, 256 granules per slice; workgroups stride over
+// the items.
+template <int G>
+__global__ __launch_bounds__(256) void k_gather_entries(uint64_t src, uint64_t dst, uint64_t eb,
+                                                        const uint32_t *__restrict__ kept, uint64_t spe,
+                                                        uint64_t items)
+{
+    for (uint64_t w = blockIdx.x; w < items; w += gridDim.x) {
+        const uint64_t j = w / spe, sl = w % spe;
+        const uint64_t x = (sl * 256 + threadIdx.x) * G;
+        if (x >= eb) continue;
+        const uint64_t si = kept ? kept[j] : j;
+        const uint64_t a = src + si * eb + x, d = dst + j * eb + x;
+        if constexpr (G == 16) {
+            store16_nt(d, load16_nt(a));
+        } else if constexpr (G == 4) {
+            *(g_u32 *)d = *(const g_u32 *)a;
+        } else {
+            *(g_u8 *)d = *(const g_u8 *)a;
+        }
+    }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
@@ -979,6 +1050,38 @@ hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, con
     if (ngroups > kScanCompactMaxGroups) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_scan_compact_small, dim3(1), dim3(1024), 0, s, tab, ngroups, counts, dirty_mask,
                        payload_arena_top, list, total, total_host);
+    return hipGetLastError();
+}
+
+hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *flags, uint64_t *offsets,
+                                uint64_t *total, uint32_t *kept, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    const uint32_t blocks = (n + 255) / 256;
+    hipLaunchKernelGGL(k_shrink_rank, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint32_t *>(scores), n,
+                       keep, flags);
+    if (hipError_t e = hipGetLastError()) return e;
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, flags, (uint64_t)n, offsets, total);
+    if (hipError_t e = hipGetLastError()) return e;
+    hipLaunchKernelGGL(k_shrink_place, dim3(blocks), dim3(256), 0, s, flags, offsets, n, kept);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_entries(uint64_t src, uint64_t dst, uint64_t entry_bytes, const uint32_t *kept,
+                                 uint64_t count, hipStream_t s)
+{
+    if (count == 0 || entry_bytes == 0) return hipSuccess;
+    const auto aligned = [&](uint64_t g) { return entry_bytes % g == 0 && src % g == 0 && dst % g == 0; };
+    const int G = aligned(16) ? 16 : aligned(4) ? 4 : 1;
+    const uint64_t spe = (entry_bytes / G + 255) / 256;
+    const uint64_t items = count * spe;
+    const uint32_t grid = (uint32_t)(items < (1u << 20) ? items : (1u << 20));
+    if (G == 16)
+        hipLaunchKernelGGL(k_gather_entries<16>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
+    else if (G == 4)
+        hipLaunchKernelGGL(k_gather_entries<4>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
+    else
+        hipLaunchKernelGGL(k_gather_entries<1>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
     return hipGetLastError();
 }
 

@@ -958,6 +958,74 @@ int pcs_classify(pcs_ctx *c, const uint64_t *d_hashes, uint32_t K, const uint64_
     });
 }
 
+int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uint64_t n_entries,
+                    const float *d_scores, uint64_t keep, uint32_t *d_kept)
+{
+    if (!c) return PCS_E_INVAL;
+    if (nparts > 64) return fail(c, PCS_E_INVAL, "at most 64 bank parts");
+    if (nparts && !parts) return fail(c, PCS_E_INVAL, "null parts");
+    if (n_entries > 65536) return fail(c, PCS_E_INVAL, "at most 65536 bank entries (%llu given)",
+                                       (unsigned long long)n_entries);
+    if (keep > n_entries)
+        return fail(c, PCS_E_INVAL, "keep %llu exceeds %llu entries", (unsigned long long)keep,
+                    (unsigned long long)n_entries);
+    if (n_entries && !d_scores) return fail(c, PCS_E_INVAL, "null scores");
+    uint64_t stage_bytes = 0;
+    for (uint32_t p = 0; p < nparts; ++p) {
+        const pcs_bank_part &q = parts[p];
+        if (q.entry_bytes == 0) return fail(c, PCS_E_INVAL, "part %u: entry_bytes must be > 0", p);
+        if (n_entries == 0) continue;
+        if (!q.src || !q.dst) return fail(c, PCS_E_INVAL, "part %u: null address", p);
+        if (q.entry_bytes > UINT64_MAX / n_entries) return fail(c, PCS_E_INVAL, "part %u: bank too large", p);
+        const uint64_t sb = n_entries * q.entry_bytes, db = keep * q.entry_bytes;
+        if (q.src > UINT64_MAX - sb || q.dst > UINT64_MAX - db)
+            return fail(c, PCS_E_INVAL, "part %u: address range wraps", p);
+        if (q.dst == q.src)
+            stage_bytes = std::max(stage_bytes, db);
+        else if (db && q.dst < q.src + sb && q.src < q.dst + db)
+            return fail(c, PCS_E_INVAL, "part %u: destination overlaps the source bank", p);
+    }
+    if (n_entries == 0) return PCS_OK;
+    Temp t(c);
+    Carver cv;
+    uint64_t o_flags, o_offs, o_total, o_kept, o_stage;
+    cv.add(&o_flags, 4 * n_entries);
+    cv.add(&o_offs, 8 * n_entries);
+    cv.add(&o_total, 8);
+    cv.add(&o_kept, 4 * n_entries);
+    cv.add(&o_stage, stage_bytes);
+    if (int e = temp_alloc(c, t, cv.total)) return e;
+    const uint64_t base = c->arena_dev + t.off;
+    uint32_t *kept = d_kept ? d_kept : (uint32_t *)(base + o_kept);
+    if (int st = launch(c, "shrink", [&] {
+            return launch_shrink_select(d_scores, (uint32_t)n_entries, (uint32_t)keep, (uint32_t *)(base + o_flags),
+                                        (uint64_t *)(base + o_offs), (uint64_t *)(base + o_total), kept, c->stream);
+        }))
+        return st;
+    if (keep == 0) return PCS_OK;
+    for (uint32_t p = 0; p < nparts; ++p) {
+        const pcs_bank_part &q = parts[p];
+        if (q.dst != q.src) {
+            if (int st = launch(c, "shrink", [&] {
+                    return launch_gather_entries(q.src, q.dst, q.entry_bytes, kept, keep, c->stream);
+                }))
+                return st;
+            continue;
+        }
+        // In place: gather into scratch, then copy the kept prefix back.
+        const uint64_t stage = base + o_stage;
+        if (int st = launch(c, "shrink", [&] {
+                return launch_gather_entries(q.src, stage, q.entry_bytes, kept, keep, c->stream);
+            }))
+            return st;
+        if (int st = launch(c, "shrink", [&] {
+                return launch_gather_entries(stage, q.dst, q.entry_bytes, nullptr, keep, c->stream);
+            }))
+            return st;
+    }
+    return PCS_OK;
+}
+
 int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent, uint32_t flags,
                    uint64_t *d_hashes, uint64_t *d_roots, uint64_t *d_sroot, pcs_snap *out)
 {

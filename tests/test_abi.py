@@ -15,8 +15,17 @@ def declared():
     return sorted(set(re.findall(r"\b(pcs_[a-z_]+)\s*\(", src)))
 
 
+def build_module():
+    """The build script, loaded by path (importing the package loads the library)."""
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("pcs_build", os.path.join(ROOT, "paper_2607_21686_amd", "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
 def test_library_exports_every_declared_symbol():
-    from paper_2607_21686_amd import build as B
+    B = build_module()
     if B.stale():
         B.build()
     lib = ctypes.CDLL(B.LIB)
@@ -35,6 +44,7 @@ def test_struct_layout_matches_header():
     from paper_2607_21686_amd import _lib
     assert ctypes.sizeof(_lib.PcsBuf) == 8 * 2 + 4 * 2 + 8 * 6
     assert ctypes.sizeof(_lib.PcsSnapInfo) == 8 * 4 + 4 * 4
+    assert ctypes.sizeof(_lib.PcsBankPart) == 8 * 3
 
 
 def test_chunk_counts_validation_on_host():

@@ -1,0 +1,126 @@
+"""GPU parity of the relevance-keyed bank shrink (pcs_bank_shrink; Sec. 5,
+Sec. 7.5, Tables 5-6) against the oracle: kept indices bit-exact, kept
+entries byte-exact, in place and out of place, and the incremental
+checkpoint that follows a shrink of the memory bank configuration."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from tests.gpu_util import arena, dev, host, log
+from tests.test_oracle_bank import tricky_scores
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def pcs():
+    import paper_2607_21686_amd as P
+    return P
+
+
+def scores_dev(s):
+    return torch.from_numpy(np.ascontiguousarray(s, dtype=np.float32).copy()).cuda()
+
+
+CASES = [
+    (1, [1, 28]),
+    (37, [1, 28, 4096, 4100]),
+    (513, [28, 16 * 60 * 104 * 2]),
+    (4099, [4, 16, 60]),
+    (65536, [4, 28]),        # the largest bank the call accepts
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[str(c[0]) for c in CASES])
+def test_shrink_matches_oracle(pcs, case):
+    n, sizes = case
+    rng = np.random.default_rng(70 + n)
+    ctx = pcs.Context(arena(256 << 20))
+    before = ctx.arena_stats()
+    s = tricky_scores(rng, n)
+    sd = scores_dev(s)
+    parts = [rng.integers(0, 256, size=n * eb, dtype=np.uint8) for eb in sizes]
+    for keep in sorted({0, 1, n // 3, n}):
+        want_kept, want = oracle.bank_shrink(list(zip(parts, sizes)), s, keep)
+        for inplace in (False, True):
+            log("bank shrink n", n, "sizes", sizes, "keep", keep, "in place" if inplace else "to new buffers")
+            srcs = [dev(p) for p in parts]
+            dsts = [None if inplace else torch.full((max(1, keep * eb),), 0xA5, dtype=torch.uint8, device="cuda")
+                    for eb in sizes]
+            kept = torch.full((max(1, keep),), -1, dtype=torch.int32, device="cuda")
+            ctx.bank_shrink([(a, d, eb) for a, d, eb in zip(srcs, dsts, sizes)], sd, keep, kept)
+            assert host(kept).view(np.uint32)[:keep].tolist() == want_kept.tolist()
+            for p, a, d, eb, w in zip(parts, srcs, dsts, sizes, want):
+                got = host(a if inplace else d)
+                assert np.array_equal(got[:keep * eb], w)
+                if inplace:
+                    assert np.array_equal(got[keep * eb:], p[keep * eb:])   # the rest is untouched
+                else:
+                    assert np.array_equal(host(a), p)                        # the source is untouched
+    assert ctx.arena_stats() == before
+    ctx.close()
+
+
+def test_shrink_rejects_bad_arguments(pcs):
+    ctx = pcs.Context(arena(16 << 20))
+    before = ctx.arena_stats()
+    a = torch.zeros(64 * 200, dtype=torch.uint8, device="cuda")   # room for 200 entries: the C checks decide
+    s = scores_dev(np.arange(100, dtype=np.float32))
+    bad = [
+        ("keep > n", lambda: ctx.bank_shrink([(a, None, 64)], s, 101)),
+        ("entry_bytes 0", lambda: ctx.bank_shrink([(a, None, 0)], s, 3)),
+        ("overlap", lambda: ctx.bank_shrink([(a, a[64:], 64)], s, 10)),
+        ("too many entries", lambda: ctx.bank_shrink([(torch.zeros(65537, dtype=torch.uint8, device="cuda"), None, 1)],
+                                                     scores_dev(np.zeros(65537, dtype=np.float32)), 1)),
+    ]
+    for name, f in bad:
+        log("bank shrink error case:", name)
+        with pytest.raises(pcs.PcsError) as e:
+            f()
+        assert e.value.code == pcs.E_INVAL, name
+        assert ctx.arena_stats() == before, name
+    ctx.bank_shrink([(a, None, 64)], scores_dev(np.zeros(0, dtype=np.float32)), 0)   # empty bank: nothing to do
+    ctx.close()
+
+
+def test_shrink_then_incremental_checkpoint_config2(pcs):
+    """The memory bank configuration at its full 512 entries: checkpoint,
+    shrink to 12% keyed by pose distance to the anchor, incremental
+    checkpoint of the shrunk bank, restore both."""
+    bank = W.config2(1)
+    E, le, pe = 512, bank.latent_entry_bytes, bank.pose_entry_bytes
+    lat, pos = dev(bank.latents), dev(bank.poses)
+    ctx = pcs.Context(arena(512 << 20))
+    st = oracle.Store()
+
+    def plan(e):
+        return [pcs.flat(lat, e * le), pcs.flat(pos, e * pe)]
+
+    log("config 2: full checkpoint of 512 entries")
+    g0 = ctx.checkpoint(plan(E), hash=True)
+    o0 = st.checkpoint(bank.prefix(E))
+    s = W.pose_scores(bank, E, anchor=0)
+    keep = pcs.keep_count(0.12, E)
+    assert keep == oracle.keep_count(0.12, E) == 61
+    kept = torch.zeros(keep, dtype=torch.int32, device="cuda")
+    log("config 2: shrink to", keep, "entries")
+    ctx.bank_shrink([(lat, None, le), (pos, None, pe)], scores_dev(s), keep, kept)
+    want_kept, (nl, npo) = oracle.bank_shrink([(bank.latents, le), (bank.poses, pe)], s, keep)
+    assert host(kept).view(np.uint32).tolist() == want_kept.tolist()
+    assert 0 in want_kept.tolist()                      # the anchor itself is the most relevant entry
+    log("config 2: incremental checkpoint of the shrunk bank")
+    g1 = ctx.checkpoint(plan(keep), parent=g0)
+    o1 = st.checkpoint([nl, npo], parent=o0)
+    stored_o = sum(1 for b in range(2) for arr, off in st.snapshot(o1).where[b] if arr is st.snapshot(o1).payload)
+    info = ctx.info(g1)
+    assert info["incremental"] == 1 and info["dirty_chunks"] == stored_o
+    assert info["state_bytes"] == keep * (le + pe)
+    outs = [torch.empty(keep * le, dtype=torch.uint8, device="cuda"), torch.empty(keep * pe, dtype=torch.uint8, device="cuda")]
+    ctx.restore(g1, [pcs.flat(o) for o in outs])
+    assert np.array_equal(host(outs[0]), nl) and np.array_equal(host(outs[1]), npo)
+    full = [torch.empty(E * le, dtype=torch.uint8, device="cuda"), torch.empty(E * pe, dtype=torch.uint8, device="cuda")]
+    ctx.restore(g0, [pcs.flat(o) for o in full])
+    assert np.array_equal(host(full[0]), bank.latents[:E * le]) and np.array_equal(host(full[1]), bank.poses[:E * pe])
+    ctx.close()

@@ -8,6 +8,7 @@ import subprocess
 
 import pytest
 
+import tests.test_oracle_bank as B
 import tests.test_oracle_contract as C
 import tests.test_oracle_hash as H
 import tests.test_oracle_ring_classify as R
@@ -30,6 +31,11 @@ MUTATIONS = {
     "classify_ignores_last_replay": ("for (uint32_t k = 1; k < K; ++k)", "for (uint32_t k = 1; k + 1 < K; ++k)"),
     "dirty_parent_index": ("(hashes[base + i] != parent_hashes[pbase + i])", "(hashes[base + i] != parent_hashes[base + i])"),
     "payload_unaligned": ("off += orc_chunk_count(nbytes[b]) * ORC_CHUNK;", "off += nbytes[b];"),
+    "shrink_positive_zero_first": ("if (sa != sb) return sa;", "if (sa != sb) return sb;"),
+    "shrink_nan_first": ("        return nb;  /* a is a number, b is NaN */", "        return na;"),
+    "shrink_ties_higher_index": ("    return ia < ib;\n}\n\nstatic const float", "    return ia > ib;\n}\n\nstatic const float"),
+    "shrink_rank_order_kept": ("    qsort(kept, keep, sizeof(uint32_t), cmp_index);\n", ""),
+    "shrink_higher_is_better": ("    if (a < b) return 1;\n    if (a > b) return 0;", "    if (a > b) return 1;\n    if (a < b) return 0;"),
 }
 
 PINS = [
@@ -44,6 +50,8 @@ PINS = [
     R.test_classify_matches_byte_comparison,
     C.test_full_round_trip_and_layout,
     C.test_incremental_dirty_set_is_byte_difference,
+    B.test_select_against_python_sort,
+    B.test_special_cases,
 ]
 
 

@@ -164,6 +164,15 @@ def config2(seed: int = 1, capacity: int = 512, latent_shape=(16, 60, 104), pose
     return Bank(lat, pos, 2 * le, 4 * pose_dim, step_entries)
 
 
+def pose_scores(bank: Bank, entries: int, anchor: int = 0) -> np.ndarray:
+    """Caller-side relevance scores for a bank shrink (lower = more relevant):
+    the squared distance, in float32, between each entry's pose position (its
+    first three pose values) and the anchor entry's."""
+    p = bank.poses[: entries * bank.pose_entry_bytes].view(np.float32).reshape(entries, -1)[:, :3]
+    d = p - p[anchor]
+    return (d * d).sum(axis=1, dtype=np.float32)
+
+
 # ---------------------------------------------------------------- config 3
 
 def kv_ring_geometry(layers: int, capacity: int, window: int, heads: int, head_dim: int,
