@@ -56,6 +56,7 @@ extern "C" {
 #define PCS_E_SHAPE (-4)   /* restore target layout differs from the snapshot's  */
 #define PCS_E_HIP (-5)     /* a HIP runtime call failed                          */
 #define PCS_E_CORRUPT (-6) /* an imported image does not match its fingerprints  */
+#define PCS_E_PROBE (-7)   /* the caller's probe reported a failure              */
 
 #define PCS_CHUNK_BYTES 4096u
 
@@ -334,6 +335,61 @@ typedef struct pcs_bank_part {
 int pcs_bank_shrink(pcs_ctx *ctx, const pcs_bank_part *h_parts, uint32_t nparts, uint64_t n_entries,
                     const float *d_scores, uint64_t keep, uint32_t *d_kept);
 
+/*
+ * Discovering PCS by measurement (Sec. 4, procedure FINGERPRINT).  The
+ * model's runtime state is k components H = {h_0 .. h_{k-1}} (pcs_buf
+ * descriptors of the live session, taken at the anchor of the probe).  The
+ * caller supplies the probe: given a snapshot that holds exactly the
+ * components whose mask byte is 1 (in component order), it restores them
+ * into a fresh session (the other components keep a fresh session's
+ * state), runs its leave-and-return trajectory and writes the
+ * return-consistency distance D >= 0 of the continuation to *d_out
+ * (Sec. 5's conformance metric; e.g. the fraction of output chunks whose
+ * fingerprint differs from an uninterrupted run, via pcs_fingerprint and
+ * pcs_classify).  It returns 0, or nonzero to abort.  The probe must not
+ * modify the live components.
+ *
+ * The call runs:
+ *   1. necessity: for each h_i, probe a snapshot of H without h_i; h_i is
+ *      necessary iff D > eps;
+ *   2. sufficiency: probe a snapshot of exactly the necessary set N; if
+ *      D <= eps, PCS = N;
+ *   3. redundancy fallback: otherwise add, one at a time, the component
+ *      whose addition gives the smallest D (ties: the lowest index) until
+ *      D <= eps or every component is in;
+ *   4. PCS and Derivable = H \ PCS go to *out.
+ * With control >= 0 it then runs Sec. 4's control against necessity tests
+ * that pass for the wrong reason: a full snapshot in which component
+ * `control` holds a wrong value (the lowest bit of its first byte flipped)
+ * is probed, and the control passes iff D > eps.
+ *
+ * Every snapshot is a full checkpoint of the subset, created before and
+ * deleted after its probe; the call waits for nothing itself (the probe may).
+ * Errors: k > 64, control >= k, an empty control component, a null probe ->
+ * PCS_E_INVAL; a probe returning nonzero or a negative or NaN distance ->
+ * PCS_E_PROBE; checkpoint errors as pcs_checkpoint.
+ */
+#define PCS_DISCOVER_MAX 64u
+
+typedef int (*pcs_probe_fn)(void *user, pcs_snap snap, const uint8_t *h_mask, uint32_t k, double *d_out);
+
+typedef struct pcs_discovery {
+    uint8_t pcs[PCS_DISCOVER_MAX];        /* 1: component i is in the returned PCS             */
+    uint8_t necessary[PCS_DISCOVER_MAX];  /* 1: step 1 found component i necessary             */
+    double d_without[PCS_DISCOVER_MAX];   /* step 1: D with component i left out               */
+    uint32_t added[PCS_DISCOVER_MAX];     /* step 3: components added, in order                */
+    double d_necessary;                   /* step 2: D with exactly the necessary set          */
+    double d_final;                       /* D with the returned PCS                           */
+    double d_control;                     /* D of the control (-1 without a control)           */
+    uint32_t n_added;                     /* entries of added[]                                */
+    uint32_t probes;                      /* probe runs                                        */
+    int32_t control_ok;                   /* 1 passed, 0 failed, -1 no control                 */
+    int32_t converged;                    /* 1 iff d_final <= eps                              */
+} pcs_discovery;
+
+int pcs_discover(pcs_ctx *ctx, const pcs_buf *h_components, uint32_t k, double eps, int32_t control,
+                 pcs_probe_fn probe, void *user, pcs_discovery *out);
+
 /* Arena accounting: bytes in use, bytes free, largest free block, live handles. */
 int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t *largest_free,
                     uint64_t *live_handles);
@@ -343,7 +399,8 @@ int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t
  * events on the context stream.  pcs_kernel_time waits for the stream, then
  * reports the number of launches and their summed duration in milliseconds
  * for the kernel family `name` ("hash", "pack_hash", "pack", "copy",
- * "verify", "merkle", "classify", "incremental", "map", "shrink") since the last reset, and resets it.
+ * "verify", "merkle", "classify", "incremental", "map", "shrink", "flip") since the last reset, and
+ * resets it.
  */
 int pcs_set_timing(pcs_ctx *ctx, int enable);
 int pcs_kernel_time(pcs_ctx *ctx, const char *name, uint64_t *launches, double *total_ms);

@@ -71,6 +71,8 @@ def _L():
         lib.orc_dirty.restype = u64
         lib.orc_bank_select.argtypes = [p, u32, u32, p]
         lib.orc_bank_select.restype = ctypes.c_int
+        lib.orc_philox4x32_10.argtypes = [p, p, p]
+        lib.orc_philox4x32_10.restype = None
         _lib = lib
     return _lib
 
@@ -365,3 +367,15 @@ def bank_shrink(parts, scores, keep: int):
         a = _bytes(data)[:n * eb].reshape(n, eb) if n else np.zeros((0, eb), dtype=np.uint8)
         out.append(a[kept.astype(np.int64)].reshape(-1).copy())
     return kept, out
+
+
+# ---------------------------------------------------------------- Philox4x32-10
+
+def philox4x32_10(counter, key):
+    """One Philox4x32-10 block: 4 uint32 outputs for a 4-word counter and a
+    2-word key (SC'11 definition)."""
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    _L().orc_philox4x32_10(c.ctypes.data, k.ctypes.data, out.ctypes.data)
+    return out

@@ -395,3 +395,36 @@ int orc_bank_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *ke
     free(order);
     return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random      */
+/* numbers: as easy as 1, 2, 3", SC'11): the counter-based generator   */
+/* the mock world model of the discovery procedure (Sec. 4) draws from */
+/* (the paper's RNG state is a Philox key and counter, Table 1).       */
+/* ------------------------------------------------------------------ */
+
+/* One block: 10 rounds over a 4 x 32-bit counter with a 2 x 32-bit key.
+ * A round multiplies counter words 0 and 2 by the two Philox constants
+ * into 64-bit products, and mixes the high halves with the other words and
+ * the key; the key is bumped by the two Weyl constants between rounds. */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
+}

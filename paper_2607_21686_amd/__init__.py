@@ -20,11 +20,12 @@ import ctypes
 
 import torch
 
-from ._lib import (CHUNK_BYTES, CKPT_HASH, E_CORRUPT, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_SHAPE, EXPORTS, FLAT,
-                   MUST_SNAPSHOT, RECOMPUTABLE, RING, PcsBankPart, PcsBuf, PcsError, PcsSnapInfo, lib)
+from ._lib import (CHUNK_BYTES, CKPT_HASH, E_CORRUPT, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_PROBE, E_SHAPE, EXPORTS,
+                   FLAT, MUST_SNAPSHOT, PROBE_FN, RECOMPUTABLE, RING, PcsBankPart, PcsBuf, PcsDiscovery, PcsError,
+                   PcsSnapInfo, lib)
 
 __all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_count", "keep_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
-           "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "E_CORRUPT",
+           "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "E_CORRUPT", "E_PROBE",
            "EXPORTS"]
 
 _L = lib()  # fails loudly if the HIP library is missing
@@ -155,6 +156,67 @@ class Context:
         n = len(chunks_per_buf)
         cpb = chunks_per_buf if isinstance(chunks_per_buf, ctypes.Array) else u64_array(chunks_per_buf)
         self._check(_L.pcs_classify(self._h, _dev_ptr(hashes), K, cpb, n, _dev_ptr(bitmap), _dev_ptr(labels)))
+
+    def distance(self, ref_hashes, bufs) -> float:
+        """Return-consistency distance at chunk granularity: the fraction of
+        the 4096-byte chunks of `bufs` whose fingerprint differs from
+        ref_hashes (device int64 tensor, one value per chunk, as fingerprint()
+        writes them).  Fingerprinting and comparison run on the GPU
+        (pcs_fingerprint, then pcs_classify with K = 2); the differing
+        chunks are counted from the bitmap on the host."""
+        import numpy as np
+        arr = _array(bufs)
+        n = len(bufs)
+        cpb = (ctypes.c_uint64 * max(1, n))()
+        total = ctypes.c_uint64()
+        if n:
+            self._check(_L.pcs_chunk_counts(arr, n, cpb, ctypes.byref(total)))
+        T = int(total.value)
+        if T == 0:
+            return 0.0
+        if ref_hashes.numel() < T:
+            raise ValueError("ref_hashes holds fewer values than the buffers have chunks")
+        h = torch.empty(2 * T, dtype=torch.int64, device=ref_hashes.device)
+        h[:T].copy_(ref_hashes.reshape(-1)[:T])
+        self.fingerprint(bufs, h[T:])
+        words = sum((int(cpb[i]) + 63) // 64 for i in range(n))
+        bitmap = torch.zeros(max(1, words), dtype=torch.int64, device=h.device)
+        labels = torch.zeros(max(1, n), dtype=torch.uint8, device=h.device)
+        self.classify(h, 2, cpb, bitmap, labels)
+        bits = np.unpackbits(bitmap.cpu().numpy().view(np.uint8)).sum()
+        return float(bits) / T
+
+    def discover(self, components, probe, eps: float = 0.0, control: int = -1) -> dict:
+        """Discovering PCS by measurement (pcs_discover; Sec. 4, procedure
+        FINGERPRINT).  components: descriptors of the live session's
+        components at the probe's anchor.  probe(snap, mask) -> D restores the
+        snapshot (the components whose mask flag is 1, in order) into a fresh
+        session, runs the leave-and-return trajectory and returns its
+        distance, e.g. with distance().  control: the component given a
+        wrong value for the control (-1: none).  An exception raised by the
+        probe is re-raised here."""
+        errors = []
+
+        def cb(user, snap, mask_ptr, k, d_out):
+            try:
+                d_out[0] = float(probe(int(snap), tuple(int(mask_ptr[i]) for i in range(k))))
+                return 0
+            except BaseException as e:  # handed back to the caller below
+                errors.append(e)
+                return 1
+
+        fn = PROBE_FN(cb)
+        out = PcsDiscovery()
+        k = len(components)
+        st = _L.pcs_discover(self._h, _array(components) if k else None, k, float(eps), int(control), fn, None,
+                             ctypes.byref(out))
+        if errors:
+            raise errors[0]
+        self._check(st)
+        return dict(pcs=list(out.pcs[:k]), necessary=list(out.necessary[:k]), d_without=list(out.d_without[:k]),
+                    d_necessary=out.d_necessary, d_final=out.d_final, d_control=out.d_control,
+                    added=list(out.added[:out.n_added]), probes=int(out.probes), control_ok=int(out.control_ok),
+                    converged=int(out.converged))
 
     # -- contract ----------------------------------------------------------
     def checkpoint(self, plan, parent: int = 0, hash: bool = False, chunk_hashes=None, roots=None,

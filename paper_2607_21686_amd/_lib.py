@@ -15,21 +15,21 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libpcs.so")
 
 OK = 0
-E_INVAL, E_NOMEM, E_HANDLE, E_SHAPE, E_HIP, E_CORRUPT = -1, -2, -3, -4, -5, -6
+E_INVAL, E_NOMEM, E_HANDLE, E_SHAPE, E_HIP, E_CORRUPT, E_PROBE = -1, -2, -3, -4, -5, -6, -7
 CHUNK_BYTES = 4096
 FLAT, RING = 0, 1
 RECOMPUTABLE, MUST_SNAPSHOT = 0, 1
 CKPT_HASH = 1
 
 _ERRNAMES = {E_INVAL: "PCS_E_INVAL", E_NOMEM: "PCS_E_NOMEM", E_HANDLE: "PCS_E_HANDLE",
-             E_SHAPE: "PCS_E_SHAPE", E_HIP: "PCS_E_HIP", E_CORRUPT: "PCS_E_CORRUPT"}
+             E_SHAPE: "PCS_E_SHAPE", E_HIP: "PCS_E_HIP", E_CORRUPT: "PCS_E_CORRUPT", E_PROBE: "PCS_E_PROBE"}
 
 # Every symbol include/pcs.h declares.
 EXPORTS = ("pcs_ctx_create", "pcs_ctx_destroy", "pcs_last_error", "pcs_chunk_counts", "pcs_fingerprint",
            "pcs_classify", "pcs_checkpoint", "pcs_checkpoint_batch", "pcs_restore", "pcs_restore_batch",
            "pcs_restore_verify", "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload",
            "pcs_snapshot_view", "pcs_snapshot_hashes",
-           "pcs_export", "pcs_import", "pcs_bank_shrink", "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
+           "pcs_export", "pcs_import", "pcs_bank_shrink", "pcs_discover", "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
 
 
 class PcsBuf(ctypes.Structure):
@@ -48,6 +48,22 @@ class PcsSnapInfo(ctypes.Structure):
 
 class PcsBankPart(ctypes.Structure):
     _fields_ = [("src", ctypes.c_uint64), ("dst", ctypes.c_uint64), ("entry_bytes", ctypes.c_uint64)]
+
+
+DISCOVER_MAX = 64
+
+
+class PcsDiscovery(ctypes.Structure):
+    _fields_ = [("pcs", ctypes.c_uint8 * DISCOVER_MAX), ("necessary", ctypes.c_uint8 * DISCOVER_MAX),
+                ("d_without", ctypes.c_double * DISCOVER_MAX), ("added", ctypes.c_uint32 * DISCOVER_MAX),
+                ("d_necessary", ctypes.c_double), ("d_final", ctypes.c_double), ("d_control", ctypes.c_double),
+                ("n_added", ctypes.c_uint32), ("probes", ctypes.c_uint32), ("control_ok", ctypes.c_int32),
+                ("converged", ctypes.c_int32)]
+
+
+# int (*)(void *user, pcs_snap snap, const uint8_t *h_mask, uint32_t k, double *d_out)
+PROBE_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_uint64, ctypes.POINTER(ctypes.c_uint8),
+                            ctypes.c_uint32, ctypes.POINTER(ctypes.c_double))
 
 
 class PcsError(RuntimeError):
@@ -90,6 +106,7 @@ def load():
         "pcs_export": ([P, U64, P, U64, PU64], I),
         "pcs_import": ([P, P, U64, PU64], I),
         "pcs_bank_shrink": ([P, ctypes.POINTER(PcsBankPart), U32, U64, P, U64, P], I),
+        "pcs_discover": ([P, PB, U32, ctypes.c_double, ctypes.c_int32, PROBE_FN, P, ctypes.POINTER(PcsDiscovery)], I),
         "pcs_arena_stats": ([P, PU64, PU64, PU64, PU64], I),
         "pcs_set_timing": ([P, I], I),
         "pcs_kernel_time": ([P, ctypes.c_char_p, PU64, ctypes.POINTER(ctypes.c_double)], I),

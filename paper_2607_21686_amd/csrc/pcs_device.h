@@ -125,6 +125,8 @@ hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, con
                                      const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
                                      uint64_t *total, uint64_t *total_host, hipStream_t s);
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
+// Flips the lowest bit of the byte at device address addr.
+hipError_t launch_flip_bit(uint64_t addr, hipStream_t s);
 // Bank shrink: flags[i] = entry i is among the `keep` best-ranked (score
 // order of pcs_bank_shrink), offsets = exclusive scan of flags, kept = the
 // kept indices in increasing order.

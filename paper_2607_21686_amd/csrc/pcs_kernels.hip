@@ -927,6 +927,13 @@ __global__ __launch_bounds__(256) void k_gather_entries(uint64_t src, uint64_t d
     }
 }
 
+// Flips the lowest bit of one byte (the control of the discovery procedure
+// gives a component a wrong value this way).
+__global__ void k_flip_bit(uint64_t addr)
+{
+    if (threadIdx.x == 0) *(g_u8 *)addr ^= 1;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
@@ -1082,6 +1089,12 @@ hipError_t launch_gather_entries(uint64_t src, uint64_t dst, uint64_t entry_byte
         hipLaunchKernelGGL(k_gather_entries<4>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
     else
         hipLaunchKernelGGL(k_gather_entries<1>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
+    return hipGetLastError();
+}
+
+hipError_t launch_flip_bit(uint64_t addr, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_flip_bit, dim3(1), dim3(64), 0, s, addr);
     return hipGetLastError();
 }
 

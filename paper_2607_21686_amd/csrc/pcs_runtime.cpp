@@ -1539,4 +1539,111 @@ int pcs_import(pcs_ctx *c, const void *h_src, uint64_t size, pcs_snap *out)
     return PCS_OK;
 }
 
+int pcs_discover(pcs_ctx *c, const pcs_buf *comps, uint32_t k, double eps, int32_t control, pcs_probe_fn probe,
+                 void *user, pcs_discovery *out)
+{
+    if (!c) return PCS_E_INVAL;
+    if (!out) return fail(c, PCS_E_INVAL, "null result");
+    if (!probe) return fail(c, PCS_E_INVAL, "null probe");
+    if (k > PCS_DISCOVER_MAX) return fail(c, PCS_E_INVAL, "at most %u components", PCS_DISCOVER_MAX);
+    if (k && !comps) return fail(c, PCS_E_INVAL, "null components");
+    if (!(eps >= 0)) return fail(c, PCS_E_INVAL, "eps must be a number >= 0");
+    if (control >= (int32_t)k) return fail(c, PCS_E_INVAL, "control component %d out of range", control);
+    std::vector<uint64_t> chunks(k ? k : 1);
+    if (k) {
+        if (int st = pcs_chunk_counts(comps, k, chunks.data(), nullptr))
+            return fail(c, st, "invalid component descriptor");
+    }
+    if (control >= 0 && chunks[control] == 0)
+        return fail(c, PCS_E_INVAL, "control component %d is empty", control);
+    memset(out, 0, sizeof *out);
+    out->d_control = -1;
+    out->control_ok = -1;
+    uint32_t probes = 0;
+
+    // One probe: a full snapshot of the masked components (with component
+    // `corrupt` given a wrong value), the caller's probe, then the delete.
+    auto run = [&](const uint8_t *mask, int32_t corrupt, double *d) -> int {
+        std::vector<pcs_buf> plan;
+        int32_t pos = -1;
+        for (uint32_t i = 0; i < k; ++i) {
+            if (!mask[i]) continue;
+            if ((int32_t)i == corrupt) pos = (int32_t)plan.size();
+            plan.push_back(comps[i]);
+        }
+        pcs_snap snap = 0;
+        if (int st = pcs_checkpoint(c, plan.data(), (uint32_t)plan.size(), 0, 0, nullptr, nullptr, nullptr, &snap))
+            return st;
+        if (pos >= 0) {
+            const auto nd = lookup(c, snap);
+            const uint64_t addr = c->arena_dev + nd->payload_off + nd->comp_off[pos];
+            if (int st = launch(c, "flip", [&] { return launch_flip_bit(addr, c->stream); })) {
+                pcs_delete(c, snap);
+                return st;
+            }
+        }
+        ++probes;
+        double dv = 0;
+        const int r = probe(user, snap, mask, k, &dv);
+        pcs_delete(c, snap);
+        if (r != 0) return fail(c, PCS_E_PROBE, "probe returned %d", r);
+        if (!(dv >= 0)) return fail(c, PCS_E_PROBE, "probe returned a negative or NaN distance");
+        *d = dv;
+        return PCS_OK;
+    };
+
+    uint8_t mask[PCS_DISCOVER_MAX], cur[PCS_DISCOVER_MAX];
+    // 1. necessity: leave each component out in turn.
+    for (uint32_t i = 0; i < k; ++i) {
+        memset(mask, 1, k);
+        mask[i] = 0;
+        double d = 0;
+        if (int st = run(mask, -1, &d)) return st;
+        out->d_without[i] = d;
+        out->necessary[i] = d > eps ? 1 : 0;
+    }
+    // 2. sufficiency: exactly the necessary set.
+    uint32_t in = 0;
+    for (uint32_t i = 0; i < k; ++i) {
+        cur[i] = out->necessary[i];
+        in += cur[i];
+    }
+    double d = 0;
+    if (int st = run(cur, -1, &d)) return st;
+    out->d_necessary = d;
+    // 3. redundancy fallback: add the component that most reduces D.
+    while (d > eps && in < k) {
+        int32_t best = -1;
+        double best_d = 0;
+        for (uint32_t j = 0; j < k; ++j) {
+            if (cur[j]) continue;
+            memcpy(mask, cur, k);
+            mask[j] = 1;
+            double dj = 0;
+            if (int st = run(mask, -1, &dj)) return st;
+            if (best < 0 || dj < best_d) {
+                best = (int32_t)j;
+                best_d = dj;
+            }
+        }
+        cur[best] = 1;
+        ++in;
+        out->added[out->n_added++] = (uint32_t)best;
+        d = best_d;
+    }
+    memcpy(out->pcs, cur, k);
+    out->d_final = d;
+    out->converged = d <= eps ? 1 : 0;
+    // The control: the full state with one component given a wrong value.
+    if (control >= 0) {
+        memset(mask, 1, k);
+        double dc = 0;
+        if (int st = run(mask, control, &dc)) return st;
+        out->d_control = dc;
+        out->control_ok = dc > eps ? 1 : 0;
+    }
+    out->probes = probes;
+    return PCS_OK;
+}
+
 }  // extern "C"

@@ -68,3 +68,27 @@ def test_chunk_counts_validation_on_host():
     assert lib.pcs_chunk_counts(bad, 1, out, ctypes.byref(tot)) == _lib.E_INVAL
     bad = (B * 1)(B(ptr=4096, kind=1, row_bytes=32, capacity=8, head=0, window=4, outer=2, outer_stride=32))
     assert lib.pcs_chunk_counts(bad, 1, out, ctypes.byref(tot)) == _lib.E_INVAL
+
+
+def test_struct_layout_matches_c_compiler(tmp_path):
+    """Sizes and field offsets of every ABI struct as gcc lays them out from
+    include/pcs.h, against the ctypes declarations of the binding."""
+    import subprocess
+    from paper_2607_21686_amd import _lib
+    structs = {"pcs_buf": _lib.PcsBuf, "pcs_snap_info": _lib.PcsSnapInfo, "pcs_bank_part": _lib.PcsBankPart,
+               "pcs_discovery": _lib.PcsDiscovery}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "pcs.h"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
+        for f, _ in py._fields_:
+            lines.append('printf("%s.%s %%zu\\n", offsetof(%s, %s));' % (cname, f, cname, f))
+    lines.append("return 0; }")
+    c = tmp_path / "layout.c"
+    c.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(c)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n") if l)
+    for cname, py in structs.items():
+        assert int(got[cname]) == ctypes.sizeof(py), cname
+        for f, _ in py._fields_:
+            assert int(got["%s.%s" % (cname, f)]) == getattr(py, f).offset, (cname, f)
