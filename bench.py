@@ -46,7 +46,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="batch", choices=["batch", "kv-ring", "sweep", "bank", "markovian"],
+    ap.add_argument("--workload", default="batch",
+                    choices=["batch", "kv-ring", "sweep", "bank", "markovian", "shrink", "discover"],
                     help="batch (default, the headline) or one of the other seeded configurations")
     ap.add_argument("--sessions", type=int, default=1024)
     ap.add_argument("--cpu-sessions", type=int, default=384, help="oracle sample size (sessions)")
@@ -607,7 +608,98 @@ def run_markovian(args):
                   "restore_us_median": round(rs_us, 1), "fingerprint_2_replays_us_median": round(fp_us, 1)})
 
 
-OTHER = {"kv-ring": run_kv_ring, "sweep": run_sweep, "bank": run_bank, "markovian": run_markovian}
+def run_shrink(args):
+    """Relevance-keyed shrink of the memory bank at its full 512 entries:
+    restore the full bank from its snapshot, shrink it in place to 12% of
+    its entries ranked by pose distance to the anchor entry, and take an
+    incremental checkpoint of the shrunk bank against the full one."""
+    import torch
+    import paper_2607_21686_amd as P
+    import workloads as W
+    bank = W.config2(1)
+    E, le, pe = 512, bank.latent_entry_bytes, bank.pose_entry_bytes
+    lat = torch.from_numpy(bank.latents.copy()).cuda()
+    pos = torch.from_numpy(bank.poses.copy()).cuda()
+    ctx = P.Context(torch.empty(768 << 20, dtype=torch.uint8, device="cuda"))
+    full = ctx.checkpoint([P.flat(lat), P.flat(pos)], hash=True)
+    scores = torch.from_numpy(W.pose_scores(bank, E, 0)).cuda()
+    keep = P.keep_count(0.12, E)
+    full_dst = P.BufArray([P.flat(lat), P.flat(pos)])
+    shrunk = P.BufArray([P.flat(lat, keep * le), P.flat(pos, keep * pe)])
+    parts = [(lat, None, le), (pos, None, pe)]
+
+    def step():
+        ctx.restore(full, full_dst)
+        ctx.bank_shrink(parts, scores, keep)
+        ctx.delete(ctx.checkpoint(shrunk, parent=full))
+    t, kt = _timed(args, ctx, step, ["shrink", "incremental", "copy"])
+    n, ms = kt["shrink"]
+    kept = keep * (le + pe)
+    # In place: the kept entries are read and written twice (through scratch); scores read once.
+    alg = 4 * kept + 4 * E
+    return _line(args, E * (le + pe) / t / 1e9, t * 1e3, "relevance-keyed shrink of the memory bank: 512 entries of "
+                 "bf16 latents [16,60,104] + fp32 pose [7], keep 12%% (%d) by pose distance to the anchor, in place; "
+                 "then an incremental checkpoint of the shrunk bank" % keep,
+                 {"entries": E, "kept": keep, "bank_bytes": E * (le + pe)}, "shrink (rank, scan, place, gather)", alg,
+                 ms / args.steps, {"shrink_ms": round(ms / args.steps, 4),
+                                   "incremental_checkpoint_ms": round(kt["incremental"][1] / args.steps, 4),
+                                   "restore_full_bank_ms": round(kt["copy"][1] / args.steps, 4)})
+
+
+def run_discover(args):
+    """Discovering PCS by measurement on the mock world model (480x832
+    frames): necessity, sufficiency and redundancy fallback over subset
+    checkpoints, plus the RNG control; every probe restores into a fresh
+    session, runs a leave-and-return trajectory and is scored by GPU chunk
+    fingerprints."""
+    import torch
+    import paper_2607_21686_amd as P
+    from workloads.mock_world import MockSpec, initial_state, trajectory
+    from workloads.mock_world_gpu import MockWorldGPU
+    spec = MockSpec(height=480, width=832, bank_cap=64, entry_words=256, kv_words=1024)
+    init = initial_state(spec, 11)
+    wa, pa = trajectory(11, 24, 8)
+    live = MockWorldGPU.from_host(spec, init)
+    live.run(wa)
+    ctx = P.Context(torch.empty(512 << 20, dtype=torch.uint8, device="cuda"))
+    descs = P.BufArray([P.flat(t) for t in live.parts])
+    ref = MockWorldGPU(spec, [t.clone() for t in live.parts]).run(pa)
+    ref_h = torch.zeros(P.chunk_count(ref.numel()), dtype=torch.int64, device="cuda")
+    ctx.fingerprint([P.flat(ref)], ref_h)
+    moved = [0]
+
+    def probe(snap, mask):
+        w = MockWorldGPU.fresh(spec)
+        ctx.restore(snap, [P.flat(w.parts[i]) for i in range(len(mask)) if mask[i]])
+        moved[0] += 2 * sum(w.parts[i].numel() for i in range(len(mask)) if mask[i])
+        return ctx.distance(ref_h, [P.flat(w.run(pa))])
+
+    result = {}
+
+    def step():
+        result.update(ctx.discover(descs, probe, eps=0.0, control=1))
+    fams = ["pack", "copy", "hash", "classify", "merkle", "map", "flip"]
+    t, kt = _timed(args, ctx, step, fams)
+    lib_ms = sum(kt[f][1] for f in fams) / args.steps
+    n, ms = kt["pack"]
+    state = sum(spec.nbytes())
+    names = ("obs", "rng", "bank", "pose", "feat", "scratch", "kv_a", "kv_b")
+    # Each probe's subset is checkpointed once (read + write) and restored once;
+    # `moved` counted 2 x the subset per probe.
+    per_launch = int(moved[0] / (args.steps + args.warmup) / max(1, result.get("probes", 1)))
+    return _line(args, moved[0] / (args.steps + args.warmup) / t / 1e9, t * 1e3,
+                 "discovering PCS by measurement on a mock world model: 8 components (obs 480x832x3 u8, RNG, "
+                 "64-entry bank, pose, feature cache, scratch, an interchangeable context pair), 8-step away + "
+                 "8-step return probe, eps 0, RNG control", {"components": 8, "state_bytes": state},
+                 "subset checkpoints (pack)", per_launch, ms / max(1, n),
+                 {"probes": result.get("probes"), "pcs": [nm for nm, f in zip(names, result.get("pcs", [])) if f],
+                  "library_kernel_ms_per_discovery": round(lib_ms, 3),
+                  "model_and_host_ms_per_discovery": round(t * 1e3 - lib_ms, 3),
+                  "control_ok": result.get("control_ok")})
+
+
+OTHER = {"kv-ring": run_kv_ring, "sweep": run_sweep, "bank": run_bank, "markovian": run_markovian,
+         "shrink": run_shrink, "discover": run_discover}
 
 
 if __name__ == "__main__":

@@ -870,21 +870,28 @@ __device__ __forceinline__ uint32_t score_key(uint32_t bits)
 // Entry i is kept iff fewer than `keep` entries rank before it (a smaller
 // key, or an equal key at a lower index).  One lane per entry counts over
 // all keys, staged through LDS in tiles that every lane reads in the same
-// order (broadcast reads).
+// order (broadcast reads, four keys per read).  A tile is padded to a
+// multiple of four with the largest key at indices past the end, which
+// never rank before anything.
 __global__ __launch_bounds__(256) void k_shrink_rank(const uint32_t *__restrict__ scores, uint32_t n, uint32_t keep,
                                                      uint32_t *__restrict__ flags)
 {
-    __shared__ uint32_t tile[2048];
+    __shared__ __attribute__((aligned(16))) uint32_t tile[2048];
     const uint32_t i = blockIdx.x * 256 + threadIdx.x;
     const uint32_t ki = i < n ? score_key(scores[i]) : 0;
+    auto before = [&](uint32_t kj, uint32_t j) -> uint32_t { return (kj < ki || (kj == ki && j < i)) ? 1u : 0u; };
     uint32_t rank = 0;
     for (uint32_t base = 0; base < n; base += 2048) {
         const uint32_t m = n - base < 2048 ? n - base : 2048;
-        for (uint32_t j = threadIdx.x; j < m; j += 256) tile[j] = score_key(scores[base + j]);
+        const uint32_t m4 = (m + 3) & ~3u;
+        for (uint32_t j = threadIdx.x; j < m4; j += 256) tile[j] = j < m ? score_key(scores[base + j]) : 0xFFFFFFFFu;
         __syncthreads();
-        for (uint32_t j = 0; j < m; ++j) {
-            const uint32_t kj = tile[j];
-            rank += (kj < ki || (kj == ki && base + j < i)) ? 1u : 0u;
+        const uint4 *t4 = reinterpret_cast<const uint4 *>(tile);
+#pragma unroll 4
+        for (uint32_t q = 0; q < m4 / 4; ++q) {
+            const uint4 v = t4[q];
+            const uint32_t j = base + 4 * q;
+            rank += before(v.x, j) + before(v.y, j + 1) + before(v.z, j + 2) + before(v.w, j + 3);
         }
         __syncthreads();
     }
