@@ -593,10 +593,24 @@ def run_markovian(args):
             torch.cuda.synchronize()
             ts.append(time.perf_counter() - t0)
         return statistics.median(ts) * 1e6
+    def call(f, reps=200):
+        # Host time of the (asynchronous) call alone; the stream drains between calls.
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            f()
+            ts.append(time.perf_counter() - t0)
+        torch.cuda.synchronize()
+        return statistics.median(ts) * 1e6
     snap = ctx.checkpoint(plan)
     ck_us = lat(lambda: ctx.delete(ctx.checkpoint(plan)))
     rs_us = lat(lambda: ctx.restore(snap, dst))
     fp_us = lat(lambda: ctx.fingerprint(both, H))
+    ck_call = call(lambda: ctx.delete(ctx.checkpoint(plan)))
+    rs_call = call(lambda: ctx.restore(snap, dst))
+    one = torch.empty(1, dtype=torch.uint8, device="cuda")
+    floor_us = lat(lambda: one.fill_(1))      # any one-kernel launch + stream sync on this device
     ctx.delete(snap)
     fp_bytes = 2 * sum(x.numel() for x in r1)
     state = r1[0].numel() + r1[1].numel()
@@ -605,7 +619,11 @@ def run_markovian(args):
                  "6 fp16 decoys; fingerprint 2 replays, classify, checkpoint+restore {obs, RNG} (latency-bound)",
                  {"fingerprinted_bytes": fp_bytes, "state_bytes": state}, "k_hash (fingerprint)", fp_bytes, ms / n,
                  {"step_us": round(t * 1e6, 1), "checkpoint_us_median": round(ck_us, 1),
-                  "restore_us_median": round(rs_us, 1), "fingerprint_2_replays_us_median": round(fp_us, 1)})
+                  "restore_us_median": round(rs_us, 1), "fingerprint_2_replays_us_median": round(fp_us, 1),
+                  "checkpoint_call_us_median": round(ck_call, 1), "restore_call_us_median": round(rs_call, 1),
+                  "launch_sync_floor_us_median": round(floor_us, 1),
+                  "pack_kernel_us": round(1e3 * kt["pack"][1] / max(1, kt["pack"][0]), 2),
+                  "restore_kernel_us": round(1e3 * kt["copy"][1] / max(1, kt["copy"][0]), 2)})
 
 
 def run_shrink(args):

@@ -60,6 +60,16 @@ struct MerkleList {
 //              kernel: a workgroup finds its buffer and first run with short
 //              searches); jobs of at most kArgBufs buffers and kArgRuns runs.
 constexpr uint32_t kArgBufs = 8, kArgRuns = 64;
+// Small jobs (at most kSmallJobGroups groups) are cut into kSmallTiles
+// sub-tiles per group, so that a few groups still spread over many CUs.
+// Fingerprint and pack tiles then write one Merkle node per sub-tile (an
+// aligned 8-chunk subtree, which the Merkle lists reduce like group nodes).
+// Smaller tiles do not pay: a tile's fingerprint is bounded by one chunk's
+// XXH64 chain (128 dependent rounds per accumulator), which 8-chunk tiles
+// overlap with their loads.
+constexpr uint64_t kSmallJobGroups = 128;
+constexpr uint32_t kSmallTiles = 8;
+inline uint32_t tile_split(uint64_t ngroups) { return ngroups <= kSmallJobGroups ? kSmallTiles : 1; }
 struct GroupRef {
     uint32_t buf;
     uint32_t run;
@@ -99,7 +109,7 @@ hipError_t launch_group_map(const JobBuf *bufs, const Run *runs, uint32_t nbuf, 
                             hipStream_t s);
 template <class Tab>
 hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint32_t *flag_count,
-                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s);
+                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group = 1);
 template <class Tab>
 hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s);
 template <class Tab>

@@ -305,8 +305,11 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
     return GroupRef{b, find_run(t.runs, jb.run_begin, jb.run_count, (G - jb.group_begin) * kGroupChunks * kChunk)};
 }
 
-// Fingerprint tile kernel.  One workgroup = one 64-chunk group of one
-// buffer.  Step k moves the k-th SL-byte slice of every chunk of the group:
+// Fingerprint tile kernel.  One workgroup = one tile of CPW chunks of one
+// buffer: a whole 64-chunk group, or for small jobs an eighth of one, so
+// that a few groups still occupy many CUs (the tile's Merkle node is then an
+// aligned 8-chunk subtree).  Step k moves the k-th SL-byte slice of every
+// chunk of the tile:
 // all T lanes load it with coalesced 16-byte loads (SL/16 lanes per chunk
 // slice), kModePack stores it to the chunk's snapshot slot (zero-padding a
 // partial last chunk) and kModeVerify to the buffer's runs, and every lane
@@ -315,7 +318,7 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
 // XXH64 accumulators 2p and 2p+1, which read exactly bytes [16p, 16p+16) of
 // each 32-byte stripe.  kModeDiff / kModeVerify ballot one flag per chunk into
 // a per-group mask (the group is one bitmap word).
-template <class Tab, int MODE, int T, int SL>
+template <class Tab, int MODE, int T, int SL, int CPW>
 __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
                                             uint32_t *__restrict__ flag_count, uint64_t *__restrict__ flag_mask,
                                             uint64_t arena_base)
@@ -323,21 +326,24 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     constexpr uint32_t kSteps = kChunk / SL;
     constexpr uint32_t kRow = SL + 32;                  // padded LDS row: lane pairs of 8 chunks hit distinct banks
     constexpr uint32_t LPS = SL / 16;                   // lanes per chunk slice
-    constexpr int U = kGroupChunks * SL / 16 / T;       // granules per lane per step
+    constexpr int U = CPW * SL / 16 / T;                // granules per lane per step
+    constexpr uint32_t kTiles = kGroupChunks / CPW;     // tiles per 64-chunk group
     constexpr bool kFromSlots = MODE == kModeVerify;    // source is the snapshot, destination the runs
-    static_assert(U >= 1 && T % LPS == 0, "tile shape");
-    __shared__ __attribute__((aligned(16))) uint8_t tile[kGroupChunks * kRow];
+    static_assert(U >= 1 && T % LPS == 0 && kGroupChunks % CPW == 0, "tile shape");
+    static_assert(CPW == kGroupChunks || (MODE != kModeDiff && MODE != kModeVerify), "flag words need whole groups");
+    __shared__ __attribute__((aligned(16))) uint8_t tile[CPW * kRow];
     __shared__ ChunkLoc cloc[kGroupChunks];
-    __shared__ uint64_t leaves[kGroupChunks];
-    __shared__ uint32_t dflag[kGroupChunks];
+    __shared__ uint64_t leaves[CPW];
+    __shared__ uint32_t dflag[CPW];
 
-    const uint64_t G = blockIdx.x;
+    const uint64_t G = blockIdx.x / kTiles;
     const GroupRef gr = group_ref(tab, G);
     const JobBuf &jb = tab.bufs[gr.buf];
     const Run *runs = tab.runs;
     const uint32_t t = threadIdx.x;
-    const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
-    const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
+    const uint64_t c0 = (G - jb.group_begin) * kGroupChunks + (blockIdx.x % kTiles) * CPW;
+    if (c0 >= jb.nchunks) return;  // a buffer's last group may end before this tile
+    const uint32_t nv = (uint32_t)umin(CPW, jb.nchunks - c0);
     const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
     const g_u64 *man = (const g_u64 *)jb.manifest;
     chunk_table(jb, runs, gr.run, c0, nv, cloc);
@@ -382,7 +388,7 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     for (int k = 0; k < U; ++k) r[k] = load_granule(k, slot);
 
     const uint32_t ci = t >> 1, p = t & 1;
-    const bool hasher = t < 2 * kGroupChunks && ci < nv;
+    const bool hasher = t < 2 * CPW && ci < nv;
     const uint32_t len = hasher ? cloc[ci].len : 0;
     const uint32_t nst = len >> 5;
     uint64_t va = p ? 0 : P1 + P2;   // accumulator 2p   (seed 0)
@@ -431,7 +437,7 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
         __syncthreads();
     }
 
-    if (t < 2 * kGroupChunks) {
+    if (t < 2 * CPW) {
         const uint64_t oa = shfl64(va, (int)(t ^ 1) & 63);
         const uint64_t ob = shfl64(vb, (int)(t ^ 1) & 63);
         if (hasher && p == 0) {
@@ -480,7 +486,7 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     if (t < 64) {
         const uint64_t v = t < nv ? leaves[t] : 0;
         const uint64_t root = wave_merkle(v, nv);
-        if (t == 0 && nodes) nodes[G] = root;
+        if (t == 0 && nodes) nodes[blockIdx.x] = root;  // the tile's Merkle node (an aligned subtree)
         if (MODE == kModeDiff || MODE == kModeVerify) {
             const uint64_t mask = __ballot(t < nv && dflag[t] != 0);
             if (t == 0) {
@@ -596,28 +602,31 @@ __global__ __launch_bounds__(256) void k_merkle_small(const ArgLists L, const ui
 
 // ---------------------------------------------------------------- copies
 
-// Copy tile kernel: one workgroup moves one 64-chunk group, SL bytes of every
-// chunk per step, with coalesced 16-byte loads and stores (the shape of the
-// fused kernel without the hash).
+// Copy tile kernel: one workgroup moves one tile of CPW chunks (a 64-chunk
+// group, or an eighth of one in small jobs), SL bytes of every chunk per
+// step, with coalesced 16-byte loads and stores (the shape of the fused
+// kernel without the hash).
 //   PACK:    the buffer's runs -> the chunk slots of the snapshot; a partial
 //            last chunk is zero-padded to the end of its slot.
 //   !PACK:   the chunk slots (contiguous, or per chunk through a manifest of
 //            arena offsets) -> the destination buffer's runs; only logical
 //            bytes are written.
-template <class Tab, bool PACK, int T, int SL>
+template <class Tab, bool PACK, int T, int SL, int CPW>
 __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
 {
     constexpr uint32_t kSteps = kChunk / SL, LPS = SL / 16;
-    constexpr int U = kGroupChunks * SL / 16 / T;
-    static_assert(U >= 1 && T % LPS == 0, "tile shape");
+    constexpr int U = CPW * SL / 16 / T;
+    constexpr uint32_t kTiles = kGroupChunks / CPW;
+    static_assert(U >= 1 && T % LPS == 0 && kGroupChunks % CPW == 0, "tile shape");
     __shared__ ChunkLoc cloc[kGroupChunks];
-    const uint64_t G = blockIdx.x;
+    const uint64_t G = blockIdx.x / kTiles;
     const GroupRef gr = group_ref(tab, G);
     const JobBuf &jb = tab.bufs[gr.buf];
     const Run *runs = tab.runs;
     const uint32_t t = threadIdx.x;
-    const uint64_t c0 = (G - jb.group_begin) * kGroupChunks;
-    const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
+    const uint64_t c0 = (G - jb.group_begin) * kGroupChunks + (blockIdx.x % kTiles) * CPW;
+    if (c0 >= jb.nchunks) return;  // a buffer's last group may end before this tile
+    const uint32_t nv = (uint32_t)umin(CPW, jb.nchunks - c0);
     const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
     const g_u64 *man = (const g_u64 *)jb.manifest;
     chunk_table(jb, runs, gr.run, c0, nv, cloc);
@@ -855,6 +864,7 @@ __global__ __launch_bounds__(64) void k_labels(const Tab tab, const uint64_t *__
 constexpr int kPackLanes = 1024, kPackSlice = 512;
 constexpr int kHashLanes = 256, kHashSlice = 512;
 constexpr int kCopyLanes = 1024, kCopySlice = 1024;
+constexpr int kSmallLanes = 256;  // sub-tiles of small jobs: 8 chunks per workgroup
 
 // ---------------------------------------------------------------- bank shrink
 
@@ -956,26 +966,39 @@ hipError_t launch_group_map(const JobBuf *bufs, const Run *runs, uint32_t nbuf, 
 
 template <class Tab>
 hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint32_t *flag_count,
-                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s)
+                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group)
 {
     if (ngroups == 0) return hipSuccess;
-    const dim3 grid((uint32_t)ngroups);
+    const bool split = tiles_per_group != 1;
+    if (split && (mode != kModeHash && mode != kModePack)) return hipErrorInvalidValue;
+    const dim3 grid((uint32_t)(ngroups * tiles_per_group));
+    if (tiles_per_group == kSmallTiles) {
+        constexpr int kCPW = kGroupChunks / kSmallTiles;
+        if (mode == kModeHash)
+            hipLaunchKernelGGL((k_hash<Tab, kModeHash, kSmallLanes, kHashSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
+                               tab, nodes, flag_count, flag_mask, arena_base);
+        else
+            hipLaunchKernelGGL((k_hash<Tab, kModePack, kSmallLanes, kPackSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
+                               tab, nodes, flag_count, flag_mask, arena_base);
+        return hipGetLastError();
+    }
+    if (split) return hipErrorInvalidValue;
     switch (mode) {
     case kModeHash:
-        hipLaunchKernelGGL((k_hash<Tab, kModeHash, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, tab, nodes,
-                           flag_count, flag_mask, arena_base);
+        hipLaunchKernelGGL((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), 0, s,
+                           tab, nodes, flag_count, flag_mask, arena_base);
         break;
     case kModePack:
-        hipLaunchKernelGGL((k_hash<Tab, kModePack, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, tab, nodes,
-                           flag_count, flag_mask, arena_base);
+        hipLaunchKernelGGL((k_hash<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), 0, s,
+                           tab, nodes, flag_count, flag_mask, arena_base);
         break;
     case kModeDiff:
-        hipLaunchKernelGGL((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice>), grid, dim3(kHashLanes), 0, s, tab, nodes,
-                           flag_count, flag_mask, arena_base);
+        hipLaunchKernelGGL((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), 0, s,
+                           tab, nodes, flag_count, flag_mask, arena_base);
         break;
     case kModeVerify:
-        hipLaunchKernelGGL((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice>), grid, dim3(kPackLanes), 0, s, tab,
-                           nodes, flag_count, flag_mask, arena_base);
+        hipLaunchKernelGGL((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), 0,
+                           s, tab, nodes, flag_count, flag_mask, arena_base);
         break;
     default:
         return hipErrorInvalidValue;
@@ -983,16 +1006,28 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
     return hipGetLastError();
 }
 
+// Copies need no per-group output, so a small job is cut into sub-tiles here.
 template <class Tab>
 hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    if (pack)
-        hipLaunchKernelGGL((k_copy<Tab, true, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0,
-                           s, tab, arena_base);
-    else
-        hipLaunchKernelGGL((k_copy<Tab, false, kCopyLanes, kCopySlice>), dim3((uint32_t)ngroups), dim3(kCopyLanes), 0,
-                           s, tab, arena_base);
+    const uint32_t tiles = tile_split(ngroups);
+    const dim3 grid((uint32_t)(ngroups * tiles));
+    if (tiles == kSmallTiles) {
+        constexpr int kCPW = kGroupChunks / kSmallTiles;
+        if (pack)
+            hipLaunchKernelGGL((k_copy<Tab, true, kSmallLanes, kCopySlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
+                               arena_base);
+        else
+            hipLaunchKernelGGL((k_copy<Tab, false, kSmallLanes, kCopySlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
+                               arena_base);
+    } else if (pack) {
+        hipLaunchKernelGGL((k_copy<Tab, true, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), 0, s,
+                           tab, arena_base);
+    } else {
+        hipLaunchKernelGGL((k_copy<Tab, false, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), 0, s,
+                           tab, arena_base);
+    }
     return hipGetLastError();
 }
 
@@ -1114,7 +1149,7 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
 
 #define PCS_INSTANTIATE(Tab)                                                                                        \
     template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint32_t *, uint64_t *, uint64_t, \
-                                         hipStream_t);                                                            \
+                                         hipStream_t, uint32_t);                                                  \
     template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t);                     \
     template hipError_t launch_compact<Tab>(const Tab &, uint64_t, const uint64_t *, const uint64_t *, uint64_t,   \
                                             uint64_t *, hipStream_t);                                             \

@@ -553,10 +553,15 @@ int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &s
     const uint32_t S = (uint32_t)sess_nbufs.size();
     const uint64_t G = job.ngroups;
     const bool small = is_small(job) && S <= 1;
+    // A small job runs as sub-tiles: one Merkle node per sub-tile, and each
+    // buffer's list covers its sub-tiles (aligned subtrees of the same tree).
+    const uint32_t tiles = tile_split(G);
+    const uint64_t per_tile = kGroupChunks / tiles;
     std::vector<MerkleList> lists;
     if (want_roots) {
         for (uint32_t b = 0; b < n; ++b)
-            lists.push_back({job.bufs[b].group_begin, job.lays[b].ngroups, {root_dst[b].d[0], root_dst[b].d[1]}});
+            lists.push_back({job.bufs[b].group_begin * tiles, div_up(job.bufs[b].nchunks, per_tile),
+                             {root_dst[b].d[0], root_dst[b].d[1]}});
         uint64_t first = 0;
         for (uint32_t s = 0; s < S; ++s) {
             lists.push_back({first, sess_nbufs[s], {sroot_dst[s].d[0], sroot_dst[s].d[1]}});
@@ -565,9 +570,9 @@ int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &s
     }
     Carver cv;
     uint64_t o_nodes, o_sa, o_sb, o_roots;
-    cv.add(&o_nodes, 8 * G);
-    cv.add(&o_sa, 8 * std::max<uint64_t>(G, n));
-    cv.add(&o_sb, 8 * std::max<uint64_t>(G, n));
+    cv.add(&o_nodes, 8 * G * tiles);
+    cv.add(&o_sa, 8 * std::max<uint64_t>(G * tiles, n));
+    cv.add(&o_sb, 8 * std::max<uint64_t>(G * tiles, n));
     cv.add(&o_roots, 8 * n);
     Temp t(c);
     Staged sg;
@@ -580,7 +585,7 @@ int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &s
     hipStream_t s = c->stream;
     int st = with_tables(sg, [&](const auto &tab) {
         return launch(c, copy ? "pack_hash" : "hash", [&] {
-            return launch_tile(tab, G, copy ? kModePack : kModeHash, d_nodes, nullptr, nullptr, 0, s);
+            return launch_tile(tab, G, copy ? kModePack : kModeHash, d_nodes, nullptr, nullptr, 0, s, tiles);
         });
     });
     if (st || !want_roots) return st;
