@@ -657,20 +657,27 @@ __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
         }
         return v;
     };
-    // All lanes move the same slice of the group's chunks in lockstep (a
-    // barrier per step); the next slice's loads are issued before this
-    // slice's stores.
+    // The lanes move the tile in lockstep steps (a barrier per step); the
+    // next step's loads are issued before this step's stores.  Chunk c moves
+    // its slices in an order rotated by c and the tile index, so that a
+    // step's accesses cover every offset within a chunk instead of one (all
+    // tiles touching the same offsets at once loads the HBM channels
+    // unevenly; the rotation is worth 3-10% on copies).
     uint4 v[U], n[U];
+    auto off = [&](int k, uint32_t step) -> uint32_t {
+        const uint32_t c = (k * T + t) / LPS;
+        return ((step + c + blockIdx.x) % kSteps) * SL + slot;
+    };
 #pragma unroll
-    for (int k = 0; k < U; ++k) v[k] = load(k, slot);
+    for (int k = 0; k < U; ++k) v[k] = load(k, off(k, 0));
     for (uint32_t step = 0; step < kSteps; ++step) {
-        const uint32_t x = step * SL + slot;
         if (step + 1 < kSteps) {
 #pragma unroll
-            for (int k = 0; k < U; ++k) n[k] = load(k, x + SL);
+            for (int k = 0; k < U; ++k) n[k] = load(k, off(k, step + 1));
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
+            const uint32_t x = off(k, step);
             if (PACK) {
                 if (sa[k]) store16_nt(sa[k] + x, v[k]);
             } else if (x < gl[k]) {
