@@ -137,7 +137,8 @@ def traffic(fetch_db, write_db, sessions=1024, restored=512):
         rows = cur.execute(q, (counter,)).fetchall()
         pick = lambda pat: [v for n, v in rows if pat in n]
         calib = max(pick("rocclr_copyBuffer"))
-        return {"pack": pick("k_hash<pcs::DevTables, 1,"), "copy": pick("k_copy<pcs::DevTables, false,"),
+        return {"pack": pick("k_hash<pcs::DevTables, 1, 1024, 512, 64>"),
+                "copy": pick("k_copy<pcs::DevTables, false, 1024, 1024, 64>"),
                 "calib": calib}
 
     f, w = per_kernel(fetch_db, "FETCH_SIZE"), per_kernel(write_db, "WRITE_SIZE")
@@ -155,13 +156,14 @@ def traffic(fetch_db, write_db, sessions=1024, restored=512):
                 "dispatches": [len(f[kind]), len(w[kind])], "traffic_bytes_per_launch": t,
                 "algorithmic_bytes_per_launch": alg, "traffic_over_algorithmic": round(t / alg, 5)}
 
-    rec = {"kernel": "k_hash<DevTables, pack> (fused pack + fingerprint)",
+    rec = {"kernel": "k_hash<DevTables, pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)",
            "workload": "batched suspend/resume, %d sessions x %d B of state" % (sessions, state),
            "sessions": sessions,
            "calibration_copy_bytes": 1 << 30, "calibration_fetch_KiB": round(f["calib"], 1),
            "calibration_write_KiB": round(w["calib"], 1), "fetch_scale": round(fs, 6), "write_scale": round(ws, 6)}
     rec.update(one("pack", sessions))
-    rec["restore_kernel"] = dict(kernel="k_copy<DevTables, unpack> (%d sessions)" % restored, **one("copy", restored))
+    rec["restore_kernel"] = dict(kernel="k_copy<DevTables, unpack, 1024 lanes, 1 KiB slices, 64 chunks> (%d sessions)"
+                                 % restored, **one("copy", restored))
     rec["kernel_source_sha256"] = kernel_source_sha()
     rec["commands"] = [
         "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/prof_fetch -o fetch -- python3 bench.py --steps 2 --warmup 1 "
