@@ -128,9 +128,13 @@ hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_
                          hipStream_t s);
 hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64_t *scratch_a,
                                uint64_t *scratch_b, hipStream_t s);
-hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total,
-                       hipStream_t s);
+hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total, hipStream_t s,
+                       uint64_t *total_host = nullptr);
 constexpr uint64_t kScanCompactMaxGroups = 4096;
+// Small incremental jobs of at most this many groups scan and compact in one
+// workgroup (one launch); larger ones scan in one workgroup and compact with
+// one workgroup per group.
+constexpr uint64_t kScanCompactFusedGroups = 16;
 hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint32_t *counts,
                                      const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
                                      uint64_t *total, uint64_t *total_host, hipStream_t s);

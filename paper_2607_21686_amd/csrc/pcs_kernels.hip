@@ -722,11 +722,18 @@ __device__ void scan_counts(const uint32_t *counts, uint64_t n, uint64_t *offset
     __syncthreads();
 }
 
+// Exclusive scan of per-group counts; the total also goes to the caller's
+// pinned host word when one is given.
 __global__ __launch_bounds__(1024) void k_scan(const uint32_t *__restrict__ counts, uint64_t n,
-                                               uint64_t *__restrict__ offsets, uint64_t *__restrict__ total)
+                                               uint64_t *__restrict__ offsets, uint64_t *__restrict__ total,
+                                               uint64_t *total_host)
 {
     __shared__ uint64_t sums[2][1024];
     scan_counts(counts, n, offsets, total, sums);
+    if (threadIdx.x == 1023 && total_host) {
+        *(volatile uint64_t *)total_host = *total;
+        __threadfence_system();
+    }
 }
 
 // Slot assignment for one chunk: dirty chunks get slots in (buffer, chunk)
@@ -1093,9 +1100,9 @@ hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64
 }
 
 hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total,
-                       hipStream_t s)
+                       hipStream_t s, uint64_t *total_host)
 {
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, counts, n, offsets, total);
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, counts, n, offsets, total, total_host);
     return hipGetLastError();
 }
 
@@ -1117,7 +1124,7 @@ hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, 
     hipLaunchKernelGGL(k_shrink_rank, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint32_t *>(scores), n,
                        keep, flags);
     if (hipError_t e = hipGetLastError()) return e;
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, flags, (uint64_t)n, offsets, total);
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, flags, (uint64_t)n, offsets, total, nullptr);
     if (hipError_t e = hipGetLastError()) return e;
     hipLaunchKernelGGL(k_shrink_place, dim3(blocks), dim3(256), 0, s, flags, offsets, n, kept);
     return hipGetLastError();

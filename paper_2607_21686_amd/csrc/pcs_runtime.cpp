@@ -1149,10 +1149,19 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         c->free_counts.pop_back();
         uint64_t *host_word = &c->counts_dev[node->count_slot];
         const uint64_t top = node->pay_top;
-        if ((st = launch(c, "incremental", [&] {
-                 return launch_scan_compact_small(sg.arg, G, d_cnt, d_mask, top, d_list, d_total, host_word, s);
-             })))
-            return st;
+        if (G <= kScanCompactFusedGroups) {
+            if ((st = launch(c, "incremental", [&] {
+                     return launch_scan_compact_small(sg.arg, G, d_cnt, d_mask, top, d_list, d_total, host_word, s);
+                 })))
+                return st;
+        } else {
+            if ((st = launch(c, "incremental", [&] { return launch_scan(d_cnt, G, d_offs, d_total, s, host_word); })))
+                return st;
+            if ((st = launch(c, "incremental", [&] {
+                     return launch_compact(sg.arg, G, d_mask, d_offs, top, d_list, s);
+                 })))
+                return st;
+        }
         if ((st = launch(c, "incremental", [&] {
                  return launch_pack_dirty(sg.arg, d_list, d_total, T, payload_top_dev, s);
              })))
