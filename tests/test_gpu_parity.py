@@ -56,6 +56,36 @@ def test_fingerprint_flat_sizes(ctx, pcs):
     assert gs == s
 
 
+@pytest.mark.parametrize("groups", [16, 17, 127, 128, 129])
+def test_small_job_boundary(ctx, pcs, groups):
+    """Jobs of at most 128 groups run as 8-chunk sub-tiles (one Merkle node
+    per sub-tile), larger ones as whole groups; both sides of the boundary,
+    with ragged tails: fingerprints, roots, the fused checkpoint and the
+    copy round trip."""
+    rng = np.random.default_rng(900 + groups)
+    sizes = [(groups - 3) * 64 * 4096 + 4096 * 5 + 77, 37 * 4096 + 100, 3]   # groups-2, 1 and 1 groups
+    assert sum((oracle.chunk_count(n) + 63) // 64 for n in sizes) == groups
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    d = [dev(b) for b in bufs]
+    descs = [pcs.flat(t, b.size) for t, b in zip(d, bufs)]
+    log("small-job boundary:", groups, "groups")
+    h, r, s = oracle_fp(bufs)
+    gh, gr, gs = gpu_fp(ctx, pcs, descs, h.size)
+    assert np.array_equal(gh, h) and np.array_equal(gr, r) and gs == s
+    ch = zeros_u64(h.size)
+    snap = ctx.checkpoint(descs, hash=True, chunk_hashes=ch)
+    assert np.array_equal(u64(ch)[:h.size], h)
+    pay = torch.empty(ctx.info(snap)["stored_bytes"], dtype=torch.uint8, device="cuda")
+    ctx.payload(snap, pay)
+    assert np.array_equal(host(pay), oracle.pack(bufs))
+    plain = ctx.checkpoint(descs)
+    outs = [torch.zeros(max(1, n), dtype=torch.uint8, device="cuda") for n in sizes]
+    ctx.restore(plain, [pcs.flat(o, n) for o, n in zip(outs, sizes)])
+    assert all(np.array_equal(host(o)[:n], b) for o, n, b in zip(outs, sizes, bufs))
+    ctx.delete(snap)
+    ctx.delete(plain)
+
+
 def test_fingerprint_each_size_alone(ctx, pcs):
     rng = np.random.default_rng(11)
     for n in FLAT_SIZES + [1 << 20, (1 << 20) + 3]:
