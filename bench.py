@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="batch",
-                    choices=["batch", "kv-ring", "sweep", "bank", "markovian", "shrink", "discover"],
+                    choices=["batch", "kv-ring", "sweep", "bank", "markovian", "shrink", "discover", "export"],
                     help="batch (default, the headline) or one of the other seeded configurations")
     ap.add_argument("--sessions", type=int, default=1024)
     ap.add_argument("--cpu-sessions", type=int, default=384, help="oracle sample size (sessions)")
@@ -718,8 +718,68 @@ def run_discover(args):
                   "control_ok": result.get("control_ok")})
 
 
+def run_export(args):
+    """Durable images across a process boundary: export (device -> host
+    image) and import (host image -> device, re-fingerprinted and compared
+    before the handle exists) of 16 sessions of the batch workload's shape,
+    into pinned and into pageable host memory.  Host-link bound; reported
+    beside the HBM numbers, never as them."""
+    import numpy as np
+    import torch
+    import paper_2607_21686_amd as P
+    import workloads as W
+    S = 16
+    plan = W.config5_plan(4, sessions=S)
+    g = plan.ring
+    rings, obs, rngs = W.config5_device(plan, 4)
+    ctx = P.Context(torch.empty(3 << 30, dtype=torch.uint8, device="cuda"))
+    snaps = [ctx.checkpoint([P.ring(rings[s], g.outer, g.capacity, g.row_bytes, plan.heads[s], g.window),
+                             P.flat(obs[s]), P.flat(rngs[s])], hash=True) for s in range(S)]
+    size = ctx.export_size(snaps[0])
+    pinned = [torch.empty(size, dtype=torch.uint8, pin_memory=True) for _ in range(S)]
+    pageable = [np.empty(size, dtype=np.uint8) for _ in range(S)]
+
+    def rate(f, reps):
+        for _ in range(args.warmup):
+            f()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            f()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / reps
+
+    def exp(bufs):
+        for s in range(S):
+            ctx.export(snaps[s], bufs[s])
+
+    def imp(bufs):
+        for s in range(S):
+            ctx.delete(ctx.import_image(bufs[s]))
+    reps = max(1, args.steps // 2)
+    t_exp_p = rate(lambda: exp(pinned), reps)
+    ctx.kernel_time("hash")
+    ctx.set_timing(True)
+    t_imp_p = rate(lambda: imp(pinned), reps)
+    ctx.set_timing(False)
+    n, ms = ctx.kernel_time("hash")
+    t_exp_g = rate(lambda: exp(pageable), reps)
+    t_imp_g = rate(lambda: imp(pageable), reps)
+    total = S * size
+    state = g.window_bytes + plan.obs_bytes + plan.rng_bytes
+    gbs = lambda t: round(total / t / 1e9, 2)
+    return _line(args, total / (t_exp_p + t_imp_p) / 1e9, (t_exp_p + t_imp_p) * 1e3,
+                 "durable images: export + import (with device re-verification) of %d sessions of %d B of state "
+                 "(KV window 4x2x2048x8x128 bf16 ring, obs 480x832x3 u8, RNG 16 B), pinned host memory" % (S, state),
+                 {"sessions": S, "image_bytes_per_session": size},
+                 "k_hash (import re-fingerprint, one session per launch)", state, ms / max(1, n),
+                 {"export_pinned_GBps": gbs(t_exp_p), "import_pinned_GBps": gbs(t_imp_p),
+                  "export_pageable_GBps": gbs(t_exp_g), "import_pageable_GBps": gbs(t_imp_g),
+                  "note": "host-link bound (PCIe); value counts image bytes moved per second"})
+
+
 OTHER = {"kv-ring": run_kv_ring, "sweep": run_sweep, "bank": run_bank, "markovian": run_markovian,
-         "shrink": run_shrink, "discover": run_discover}
+         "shrink": run_shrink, "discover": run_discover, "export": run_export}
 
 
 if __name__ == "__main__":

@@ -89,6 +89,20 @@ class BufArray:
         return len(self.bufs)
 
 
+def _host_ptr(a):
+    """Address and byte size of a contiguous host buffer (numpy array or CPU tensor)."""
+    import numpy as np
+    if isinstance(a, torch.Tensor):
+        if a.is_cuda or not a.is_contiguous():
+            raise ValueError("expected a contiguous CPU tensor")
+        return a.data_ptr(), a.numel() * a.element_size()
+    if isinstance(a, np.ndarray):
+        if not a.flags["C_CONTIGUOUS"]:
+            raise ValueError("expected a contiguous array")
+        return a.ctypes.data, a.nbytes
+    raise TypeError("expected a numpy array or a CPU tensor")
+
+
 def _array(bufs):
     if isinstance(bufs, BufArray):
         return bufs.arr
@@ -266,21 +280,41 @@ class Context:
         self._check(_L.pcs_snapshot_view(self._h, snap, ctypes.byref(a), ctypes.byref(n)))
         return int(a.value), int(n.value)
 
-    def export(self, snap: int):
-        """The snapshot's self-contained host image (numpy uint8)."""
-        import numpy as np
+    def export_size(self, snap: int) -> int:
+        """Bytes of the snapshot's self-contained image."""
         size = ctypes.c_uint64()
         self._check(_L.pcs_export(self._h, snap, None, 0, ctypes.byref(size)))
-        img = np.empty(size.value, dtype=np.uint8)
-        self._check(_L.pcs_export(self._h, snap, img.ctypes.data_as(ctypes.c_void_p), img.size, ctypes.byref(size)))
-        return img
+        return int(size.value)
 
-    def import_image(self, img) -> int:
-        """A new full snapshot from an image written by export (verified)."""
+    def export(self, snap: int, out=None):
+        """The snapshot's self-contained host image: into `out` (a CPU uint8
+        torch tensor, e.g. pinned memory, or a numpy uint8 array of at least
+        export_size() bytes) and returned, or into a new numpy array."""
         import numpy as np
-        a = np.ascontiguousarray(img, dtype=np.uint8)
+        size = self.export_size(snap)
+        if out is None:
+            out = np.empty(size, dtype=np.uint8)
+        ptr, cap = _host_ptr(out)
+        if cap < size:
+            raise ValueError("export needs %d bytes, out holds %d" % (size, cap))
+        n = ctypes.c_uint64()
+        self._check(_L.pcs_export(self._h, snap, ctypes.c_void_p(ptr), cap, ctypes.byref(n)))
+        return out
+
+    def import_image(self, img, nbytes: int | None = None) -> int:
+        """A new full snapshot from an image written by export (verified on
+        the device).  img: numpy uint8 array, bytes, or CPU uint8 tensor."""
+        import numpy as np
+        if not isinstance(img, (np.ndarray, torch.Tensor)):
+            img = np.frombuffer(bytes(img), dtype=np.uint8)
+        if isinstance(img, np.ndarray):
+            img = np.ascontiguousarray(img, dtype=np.uint8)
+        ptr, cap = _host_ptr(img)
+        size = cap if nbytes is None else nbytes
+        if size > cap:
+            raise ValueError("nbytes exceeds the image buffer")
         out = ctypes.c_uint64()
-        self._check(_L.pcs_import(self._h, a.ctypes.data_as(ctypes.c_void_p), a.size, ctypes.byref(out)))
+        self._check(_L.pcs_import(self._h, ctypes.c_void_p(ptr), size, ctypes.byref(out)))
         return int(out.value)
 
     def bank_shrink(self, parts, scores, keep: int, kept=None):

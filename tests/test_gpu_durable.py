@@ -81,6 +81,43 @@ def test_export_of_incremental_chain(pcs):
     ctx.close()
 
 
+def test_export_into_caller_buffers_and_import_from_tensors(pcs):
+    """Images written into caller memory (a pinned tensor, an oversized numpy
+    array) equal the oracle's and import from a CPU tensor or a prefix."""
+    obs, rs, g, ring = state(9)
+    logical = [obs, rs, oracle.ring_window(ring, g.outer, g.outer_stride, g.capacity, g.row_bytes, g.head, g.window)]
+    want = np.frombuffer(oracle.export_image(logical, [(0, 0, 0, 0), (0, 0, 0, 0), (1, g.row_bytes, g.window, g.outer)]),
+                         dtype=np.uint8)
+    ctx = pcs.Context(arena(64 << 20))
+    d = [dev(obs), dev(rs), dev(ring)]
+    s = ctx.checkpoint(plan_of(pcs, d[0], d[1], d[2], g), hash=True)
+    size = ctx.export_size(s)
+    assert size == want.size
+    pinned = torch.empty(size, dtype=torch.uint8, pin_memory=True)
+    log("export into pinned memory")
+    assert ctx.export(s, pinned) is pinned
+    assert np.array_equal(pinned.numpy(), want)
+    big = np.full(size + 4096, 0xEE, dtype=np.uint8)
+    ctx.export(s, big)
+    assert np.array_equal(big[:size], want) and (big[size:] == 0xEE).all()
+    with pytest.raises(ValueError):
+        ctx.export(s, np.empty(size - 1, dtype=np.uint8))
+    before = ctx.arena_stats()
+    for img, n in ((pinned, None), (big, size)):
+        s2 = ctx.import_image(img, n)
+        outs = [torch.empty_like(d[0]), torch.empty_like(d[1]), dev(np.zeros(g.ring_bytes, dtype=np.uint8))]
+        ctx.restore(s2, [pcs.flat(outs[0]), pcs.flat(outs[1]), pcs.ring(outs[2], g.outer, g.capacity, g.row_bytes, 5,
+                                                                          g.window)])
+        assert np.array_equal(host(outs[0]), obs) and np.array_equal(host(outs[1]), rs)
+        ctx.delete(s2)
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.import_image(big)                       # the trailing bytes make the image inconsistent
+    assert e.value.code == pcs.E_CORRUPT
+    assert ctx.arena_stats() == before
+    ctx.delete(s)
+    ctx.close()
+
+
 def test_import_refuses_corruption(pcs):
     obs, rs, g, ring = state(6)
     logical = [obs, rs]
