@@ -358,14 +358,26 @@ template <class F>
 int launch(pcs_ctx *c, const char *name, F &&f)
 {
     hipEvent_t a = nullptr, b = nullptr;
+    auto drop = [&] {
+        if (a) (void)hipEventDestroy(a);
+        if (b) (void)hipEventDestroy(b);
+    };
     if (c->timing) {
-        HIP_TRY(c, hipEventCreate(&a));
-        HIP_TRY(c, hipEventCreate(&b));
-        HIP_TRY(c, hipEventRecord(a, c->stream));
+        hipError_t te = hipEventCreate(&a);
+        if (te == hipSuccess) te = hipEventCreate(&b);
+        if (te == hipSuccess) te = hipEventRecord(a, c->stream);
+        if (te != hipSuccess) {
+            drop();
+            return hip_fail(c, te, "timing event");
+        }
     }
     const hipError_t e = f();
     if (c->timing) {
-        HIP_TRY(c, hipEventRecord(b, c->stream));
+        const hipError_t te = hipEventRecord(b, c->stream);
+        if (te != hipSuccess) {
+            drop();
+            return hip_fail(c, te, "timing event");
+        }
         c->timers[name].push_back({a, b});
     }
     if (e != hipSuccess) return hip_fail(c, e, name);
