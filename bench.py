@@ -101,7 +101,8 @@ def summarize(dbs):
 
 
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "k_hash_copy_batch1024_traffic.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_21686_amd", "csrc", f) for f in ("pcs_kernels.hip", "pcs_device.h")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_21686_amd", "csrc", f)
+                  for f in ("pcs_kernels.hip", "pcs_device.h", "pcs_layout.h")]
 
 
 def kernel_source_sha():

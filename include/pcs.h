@@ -78,7 +78,8 @@ typedef uint64_t pcs_snap; /* opaque snapshot handle; 0 is never a valid handle 
  * One candidate buffer of a session's runtime state.
  *
  * PCS_FLAT: `nbytes` bytes starting at `ptr`.  `ptr` must be 16-byte aligned;
- *   nbytes may be any value, including 0.  Ring fields are ignored.
+ *   nbytes may be any value, including 0, as long as ptr + nbytes stays
+ *   below 2^64.  Ring fields are ignored.
  *
  * PCS_RING: the windowed KV context of the paper's addressable-memory model
  *   (Table 1; Sec. 7.11: a context capped by a local window and written at
@@ -90,8 +91,10 @@ typedef uint64_t pcs_snap; /* opaque snapshot handle; 0 is never a valid handle 
  *   bytes are ring 0's window rows in order, then ring 1's, and so on:
  *   nbytes = outer * window * row_bytes (pass that value or 0).
  *   Requirements: ptr, row_bytes and outer_stride multiples of 16;
- *   1 <= window <= capacity; head < capacity;
- *   outer_stride >= capacity * row_bytes (rings do not overlap).
+ *   0 <= window <= capacity (an empty window holds no bytes); head <
+ *   capacity; outer <= 2^30; outer_stride >= capacity * row_bytes when
+ *   outer > 1 (rings do not overlap); ptr + (outer - 1) * outer_stride +
+ *   capacity * row_bytes stays below 2^64.
  *
  * Fingerprints and snapshots of a ring cover its logical window, so they do
  * not depend on the head offset: a window restored at a different head
@@ -291,9 +294,14 @@ int pcs_snapshot_hashes(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_dst, uint64_t c
  *   the payload (components 4096-aligned, zero padded).
  *
  * pcs_import rebuilds a full snapshot (with fingerprints) from such an image
- * in this context, fingerprints the imported bytes on the device and returns
- * PCS_E_CORRUPT, creating no handle, if any chunk or root differs from the
- * image.  It waits for the stream.
+ * of `size` bytes in this context, fingerprints the imported bytes on the
+ * device and returns PCS_E_CORRUPT, creating no handle, if any chunk or root
+ * differs from the image.  The header is checked on the host before any byte
+ * is copied: a wrong magic, version or flags, nonzero reserved fields, a ring
+ * whose shape does not give its size, totals that do not add up, sums that
+ * overflow 64 bits, or a size other than the one the header implies are
+ * PCS_E_CORRUPT too.  It waits for the stream (also on errors, so the image
+ * may be freed when it returns).
  */
 int pcs_export(pcs_ctx *ctx, pcs_snap snap, void *h_dst, uint64_t cap, uint64_t *written);
 int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);

@@ -9,7 +9,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libpcs.so")
 SOURCES = [os.path.join(HERE, "csrc", "pcs_kernels.hip"), os.path.join(HERE, "csrc", "pcs_runtime.cpp")]
-HEADERS = [os.path.join(HERE, "csrc", "pcs_device.h"), os.path.join(ROOT, "include", "pcs.h")]
+HEADERS = [os.path.join(HERE, "csrc", h) for h in ("pcs_device.h", "pcs_layout.h", "pcs_host.h")] + [
+    os.path.join(ROOT, "include", "pcs.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -103,23 +103,6 @@ __device__ uint64_t wave_merkle(uint64_t v, uint32_t m)
     return v;
 }
 
-// The run of a buffer that holds a logical offset, with the physical
-// displacement of that run and where it ends.
-struct Cursor {
-    const Run *runs;
-    uint32_t idx, last;  // current run, last run of the buffer
-    uint64_t run_end;    // logical end of the current run
-    uint64_t delta;      // physical address minus logical offset (mod 2^64)
-    uint64_t nbytes;
-};
-
-__device__ __forceinline__ void cursor_load(Cursor &c)
-{
-    const Run r = c.runs[c.idx];
-    c.delta = r.addr - r.lstart;
-    c.run_end = c.idx < c.last ? c.runs[c.idx + 1].lstart : c.nbytes;
-}
-
 // The run of [begin, begin + count) that holds logical offset L: the largest
 // index whose lstart <= L (runs are sorted by lstart, the first at 0).
 __device__ __forceinline__ uint32_t find_run(const Run *runs, uint32_t begin, uint32_t count, uint64_t L)
@@ -130,18 +113,6 @@ __device__ __forceinline__ uint32_t find_run(const Run *runs, uint32_t begin, ui
         if (runs[mid].lstart <= L) lo = mid; else hi = mid;
     }
     return lo;
-}
-
-__device__ __forceinline__ Cursor cursor_seek(const Run *runs, uint32_t begin, uint32_t count,
-                                              uint64_t nbytes, uint64_t L)
-{
-    Cursor c;
-    c.runs = runs;
-    c.last = begin + count - 1;
-    c.nbytes = nbytes;
-    c.idx = find_run(runs, begin, count, L);
-    cursor_load(c);
-    return c;
 }
 
 // Device addresses arrive as integers; casting them to the global address

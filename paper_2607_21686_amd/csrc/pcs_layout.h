@@ -1,0 +1,98 @@
+// pcs_layout.h -- descriptors and constants shared by the host runtime and
+// the gfx950 kernels of libpcs: plain structs with fixed layouts, no HIP.
+// Internal to the library (not part of the C ABI).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pcs {
+
+constexpr uint64_t kChunk = 4096;       // fingerprint and snapshot granule (bytes)
+constexpr uint32_t kGroupChunks = 64;   // chunks per work group and per bitmap word
+
+// A maximal physically contiguous piece of a buffer's logical byte stream:
+// logical bytes [lstart, next run's lstart) live at addr onwards.  A flat
+// buffer is one run; a ring window is at most two runs per ring (before and
+// after the wrap), merged where physically adjacent.
+struct Run {
+    uint64_t lstart;
+    uint64_t addr;
+};
+
+// One buffer of a job.  Every kernel grids over 64-chunk groups of one
+// buffer; group_begin is this buffer's first group in the job.
+struct JobBuf {
+    uint64_t nbytes;          // logical bytes
+    uint64_t nchunks;         // ceil(nbytes / 4096)
+    uint64_t chunk_begin;     // first chunk of this buffer in job-wide chunk order
+    uint64_t group_begin;     // first 64-chunk group of this buffer in the job
+    uint64_t payload;         // device address of chunk 0's 4096-byte slot (pack dst, restore src)
+    uint64_t manifest;        // restore: device address of uint64 arena offsets, one per chunk
+                              // incremental pack: where this buffer's new manifest entries go
+    uint64_t hash_dst[2];     // device addresses of chunk 0's fingerprint outputs (0 = none)
+    uint64_t root_dst[2];     // device addresses of the root outputs (0 = none)
+    uint64_t parent_hash;     // incremental: device address of the parent's chunk-0 fingerprint;
+                              // verified restore: of the snapshot's stored chunk-0 fingerprint
+    uint64_t parent_chunks;   // incremental: chunks the parent held for this buffer
+    uint64_t parent_manifest; // incremental: parent's manifest entries (0 if the parent is full)
+    uint64_t parent_slot0;    // incremental, full parent: arena offset of the parent's chunk-0 slot
+    uint32_t run_begin;       // this buffer's runs in the job's run table
+    uint32_t run_count;
+    uint32_t pad[2];
+};
+static_assert(sizeof(JobBuf) == 128, "JobBuf layout");
+
+// A list reduced by the Merkle kernel: values [begin, begin + count) of the
+// input array; the root goes to dst[0] / dst[1] (0 = none) and scratch[idx].
+struct MerkleList {
+    uint64_t begin;
+    uint64_t count;
+    uint64_t dst[2];
+};
+
+// Where a launch finds its buffer and run tables.
+//   DevTables: in device memory (uploaded per call), with a group map
+//              written by k_group_map that gives each group its buffer and
+//              the run holding its first byte; any job size.
+//   ArgTables: carried in the kernel arguments themselves (no upload, no map
+//              kernel: a workgroup finds its buffer and first run with short
+//              searches); jobs of at most kArgBufs buffers and kArgRuns runs.
+constexpr uint32_t kArgBufs = 8, kArgRuns = 64;
+// Small jobs (at most kSmallJobGroups groups) are cut into kSmallTiles
+// sub-tiles per group, so that a few groups still spread over many CUs.
+// Fingerprint and pack tiles then write one Merkle node per sub-tile (an
+// aligned 8-chunk subtree, which the Merkle lists reduce like group nodes).
+// Smaller tiles do not pay: a tile's fingerprint is bounded by one chunk's
+// XXH64 chain (128 dependent rounds per accumulator), which 8-chunk tiles
+// overlap with their loads.
+constexpr uint64_t kSmallJobGroups = 128;
+constexpr uint32_t kSmallTiles = 8;
+inline uint32_t tile_split(uint64_t ngroups) { return ngroups <= kSmallJobGroups ? kSmallTiles : 1; }
+struct GroupRef {
+    uint32_t buf;
+    uint32_t run;
+};
+struct DevTables {
+    const JobBuf *bufs;
+    const Run *runs;
+    const GroupRef *map;
+    uint32_t nbuf;
+    uint32_t pad;
+};
+struct ArgTables {
+    uint32_t nbuf;
+    uint32_t pad;
+    JobBuf bufs[kArgBufs];
+    Run runs[kArgRuns];
+};
+// Merkle lists carried in the kernel arguments: the first nbuf_lists reduce
+// group nodes to buffer roots, the rest reduce those roots to session roots
+// (their begin/count index the buffer lists).
+struct ArgLists {
+    uint32_t nbuf_lists;
+    uint32_t nlists;
+    MerkleList lists[kArgBufs + 1];
+};
+
+}  // namespace pcs

@@ -20,97 +20,14 @@
 
 #include "../../include/pcs.h"
 #include "pcs_device.h"
+#include "pcs_host.h"
 
 namespace pcs {
 namespace {
 
-constexpr uint64_t kAlign = 4096;
 constexpr uint64_t kMaxGroups = (1ULL << 32) / 256 - 1;  // grid limit of the 256-lane kernels
 constexpr uint32_t kStagingSlots = 8;
 constexpr uint32_t kCountSlots = 4096;
-
-uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
-uint64_t div_up(uint64_t x, uint64_t a) { return (x + a - 1) / a; }
-
-// First-fit allocator over [0, size) in 4096-byte units.
-class Arena {
-  public:
-    void init(uint64_t size)
-    {
-        size_ = size;
-        used_ = 0;
-        free_.clear();
-        if (size) free_[0] = size;
-    }
-    bool alloc(uint64_t bytes, uint64_t *off)
-    {
-        bytes = std::max<uint64_t>(kAlign, round_up(bytes, kAlign));
-        for (auto it = free_.begin(); it != free_.end(); ++it) {
-            if (it->second < bytes) continue;
-            *off = it->first;
-            const uint64_t rest = it->second - bytes, noff = it->first + bytes;
-            free_.erase(it);
-            if (rest) free_[noff] = rest;
-            used_ += bytes;
-            return true;
-        }
-        return false;
-    }
-    // Highest-address fit: [end - bytes, end) of the highest free range that
-    // holds it.  Incremental payload reservations come from the top, so the
-    // part a reservation gives back (its low end) merges with free space.
-    bool alloc_top(uint64_t bytes, uint64_t *off)
-    {
-        bytes = std::max<uint64_t>(kAlign, round_up(bytes, kAlign));
-        for (auto it = free_.rbegin(); it != free_.rend(); ++it) {
-            if (it->second < bytes) continue;
-            const uint64_t start = it->first, size = it->second;
-            *off = start + size - bytes;
-            if (size == bytes) free_.erase(start);
-            else free_[start] = size - bytes;
-            used_ += bytes;
-            return true;
-        }
-        return false;
-    }
-    void release(uint64_t off, uint64_t bytes)
-    {
-        bytes = std::max<uint64_t>(kAlign, round_up(bytes, kAlign));
-        used_ -= bytes;
-        auto it = free_.emplace(off, bytes).first;
-        auto nx = std::next(it);
-        if (nx != free_.end() && it->first + it->second == nx->first) {
-            it->second += nx->second;
-            free_.erase(nx);
-        }
-        if (it != free_.begin()) {
-            auto pv = std::prev(it);
-            if (pv->first + pv->second == it->first) {
-                pv->second += it->second;
-                free_.erase(it);
-            }
-        }
-    }
-    uint64_t used() const { return used_; }
-    uint64_t size() const { return size_; }
-    uint64_t largest() const
-    {
-        uint64_t m = 0;
-        for (auto &kv : free_) m = std::max(m, kv.second);
-        return m;
-    }
-
-  private:
-    uint64_t size_ = 0, used_ = 0;
-    std::map<uint64_t, uint64_t> free_;
-};
-
-// A plan buffer resolved into its logical byte stream.
-struct Layout {
-    uint32_t kind;
-    uint64_t nbytes, nchunks, ngroups;
-    uint64_t row_bytes, window, outer;  // RING shape (restore compatibility)
-};
 
 struct SnapNode;
 
@@ -197,72 +114,13 @@ int hip_fail(pcs_ctx *c, hipError_t e, const char *what)
         if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr);        \
     } while (0)
 
-bool mul_ok(uint64_t a, uint64_t b, uint64_t *out)
+// Validates one descriptor and appends its runs (see pcs::describe); the
+// reason for a rejection becomes the context's last error.
+int check_buf(pcs_ctx *c, const pcs_buf &b, uint32_t idx, Layout *lay, std::vector<Run> *runs)
 {
-    return !__builtin_mul_overflow(a, b, out);
-}
-
-// Validates one descriptor and appends its runs (logical start, physical
-// address), merging physically adjacent pieces.
-int describe(pcs_ctx *c, const pcs_buf &b, uint32_t idx, Layout *lay, std::vector<Run> *runs)
-{
-    if (b.flags != 0) return fail(c, PCS_E_INVAL, "buffer %u: flags must be 0", idx);
-    Layout L{};
-    L.kind = b.kind;
-    std::vector<Run> rs;
-    if (b.kind == PCS_FLAT) {
-        if (b.nbytes && (b.ptr == 0 || b.ptr % 16))
-            return fail(c, PCS_E_INVAL, "buffer %u: flat ptr must be non-null and 16-byte aligned", idx);
-        L.nbytes = b.nbytes;
-        rs.push_back({0, b.ptr});
-    } else if (b.kind == PCS_RING) {
-        if (b.row_bytes == 0 || b.row_bytes % 16 || b.ptr % 16 || b.outer_stride % 16)
-            return fail(c, PCS_E_INVAL, "buffer %u: ring ptr, row_bytes and outer_stride must be multiples of 16", idx);
-        if (b.capacity == 0 || b.window > b.capacity || b.head >= b.capacity)
-            return fail(c, PCS_E_INVAL, "buffer %u: ring needs 0 <= window <= capacity and head < capacity", idx);
-        uint64_t ring_span, win_bytes, total;
-        if (!mul_ok(b.capacity, b.row_bytes, &ring_span) || !mul_ok(b.window, b.row_bytes, &win_bytes) ||
-            !mul_ok(win_bytes, b.outer, &total))
-            return fail(c, PCS_E_INVAL, "buffer %u: ring size overflows", idx);
-        if (b.outer > 1 && b.outer_stride < ring_span)
-            return fail(c, PCS_E_INVAL, "buffer %u: outer_stride < capacity*row_bytes (rings overlap)", idx);
-        if (b.nbytes != 0 && b.nbytes != total)
-            return fail(c, PCS_E_INVAL, "buffer %u: ring nbytes must be 0 or outer*window*row_bytes", idx);
-        if (total && b.ptr == 0) return fail(c, PCS_E_INVAL, "buffer %u: null ring pointer", idx);
-        if (b.outer > (1ULL << 30)) return fail(c, PCS_E_INVAL, "buffer %u: too many rings", idx);
-        L.nbytes = total;
-        L.row_bytes = b.row_bytes;
-        L.window = b.window;
-        L.outer = b.outer;
-        uint64_t lpos = 0;
-        auto add = [&](uint64_t addr, uint64_t len) {
-            if (len == 0) return;
-            if (!rs.empty()) {
-                const uint64_t prev_end_l = lpos;  // logical end so far
-                const Run &p = rs.back();
-                if (p.addr + (prev_end_l - p.lstart) == addr) {
-                    lpos += len;
-                    return;
-                }
-            }
-            rs.push_back({lpos, addr});
-            lpos += len;
-        };
-        for (uint64_t o = 0; o < b.outer && total; ++o) {
-            const uint64_t base = b.ptr + o * b.outer_stride;
-            const uint64_t first = std::min(b.window, b.capacity - b.head);
-            add(base + b.head * b.row_bytes, first * b.row_bytes);
-            add(base, (b.window - first) * b.row_bytes);
-        }
-        if (rs.empty()) rs.push_back({0, b.ptr});
-    } else {
-        return fail(c, PCS_E_INVAL, "buffer %u: unknown kind %u", idx, b.kind);
-    }
-    L.nchunks = div_up(L.nbytes, kChunk);
-    L.ngroups = div_up(L.nchunks, kGroupChunks);
-    *lay = L;
-    runs->insert(runs->end(), rs.begin(), rs.end());
-    return PCS_OK;
+    std::string why;
+    const int st = describe(b, idx, lay, runs, &why);
+    return st ? fail(c, st, "%s", why.c_str()) : PCS_OK;
 }
 
 // A job under construction: buffer table, run table, and group totals.
@@ -278,7 +136,7 @@ int add_buffers(pcs_ctx *c, Job &job, const pcs_buf *bufs, uint32_t n, uint32_t 
     for (uint32_t i = 0; i < n; ++i) {
         Layout lay;
         const size_t r0 = job.runs.size();
-        const int st = describe(c, bufs[i], idx0 + i, &lay, &job.runs);
+        const int st = check_buf(c, bufs[i], idx0 + i, &lay, &job.runs);
         if (st) return st;
         if (job.runs.size() > (1ULL << 31)) return fail(c, PCS_E_INVAL, "too many runs");
         JobBuf jb{};
@@ -783,48 +641,6 @@ int restore_impl(pcs_ctx *c, const pcs_snap *snaps, uint32_t m, const pcs_buf *d
 }
 
 
-// ---------------------------------------------------------------- snapshot images
-//
-// A self-contained host image of a snapshot (little-endian):
-//   [0, 8)    magic "PCSIMG01"
-//   [8, 12)   u32 version (1)         [12, 16)  u32 nbufs n
-//   [16, 24)  u64 total chunks T      [24, 32)  u64 state bytes
-//   [32, 40)  u64 payload bytes       [40, 48)  u64 flags (0)
-//   n x 48 B  per buffer: u32 kind, u32 0, u64 nbytes, u64 row_bytes,
-//             u64 window, u64 outer, u64 0   (ring fields 0 for flat buffers)
-//   (n+1) x 8 buffer roots, then the session root
-//   T x 8     chunk fingerprints, buffer-major
-//   zero padding to a 4096-byte boundary, then the payload in the canonical
-//   full-snapshot layout (components 4096-aligned, zero padded).
-constexpr char kImageMagic[8] = {'P', 'C', 'S', 'I', 'M', 'G', '0', '1'};
-constexpr uint64_t kImageHead = 48, kImageDesc = 48;
-
-struct ImageLayout {
-    uint64_t roots_off, hashes_off, data_off, size, payload;
-    std::vector<uint64_t> comp_off;
-};
-
-ImageLayout image_layout(const std::vector<Layout> &bufs, uint64_t T)
-{
-    ImageLayout L;
-    const uint64_t n = bufs.size();
-    L.roots_off = kImageHead + kImageDesc * n;
-    L.hashes_off = L.roots_off + 8 * (n + 1);
-    L.data_off = round_up(L.hashes_off + 8 * T, kAlign);
-    L.payload = 0;
-    for (auto &b : bufs) {
-        L.comp_off.push_back(L.payload);
-        L.payload += b.nchunks * kChunk;
-    }
-    L.size = L.data_off + L.payload;
-    return L;
-}
-
-void put32(uint8_t *p, uint32_t v) { memcpy(p, &v, 4); }
-void put64(uint8_t *p, uint64_t v) { memcpy(p, &v, 8); }
-uint32_t get32(const uint8_t *p) { uint32_t v; memcpy(&v, p, 4); return v; }
-uint64_t get64(const uint8_t *p) { uint64_t v; memcpy(&v, p, 8); return v; }
-
 // Fingerprints flat device regions (e.g. payload components) into device
 // arrays: chunk hashes (buffer-major), buffer roots, session root.
 int fingerprint_regions(pcs_ctx *c, const std::vector<uint64_t> &addr, const std::vector<uint64_t> &nbytes,
@@ -913,7 +729,7 @@ int pcs_chunk_counts(const pcs_buf *bufs, uint32_t n, uint64_t *chunks, uint64_t
     for (uint32_t i = 0; i < n; ++i) {
         Layout lay;
         std::vector<Run> rs;
-        if (int st = describe(nullptr, bufs[i], i, &lay, &rs)) return st;
+        if (int st = check_buf(nullptr, bufs[i], i, &lay, &rs)) return st;
         if (chunks) chunks[i] = lay.nchunks;
         t += lay.nchunks;
     }
@@ -1422,27 +1238,13 @@ int pcs_export(pcs_ctx *c, pcs_snap snap, void *h_dst, uint64_t cap, uint64_t *w
     if (!nd->settled) settle(c, true);
     const uint32_t n = nd->nbufs;
     const uint64_t T = nd->total_chunks;
-    const ImageLayout L = image_layout(nd->bufs, T);
+    ImageLayout L;
+    if (!image_layout(nd->bufs, T, &L)) return fail(c, PCS_E_INVAL, "snapshot too large for an image");
     if (written) *written = L.size;
     if (!h_dst) return PCS_OK;
     if (cap < L.size) return fail(c, PCS_E_INVAL, "image needs %llu bytes", (unsigned long long)L.size);
     uint8_t *img = (uint8_t *)h_dst;
-    memset(img, 0, L.data_off);
-    memcpy(img, kImageMagic, 8);
-    put32(img + 8, 1);
-    put32(img + 12, n);
-    put64(img + 16, T);
-    put64(img + 24, nd->state_bytes);
-    put64(img + 32, L.payload);
-    for (uint32_t b = 0; b < n; ++b) {
-        uint8_t *d = img + kImageHead + kImageDesc * b;
-        const Layout &y = nd->bufs[b];
-        put32(d, y.kind);
-        put64(d + 8, y.nbytes);
-        put64(d + 16, y.kind == PCS_RING ? y.row_bytes : 0);
-        put64(d + 24, y.kind == PCS_RING ? y.window : 0);
-        put64(d + 32, y.kind == PCS_RING ? y.outer : 0);
-    }
+    write_image_header(img, nd->bufs, T, nd->state_bytes, L);
     hipStream_t s = c->stream;
     // Canonical payload: a full snapshot already is one; an incremental one is
     // laid out flat through its manifest into scratch first.
@@ -1490,32 +1292,12 @@ int pcs_import(pcs_ctx *c, const void *h_src, uint64_t size, pcs_snap *out)
     if (!c) return PCS_E_INVAL;
     if (!out || !h_src) return fail(c, PCS_E_INVAL, "null argument");
     const uint8_t *img = (const uint8_t *)h_src;
-    if (size < kImageHead || memcmp(img, kImageMagic, 8) != 0) return fail(c, PCS_E_CORRUPT, "not a snapshot image");
-    if (get32(img + 8) != 1) return fail(c, PCS_E_CORRUPT, "unknown image version %u", get32(img + 8));
-    const uint32_t n = get32(img + 12);
-    const uint64_t T = get64(img + 16), state = get64(img + 24), payload = get64(img + 32);
-    if (n > (1u << 24) || size < kImageHead + kImageDesc * (uint64_t)n)
-        return fail(c, PCS_E_CORRUPT, "truncated image header");
-    std::vector<Layout> lays(n);
-    uint64_t sum_chunks = 0, sum_bytes = 0;
-    for (uint32_t b = 0; b < n; ++b) {
-        const uint8_t *d = img + kImageHead + kImageDesc * b;
-        Layout y{};
-        y.kind = get32(d);
-        y.nbytes = get64(d + 8);
-        y.row_bytes = get64(d + 16);
-        y.window = get64(d + 24);
-        y.outer = get64(d + 32);
-        if (y.kind != PCS_FLAT && y.kind != PCS_RING) return fail(c, PCS_E_CORRUPT, "buffer %u: bad kind", b);
-        y.nchunks = div_up(y.nbytes, kChunk);
-        y.ngroups = div_up(y.nchunks, kGroupChunks);
-        sum_chunks += y.nchunks;
-        sum_bytes += y.nbytes;
-        lays[b] = y;
-    }
-    const ImageLayout L = image_layout(lays, sum_chunks);
-    if (sum_chunks != T || sum_bytes != state || L.payload != payload || L.size != size)
-        return fail(c, PCS_E_CORRUPT, "image header is inconsistent with its size");
+    std::vector<Layout> lays;
+    ImageLayout L;
+    std::string why;
+    if (int st = parse_image_header(img, size, &lays, &L, &why)) return fail(c, st, "%s", why.c_str());
+    const uint32_t n = (uint32_t)lays.size();
+    const uint64_t T = get64(img + 16), payload = L.payload;
 
     // A full snapshot with fingerprints, filled from the image.
     Job job;
@@ -1534,24 +1316,34 @@ int pcs_import(pcs_ctx *c, const void *h_src, uint64_t size, pcs_snap *out)
     if (!alloc_block(c, fp.block, &boff))
         return fail(c, PCS_E_NOMEM, "arena cannot hold the imported snapshot (%llu bytes)", (unsigned long long)fp.block);
     auto node = make_node(c, job, 0, n, fp, boff, true);
-    hipStream_t s = c->stream;
-    HIP_TRY(c, hipMemcpyAsync((void *)(c->arena_dev + node->roots_off), img + L.roots_off, 8 * (n + 1),
-                              hipMemcpyHostToDevice, s));
-    if (T) HIP_TRY(c, hipMemcpyAsync((void *)(c->arena_dev + node->hashes_off), img + L.hashes_off, 8 * T,
-                                     hipMemcpyHostToDevice, s));
-    if (payload) HIP_TRY(c, hipMemcpyAsync((void *)(c->arena_dev + node->payload_off), img + L.data_off, payload,
-                                           hipMemcpyHostToDevice, s));
-    // Verify: fingerprint the imported payload and compare with the image.
+    // Scratch for the verification, reserved before anything reads the
+    // caller's image, so that no error return leaves a copy from it in flight.
     Temp t(c);
     if (int st = temp_alloc(c, t, 8 * T + 8 * (n + 1))) return st;
     const uint64_t h_dev = c->arena_dev + t.off, r_dev = h_dev + 8 * T;
+    hipStream_t s = c->stream;
+    // Any failure from here on first waits for the copies already enqueued.
+    auto drain = [&](int st) {
+        (void)hipStreamSynchronize(s);
+        return st;
+    };
+    hipError_t e = hipMemcpyAsync((void *)(c->arena_dev + node->roots_off), img + L.roots_off, 8 * (n + 1),
+                                  hipMemcpyHostToDevice, s);
+    if (e == hipSuccess && T)
+        e = hipMemcpyAsync((void *)(c->arena_dev + node->hashes_off), img + L.hashes_off, 8 * T,
+                           hipMemcpyHostToDevice, s);
+    if (e == hipSuccess && payload)
+        e = hipMemcpyAsync((void *)(c->arena_dev + node->payload_off), img + L.data_off, payload,
+                           hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return drain(hip_fail(c, e, "image upload"));
+    // Verify: fingerprint the imported payload and compare with the image.
     std::vector<uint64_t> addr(n), nb(n);
     for (uint32_t b = 0; b < n; ++b) {
         addr[b] = c->arena_dev + node->payload_off + node->comp_off[b];
         nb[b] = lays[b].nbytes;
     }
     if (int st = fingerprint_regions(c, addr, nb, (uint64_t *)h_dev, (uint64_t *)r_dev, (uint64_t *)(r_dev + 8 * n)))
-        return st;
+        return drain(st);
     std::vector<uint64_t> got(T + n + 1);
     HIP_TRY(c, hipMemcpyAsync(got.data(), (void *)h_dev, 8 * (T + n + 1), hipMemcpyDeviceToHost, s));
     HIP_TRY(c, hipStreamSynchronize(s));

@@ -132,6 +132,14 @@ def test_import_refuses_corruption(pcs):
         "root": lambda a: a.__setitem__(48 + 96 + 8, a[48 + 96 + 8] ^ 1),
         "magic": lambda a: a.__setitem__(0, 0),
         "size field": lambda a: a.__setitem__(24, a[24] ^ 1),
+        # Header checks made on the host before any copy (a size crafted to
+        # wrap 64-bit sums is refused by the same checks; the host-logic test
+        # covers it without a device).
+        "flags": lambda a: a.__setitem__(40, 1),
+        "reserved word": lambda a: a.__setitem__(48 + 4, 1),
+        "reserved quad": lambda a: a.__setitem__(48 + 40, 1),
+        "flat buffer with a row size": lambda a: a.__setitem__(48 + 16, 16),
+        "kind": lambda a: a.__setitem__(48, 2),
     }
     for name, mutate in cases.items():
         log("import of a corrupted image:", name)
