@@ -56,8 +56,8 @@ def flat(t: torch.Tensor, nbytes: int | None = None) -> PcsBuf:
     """A PCS_FLAT descriptor over a contiguous device tensor (or its first nbytes)."""
     size = t.numel() * t.element_size()
     n = size if nbytes is None else nbytes
-    if n > size:
-        raise ValueError("nbytes exceeds the tensor")
+    if n < 0 or n > size:
+        raise ValueError("nbytes must lie in [0, tensor bytes]")
     b = PcsBuf(ptr=_dev_ptr(t), nbytes=n, kind=FLAT)
     b._tensor = t  # the descriptor keeps its memory alive until the call has been enqueued
     return b
@@ -67,6 +67,8 @@ def ring(t: torch.Tensor, outer: int, capacity: int, row_bytes: int, head: int, 
          outer_stride: int | None = None) -> PcsBuf:
     """A PCS_RING descriptor: `outer` rings of `capacity` rows inside tensor t."""
     stride = capacity * row_bytes if outer_stride is None else outer_stride
+    if min(outer, capacity, row_bytes, head, window, stride) < 0:
+        raise ValueError("ring geometry must be non-negative")
     need = (outer - 1) * stride + capacity * row_bytes if outer else 0
     if need > t.numel() * t.element_size():
         raise ValueError("ring geometry exceeds the tensor")
