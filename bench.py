@@ -197,6 +197,16 @@ def main():
     run_batch(args)
 
 
+def _pct(sorted_vals, q):
+    """q-th percentile of sorted values (linear interpolation between ranks)."""
+    if not sorted_vals:
+        return float("nan")
+    x = (len(sorted_vals) - 1) * q / 100.0
+    lo = int(x)
+    hi = min(lo + 1, len(sorted_vals) - 1)
+    return sorted_vals[lo] + (sorted_vals[hi] - sorted_vals[lo]) * (x - lo)
+
+
 def run_batch(args):
     import numpy as np
     import torch
@@ -277,14 +287,20 @@ def run_batch(args):
     torch.cuda.synchronize()
 
     ctx.set_timing(True)
+    # Events between steps on the context's stream give each step's device
+    # time without synchronising inside the timed region.
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    marks[0].record()
+    for i in range(args.steps):
         step()
+        marks[i + 1].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ctx.set_timing(False)
     kt = {k: ctx.kernel_time(k) for k in ("pack_hash", "copy", "classify", "merkle", "map")}
+    step_ms = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
 
     # Fingerprint-only pass over every session's state (read once), timed the
     # same way: the "fingerprint GB/s" half of the metric.
@@ -353,6 +369,8 @@ def run_batch(args):
                         "frac_of_peak": round(ckpt_state / (avg_fp * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                         "kernel_ms": round(avg_fp, 4), "bytes": ckpt_state,
                         "what": "pcs_fingerprint of all sessions (read once, chunk hashes + roots)"},
+        "step_ms_device": {"p10": round(_pct(step_ms, 10), 4), "p50": round(_pct(step_ms, 50), 4),
+                           "p90": round(_pct(step_ms, 90), 4)},
         "breakdown": {
             "checkpoint_fingerprint_GBps_state": round(ckpt_state / (avg_ph * 1e-3) / 1e9, 1),
             "restore_kernel_GBps_hbm": round(achieved_restore, 1),
