@@ -4,6 +4,7 @@ import in another context or process, restore byte-identically; a corrupted
 image is refused.  Images are compared byte for byte with the oracle's
 writer of the same format."""
 import os
+import signal
 import subprocess
 import sys
 
@@ -158,7 +159,7 @@ def test_import_refuses_corruption(pcs):
 
 
 CHILD = r"""
-import os, sys
+import os, signal, sys
 sys.path.insert(0, {root!r})
 import numpy as np, torch
 import paper_2607_21686_amd as P
@@ -174,7 +175,8 @@ with open({path!r}, "wb") as f:
     f.flush()
     os.fsync(f.fileno())
 print("exported", img.size, flush=True)
-os._exit(0)   # the process dies without any cleanup
+torch.cuda.synchronize()                 # no GPU work left in flight
+os.kill(os.getpid(), signal.SIGKILL)     # the process dies without any cleanup
 """
 
 
@@ -183,7 +185,7 @@ def test_checkpoint_then_die_then_resume(pcs, tmp_path):
     log("child process: checkpoint, export, die")
     r = subprocess.run([sys.executable, "-c", CHILD.format(root=ROOT, path=path)], cwd=ROOT, capture_output=True,
                        text=True, timeout=240)
-    assert r.returncode == 0, r.stderr[-2000:]
+    assert r.returncode == -signal.SIGKILL, (r.returncode, r.stderr[-2000:])
     assert "exported" in r.stdout
     img = np.fromfile(path, dtype=np.uint8)
     obs, rs, g, ring = state(7)

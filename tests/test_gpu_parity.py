@@ -396,6 +396,31 @@ def test_errors_enqueue_nothing(ctx, pcs):
     ctx.delete(s)
 
 
+def test_batch_checkpoint_is_all_or_nothing(pcs):
+    # Three sessions of 3 MiB each do not fit an 8 MiB arena together: the
+    # batch fails as a whole (no handle, no reserved block left behind) and
+    # the same call over two of them succeeds.
+    srcs = [torch.full((3 << 20,), k + 1, dtype=torch.uint8, device="cuda") for k in range(3)]
+    c = pcs.Context(arena(8 << 20))
+    before = c.arena_stats()
+    log("batch checkpoint that does not fit")
+    with pytest.raises(pcs.PcsError) as e:
+        c.checkpoint_batch([[pcs.flat(t)] for t in srcs], hash=True)
+    assert e.value.code == pcs.E_NOMEM
+    assert c.arena_stats() == before
+    snaps = c.checkpoint_batch([[pcs.flat(t)] for t in srcs[:2]], hash=True)
+    outs = [torch.zeros(3 << 20, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    c.restore_batch(snaps, [[pcs.flat(o)] for o in outs])
+    assert all(np.all(host(o) == k + 1) for k, o in enumerate(outs))
+    c.delete(snaps[0])
+    with pytest.raises(pcs.PcsError) as e:
+        c.restore(snaps[0], [pcs.flat(outs[0])])              # a deleted handle
+    assert e.value.code == pcs.E_HANDLE
+    c.delete(snaps[1])
+    assert c.arena_stats() == before
+    c.close()
+
+
 def test_incremental_chain_in_tight_arena(pcs):
     # 64 growing incremental checkpoints whose final state is ~6.4 MiB must fit
     # in a 16 MiB arena: worst-case reservations are given back without
