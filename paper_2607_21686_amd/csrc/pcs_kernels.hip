@@ -117,18 +117,29 @@ __device__ __forceinline__ uint32_t find_run(const Run *runs, uint32_t begin, ui
 
 // The tile a workgroup takes.  The dispatcher deals the workgroups of a
 // launch to the eight XCDs in turn (workgroup b runs on XCD b mod 8), so the
-// tiles are handed out XCD by XCD: XCD x works through the x-th eighth of
-// the job in order, starting at a point staggered by x/8 of its share so
-// that the eight streams do not walk over the same memory channels in step.
-// (Measured on MI355X against the plain blockIdx order: pack + fingerprint
-// of a 512 MiB ring window 204 -> 190 us, restore 189 -> 180 us, 4 GiB pack
-// + fingerprint 1366 -> 1333 us; the same split over 7 or 16-64 groups of
-// workgroups, not aligned with the XCDs, gained less or lost.)  A bijection
-// of [0, gridDim.x).
+// tiles are handed out XCD by XCD:
+//   - up to kXcdBlockJobs tiles: XCD x works through the x-th contiguous
+//     eighth of the job in order, starting at a point staggered by x/8 of its
+//     share, so that the eight streams do not walk over the same memory
+//     channels in step;
+//   - larger jobs: blocks of kXcdBlock consecutive tiles are dealt to the
+//     XCDs in turn, so every XCD streams through every part of the job and
+//     none is left with a stretch of memory that happens to be slower (a
+//     tail of fewer than eight blocks keeps the launch order).
+// Measured on MI355X against the plain blockIdx order: pack + fingerprint of
+// a 512 MiB ring window 204 -> 190-198 us, restore 189 -> 180-185 us; on the
+// 1024-session batch the fused kernel 11.5 -> 10.9-11.0 ms in every input
+// placement tried, where contiguous eighths alone gave 11.45 ms in some.
+// A bijection of [0, gridDim.x) in both cases.
+constexpr uint32_t kXcds = 8, kXcdBlock = 512, kXcdBlockJobs = 16384;
 __device__ __forceinline__ uint32_t xcd_tile()
 {
-    constexpr uint32_t kXcds = 8;
     const uint32_t nb = gridDim.x, b = blockIdx.x, x = b % kXcds, i = b / kXcds;
+    if (nb >= kXcdBlockJobs) {
+        const uint32_t full = nb / (kXcds * kXcdBlock);  // whole rounds of blocks
+        if (b >= full * kXcds * kXcdBlock) return b;
+        return ((i / kXcdBlock) * kXcds + x) * kXcdBlock + i % kXcdBlock;
+    }
     const uint32_t per = nb / kXcds, rem = nb % kXcds;
     const uint32_t n = per + (x < rem ? 1u : 0u);  // tiles of XCD x (>= 1 when workgroup b exists)
     return x * per + (x < rem ? x : rem) + (i + x * (n / kXcds)) % n;
