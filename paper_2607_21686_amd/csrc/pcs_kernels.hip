@@ -314,23 +314,27 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
 // all T lanes load it with coalesced 16-byte loads (SL/16 lanes per chunk
 // slice), kModePack stores it to the chunk's snapshot slot (zero-padding a
 // partial last chunk) and kModeVerify to the buffer's runs, and every lane
-// writes it to an LDS tile; then lane pairs of the first two wavefronts hash
-// the tile while the next slice's loads are in flight.  Lane p of a pair owns
-// XXH64 accumulators 2p and 2p+1, which read exactly bytes [16p, 16p+16) of
-// each 32-byte stripe.  kModeDiff / kModeVerify ballot one flag per chunk into
-// a per-group mask (the group is one bitmap word).
+// writes it to an LDS tile; then lane quads of the first 4*CPW lanes hash
+// the tile while the next slice's loads are in flight.  Lane q of a quad owns
+// XXH64 accumulator q, which reads exactly bytes [8q, 8q+8) of each 32-byte
+// stripe: one accumulator per lane keeps a chunk's serial chain of rounds as
+// short as a wavefront can issue it (a round is mostly quarter-rate 32-bit
+// multiplies) and spreads the hashing over twice as many wavefronts as lane
+// pairs would.  kModeDiff / kModeVerify ballot one flag per chunk into a
+// per-group mask (the group is one bitmap word).
 template <class Tab, int MODE, int T, int SL, int CPW>
 __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
                                             uint32_t *__restrict__ flag_count, uint64_t *__restrict__ flag_mask,
                                             uint64_t arena_base)
 {
     constexpr uint32_t kSteps = kChunk / SL;
-    constexpr uint32_t kRow = SL + 32;                  // padded LDS row: lane pairs of 8 chunks hit distinct banks
+    constexpr uint32_t kRow = SL + 32;                  // padded LDS row: the quads of 8 chunks hit distinct banks
     constexpr uint32_t LPS = SL / 16;                   // lanes per chunk slice
     constexpr int U = CPW * SL / 16 / T;                // granules per lane per step
     constexpr uint32_t kTiles = kGroupChunks / CPW;     // tiles per 64-chunk group
     constexpr bool kFromSlots = MODE == kModeVerify;    // source is the snapshot, destination the runs
     static_assert(U >= 1 && T % LPS == 0 && kGroupChunks % CPW == 0, "tile shape");
+    static_assert(T >= 4 * CPW, "one lane per accumulator");
     static_assert(CPW == kGroupChunks || (MODE != kModeDiff && MODE != kModeVerify), "flag words need whole groups");
     __shared__ __attribute__((aligned(16))) uint8_t tile[CPW * kRow];
     __shared__ ChunkLoc cloc[kGroupChunks];
@@ -389,12 +393,12 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
 #pragma unroll
     for (int k = 0; k < U; ++k) r[k] = load_granule(k, slot);
 
-    const uint32_t ci = t >> 1, p = t & 1;
-    const bool hasher = t < 2 * CPW && ci < nv;
+    const uint32_t ci = t >> 2, q = t & 3;
+    const bool hasher = t < 4 * CPW && ci < nv;
     const uint32_t len = hasher ? cloc[ci].len : 0;
     const uint32_t nst = len >> 5;
-    uint64_t va = p ? 0 : P1 + P2;   // accumulator 2p   (seed 0)
-    uint64_t vb = p ? 0 - P1 : P2;   // accumulator 2p+1
+    // Accumulator q with seed 0: P1 + P2, P2, 0, -P1.
+    uint64_t va = q == 0 ? P1 + P2 : q == 1 ? P2 : q == 2 ? 0 : 0 - P1;
     uint64_t tw0 = 0, tw1 = 0, tw2 = 0, tw3 = 0;  // the chunk's tail (< 32 bytes), zero padded
 
     for (uint32_t step = 0; step < kSteps; ++step) {
@@ -422,12 +426,11 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
             const uint32_t ns = nst > s0 ? umin(SL / 32, nst - s0) : 0;
 #pragma unroll 8
             for (uint32_t s = 0; s < ns; ++s) {
-                const uint4 d = *reinterpret_cast<const uint4 *>(row + 32 * s + 16 * p);
+                const uint2 d = *reinterpret_cast<const uint2 *>(row + 32 * s + 8 * q);
                 va = xround(va, ((uint64_t)d.y << 32) | d.x);
-                vb = xround(vb, ((uint64_t)d.w << 32) | d.z);
             }
             const uint32_t tp = nst * 32;  // tail start, 32-aligned, inside this slice if here
-            if (p == 0 && tp < len && tp >= step * SL && tp < (step + 1) * SL) {
+            if (q == 0 && tp < len && tp >= step * SL && tp < (step + 1) * SL) {
                 const uint4 x = *reinterpret_cast<const uint4 *>(row + tp - step * SL);
                 const uint4 y = *reinterpret_cast<const uint4 *>(row + tp - step * SL + 16);
                 tw0 = ((uint64_t)x.y << 32) | x.x;
@@ -439,17 +442,20 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
         __syncthreads();
     }
 
-    if (t < 2 * CPW) {
-        const uint64_t oa = shfl64(va, (int)(t ^ 1) & 63);
-        const uint64_t ob = shfl64(vb, (int)(t ^ 1) & 63);
-        if (hasher && p == 0) {
+    if (t < 4 * CPW) {
+        // Accumulators 1-3 of a quad to its lane 0 (a quad never straddles
+        // a wavefront).
+        const uint64_t v2 = shfl64(va, (int)(t + 1) & 63);
+        const uint64_t v3 = shfl64(va, (int)(t + 2) & 63);
+        const uint64_t v4 = shfl64(va, (int)(t + 3) & 63);
+        if (hasher && q == 0) {
             uint64_t acc;
             if (len >= 32) {
-                acc = rotl(va, 1) + rotl(vb, 7) + rotl(oa, 12) + rotl(ob, 18);
+                acc = rotl(va, 1) + rotl(v2, 7) + rotl(v3, 12) + rotl(v4, 18);
                 acc = xmerge(acc, va);
-                acc = xmerge(acc, vb);
-                acc = xmerge(acc, oa);
-                acc = xmerge(acc, ob);
+                acc = xmerge(acc, v2);
+                acc = xmerge(acc, v3);
+                acc = xmerge(acc, v4);
             } else {
                 acc = P5;
             }
