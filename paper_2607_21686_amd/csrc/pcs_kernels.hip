@@ -317,10 +317,11 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
 // writes it to an LDS tile; then lane quads of the first 4*CPW lanes hash
 // the tile while the next slice's loads are in flight.  Lane q of a quad owns
 // XXH64 accumulator q, which reads exactly bytes [8q, 8q+8) of each 32-byte
-// stripe: one accumulator per lane keeps a chunk's serial chain of rounds as
-// short as a wavefront can issue it (a round is mostly quarter-rate 32-bit
-// multiplies) and spreads the hashing over twice as many wavefronts as lane
-// pairs would.  kModeDiff / kModeVerify ballot one flag per chunk into a
+// stripe.  A wavefront issues a lane's rounds one after another (a round is
+// about ten instructions, most of them 32-bit multiply steps of the 64-bit
+// products), so one accumulator per lane halves the instructions a chunk's
+// chain costs each wavefront and spreads the hashing over twice as many
+// wavefronts as lane pairs with two accumulators each would.  kModeDiff / kModeVerify ballot one flag per chunk into a
 // per-group mask (the group is one bitmap word).
 template <class Tab, int MODE, int T, int SL, int CPW>
 __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
