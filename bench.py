@@ -139,7 +139,7 @@ def traffic(fetch_db, write_db, sessions=1024, restored=512):
         pick = lambda pat: [v for n, v in rows if pat in n]
         calib = max(pick("rocclr_copyBuffer"))
         return {"pack": pick("k_hash<pcs::DevTables, 1, 1024, 512, 64>"),
-                "copy": pick("k_copy<pcs::DevTables, false, 1024, 1024, 64>"),
+                "copy": pick("k_copy<pcs::DevTables, false, 512, 1024, 64>"),
                 "calib": calib}
 
     f, w = per_kernel(fetch_db, "FETCH_SIZE"), per_kernel(write_db, "WRITE_SIZE")
@@ -163,7 +163,7 @@ def traffic(fetch_db, write_db, sessions=1024, restored=512):
            "calibration_copy_bytes": 1 << 30, "calibration_fetch_KiB": round(f["calib"], 1),
            "calibration_write_KiB": round(w["calib"], 1), "fetch_scale": round(fs, 6), "write_scale": round(ws, 6)}
     rec.update(one("pack", sessions))
-    rec["restore_kernel"] = dict(kernel="k_copy<DevTables, unpack, 1024 lanes, 1 KiB slices, 64 chunks> (%d sessions)"
+    rec["restore_kernel"] = dict(kernel="k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (%d sessions)"
                                  % restored, **one("copy", restored))
     rec["kernel_source_sha256"] = kernel_source_sha()
     rec["commands"] = [

@@ -887,7 +887,7 @@ __global__ __launch_bounds__(64) void k_labels(const Tab tab, const uint64_t *__
 // measurement on MI355X.
 constexpr int kPackLanes = 1024, kPackSlice = 512;
 constexpr int kHashLanes = 256, kHashSlice = 512;
-constexpr int kCopyLanes = 1024, kCopySlice = 1024;
+constexpr int kCopyLanes = 512, kCopySlice = 1024;
 constexpr int kSmallLanes = 256;  // sub-tiles of small jobs: 8 chunks per workgroup
 
 // ---------------------------------------------------------------- bank shrink
