@@ -1,0 +1,160 @@
+/*
+ * A client of libpcs written against the C ABI alone (include/pcs.h plus the
+ * HIP runtime's allocation and copy calls): no Python, no torch.  It builds
+ * a session of two buffers (a flat buffer with a ragged size and a wrapped
+ * ring window), fingerprints it, checkpoints it with fingerprints, forks the
+ * snapshot, overwrites the session, restores the fork into it (the ring at
+ * a new head) and exports the snapshot to a host image.
+ *
+ * Prints, one per line: "hash <i> <hex>" for every chunk fingerprint,
+ * "root <b> <hex>", "session <hex>", "restored <0|1>" (1 when every logical
+ * byte came back) and "image <bytes>"; exits 0 when every call succeeded.
+ * tests/test_gpu_c_client.py builds it, runs it and checks the fingerprints
+ * against the oracle.
+ */
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "pcs.h"
+
+#define FLAT_BYTES (3 * 4096 + 777)
+#define OUTER 2u
+#define CAPACITY 16u
+#define ROW 256u
+#define HEAD 11u
+#define WINDOW 12u
+#define NEW_HEAD 3u
+#define RING_BYTES (OUTER * CAPACITY * ROW)
+
+static uint8_t pattern(uint32_t buf, uint64_t i)
+{
+    return (uint8_t)((i * 131u + buf * 17u + (i >> 8)) & 0xFFu);
+}
+
+#define HIP_OK(x)                                                             \
+    do {                                                                      \
+        hipError_t e_ = (x);                                                  \
+        if (e_ != hipSuccess) {                                               \
+            fprintf(stderr, "%s: %s\n", #x, hipGetErrorString(e_));           \
+            return 1;                                                         \
+        }                                                                     \
+    } while (0)
+
+#define PCS_OK_(ctx, x)                                                       \
+    do {                                                                      \
+        int s_ = (x);                                                         \
+        if (s_ != PCS_OK) {                                                   \
+            fprintf(stderr, "%s: %d %s\n", #x, s_, pcs_last_error(ctx));      \
+            return 1;                                                         \
+        }                                                                     \
+    } while (0)
+
+static pcs_buf ring_desc(void *p, uint64_t head)
+{
+    pcs_buf b;
+    memset(&b, 0, sizeof b);
+    b.ptr = (uint64_t)(uintptr_t)p;
+    b.kind = PCS_RING;
+    b.row_bytes = ROW;
+    b.capacity = CAPACITY;
+    b.head = head;
+    b.window = WINDOW;
+    b.outer = OUTER;
+    b.outer_stride = CAPACITY * ROW;
+    return b;
+}
+
+int main(void)
+{
+    uint8_t *h_flat = malloc(FLAT_BYTES), *h_ring = malloc(RING_BYTES), *h_back = malloc(RING_BYTES);
+    if (!h_flat || !h_ring || !h_back) return 1;
+    for (uint64_t i = 0; i < FLAT_BYTES; ++i) h_flat[i] = pattern(0, i);
+    for (uint64_t i = 0; i < RING_BYTES; ++i) h_ring[i] = pattern(1, i);
+
+    void *d_arena = NULL, *d_flat = NULL, *d_ring = NULL, *d_hashes = NULL, *d_roots = NULL, *d_sroot = NULL;
+    const uint64_t arena_bytes = 8u << 20;
+    HIP_OK(hipMalloc(&d_arena, arena_bytes));
+    HIP_OK(hipMalloc(&d_flat, FLAT_BYTES));
+    HIP_OK(hipMalloc(&d_ring, RING_BYTES));
+    HIP_OK(hipMemcpy(d_flat, h_flat, FLAT_BYTES, hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(d_ring, h_ring, RING_BYTES, hipMemcpyHostToDevice));
+
+    pcs_buf plan[2];
+    memset(&plan[0], 0, sizeof plan[0]);
+    plan[0].ptr = (uint64_t)(uintptr_t)d_flat;
+    plan[0].nbytes = FLAT_BYTES;
+    plan[0].kind = PCS_FLAT;
+    plan[1] = ring_desc(d_ring, HEAD);
+
+    uint64_t chunks[2], total = 0;
+    if (pcs_chunk_counts(plan, 2, chunks, &total) != PCS_OK) return 1;
+    HIP_OK(hipMalloc(&d_hashes, 8 * total));
+    HIP_OK(hipMalloc(&d_roots, 16));
+    HIP_OK(hipMalloc(&d_sroot, 8));
+
+    pcs_ctx *ctx = NULL;
+    if (pcs_ctx_create(d_arena, arena_bytes, NULL, &ctx) != PCS_OK) return 1;
+    PCS_OK_(ctx, pcs_fingerprint(ctx, plan, 2, d_hashes, d_roots, d_sroot));
+
+    pcs_snap snap = 0, fork = 0;
+    PCS_OK_(ctx, pcs_checkpoint(ctx, plan, 2, 0, PCS_CKPT_HASH, NULL, NULL, NULL, &snap));
+    PCS_OK_(ctx, pcs_fork(ctx, snap, &fork));
+
+    /* Overwrite the session, then restore the fork into it, the ring at a new head. */
+    HIP_OK(hipMemset(d_flat, 0, FLAT_BYTES));
+    HIP_OK(hipMemset(d_ring, 0, RING_BYTES));
+    pcs_buf dst[2] = {plan[0], ring_desc(d_ring, NEW_HEAD)};
+    PCS_OK_(ctx, pcs_restore(ctx, fork, dst, 2));
+    HIP_OK(hipDeviceSynchronize());
+
+    int ok = 1;
+    uint8_t *h_flat_back = malloc(FLAT_BYTES);
+    if (!h_flat_back) return 1;
+    HIP_OK(hipMemcpy(h_flat_back, d_flat, FLAT_BYTES, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(h_back, d_ring, RING_BYTES, hipMemcpyDeviceToHost));
+    if (memcmp(h_flat_back, h_flat, FLAT_BYTES) != 0) ok = 0;
+    for (uint32_t o = 0; o < OUTER; ++o)
+        for (uint32_t t = 0; t < WINDOW; ++t) {
+            const uint8_t *want = h_ring + o * CAPACITY * ROW + ((HEAD + t) % CAPACITY) * ROW;
+            const uint8_t *got = h_back + o * CAPACITY * ROW + ((NEW_HEAD + t) % CAPACITY) * ROW;
+            if (memcmp(want, got, ROW) != 0) ok = 0;
+        }
+
+    uint64_t image_bytes = 0;
+    PCS_OK_(ctx, pcs_export(ctx, snap, NULL, 0, &image_bytes));
+    void *image = malloc(image_bytes);
+    if (!image) return 1;
+    PCS_OK_(ctx, pcs_export(ctx, snap, image, image_bytes, &image_bytes));
+
+    uint64_t *h_hashes = malloc(8 * total), h_roots[2], h_sroot;
+    if (!h_hashes) return 1;
+    HIP_OK(hipMemcpy(h_hashes, d_hashes, 8 * total, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(h_roots, d_roots, 16, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(&h_sroot, d_sroot, 8, hipMemcpyDeviceToHost));
+    for (uint64_t i = 0; i < total; ++i) printf("hash %llu %016llx\n", (unsigned long long)i, (unsigned long long)h_hashes[i]);
+    for (int b = 0; b < 2; ++b) printf("root %d %016llx\n", b, (unsigned long long)h_roots[b]);
+    printf("session %016llx\n", (unsigned long long)h_sroot);
+    printf("restored %d\n", ok);
+    printf("image %llu\n", (unsigned long long)image_bytes);
+
+    PCS_OK_(ctx, pcs_delete(ctx, fork));
+    PCS_OK_(ctx, pcs_delete(ctx, snap));
+    PCS_OK_(ctx, pcs_ctx_destroy(ctx));
+    free(image);
+    free(h_hashes);
+    free(h_flat_back);
+    free(h_flat);
+    free(h_ring);
+    free(h_back);
+    (void)hipFree(d_hashes);
+    (void)hipFree(d_roots);
+    (void)hipFree(d_sroot);
+    (void)hipFree(d_flat);
+    (void)hipFree(d_ring);
+    (void)hipFree(d_arena);
+    return 0;
+}
