@@ -50,7 +50,7 @@ constexpr uint64_t kScanCompactMaxGroups = 4096;
 // Small incremental jobs of at most this many groups scan and compact in one
 // workgroup (one launch); larger ones scan in one workgroup and compact with
 // one workgroup per group.
-constexpr uint64_t kScanCompactFusedGroups = 16;
+constexpr uint64_t kScanCompactFusedGroups = 64;
 hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint32_t *counts,
                                      const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
                                      uint64_t *total, uint64_t *total_host, hipStream_t s);

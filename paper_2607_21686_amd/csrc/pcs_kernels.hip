@@ -791,14 +791,15 @@ __global__ __launch_bounds__(1024) void k_scan_compact_small(const ArgTables tab
     __shared__ uint64_t sums[2][1024];
     __shared__ uint64_t offs[kScanCompactMaxGroups];
     scan_counts(counts, ngroups, offs, total, sums);
-    for (uint64_t g = threadIdx.x; g < ngroups; g += 1024) {
+    // One thread per chunk (a chunk's slot depends only on its group's mask
+    // and offset): 16 groups are one pass of the workgroup.
+    for (uint64_t e = threadIdx.x; e < ngroups * kGroupChunks; e += 1024) {
+        const uint64_t g = e / kGroupChunks;
+        const uint32_t lane = (uint32_t)(e % kGroupChunks);
         const uint32_t b = buf_index(tab, g);
         const JobBuf &jb = tab.bufs[b];
-        const uint64_t c0 = (g - jb.group_begin) * kGroupChunks;
-        const uint32_t nv = (uint32_t)umin(kGroupChunks, jb.nchunks - c0);
-        const uint64_t mask = dirty_mask[g];
-        for (uint32_t lane = 0; lane < nv; ++lane)
-            compact_chunk(jb, b, c0 + lane, lane, mask, offs[g], payload_arena_top, list);
+        const uint64_t i = (g - jb.group_begin) * kGroupChunks + lane;
+        if (i < jb.nchunks) compact_chunk(jb, b, i, lane, dirty_mask[g], offs[g], payload_arena_top, list);
     }
     if (threadIdx.x == 1023 && total_host) {
         *(volatile uint64_t *)total_host = *total;
