@@ -890,6 +890,9 @@ constexpr int kPackLanes = 1024, kPackSlice = 512;
 constexpr int kHashLanes = 256, kHashSlice = 512;
 constexpr int kCopyLanes = 512, kCopySlice = 1024;
 constexpr int kSmallLanes = 256;  // sub-tiles of small jobs: 8 chunks per workgroup
+// A sub-tile moves whole chunks in one step (8 granules per lane): a small
+// job's time is a tile's latency, one load round trip per step.
+constexpr int kSmallSlice = 4096;
 
 // ---------------------------------------------------------------- bank shrink
 
@@ -1000,10 +1003,10 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
     if (tiles_per_group == kSmallTiles) {
         constexpr int kCPW = kGroupChunks / kSmallTiles;
         if (mode == kModeHash)
-            hipLaunchKernelGGL((k_hash<Tab, kModeHash, kSmallLanes, kHashSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
+            hipLaunchKernelGGL((k_hash<Tab, kModeHash, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
                                tab, nodes, flag_count, flag_mask, arena_base);
         else
-            hipLaunchKernelGGL((k_hash<Tab, kModePack, kSmallLanes, kPackSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
+            hipLaunchKernelGGL((k_hash<Tab, kModePack, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
                                tab, nodes, flag_count, flag_mask, arena_base);
         return hipGetLastError();
     }
@@ -1041,10 +1044,10 @@ hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t are
     if (tiles == kSmallTiles) {
         constexpr int kCPW = kGroupChunks / kSmallTiles;
         if (pack)
-            hipLaunchKernelGGL((k_copy<Tab, true, kSmallLanes, kCopySlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
+            hipLaunchKernelGGL((k_copy<Tab, true, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
                                arena_base);
         else
-            hipLaunchKernelGGL((k_copy<Tab, false, kSmallLanes, kCopySlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
+            hipLaunchKernelGGL((k_copy<Tab, false, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
                                arena_base);
     } else if (pack) {
         hipLaunchKernelGGL((k_copy<Tab, true, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), 0, s,
