@@ -16,7 +16,9 @@ namespace pcs {
 enum TileMode : int {
     kModeHash = 0,    // fingerprint the buffer's runs
     kModePack = 1,    // ... and store every chunk to its snapshot slot (checkpoint)
-    kModeDiff = 2,    // ... and mark chunks new or changed against the parent (incremental)
+    kModeDiff = 2,    // ... and mark chunks new or changed against the parent (incremental):
+                      // bit c of the group's 64-bit mask (an 8-chunk sub-tile writes its
+                      // byte of it)
     kModeVerify = 3,  // copy snapshot slots to the buffer's runs (restore), fingerprint
                       // the restored bytes and mark chunks whose fingerprint differs
                       // from the one stored at checkpoint time
@@ -24,8 +26,8 @@ enum TileMode : int {
 hipError_t launch_group_map(const JobBuf *bufs, const Run *runs, uint32_t nbuf, uint64_t ngroups, GroupRef *map,
                             hipStream_t s);
 template <class Tab>
-hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint32_t *flag_count,
-                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group = 1);
+hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint64_t *flag_mask,
+                       uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group = 1);
 template <class Tab>
 hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s);
 template <class Tab>
@@ -44,16 +46,18 @@ hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_
                          hipStream_t s);
 hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64_t *scratch_a,
                                uint64_t *scratch_b, hipStream_t s);
-hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total, hipStream_t s,
+// Exclusive scan of the set-bit counts of per-group dirty masks (offsets
+// and total), the total also to a pinned host word when given.
+hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total, hipStream_t s,
                        uint64_t *total_host = nullptr);
 constexpr uint64_t kScanCompactMaxGroups = 4096;
 // Small incremental jobs of at most this many groups scan and compact in one
 // workgroup (one launch); larger ones scan in one workgroup and compact with
 // one workgroup per group.
 constexpr uint64_t kScanCompactFusedGroups = 64;
-hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint32_t *counts,
-                                     const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
-                                     uint64_t *total, uint64_t *total_host, hipStream_t s);
+hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint64_t *dirty_mask,
+                                     uint64_t payload_arena_top, uint64_t *list, uint64_t *total,
+                                     uint64_t *total_host, hipStream_t s);
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
 // Flips the lowest bit of the byte at device address addr.
 hipError_t launch_flip_bit(uint64_t addr, hipStream_t s);

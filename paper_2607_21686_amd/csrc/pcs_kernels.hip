@@ -325,8 +325,7 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
 // per-group mask (the group is one bitmap word).
 template <class Tab, int MODE, int T, int SL, int CPW>
 __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
-                                            uint32_t *__restrict__ flag_count, uint64_t *__restrict__ flag_mask,
-                                            uint64_t arena_base)
+                                            uint64_t *__restrict__ flag_mask, uint64_t arena_base)
 {
     constexpr uint32_t kSteps = kChunk / SL;
     constexpr uint32_t kRow = SL + 32;                  // padded LDS row: the quads of 8 chunks hit distinct banks
@@ -336,7 +335,8 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     constexpr bool kFromSlots = MODE == kModeVerify;    // source is the snapshot, destination the runs
     static_assert(U >= 1 && T % LPS == 0 && kGroupChunks % CPW == 0, "tile shape");
     static_assert(T >= 4 * CPW, "one lane per accumulator");
-    static_assert(CPW == kGroupChunks || (MODE != kModeDiff && MODE != kModeVerify), "flag words need whole groups");
+    static_assert(CPW == kGroupChunks || MODE != kModeVerify, "verify flags need whole groups");
+    static_assert(CPW == kGroupChunks || CPW == 8 || MODE != kModeDiff, "a diff sub-tile writes one mask byte");
     __shared__ __attribute__((aligned(16))) uint8_t tile[CPW * kRow];
     __shared__ ChunkLoc cloc[kGroupChunks];
     __shared__ uint64_t leaves[CPW];
@@ -349,7 +349,13 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     const Run *runs = tab.runs;
     const uint32_t t = threadIdx.x;
     const uint64_t c0 = (G - jb.group_begin) * kGroupChunks + (tile_id % kTiles) * CPW;
-    if (c0 >= jb.nchunks) return;  // a buffer's last group may end before this tile
+    if (c0 >= jb.nchunks) {  // a buffer's last group may end before this tile
+        // A diff sub-tile owns byte (tile % 8) of its group's dirty mask:
+        // an empty one writes it as 0 so every byte of the mask is defined.
+        if (MODE == kModeDiff && kTiles > 1 && t == 0 && flag_mask)
+            ((g_u8 *)flag_mask)[G * kTiles + tile_id % kTiles] = 0;
+        return;
+    }
     const uint32_t nv = (uint32_t)umin(CPW, jb.nchunks - c0);
     const uint32_t run_begin = jb.run_begin, run_count = jb.run_count;
     const g_u64 *man = (const g_u64 *)jb.manifest;
@@ -497,10 +503,12 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
         const uint64_t root = wave_merkle(v, nv);
         if (t == 0 && nodes) nodes[tile_id] = root;  // the tile's Merkle node (an aligned subtree)
         if (MODE == kModeDiff || MODE == kModeVerify) {
+            // Bit c of group G's mask = chunk c of the group; a sub-tile
+            // writes its 8 bits as byte (tile % 8) of the little-endian word.
             const uint64_t mask = __ballot(t < nv && dflag[t] != 0);
-            if (t == 0) {
-                if (flag_mask) flag_mask[G] = mask;
-                if (flag_count) flag_count[G] = (uint32_t)__popcll(mask);
+            if (t == 0 && flag_mask) {
+                if (kTiles == 1) flag_mask[G] = mask;
+                else ((g_u8 *)flag_mask)[G * kTiles + tile_id % kTiles] = (uint8_t)mask;
             }
         }
     }
@@ -703,17 +711,30 @@ __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
 
 // ---------------------------------------------------------------- incremental
 
-// Exclusive scan of per-group dirty counts (one workgroup; Hillis-Steele
-// over 1024 per-thread partial sums).  Writes offsets[] and *total; returns
-// nothing else.  `offsets` may be LDS or global memory.
-__device__ void scan_counts(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total,
+// Where a scan takes entry j's count from: a count array (keep flags of a
+// bank shrink), or the number of set bits of a 64-bit dirty mask (one per
+// 64-chunk group of an incremental checkpoint).
+struct CountArray {
+    const uint32_t *p;
+    __device__ uint64_t operator()(uint64_t j) const { return p[j]; }
+};
+struct MaskBits {
+    const uint64_t *p;
+    __device__ uint64_t operator()(uint64_t j) const { return (uint64_t)__popcll(p[j]); }
+};
+
+// Exclusive scan of n counts (one workgroup; Hillis-Steele over 1024
+// per-thread partial sums).  Writes offsets[] and *total; returns nothing
+// else.  `offsets` may be LDS or global memory.
+template <class Count>
+__device__ void scan_counts(const Count counts, uint64_t n, uint64_t *offsets, uint64_t *total,
                             uint64_t (*sums)[1024])
 {
     const uint32_t t = threadIdx.x;
     const uint64_t per = (n + 1023) / 1024;
     const uint64_t s0 = umin(n, t * per), s1 = umin(n, s0 + per);
     uint64_t s = 0;
-    for (uint64_t j = s0; j < s1; ++j) s += counts[j];
+    for (uint64_t j = s0; j < s1; ++j) s += counts(j);
     int cur = 0;
     sums[0][t] = s;
     __syncthreads();
@@ -726,17 +747,17 @@ __device__ void scan_counts(const uint32_t *counts, uint64_t n, uint64_t *offset
     uint64_t run = sums[cur][t] - s;  // exclusive prefix of this thread's segment
     for (uint64_t j = s0; j < s1; ++j) {
         offsets[j] = run;
-        run += counts[j];
+        run += counts(j);
     }
     if (t == 1023) *total = sums[cur][t];
     __syncthreads();
 }
 
-// Exclusive scan of per-group counts; the total also goes to the caller's
-// pinned host word when one is given.
-__global__ __launch_bounds__(1024) void k_scan(const uint32_t *__restrict__ counts, uint64_t n,
-                                               uint64_t *__restrict__ offsets, uint64_t *__restrict__ total,
-                                               uint64_t *total_host)
+// Exclusive scan of counts; the total also goes to the caller's pinned host
+// word when one is given.
+template <class Count>
+__global__ __launch_bounds__(1024) void k_scan(const Count counts, uint64_t n, uint64_t *__restrict__ offsets,
+                                               uint64_t *__restrict__ total, uint64_t *total_host)
 {
     __shared__ uint64_t sums[2][1024];
     scan_counts(counts, n, offsets, total, sums);
@@ -783,14 +804,13 @@ __global__ __launch_bounds__(64) void k_compact(const Tab tab, const uint64_t *_
 // workgroup (offsets in LDS), and the stored-chunk count written both to
 // device memory and to the caller's pinned host word.
 __global__ __launch_bounds__(1024) void k_scan_compact_small(const ArgTables tab, uint64_t ngroups,
-                                                             const uint32_t *__restrict__ counts,
                                                              const uint64_t *__restrict__ dirty_mask,
                                                              uint64_t payload_arena_top, uint64_t *__restrict__ list,
                                                              uint64_t *__restrict__ total, uint64_t *total_host)
 {
     __shared__ uint64_t sums[2][1024];
-    __shared__ uint64_t offs[kScanCompactMaxGroups];
-    scan_counts(counts, ngroups, offs, total, sums);
+    __shared__ uint64_t offs[kScanCompactFusedGroups];
+    scan_counts(MaskBits{dirty_mask}, ngroups, offs, total, sums);
     // One thread per chunk (a chunk's slot depends only on its group's mask
     // and offset): 16 groups are one pass of the workgroup.
     for (uint64_t e = threadIdx.x; e < ngroups * kGroupChunks; e += 1024) {
@@ -993,40 +1013,44 @@ hipError_t launch_group_map(const JobBuf *bufs, const Run *runs, uint32_t nbuf, 
 }
 
 template <class Tab>
-hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint32_t *flag_count,
-                       uint64_t *flag_mask, uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group)
+hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint64_t *flag_mask,
+                       uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group)
 {
     if (ngroups == 0) return hipSuccess;
     const bool split = tiles_per_group != 1;
-    if (split && (mode != kModeHash && mode != kModePack)) return hipErrorInvalidValue;
+    if (split && (mode != kModeHash && mode != kModePack && mode != kModeDiff)) return hipErrorInvalidValue;
     const dim3 grid((uint32_t)(ngroups * tiles_per_group));
     if (tiles_per_group == kSmallTiles) {
         constexpr int kCPW = kGroupChunks / kSmallTiles;
+        static_assert(kCPW == 8, "a diff sub-tile writes one mask byte");
         if (mode == kModeHash)
             hipLaunchKernelGGL((k_hash<Tab, kModeHash, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
-                               tab, nodes, flag_count, flag_mask, arena_base);
-        else
+                               tab, nodes, flag_mask, arena_base);
+        else if (mode == kModePack)
             hipLaunchKernelGGL((k_hash<Tab, kModePack, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
-                               tab, nodes, flag_count, flag_mask, arena_base);
+                               tab, nodes, flag_mask, arena_base);
+        else
+            hipLaunchKernelGGL((k_hash<Tab, kModeDiff, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
+                               tab, nodes, flag_mask, arena_base);
         return hipGetLastError();
     }
     if (split) return hipErrorInvalidValue;
     switch (mode) {
     case kModeHash:
         hipLaunchKernelGGL((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), 0, s,
-                           tab, nodes, flag_count, flag_mask, arena_base);
+                           tab, nodes, flag_mask, arena_base);
         break;
     case kModePack:
         hipLaunchKernelGGL((k_hash<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), 0, s,
-                           tab, nodes, flag_count, flag_mask, arena_base);
+                           tab, nodes, flag_mask, arena_base);
         break;
     case kModeDiff:
         hipLaunchKernelGGL((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), 0, s,
-                           tab, nodes, flag_count, flag_mask, arena_base);
+                           tab, nodes, flag_mask, arena_base);
         break;
     case kModeVerify:
         hipLaunchKernelGGL((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), 0,
-                           s, tab, nodes, flag_count, flag_mask, arena_base);
+                           s, tab, nodes, flag_mask, arena_base);
         break;
     default:
         return hipErrorInvalidValue;
@@ -1113,19 +1137,20 @@ hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const uint32_t *counts, uint64_t n, uint64_t *offsets, uint64_t *total,
+hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total,
                        hipStream_t s, uint64_t *total_host)
 {
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, counts, n, offsets, total, total_host);
+    hipLaunchKernelGGL(k_scan<MaskBits>, dim3(1), dim3(1024), 0, s, MaskBits{dirty_mask}, n, offsets, total,
+                       total_host);
     return hipGetLastError();
 }
 
-hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint32_t *counts,
-                                     const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
-                                     uint64_t *total, uint64_t *total_host, hipStream_t s)
+hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint64_t *dirty_mask,
+                                     uint64_t payload_arena_top, uint64_t *list, uint64_t *total,
+                                     uint64_t *total_host, hipStream_t s)
 {
-    if (ngroups > kScanCompactMaxGroups) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_scan_compact_small, dim3(1), dim3(1024), 0, s, tab, ngroups, counts, dirty_mask,
+    if (ngroups > kScanCompactFusedGroups) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_scan_compact_small, dim3(1), dim3(1024), 0, s, tab, ngroups, dirty_mask,
                        payload_arena_top, list, total, total_host);
     return hipGetLastError();
 }
@@ -1138,7 +1163,8 @@ hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, 
     hipLaunchKernelGGL(k_shrink_rank, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint32_t *>(scores), n,
                        keep, flags);
     if (hipError_t e = hipGetLastError()) return e;
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, flags, (uint64_t)n, offsets, total, nullptr);
+    hipLaunchKernelGGL(k_scan<CountArray>, dim3(1), dim3(1024), 0, s, CountArray{flags}, (uint64_t)n, offsets,
+                       total, nullptr);
     if (hipError_t e = hipGetLastError()) return e;
     hipLaunchKernelGGL(k_shrink_place, dim3(blocks), dim3(256), 0, s, flags, offsets, n, kept);
     return hipGetLastError();
@@ -1176,8 +1202,8 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
 }
 
 #define PCS_INSTANTIATE(Tab)                                                                                        \
-    template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint32_t *, uint64_t *, uint64_t, \
-                                         hipStream_t, uint32_t);                                                  \
+    template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint64_t *, uint64_t, hipStream_t, \
+                                         uint32_t);                                                               \
     template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t);                     \
     template hipError_t launch_compact<Tab>(const Tab &, uint64_t, const uint64_t *, const uint64_t *, uint64_t,   \
                                             uint64_t *, hipStream_t);                                             \

@@ -455,7 +455,7 @@ int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &s
     hipStream_t s = c->stream;
     int st = with_tables(sg, [&](const auto &tab) {
         return launch(c, copy ? "pack_hash" : "hash", [&] {
-            return launch_tile(tab, G, copy ? kModePack : kModeHash, d_nodes, nullptr, nullptr, 0, s, tiles);
+            return launch_tile(tab, G, copy ? kModePack : kModeHash, d_nodes, nullptr, 0, s, tiles);
         });
     });
     if (st || !want_roots) return st;
@@ -919,6 +919,10 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     if (hipEventCreateWithFlags(&node->ev, hipEventDisableTiming) != hipSuccess)
         return fail(c, PCS_E_HIP, "hipEventCreate failed");
 
+    // A small job fingerprints and diffs as sub-tiles; the Merkle lists then
+    // reduce one node per sub-tile (an aligned 8-chunk subtree).
+    const uint32_t tiles = tile_split(G);
+    const uint64_t per_tile = kGroupChunks / tiles;
     std::vector<MerkleList> lists;
     for (uint32_t b = 0; b < n; ++b) {
         JobBuf &jb = job.bufs[b];
@@ -932,7 +936,7 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         } else {
             jb.parent_slot0 = par->payload_off + par->comp_off[b];
         }
-        lists.push_back({jb.group_begin, job.lays[b].ngroups,
+        lists.push_back({jb.group_begin * tiles, div_up(jb.nchunks, per_tile),
                          {c->arena_dev + node->roots_off + 8 * b, d_roots ? (uint64_t)(d_roots + b) : 0}});
     }
     lists.push_back({0, n, {c->arena_dev + node->roots_off + 8 * n, (uint64_t)d_sroot}});
@@ -942,12 +946,11 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     // writes the stored-chunk count to pinned host memory), dirty copy.
     const bool small = is_small(job) && !exact && G <= kScanCompactMaxGroups;
     Carver cv;
-    uint64_t o_nodes, o_sa, o_sb, o_roots, o_cnt, o_mask, o_offs, o_total, o_list;
-    cv.add(&o_nodes, 8 * G);
-    cv.add(&o_sa, 8 * std::max<uint64_t>(G, n));
-    cv.add(&o_sb, 8 * std::max<uint64_t>(G, n));
+    uint64_t o_nodes, o_sa, o_sb, o_roots, o_mask, o_offs, o_total, o_list;
+    cv.add(&o_nodes, 8 * G * tiles);
+    cv.add(&o_sa, 8 * std::max<uint64_t>(G * tiles, n));
+    cv.add(&o_sb, 8 * std::max<uint64_t>(G * tiles, n));
     cv.add(&o_roots, 8 * n);
-    cv.add(&o_cnt, 4 * G);
     cv.add(&o_mask, 8 * G);
     cv.add(&o_offs, 8 * G);
     cv.add(&o_total, 8);
@@ -960,14 +963,13 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     uint64_t *d_nodes = (uint64_t *)(scr + o_nodes);
     uint64_t *d_sa = (uint64_t *)(scr + o_sa), *d_sb = (uint64_t *)(scr + o_sb);
     uint64_t *d_roots_tmp = (uint64_t *)(scr + o_roots);
-    uint32_t *d_cnt = (uint32_t *)(scr + o_cnt);
     uint64_t *d_mask = (uint64_t *)(scr + o_mask), *d_offs = (uint64_t *)(scr + o_offs);
     uint64_t *d_total = (uint64_t *)(scr + o_total), *d_list = (uint64_t *)(scr + o_list);
     hipStream_t s = c->stream;
     uint64_t payload_top_dev = c->arena_dev + node->pay_top;
     int st = with_tables(sg, [&](const auto &tab) {
         return launch(c, "incremental", [&] {
-            return launch_tile(tab, G, kModeDiff, d_nodes, d_cnt, d_mask, 0, s);
+            return launch_tile(tab, G, kModeDiff, d_nodes, d_mask, 0, s, tiles);
         });
     });
     if (st) return st;
@@ -979,11 +981,11 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         const uint64_t top = node->pay_top;
         if (G <= kScanCompactFusedGroups) {
             if ((st = launch(c, "incremental", [&] {
-                     return launch_scan_compact_small(sg.arg, G, d_cnt, d_mask, top, d_list, d_total, host_word, s);
+                     return launch_scan_compact_small(sg.arg, G, d_mask, top, d_list, d_total, host_word, s);
                  })))
                 return st;
         } else {
-            if ((st = launch(c, "incremental", [&] { return launch_scan(d_cnt, G, d_offs, d_total, s, host_word); })))
+            if ((st = launch(c, "incremental", [&] { return launch_scan(d_mask, G, d_offs, d_total, s, host_word); })))
                 return st;
             if ((st = launch(c, "incremental", [&] {
                      return launch_compact(sg.arg, G, d_mask, d_offs, top, d_list, s);
@@ -1000,7 +1002,7 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         *out = new_handle(c, node);
         return PCS_OK;
     }
-    if ((st = launch(c, "incremental", [&] { return launch_scan(d_cnt, G, d_offs, d_total, s); }))) return st;
+    if ((st = launch(c, "incremental", [&] { return launch_scan(d_mask, G, d_offs, d_total, s); }))) return st;
     if (exact) {
         HIP_TRY(c, hipMemcpyAsync(&c->counts[c->free_counts.back()], d_total, 8, hipMemcpyDeviceToHost, s));
         HIP_TRY(c, hipEventRecord(node->ev, s));
@@ -1090,7 +1092,7 @@ int pcs_restore_verify(pcs_ctx *c, pcs_snap snap, const pcs_buf *dst, uint32_t n
     const uint64_t G = job.ngroups;
     return with_tables(sg, [&](const auto &tab) {
         if (int st = launch(c, "verify", [&] {
-                return launch_tile(tab, G, kModeVerify, nullptr, nullptr, d_bad_bitmap, c->arena_dev, c->stream);
+                return launch_tile(tab, G, kModeVerify, nullptr, d_bad_bitmap, c->arena_dev, c->stream);
             }))
             return st;
         if (!d_bad_labels) return (int)PCS_OK;
