@@ -321,8 +321,9 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
 // about ten instructions, most of them 32-bit multiply steps of the 64-bit
 // products), so one accumulator per lane halves the instructions a chunk's
 // chain costs each wavefront and spreads the hashing over twice as many
-// wavefronts as lane pairs with two accumulators each would.  kModeDiff / kModeVerify ballot one flag per chunk into a
-// per-group mask (the group is one bitmap word).
+// wavefronts as lane pairs with two accumulators each would.  kModeDiff /
+// kModeVerify ballot one flag per chunk into a per-group mask (the group is
+// one bitmap word; a diff sub-tile writes its byte of the word).
 template <class Tab, int MODE, int T, int SL, int CPW>
 __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
                                             uint64_t *__restrict__ flag_mask, uint64_t arena_base)
