@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="batch",
-                    choices=["batch", "kv-ring", "sweep", "bank", "markovian", "shrink", "discover", "export"],
+                    choices=["batch", "kv-ring", "verify", "sweep", "bank", "markovian", "shrink", "discover", "export"],
                     help="batch (default, the headline) or one of the other seeded configurations")
     ap.add_argument("--sessions", type=int, default=1024)
     ap.add_argument("--cpu-sessions", type=int, default=384, help="oracle sample size (sessions)")
@@ -500,6 +500,44 @@ def run_kv_ring(args):
                  {"restore_ms": round(mc / nc, 4), "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
 
 
+def run_verify(args):
+    """Verify-on-restore on the windowed KV context: one snapshot of the 512
+    MiB window (taken with fingerprints, outside the timed steps); each step
+    restores it with verification (restore fused with fingerprinting of the
+    bytes written and a comparison with the stored fingerprints) at one new
+    head and without verification at another, so the two rates sit side by
+    side."""
+    import torch
+    import paper_2607_21686_amd as P
+    import workloads as W
+    ring, g, h2 = W.config3_device(2)
+    ctx = P.Context(torch.empty((512 << 20) + (64 << 20), dtype=torch.uint8, device="cuda"))
+    src = P.BufArray([P.ring(ring, g.outer, g.capacity, g.row_bytes, g.head, g.window)])
+    snap = ctx.checkpoint(src, hash=True)
+    a, b = torch.empty_like(ring), torch.empty_like(ring)
+    da = P.BufArray([P.ring(a, g.outer, g.capacity, g.row_bytes, h2, g.window)])
+    db = P.BufArray([P.ring(b, g.outer, g.capacity, g.row_bytes, (h2 + 1234) % g.capacity, g.window)])
+    words = (g.window_bytes // 4096 + 63) // 64
+    bad = torch.zeros(words, dtype=torch.int64, device="cuda")
+
+    def step():
+        ctx.restore_verify(snap, da, bad)      # no per-buffer labels: one kernel per call
+        ctx.restore(snap, db)
+    t, kt = _timed(args, ctx, step, ["verify", "copy"])
+    assert not bad.any().item(), "verification flagged an intact snapshot"
+    W_ = g.window_bytes
+    nv, mv = kt["verify"]
+    nc, mc = kt["copy"]
+    v_ms = mv / nv
+    ctx.delete(snap)
+    return _line(args, 2 * W_ / t / 1e9, t * 1e3, "verify on restore, windowed KV ring: 32 layers x 2 x 8192 slots x 8 "
+                 "x 128 bf16 (1 GiB), 4096-token window; per step one restore with verification and one without",
+                 {"window_bytes": W_}, "k_hash<verify>", 2 * W_, v_ms,
+                 {"verify_ms": round(v_ms, 4), "restore_ms": round(mc / nc, 4),
+                  "verify_GBps_hbm": round(2 * W_ / (v_ms * 1e-3) / 1e9, 1),
+                  "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
+
+
 def run_sweep(args):
     """Classification sweep: fingerprint all 8 replays of 64 buffers in one
     call, then classify (K = 8)."""
@@ -797,7 +835,7 @@ def run_export(args):
                   "note": "host-link bound (PCIe); value counts image bytes moved per second"})
 
 
-OTHER = {"kv-ring": run_kv_ring, "sweep": run_sweep, "bank": run_bank, "markovian": run_markovian,
+OTHER = {"kv-ring": run_kv_ring, "verify": run_verify, "sweep": run_sweep, "bank": run_bank, "markovian": run_markovian,
          "shrink": run_shrink, "discover": run_discover, "export": run_export}
 
 
