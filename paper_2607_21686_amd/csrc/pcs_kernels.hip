@@ -927,8 +927,8 @@ __device__ __forceinline__ uint32_t score_key(uint32_t bits)
 }
 
 // Entry i is kept iff fewer than `keep` entries rank before it (a smaller
-// key, or an equal key at a lower index).  One lane per entry counts over
-// all keys, staged through LDS in tiles that every lane reads in the same
+// key, or an equal key at a lower index).  A lane quad per entry counts over
+// all keys, staged through LDS in tiles that the quads read in the same
 // order (broadcast reads, four keys per read).  A tile is padded to a
 // multiple of four with the largest key at indices past the end, which
 // never rank before anything.
@@ -936,7 +936,10 @@ __global__ __launch_bounds__(256) void k_shrink_rank(const uint32_t *__restrict_
                                                      uint32_t *__restrict__ flags)
 {
     __shared__ __attribute__((aligned(16))) uint32_t tile[2048];
-    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+    // Lane `part` of the quad compares against every fourth group of four
+    // keys of each tile; the quad sums its partial counts by shuffles.
+    const uint32_t gt = blockIdx.x * 256 + threadIdx.x;
+    const uint32_t i = gt >> 2, part = gt & 3;
     const uint32_t ki = i < n ? score_key(scores[i]) : 0;
     auto before = [&](uint32_t kj, uint32_t j) -> uint32_t { return (kj < ki || (kj == ki && j < i)) ? 1u : 0u; };
     uint32_t rank = 0;
@@ -947,14 +950,16 @@ __global__ __launch_bounds__(256) void k_shrink_rank(const uint32_t *__restrict_
         __syncthreads();
         const uint4 *t4 = reinterpret_cast<const uint4 *>(tile);
 #pragma unroll 4
-        for (uint32_t q = 0; q < m4 / 4; ++q) {
+        for (uint32_t q = part; q < m4 / 4; q += 4) {
             const uint4 v = t4[q];
             const uint32_t j = base + 4 * q;
             rank += before(v.x, j) + before(v.y, j + 1) + before(v.z, j + 2) + before(v.w, j + 3);
         }
         __syncthreads();
     }
-    if (i < n) flags[i] = rank < keep ? 1u : 0u;
+    rank += (uint32_t)__shfl_xor((int)rank, 1, 64);
+    rank += (uint32_t)__shfl_xor((int)rank, 2, 64);
+    if (part == 0 && i < n) flags[i] = rank < keep ? 1u : 0u;
 }
 
 // Kept entry i goes to position offsets[i] (exclusive scan of the flags), so
@@ -1161,8 +1166,8 @@ hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, 
 {
     if (n == 0) return hipSuccess;
     const uint32_t blocks = (n + 255) / 256;
-    hipLaunchKernelGGL(k_shrink_rank, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint32_t *>(scores), n,
-                       keep, flags);
+    hipLaunchKernelGGL(k_shrink_rank, dim3((n + 63) / 64), dim3(256), 0, s, reinterpret_cast<const uint32_t *>(scores),
+                       n, keep, flags);
     if (hipError_t e = hipGetLastError()) return e;
     hipLaunchKernelGGL(k_scan<CountArray>, dim3(1), dim3(1024), 0, s, CountArray{flags}, (uint64_t)n, offsets,
                        total, nullptr);
