@@ -34,9 +34,14 @@
  *     handles are valid when the call returns.  Buffers a call reads must not
  *     be modified, and buffers it writes must not be read, by other streams
  *     until then (I2 durability is defined in stream order).
- *   - Status: PCS_OK (0) or a negative PCS_E_* code.  On any error other
- *     than PCS_E_HIP nothing has been enqueued and no handle was created;
- *     pcs_last_error() describes the failure.  PCS_E_HIP means a HIP call
+ *   - Status: PCS_OK (0) or a negative PCS_E_* code.  On an error no handle
+ *     was created and pcs_last_error() describes the failure.  Nothing has
+ *     been enqueued either, except where an entry point says otherwise: an
+ *     image that fails pcs_import's device check (PCS_E_CORRUPT), an
+ *     incremental checkpoint that waited for its stored-chunk count and then
+ *     found no room for the chunks (PCS_E_NOMEM; its fingerprint outputs were
+ *     written), and pcs_discover after its probes ran; each of these has
+ *     waited for its work when it returns.  PCS_E_HIP means a HIP call
  *     failed after some work may have been enqueued.
  *   - A context is not thread-safe: use one context per host thread.
  */
