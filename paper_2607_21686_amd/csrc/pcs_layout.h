@@ -58,7 +58,7 @@ struct MerkleList {
 //   ArgTables: carried in the kernel arguments themselves (no upload, no map
 //              kernel: a workgroup finds its buffer and first run with short
 //              searches); jobs of at most kArgBufs buffers and kArgRuns runs.
-constexpr uint32_t kArgBufs = 8, kArgRuns = 64;
+constexpr uint32_t kArgBufs = 16, kArgRuns = 64;
 // Small jobs (at most kSmallJobGroups groups) are cut into kSmallTiles
 // sub-tiles per group, so that a few groups still spread over many CUs.
 // Fingerprint and pack tiles then write one Merkle node per sub-tile (an

@@ -86,6 +86,53 @@ def test_small_job_boundary(ctx, pcs, groups):
     ctx.delete(plain)
 
 
+@pytest.mark.parametrize("nbuf", [8, 9, 16, 17])
+def test_argument_table_boundary(ctx, pcs, nbuf):
+    """Jobs of at most 16 buffers and 64 runs carry their tables in the kernel
+    arguments, larger ones upload them: both sides of the buffer limit, with
+    empty and ragged buffers and a wrapped ring: fingerprints, roots, the
+    fused checkpoint, restore, and an incremental checkpoint with changes."""
+    rng = np.random.default_rng(700 + nbuf)
+    sizes = [int(x) for x in rng.choice([0, 1, 17, 4095, 4096, 9000, 64 * 4096 + 3, 70 * 4096], size=nbuf - 1)]
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    g = W.Ring(3, 40, 1024, 33, 29)
+    ring = rng.integers(0, 256, size=g.ring_bytes, dtype=np.uint8)
+    logical = bufs + [oracle.ring_window(ring, g.outer, g.outer_stride, g.capacity, g.row_bytes, g.head, g.window)]
+    d = [dev(b) for b in bufs] + [dev(ring)]
+    descs = [pcs.flat(t, b.size) for t, b in zip(d, bufs)] + [pcs.ring(d[-1], g.outer, g.capacity, g.row_bytes,
+                                                                       g.head, g.window)]
+    log("argument-table boundary:", nbuf, "buffers")
+    h, r, s_ = oracle_fp(logical)
+    gh, gr, gs = gpu_fp(ctx, pcs, descs, h.size)
+    assert np.array_equal(gh, h) and np.array_equal(gr, r) and gs == s_
+    ch = zeros_u64(h.size)
+    snap = ctx.checkpoint(descs, hash=True, chunk_hashes=ch)
+    assert np.array_equal(u64(ch)[:h.size], h)
+    pay = torch.empty(max(1, ctx.info(snap)["stored_bytes"]), dtype=torch.uint8, device="cuda")
+    ctx.payload(snap, pay)
+    assert np.array_equal(host(pay)[:ctx.info(snap)["stored_bytes"]], oracle.pack(logical))
+    # Change a byte in every non-empty flat buffer, then checkpoint against the snapshot.
+    new = [b.copy() for b in bufs]
+    for k, b in enumerate(new):
+        if b.size:
+            b[int(rng.integers(0, b.size))] ^= 0x5A
+            d[k].copy_(torch.from_numpy(b).cuda())
+    st = oracle.Store()
+    po = st.checkpoint(logical)
+    co = st.checkpoint(new + [logical[-1]], po)
+    inc = ctx.checkpoint(descs, parent=snap)
+    assert ctx.info(inc)["dirty_chunks"] * 4096 == st.payload(co).size
+    outs = [torch.zeros(max(1, n), dtype=torch.uint8, device="cuda") for n in sizes]
+    rout = torch.zeros(g.ring_bytes, dtype=torch.uint8, device="cuda")
+    ctx.restore(inc, [pcs.flat(o, n) for o, n in zip(outs, sizes)] + [pcs.ring(rout, g.outer, g.capacity, g.row_bytes,
+                                                                               5, g.window)])
+    assert all(np.array_equal(host(o)[:n], b) for o, n, b in zip(outs, sizes, new))
+    assert np.array_equal(oracle.ring_window(host(rout), g.outer, g.outer_stride, g.capacity, g.row_bytes, 5,
+                                             g.window), logical[-1])
+    ctx.delete(inc)
+    ctx.delete(snap)
+
+
 def test_fingerprint_each_size_alone(ctx, pcs):
     rng = np.random.default_rng(11)
     for n in FLAT_SIZES + [1 << 20, (1 << 20) + 3]:
