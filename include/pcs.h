@@ -288,7 +288,8 @@ int pcs_snapshot_hashes(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_dst, uint64_t c
  * "Across a process boundary").
  *
  * pcs_export writes a self-contained image of the snapshot to host memory
- * h_dst (capacity `cap`) and waits for it: a header (layout of every buffer,
+ * h_dst (capacity `cap`) and waits for it, also when it returns an error, so
+ * no copy into h_dst is in flight when it returns: a header (layout of every buffer,
  * Merkle roots, chunk fingerprints) and the full logical state in the
  * canonical layout, whether the snapshot is full or incremental.  With
  * h_dst == NULL it only reports the size in *written.  Layout (little-endian):

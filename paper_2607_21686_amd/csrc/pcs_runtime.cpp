@@ -1215,18 +1215,26 @@ int pcs_kernel_time(pcs_ctx *c, const char *name, uint64_t *launches, double *to
     HIP_TRY(c, hipStreamSynchronize(c->stream));
     double ms = 0;
     uint64_t k = 0;
+    hipError_t e = hipSuccess;
     auto it = c->timers.find(name);
     if (it != c->timers.end()) {
+        // Every pair is destroyed and the name's record cleared, also when a
+        // query fails (then the first failure is returned).
         for (auto &ab : it->second) {
             float t = 0;
-            HIP_TRY(c, hipEventElapsedTime(&t, ab.first, ab.second));
-            ms += t;
-            ++k;
+            const hipError_t q = e == hipSuccess ? hipEventElapsedTime(&t, ab.first, ab.second) : e;
+            if (q == hipSuccess) {
+                ms += t;
+                ++k;
+            } else {
+                e = q;
+            }
             (void)hipEventDestroy(ab.first);
             (void)hipEventDestroy(ab.second);
         }
         c->timers.erase(it);
     }
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventElapsedTime");
     if (launches) *launches = k;
     if (total_ms) *total_ms = ms;
     return PCS_OK;
@@ -1281,11 +1289,16 @@ int pcs_export(pcs_ctx *c, pcs_snap snap, void *h_dst, uint64_t cap, uint64_t *w
                                          (uint64_t *)(roots_dev + 8 * n)))
             return st;
     }
-    HIP_TRY(c, hipMemcpyAsync(img + L.roots_off, (void *)roots_dev, 8 * (n + 1), hipMemcpyDeviceToHost, s));
-    if (T) HIP_TRY(c, hipMemcpyAsync(img + L.hashes_off, (void *)hashes_dev, 8 * T, hipMemcpyDeviceToHost, s));
-    if (L.payload)
-        HIP_TRY(c, hipMemcpyAsync(img + L.data_off, (void *)payload_dev, L.payload, hipMemcpyDeviceToHost, s));
-    HIP_TRY(c, hipStreamSynchronize(s));
+    // The copies write into the caller's image: an error after the first one
+    // was enqueued waits for the stream before returning, so no copy is still
+    // in flight when the caller regains the image.
+    hipError_t e = hipMemcpyAsync(img + L.roots_off, (void *)roots_dev, 8 * (n + 1), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess && T) e = hipMemcpyAsync(img + L.hashes_off, (void *)hashes_dev, 8 * T, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess && L.payload)
+        e = hipMemcpyAsync(img + L.data_off, (void *)payload_dev, L.payload, hipMemcpyDeviceToHost, s);
+    const hipError_t w = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(c, e, "image download");
+    if (w != hipSuccess) return hip_fail(c, w, "hipStreamSynchronize");
     return PCS_OK;
 }
 
