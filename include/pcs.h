@@ -33,7 +33,8 @@
  *     device outputs are valid once that stream reaches the call's end;
  *     handles are valid when the call returns.  Buffers a call reads must not
  *     be modified, and buffers it writes must not be read, by other streams
- *     until then (I2 durability is defined in stream order).
+ *     until then (I2 durability is defined in stream order); every device
+ *     buffer a call names stays allocated until then as well.
  *   - Status: PCS_OK (0) or a negative PCS_E_* code.  On an error no handle
  *     was created and pcs_last_error() describes the failure.  Nothing has
  *     been enqueued either, except where an entry point says otherwise: an
@@ -136,8 +137,10 @@ typedef struct pcs_snap_info {
  * itself.  `hip_stream` is a hipStream_t (NULL = the null stream) on which
  * every call of this context is enqueued.  The arena and the stream are
  * borrowed: the caller keeps them alive until pcs_ctx_destroy returns.
- * d_arena must be 4096-byte aligned.  Small pinned host buffers are
- * allocated for descriptor uploads.
+ * d_arena must be 16-byte aligned; the library uses the arena from its first
+ * 4096-byte boundary on, in whole 4096-byte units, and PCS_E_INVAL results if
+ * less than one unit remains.  Small pinned host buffers are allocated for
+ * descriptor uploads.
  */
 int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ctx **out);
 
@@ -289,7 +292,8 @@ int pcs_snapshot_hashes(pcs_ctx *ctx, pcs_snap snap, uint64_t *d_dst, uint64_t c
  *
  * pcs_export writes a self-contained image of the snapshot to host memory
  * h_dst (capacity `cap`) and waits for it, also when it returns an error, so
- * no copy into h_dst is in flight when it returns: a header (layout of every buffer,
+ * no copy into h_dst is in flight when it returns (after an error h_dst may
+ * hold part of an image): a header (layout of every buffer,
  * Merkle roots, chunk fingerprints) and the full logical state in the
  * canonical layout, whether the snapshot is full or incremental.  With
  * h_dst == NULL it only reports the size in *written.  Layout (little-endian):

@@ -128,7 +128,14 @@ def chunk_counts(bufs):
 
 
 class Context:
-    """A libpcs context over a caller-owned uint8 device arena, bound to a stream."""
+    """A libpcs context over a caller-owned uint8 device arena, bound to a stream.
+
+    Every call is enqueued on that stream and returns before its kernels
+    run.  A tensor named in a call must stay allocated until the stream has
+    passed the call: torch's caching allocator only orders a freed block
+    after the work of the stream it was allocated on, so when the context's
+    stream is another one, hold the tensor or call
+    ``tensor.record_stream(ctx.stream)`` before dropping it."""
 
     def __init__(self, arena: torch.Tensor, stream: torch.cuda.Stream | None = None):
         if arena.dtype != torch.uint8:
