@@ -166,12 +166,14 @@ def traffic(fetch_db, write_db, sessions=1024, restored=512):
     rec["restore_kernel"] = dict(kernel="k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (%d sessions)"
                                  % restored, **one("copy", restored))
     rec["kernel_source_sha256"] = kernel_source_sha()
-    rec["commands"] = [
-        "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/prof_fetch -o fetch -- python3 bench.py --steps 2 --warmup 1 "
-        "--no-cpu-baseline --calibrate-copy",
-        "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/prof_write -o write -- python3 bench.py --steps 2 --warmup 1 "
-        "--no-cpu-baseline --calibrate-copy",
-        "python3 bench.py --traffic gpurun_out/prof_fetch/fetch_results.db gpurun_out/prof_write/write_results.db"]
+    # The commands that made the two databases (rocprofv3 writes <dir>/<name>_results.db).
+    def pmc_cmd(counter, db):
+        rel = os.path.relpath(db)
+        name = os.path.basename(rel)[:-len("_results.db")] if rel.endswith("_results.db") else "pmc"
+        return ("rocprofv3 --pmc %s -d %s -o %s -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline "
+                "--calibrate-copy" % (counter, os.path.dirname(rel) or ".", name))
+    rec["commands"] = [pmc_cmd("FETCH_SIZE", fetch_db), pmc_cmd("WRITE_SIZE", write_db),
+                       "python3 bench.py --traffic %s %s" % (os.path.relpath(fetch_db), os.path.relpath(write_db))]
     with open(TRAFFIC_JSON, "w") as fh:
         json.dump(rec, fh, indent=1)
         fh.write("\n")
@@ -187,8 +189,9 @@ def main():
         traffic(*args.traffic)
         return
     if args.gpus != 1:
-        print("bench.py runs on one GPU: this build has no multi-GPU path (sessions shard across GPUs "
-              "with no exchange; see the design notes).", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path.  Sessions are independent, so "
+              "each GPU would run its own share of them with its own arena and stream, with no exchange "
+              "between GPUs.", file=sys.stderr)
         sys.exit(2)
     if args.workload != "batch":
         out = OTHER[args.workload](args)
