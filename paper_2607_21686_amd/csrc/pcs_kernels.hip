@@ -681,7 +681,8 @@ __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
     // its slices in an order rotated by c and the tile index, so that a
     // step's accesses cover every offset within a chunk instead of one (all
     // tiles touching the same offsets at once loads the HBM channels
-    // unevenly; the rotation is worth 3-10% on copies).
+    // unevenly): restores of flat buffers are 3-8% faster with the rotation,
+    // the 1024-session batch 1.5% slower.
     uint4 v[U], n[U];
     auto off = [&](int k, uint32_t step) -> uint32_t {
         const uint32_t c = (k * T + t) / LPS;

@@ -86,6 +86,9 @@ struct ArgTables {
     JobBuf bufs[kArgBufs];
     Run runs[kArgRuns];
 };
+// Kernel arguments are limited to 4 KiB; a launch passes one ArgTables and at
+// most a few pointers and sizes besides.
+static_assert(sizeof(ArgTables) + 256 <= 4096, "argument tables must fit in the kernel arguments");
 // Merkle lists carried in the kernel arguments: the first nbuf_lists reduce
 // group nodes to buffer roots, the rest reduce those roots to session roots
 // (their begin/count index the buffer lists).
@@ -94,5 +97,6 @@ struct ArgLists {
     uint32_t nlists;
     MerkleList lists[kArgBufs + 1];
 };
+static_assert(sizeof(ArgLists) + 256 <= 4096, "Merkle lists must fit in the kernel arguments");
 
 }  // namespace pcs
