@@ -271,29 +271,39 @@ void settle(pcs_ctx *c, bool wait)
     c->pending.swap(keep);
 }
 
-// Allocates a snapshot block, first settling finished incremental
-// snapshots, then (if still short) waiting for all of them.
-bool alloc_block(pcs_ctx *c, uint64_t bytes, uint64_t *off)
+// Waits for the oldest incremental snapshot still pending (the stream
+// finishes them in order), then settles it and every other one that has
+// finished.  False if none is pending, or if the oldest one could not be
+// settled (a failed wait), so that callers never retry without progress.
+bool settle_oldest(pcs_ctx *c)
 {
-    settle(c, false);
-    if (c->arena.alloc(bytes, off)) return true;
-    if (!c->pending.empty()) {
-        settle(c, true);
-        return c->arena.alloc(bytes, off);
+    for (auto &w : c->pending) {
+        auto n = w.lock();
+        if (!n || n->settled) continue;
+        (void)hipEventSynchronize(n->ev);
+        settle(c, false);
+        return n->settled;
     }
+    c->pending.clear();
     return false;
 }
 
-bool alloc_block_top(pcs_ctx *c, uint64_t bytes, uint64_t *off)
+// Allocates a snapshot block (from the bottom, or the top of the arena),
+// first settling finished incremental snapshots, then waiting for pending
+// ones oldest first until the block fits: the wait ends as soon as enough
+// reserved payload space has been trimmed, not when the stream is idle.
+bool alloc_settled(pcs_ctx *c, uint64_t bytes, uint64_t *off, bool top)
 {
+    auto try_alloc = [&] { return top ? c->arena.alloc_top(bytes, off) : c->arena.alloc(bytes, off); };
     settle(c, false);
-    if (c->arena.alloc_top(bytes, off)) return true;
-    if (!c->pending.empty()) {
-        settle(c, true);
-        return c->arena.alloc_top(bytes, off);
-    }
+    if (try_alloc()) return true;
+    while (settle_oldest(c))
+        if (try_alloc()) return true;
     return false;
 }
+
+bool alloc_block(pcs_ctx *c, uint64_t bytes, uint64_t *off) { return alloc_settled(c, bytes, off, false); }
+bool alloc_block_top(pcs_ctx *c, uint64_t bytes, uint64_t *off) { return alloc_settled(c, bytes, off, true); }
 
 std::shared_ptr<SnapNode> lookup(pcs_ctx *c, pcs_snap h)
 {
