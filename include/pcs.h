@@ -197,7 +197,9 @@ int pcs_classify(pcs_ctx *ctx, const uint64_t *d_hashes, uint32_t K, const uint6
  *     always stored (flags are ignored).  The call normally reserves one slot
  *     per chunk and returns the unused part to the arena once the stream has
  *     produced the stored-chunk count; if the arena cannot hold that
- *     reservation it waits for the stream and allocates exactly, and if even
+ *     reservation it first waits for earlier incremental checkpoints (oldest
+ *     first) until their unused reservations are returned, then for its own
+ *     count and allocates exactly, and if even
  *     that fails it returns PCS_E_NOMEM after its fingerprint outputs were
  *     written.
  *   d_chunk_hashes, d_roots, d_session_root: optional copies of the
