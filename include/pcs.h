@@ -232,7 +232,10 @@ int pcs_checkpoint_batch(pcs_ctx *ctx, const pcs_buf *h_plans, const uint32_t *h
  * be restored at a new head).  Only window rows are written.  Destinations
  * must not overlap each other.  Returns PCS_E_SHAPE on a layout mismatch.
  * Restores copy out of the snapshot, so two restores of one snapshot (or of
- * a fork) are independent (I3).
+ * a fork) are independent (I3).  A restore of at most 16 buffers and 64
+ * physical runs carries its tables in the kernel arguments and takes no
+ * arena space; a larger one uploads them into arena scratch and returns
+ * PCS_E_NOMEM if the arena cannot hold that.
  */
 int pcs_restore(pcs_ctx *ctx, pcs_snap snap, const pcs_buf *h_dst, uint32_t n);
 

@@ -354,11 +354,16 @@ int stage(pcs_ctx *c, const Job &job, bool small, Temp &t, const std::vector<uin
     if (!extra.empty()) cv.add(&o_extra, extra.size());
     const uint64_t hb = cv.total;
     if (!small) cv.add(&o_map, sizeof(GroupRef) * G);
-    cv.add(&o_scr, dev_bytes);
-    if (int e = temp_alloc(c, t, cv.total)) return e;
-    const uint64_t base = c->arena_dev + t.off;
-    extra_dev = base + o_extra;
-    scratch_dev = base + o_scr;
+    if (dev_bytes) cv.add(&o_scr, dev_bytes);
+    // A small job with nothing to upload and no device scratch (a restore,
+    // a plain pack, classify) takes no arena space at all.
+    uint64_t base = 0;
+    if (cv.total) {
+        if (int e = temp_alloc(c, t, cv.total)) return e;
+        base = c->arena_dev + t.off;
+    }
+    extra_dev = extra.empty() ? 0 : base + o_extra;
+    scratch_dev = dev_bytes ? base + o_scr : 0;
     sg.small = small;
     if (small) {
         memset(&sg.arg, 0, sizeof sg.arg);
