@@ -50,7 +50,7 @@ def parse():
                     choices=["batch", "kv-ring", "verify", "sweep", "bank", "markovian", "shrink", "discover", "export"],
                     help="batch (default, the headline) or one of the other seeded configurations")
     ap.add_argument("--sessions", type=int, default=1024)
-    ap.add_argument("--cpu-sessions", type=int, default=384, help="oracle sample size (sessions)")
+    ap.add_argument("--cpu-sessions", type=int, default=512, help="oracle sample size (sessions)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (for HBM counter scaling)")
