@@ -4,8 +4,9 @@
 //
 // Work decomposition shared by every kernel: a job is a table of buffers,
 // each cut into 4096-byte chunks, and the chunks of one buffer into aligned
-// groups of 64.  One workgroup handles one group; it finds its buffer through
-// a group-to-buffer map (k_group_map) when the tables live in device memory,
+// groups of 64.  One workgroup handles one group (in a job of at most 128
+// groups, an eighth of one); it finds its buffer through a group-to-buffer
+// map (k_group_map) when the tables live in device memory,
 // or by a short search when a small job carries its tables in the kernel
 // arguments (no upload and no map launch).  Groups never straddle
 // buffers, so a group's 64 chunk fingerprints reduce to one Merkle node
@@ -622,8 +623,10 @@ __global__ __launch_bounds__(256) void k_merkle_small(const ArgLists L, const ui
 
 // Copy tile kernel: one workgroup moves one tile of CPW chunks (a 64-chunk
 // group, or an eighth of one in small jobs), SL bytes of every chunk per
-// step, with coalesced 16-byte loads and stores (the shape of the fused
-// kernel without the hash).
+// step, with coalesced 16-byte loads and stores: the fused kernel's tile
+// without the hash and the LDS staging, in a shape of its own (512 lanes and
+// 1 KiB slices for whole groups, measured faster for copies than the fused
+// kernel's 1024 lanes and 512-byte slices).
 //   PACK:    the buffer's runs -> the chunk slots of the snapshot; a partial
 //            last chunk is zero-padded to the end of its slot.
 //   !PACK:   the chunk slots (contiguous, or per chunk through a manifest of
