@@ -456,18 +456,25 @@ def _line(args, metric_value, ms_per_step, workload, cfg, roof_kernel, alg_bytes
 
 
 def _timed(args, ctx, step, kernels):
+    """Wall time per step from a pass without the library's per-launch timing
+    events (which cost a few microseconds of host time per launch, enough to
+    slow workloads of many small launches), then kernel times from a second
+    pass of the same steps with them."""
     import torch
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    for k in kernels:
-        ctx.kernel_time(k)
-    ctx.set_timing(True)
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    for k in kernels:
+        ctx.kernel_time(k)
+    ctx.set_timing(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
     ctx.set_timing(False)
     return elapsed / args.steps, {k: ctx.kernel_time(k) for k in kernels}
 
@@ -581,7 +588,11 @@ def run_bank(args):
     bank = W.config2(1)
     lat = torch.from_numpy(bank.latents.copy()).cuda()
     pos = torch.from_numpy(bank.poses.copy()).cuda()
-    ctx = P.Context(torch.empty(768 << 20, dtype=torch.uint8, device="cuda"))
+    # 4 GiB of arena: each incremental checkpoint reserves one slot per chunk
+    # until its stored-chunk count is known, and the reservations of the
+    # checkpoints in flight reach 3.3 GB; a tighter arena makes calls wait for
+    # the GPU (768 MiB: 3.1 instead of 2.5 ms of checkpoints per run).
+    ctx = P.Context(torch.empty(4 << 30, dtype=torch.uint8, device="cuda"))
     plans = [P.BufArray([P.flat(lat, 8 * j * bank.latent_entry_bytes), P.flat(pos, 8 * j * bank.pose_entry_bytes)])
              for j in range(1, 65)]
     out_l, out_p = torch.empty_like(lat), torch.empty_like(pos)
