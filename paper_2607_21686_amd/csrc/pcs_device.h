@@ -51,13 +51,16 @@ hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64
 hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total, hipStream_t s,
                        uint64_t *total_host = nullptr);
 constexpr uint64_t kScanCompactMaxGroups = 4096;
-// Small incremental jobs of at most this many groups scan and compact in one
-// workgroup (one launch); larger ones scan in one workgroup and compact with
-// one workgroup per group.
+// Small incremental jobs (tables in the kernel arguments, at most
+// kScanCompactMaxGroups groups): one single-workgroup launch reduces the
+// Merkle lists and scans the dirty masks (total also to the pinned host
+// word); up to kScanCompactFusedGroups groups it also assigns the slots,
+// otherwise the offsets go to `offsets` and launch_compact follows.
 constexpr uint64_t kScanCompactFusedGroups = 64;
-hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint64_t *dirty_mask,
-                                     uint64_t payload_arena_top, uint64_t *list, uint64_t *total,
-                                     uint64_t *total_host, hipStream_t s);
+hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
+                                    uint64_t *scratch_b, const ArgTables &tab, uint64_t ngroups,
+                                    const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
+                                    uint64_t *offsets, uint64_t *total, uint64_t *total_host, hipStream_t s);
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
 // Flips the lowest bit of the byte at device address addr.
 hipError_t launch_flip_bit(uint64_t addr, hipStream_t s);

@@ -519,14 +519,16 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
 // ---------------------------------------------------------------- Merkle lists
 
 // Promote-odd Merkle root of src[0, m), computed by the whole workgroup
-// (256 lanes); the result is valid in thread 0.  Aligned 64-value blocks
+// (NT lanes); the result is valid in thread 0.  Aligned 64-value blocks
 // reduce independently (one wavefront each); up to two passes through global
 // scratch sa/sb (each read only after it is fully written) bring the list to
 // <= 4096 values, then the rest happens in LDS.  Ends with a barrier so the
 // LDS buffers can be reused.
+template <int NT>
 __device__ uint64_t reduce_list(const uint64_t *src, uint64_t m, uint64_t *sa, uint64_t *sb, uint64_t *lds,
                                 uint64_t *lds2)
 {
+    constexpr uint32_t NW = NT / 64;  // wavefronts
     const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
     uint64_t root = 0;
     if (m == 0) {
@@ -535,7 +537,7 @@ __device__ uint64_t reduce_list(const uint64_t *src, uint64_t m, uint64_t *sa, u
         uint64_t *scratch[2] = {sa, sb};
         for (int k = 0; k < 2 && m > 4096; ++k) {
             const uint64_t nb = (m + 63) / 64;
-            for (uint64_t blk = wave; blk < nb; blk += 4) {
+            for (uint64_t blk = wave; blk < nb; blk += NW) {
                 const uint32_t cnt = (uint32_t)umin(64, m - 64 * blk);
                 const uint64_t v = lane < cnt ? src[64 * blk + lane] : 0;
                 const uint64_t r = wave_merkle(v, cnt);
@@ -545,12 +547,12 @@ __device__ uint64_t reduce_list(const uint64_t *src, uint64_t m, uint64_t *sa, u
             src = scratch[k];
             m = nb;
         }
-        for (uint64_t j = t; j < m; j += 256) lds[j] = src[j];
+        for (uint64_t j = t; j < m; j += NT) lds[j] = src[j];
         __syncthreads();
         const uint64_t *ls = lds;
         if (m > 64) {
             const uint64_t nb = (m + 63) / 64;
-            for (uint64_t blk = wave; blk < nb; blk += 4) {
+            for (uint64_t blk = wave; blk < nb; blk += NW) {
                 const uint32_t cnt = (uint32_t)umin(64, m - 64 * blk);
                 const uint64_t v = lane < cnt ? lds[64 * blk + lane] : 0;
                 const uint64_t r = wave_merkle(v, cnt);
@@ -578,7 +580,7 @@ __global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ l
     __shared__ uint64_t lds[4096];
     __shared__ uint64_t lds2[64];
     const MerkleList Lst = lists[blockIdx.x];
-    const uint64_t root = reduce_list(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
+    const uint64_t root = reduce_list<256>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
     if (threadIdx.x == 0) {
         if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
         if (Lst.dst[1]) *(g_u64 *)Lst.dst[1] = root;
@@ -586,17 +588,16 @@ __global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ l
     }
 }
 
-// One workgroup for a small job: every buffer list, then every session list
-// over the buffer roots just computed (kept in LDS).
-__global__ __launch_bounds__(256) void k_merkle_small(const ArgLists L, const uint64_t *__restrict__ in,
-                                                      uint64_t *__restrict__ sa, uint64_t *__restrict__ sb)
+// The lists of a small job, reduced by one workgroup of NT lanes: every
+// buffer list, then every session list over the buffer roots just computed
+// (kept in LDS).  Ends with a barrier.
+template <int NT>
+__device__ void merkle_lists(const ArgLists &L, const uint64_t *in, uint64_t *sa, uint64_t *sb, uint64_t *lds,
+                             uint64_t *lds2, uint64_t *roots)
 {
-    __shared__ uint64_t lds[4096];
-    __shared__ uint64_t lds2[64];
-    __shared__ uint64_t roots[kArgBufs];
     for (uint32_t j = 0; j < L.nbuf_lists; ++j) {
         const MerkleList &Lst = L.lists[j];
-        const uint64_t root = reduce_list(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
+        const uint64_t root = reduce_list<NT>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
         if (threadIdx.x == 0) {
             roots[j] = root;
             if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
@@ -617,6 +618,17 @@ __global__ __launch_bounds__(256) void k_merkle_small(const ArgLists L, const ui
             }
         }
     }
+    __syncthreads();
+}
+
+// One workgroup for a small job's Merkle lists.
+__global__ __launch_bounds__(256) void k_merkle_small(const ArgLists L, const uint64_t *__restrict__ in,
+                                                      uint64_t *__restrict__ sa, uint64_t *__restrict__ sb)
+{
+    __shared__ uint64_t lds[4096];
+    __shared__ uint64_t lds2[64];
+    __shared__ uint64_t roots[kArgBufs];
+    merkle_lists<256>(L, in, sa, sb, lds, lds2, roots);
 }
 
 // ---------------------------------------------------------------- copies
@@ -805,26 +817,42 @@ __global__ __launch_bounds__(64) void k_compact(const Tab tab, const uint64_t *_
     compact_chunk(jb, b, i, lane, dirty_mask[G], offsets[G], payload_arena_top, list);
 }
 
-// Small incremental jobs: the scan and the slot assignment in one
-// workgroup (offsets in LDS), and the stored-chunk count written both to
-// device memory and to the caller's pinned host word.
-__global__ __launch_bounds__(1024) void k_scan_compact_small(const ArgTables tab, uint64_t ngroups,
-                                                             const uint64_t *__restrict__ dirty_mask,
-                                                             uint64_t payload_arena_top, uint64_t *__restrict__ list,
-                                                             uint64_t *__restrict__ total, uint64_t *total_host)
+// Small incremental jobs (tables in the kernel arguments), after the
+// fingerprint + diff tiles, in one workgroup and one launch: the Merkle
+// lists (buffer and session roots), then the exclusive scan of the dirty
+// masks' set bits, with the stored-chunk count written to device memory and
+// to the caller's pinned host word.  kCompact (at most
+// kScanCompactFusedGroups groups): the offsets stay in LDS and the slot
+// assignment follows here, one thread per chunk (a chunk's slot depends only
+// on its group's mask and offset); otherwise the offsets go to `offsets` for
+// k_compact.
+template <bool kCompact>
+__global__ __launch_bounds__(1024) void k_merkle_scan_small(const ArgLists L, const uint64_t *__restrict__ nodes,
+                                                            uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
+                                                            const ArgTables tab, uint64_t ngroups,
+                                                            const uint64_t *__restrict__ dirty_mask,
+                                                            uint64_t payload_arena_top, uint64_t *__restrict__ list,
+                                                            uint64_t *__restrict__ offsets,
+                                                            uint64_t *__restrict__ total, uint64_t *total_host)
 {
+    __shared__ uint64_t lds[4096];
+    __shared__ uint64_t lds2[64];
+    __shared__ uint64_t roots[kArgBufs];
     __shared__ uint64_t sums[2][1024];
-    __shared__ uint64_t offs[kScanCompactFusedGroups];
-    scan_counts(MaskBits{dirty_mask}, ngroups, offs, total, sums);
-    // One thread per chunk (a chunk's slot depends only on its group's mask
-    // and offset): 16 groups are one pass of the workgroup.
-    for (uint64_t e = threadIdx.x; e < ngroups * kGroupChunks; e += 1024) {
-        const uint64_t g = e / kGroupChunks;
-        const uint32_t lane = (uint32_t)(e % kGroupChunks);
-        const uint32_t b = buf_index(tab, g);
-        const JobBuf &jb = tab.bufs[b];
-        const uint64_t i = (g - jb.group_begin) * kGroupChunks + lane;
-        if (i < jb.nchunks) compact_chunk(jb, b, i, lane, dirty_mask[g], offs[g], payload_arena_top, list);
+    __shared__ uint64_t offs[kCompact ? kScanCompactFusedGroups : 1];
+    merkle_lists<1024>(L, nodes, sa, sb, lds, lds2, roots);
+    if constexpr (kCompact) {
+        scan_counts(MaskBits{dirty_mask}, ngroups, offs, total, sums);
+        for (uint64_t e = threadIdx.x; e < ngroups * kGroupChunks; e += 1024) {
+            const uint64_t g = e / kGroupChunks;
+            const uint32_t lane = (uint32_t)(e % kGroupChunks);
+            const uint32_t b = buf_index(tab, g);
+            const JobBuf &jb = tab.bufs[b];
+            const uint64_t i = (g - jb.group_begin) * kGroupChunks + lane;
+            if (i < jb.nchunks) compact_chunk(jb, b, i, lane, dirty_mask[g], offs[g], payload_arena_top, list);
+        }
+    } else {
+        scan_counts(MaskBits{dirty_mask}, ngroups, offsets, total, sums);
     }
     if (threadIdx.x == 1023 && total_host) {
         *(volatile uint64_t *)total_host = *total;
@@ -1155,13 +1183,18 @@ hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets
     return hipGetLastError();
 }
 
-hipError_t launch_scan_compact_small(const ArgTables &tab, uint64_t ngroups, const uint64_t *dirty_mask,
-                                     uint64_t payload_arena_top, uint64_t *list, uint64_t *total,
-                                     uint64_t *total_host, hipStream_t s)
+hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
+                                    uint64_t *scratch_b, const ArgTables &tab, uint64_t ngroups,
+                                    const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
+                                    uint64_t *offsets, uint64_t *total, uint64_t *total_host, hipStream_t s)
 {
-    if (ngroups > kScanCompactFusedGroups) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_scan_compact_small, dim3(1), dim3(1024), 0, s, tab, ngroups, dirty_mask,
-                       payload_arena_top, list, total, total_host);
+    if (ngroups > kScanCompactMaxGroups) return hipErrorInvalidValue;
+    if (ngroups <= kScanCompactFusedGroups)
+        hipLaunchKernelGGL(k_merkle_scan_small<true>, dim3(1), dim3(1024), 0, s, lists, nodes, scratch_a, scratch_b,
+                           tab, ngroups, dirty_mask, payload_arena_top, list, offsets, total, total_host);
+    else
+        hipLaunchKernelGGL(k_merkle_scan_small<false>, dim3(1), dim3(1024), 0, s, lists, nodes, scratch_a, scratch_b,
+                           tab, ngroups, dirty_mask, payload_arena_top, list, offsets, total, total_host);
     return hipGetLastError();
 }
 

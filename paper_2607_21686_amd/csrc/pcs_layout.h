@@ -98,5 +98,7 @@ struct ArgLists {
     MerkleList lists[kArgBufs + 1];
 };
 static_assert(sizeof(ArgLists) + 256 <= 4096, "Merkle lists must fit in the kernel arguments");
+// The small incremental launch passes both, with a few pointers and sizes.
+static_assert(sizeof(ArgLists) + sizeof(ArgTables) + 128 <= 4096, "Merkle lists and tables must fit together");
 
 }  // namespace pcs

@@ -957,8 +957,10 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     lists.push_back({0, n, {c->arena_dev + node->roots_off + 8 * n, (uint64_t)d_sroot}});
 
     // A small job (tables in kernel arguments) that took the pipelined
-    // reservation runs as: fingerprint+diff, Merkle, scan+compact (which also
-    // writes the stored-chunk count to pinned host memory), dirty copy.
+    // reservation runs as: fingerprint+diff, then one single-workgroup launch
+    // for the Merkle lists and the scan (+ the slot assignment up to 64
+    // groups; it also writes the stored-chunk count to pinned host memory),
+    // the slot assignment above 64 groups, the dirty copy.
     const bool small = is_small(job) && !exact && G <= kScanCompactMaxGroups;
     Carver cv;
     uint64_t o_nodes, o_sa, o_sb, o_roots, o_mask, o_offs, o_total, o_list;
@@ -988,25 +990,20 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         });
     });
     if (st) return st;
-    if ((st = run_merkle(c, small, lists, n, lists_dev, d_nodes, d_sa, d_sb, d_roots_tmp))) return st;
     if (small) {
         node->count_slot = (int)c->free_counts.back();
         c->free_counts.pop_back();
         uint64_t *host_word = &c->counts_dev[node->count_slot];
         const uint64_t top = node->pay_top;
-        if (G <= kScanCompactFusedGroups) {
-            if ((st = launch(c, "incremental", [&] {
-                     return launch_scan_compact_small(sg.arg, G, d_mask, top, d_list, d_total, host_word, s);
-                 })))
-                return st;
-        } else {
-            if ((st = launch(c, "incremental", [&] { return launch_scan(d_mask, G, d_offs, d_total, s, host_word); })))
-                return st;
-            if ((st = launch(c, "incremental", [&] {
-                     return launch_compact(sg.arg, G, d_mask, d_offs, top, d_list, s);
-                 })))
-                return st;
-        }
+        const ArgLists al = arg_lists(lists, n);
+        if ((st = launch(c, "incremental", [&] {
+                 return launch_merkle_scan_small(al, d_nodes, d_sa, d_sb, sg.arg, G, d_mask, top, d_list, d_offs,
+                                                 d_total, host_word, s);
+             })))
+            return st;
+        if (G > kScanCompactFusedGroups &&
+            (st = launch(c, "incremental", [&] { return launch_compact(sg.arg, G, d_mask, d_offs, top, d_list, s); })))
+            return st;
         if ((st = launch(c, "incremental", [&] {
                  return launch_pack_dirty(sg.arg, d_list, d_total, T, payload_top_dev, s);
              })))
@@ -1017,6 +1014,7 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         *out = new_handle(c, node);
         return PCS_OK;
     }
+    if ((st = run_merkle(c, small, lists, n, lists_dev, d_nodes, d_sa, d_sb, d_roots_tmp))) return st;
     if ((st = launch(c, "incremental", [&] { return launch_scan(d_mask, G, d_offs, d_total, s); }))) return st;
     if (exact) {
         HIP_TRY(c, hipMemcpyAsync(&c->counts[c->free_counts.back()], d_total, 8, hipMemcpyDeviceToHost, s));
