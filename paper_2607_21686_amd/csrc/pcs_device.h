@@ -41,6 +41,11 @@ hipError_t launch_classify(const Tab &tab, uint64_t ngroups, const uint64_t *has
                            uint64_t *bitmap, hipStream_t s);
 template <class Tab>
 hipError_t launch_labels(const Tab &tab, const uint64_t *bitmap, uint8_t *labels, hipStream_t s);
+// Classification and labels of a small job (tables in the kernel arguments,
+// at most kClassifyFusedGroups groups) in one single-workgroup launch.
+constexpr uint64_t kClassifyFusedGroups = 1024;
+hipError_t launch_classify_small(const ArgTables &tab, uint64_t ngroups, const uint64_t *hashes, uint32_t K,
+                                 uint64_t total, uint64_t *bitmap, uint8_t *labels, hipStream_t s);
 hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_t *in,
                          uint64_t *scratch_a, uint64_t *scratch_b, uint64_t *roots_out,
                          hipStream_t s);

@@ -901,16 +901,14 @@ __global__ __launch_bounds__(256) void k_reverse_slots(uint64_t top, uint64_t ds
 
 // ---------------------------------------------------------------- classify
 
-// One wavefront per bitmap word (= one 64-chunk group of one buffer): chunk
-// i differs iff its K replay fingerprints are not all equal; the wave's
-// ballot is the word.
+// Bitmap word G (= one 64-chunk group of one buffer), computed by one
+// wavefront: chunk i differs iff its K replay fingerprints are not all equal;
+// the wave's ballot is the word.
 template <class Tab>
-__global__ __launch_bounds__(64) void k_classify(const Tab tab, const uint64_t *__restrict__ hashes, uint32_t K,
-                                                 uint64_t total, uint64_t *__restrict__ bitmap)
+__device__ __forceinline__ uint64_t classify_word(const Tab &tab, uint64_t G, uint32_t lane,
+                                                  const uint64_t *hashes, uint32_t K, uint64_t total)
 {
-    const uint64_t G = blockIdx.x;
     const JobBuf &jb = tab.bufs[buf_index(tab, G)];
-    const uint32_t lane = threadIdx.x;
     const uint64_t i = (G - jb.group_begin) * kGroupChunks + lane;
     bool differs = false;
     if (i < jb.nchunks) {
@@ -918,8 +916,16 @@ __global__ __launch_bounds__(64) void k_classify(const Tab tab, const uint64_t *
         const uint64_t h0 = hashes[idx];
         for (uint32_t k = 1; k < K; ++k) differs |= hashes[(uint64_t)k * total + idx] != h0;
     }
-    const uint64_t word = __ballot(differs);
-    if (lane == 0) bitmap[G] = word;
+    return __ballot(differs);
+}
+
+// One wavefront per bitmap word.
+template <class Tab>
+__global__ __launch_bounds__(64) void k_classify(const Tab tab, const uint64_t *__restrict__ hashes, uint32_t K,
+                                                 uint64_t total, uint64_t *__restrict__ bitmap)
+{
+    const uint64_t word = classify_word(tab, blockIdx.x, threadIdx.x, hashes, K, total);
+    if (threadIdx.x == 0) bitmap[blockIdx.x] = word;
 }
 
 // Per buffer: 1 iff any of its bitmap words is non-zero (one wavefront per
@@ -935,6 +941,35 @@ __global__ __launch_bounds__(64) void k_labels(const Tab tab, const uint64_t *__
     for (uint64_t w = threadIdx.x; w < nw; w += 64) any |= bitmap[jb.group_begin + w];
     const bool set = __ballot(any != 0) != 0;
     if (threadIdx.x == 0) labels[b] = set ? 1 : 0;
+}
+
+// Small jobs (tables in the kernel arguments, at most kClassifyFusedGroups
+// groups): the bitmap and the labels in one workgroup and one launch.
+// Wavefront w computes words w, w + 16, ... (also kept in LDS); after a
+// barrier, one wavefront per buffer ORs its words into the buffer's label.
+__global__ __launch_bounds__(1024) void k_classify_small(const ArgTables tab, uint64_t ngroups,
+                                                         const uint64_t *__restrict__ hashes, uint32_t K,
+                                                         uint64_t total, uint64_t *__restrict__ bitmap,
+                                                         uint8_t *__restrict__ labels)
+{
+    __shared__ uint64_t words[kClassifyFusedGroups];
+    const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    for (uint64_t G = wave; G < ngroups; G += 16) {
+        const uint64_t word = classify_word(tab, G, lane, hashes, K, total);
+        if (lane == 0) {
+            bitmap[G] = word;
+            words[G] = word;
+        }
+    }
+    __syncthreads();
+    for (uint32_t b = wave; b < tab.nbuf; b += 16) {
+        const JobBuf &jb = tab.bufs[b];
+        const uint64_t nw = (jb.nchunks + kGroupChunks - 1) / kGroupChunks;
+        uint64_t any = 0;
+        for (uint64_t w = lane; w < nw; w += 64) any |= words[jb.group_begin + w];
+        const bool set = __ballot(any != 0) != 0;
+        if (lane == 0) labels[b] = set ? 1 : 0;
+    }
 }
 
 // Workgroup sizes (lanes) and slice bytes of the tile kernels, from
@@ -1155,6 +1190,15 @@ hipError_t launch_labels(const Tab &tab, const uint64_t *bitmap, uint8_t *labels
 {
     if (tab.nbuf == 0) return hipSuccess;
     hipLaunchKernelGGL((k_labels<Tab>), dim3(tab.nbuf), dim3(64), 0, s, tab, bitmap, labels);
+    return hipGetLastError();
+}
+
+hipError_t launch_classify_small(const ArgTables &tab, uint64_t ngroups, const uint64_t *hashes, uint32_t K,
+                                 uint64_t total, uint64_t *bitmap, uint8_t *labels, hipStream_t s)
+{
+    if (ngroups > kClassifyFusedGroups) return hipErrorInvalidValue;
+    if (tab.nbuf == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_classify_small, dim3(1), dim3(1024), 0, s, tab, ngroups, hashes, K, total, bitmap, labels);
     return hipGetLastError();
 }
 

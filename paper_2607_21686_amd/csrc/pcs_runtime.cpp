@@ -797,6 +797,10 @@ int pcs_classify(pcs_ctx *c, const uint64_t *d_hashes, uint32_t K, const uint64_
     uint64_t xd, scr;
     if (int st = stage(c, job, is_small(job), t, {}, 0, sg, xd, scr)) return st;
     const uint64_t G = job.ngroups, T = job.nchunks;
+    if (sg.small && G <= kClassifyFusedGroups)
+        return launch(c, "classify", [&] {
+            return launch_classify_small(sg.arg, G, d_hashes, K, T, d_bitmap, d_labels, c->stream);
+        });
     return with_tables(sg, [&](const auto &tab) {
         if (int st = launch(c, "classify", [&] {
                 return launch_classify(tab, G, d_hashes, K, T, d_bitmap, c->stream);

@@ -215,6 +215,39 @@ def test_classify_matches_oracle(ctx, pcs):
         assert np.array_equal(host(lab)[:len(sizes)], olab)
 
 
+@pytest.mark.parametrize("cpb", [
+    [64 * 1000 + 7, 0, 130],          # 1006 groups: one workgroup, many words per wavefront
+    [64 * 1024],                      # exactly 1024 groups
+    [64 * 1024 + 1, 3],               # 1026 groups: the two-launch path with tables in the arguments
+    [5, 0, 70] * 6,                   # 18 buffers: tables in device memory
+])
+def test_classify_group_count_paths(ctx, pcs, cpb):
+    """Classification straight from fingerprint arrays (the oracle's
+    definition needs only the K x total array): random fingerprints, replays
+    equal to the first except at planted chunks, some of them in every
+    buffer but one."""
+    rng = np.random.default_rng(sum(cpb) % 1000)
+    K = 3
+    total = sum(cpb)
+    base = rng.integers(0, 1 << 63, size=total, dtype=np.int64).astype(np.uint64)
+    oh = np.stack([base.copy() for _ in range(K)])
+    starts = np.cumsum([0] + cpb[:-1])
+    for b, (s0, n) in enumerate(zip(starts, cpb)):
+        if n == 0 or b == 1:
+            continue
+        for _ in range(int(rng.integers(1, 8))):
+            oh[int(rng.integers(1, K)), s0 + int(rng.integers(0, n))] ^= np.uint64(1 << int(rng.integers(0, 64)))
+    obm, olab = oracle.classify(oh, cpb)
+    log("classify paths", len(cpb), "buffers,", oracle.bitmap_words(cpb), "words")
+    gh = torch.from_numpy(oh.reshape(-1).view(np.int64).copy()).cuda()
+    nw = oracle.bitmap_words(cpb)
+    bm = torch.full((max(nw, 1),), -1, dtype=torch.int64, device="cuda")
+    lab = torch.full((len(cpb),), 7, dtype=torch.uint8, device="cuda")
+    ctx.classify(gh, K, cpb, bm, lab)
+    assert np.array_equal(u64(bm)[:nw], obm)
+    assert np.array_equal(host(lab), olab)
+
+
 def test_checkpoint_restore_flat(ctx, pcs):
     rng = np.random.default_rng(13)
     sizes = [0, 16, 100, 4096, 4097, 70 * 4096 + 9, 3]
