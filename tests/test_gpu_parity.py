@@ -381,6 +381,49 @@ def test_incremental_chain_small(ctx, pcs):
     assert all(np.array_equal(host(o), w) for o, w in zip(outs, want))
 
 
+@pytest.mark.parametrize("groups", [64, 65, 128, 129])
+def test_incremental_group_boundaries(ctx, pcs, groups):
+    """Incremental checkpoints on both sides of the job sizes where the
+    small path changes shape: the Merkle lists, scan and slot assignment in
+    one launch up to 64 groups (slot assignment separate above), 8-chunk
+    sub-tiles up to 128 groups.  Two buffers, the second one partial; a
+    chain of two incremental checkpoints; stored bytes, fingerprints and
+    restores against the oracle."""
+    rng = np.random.default_rng(300 + groups)
+    sizes = [(groups - 1) * 64 * 4096, 33 * 4096 + 100]
+    cur = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    d = [dev(b) for b in cur]
+    st = oracle.Store()
+    log("incremental boundaries", groups, "groups")
+    s = ctx.checkpoint([pcs.flat(t) for t in d], hash=True)
+    o = st.checkpoint(cur)
+    chain = [(s, o, [b.copy() for b in cur])]
+    for step in range(2):
+        for b in cur:  # rewrite a few chunks of each buffer, the partial last one included
+            for c in list(rng.integers(0, oracle.chunk_count(b.size), size=5)) + [oracle.chunk_count(b.size) - 1]:
+                a = int(c) * 4096
+                b[a:min(b.size, a + 4096)] = rng.integers(0, 256, size=min(4096, b.size - a), dtype=np.uint8)
+        for t, b in zip(d, cur):
+            t.copy_(torch.from_numpy(b))
+        total = sum(oracle.chunk_count(n) for n in sizes)
+        ch, rt, sr = zeros_u64(total), zeros_u64(2), zeros_u64(1)
+        s = ctx.checkpoint([pcs.flat(t) for t in d], parent=chain[-1][0], chunk_hashes=ch, roots=rt, session_root=sr)
+        o = st.checkpoint(cur, chain[-1][1])
+        want_h, want_r, want_s = oracle.fingerprint(cur)
+        assert np.array_equal(u64(ch)[:total], want_h)
+        assert np.array_equal(u64(rt)[:2], want_r) and int(u64(sr)[0]) == int(want_s)
+        inf = ctx.info(s)
+        pay = torch.empty(max(1, inf["stored_bytes"]), dtype=torch.uint8, device="cuda")
+        ctx.payload(s, pay)
+        assert inf["stored_bytes"] == st.payload(o).size
+        assert np.array_equal(host(pay)[:inf["stored_bytes"]], st.payload(o))
+        chain.append((s, o, [b.copy() for b in cur]))
+    for s, _, want in chain:
+        outs = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in sizes]
+        ctx.restore(s, [pcs.flat(t) for t in outs])
+        assert all(np.array_equal(host(t), w) for t, w in zip(outs, want))
+
+
 def test_incremental_changes_and_shrink(ctx, pcs):
     rng = np.random.default_rng(16)
     base = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in (20 * 4096 + 7, 3 * 4096, 100, 2 * 4096 + 9, 70 * 4096)]
