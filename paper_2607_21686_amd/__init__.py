@@ -32,6 +32,7 @@ _L = lib()  # fails loudly if the HIP library is missing
 
 
 def chunk_count(nbytes: int) -> int:
+    """Number of 4096-byte chunks of a buffer of nbytes logical bytes."""
     return (nbytes + CHUNK_BYTES - 1) // CHUNK_BYTES
 
 
@@ -118,6 +119,8 @@ def u64_array(values):
 
 
 def chunk_counts(bufs):
+    """(chunks of each descriptor, total) as pcs_chunk_counts computes them;
+    validates the descriptors on the host."""
     arr = _array(bufs)
     out = (ctypes.c_uint64 * max(1, len(bufs)))()
     total = ctypes.c_uint64()
@@ -154,6 +157,7 @@ class Context:
             raise PcsError(st, _L.pcs_last_error(self._h).decode())
 
     def close(self):
+        """Waits for the context's stream and frees every handle (pcs_ctx_destroy)."""
         if getattr(self, "_h", None):
             _L.pcs_ctx_destroy(self._h)
             self._h = None
@@ -172,10 +176,17 @@ class Context:
 
     # -- fingerprint / classify ------------------------------------------
     def fingerprint(self, bufs, chunk_hashes=None, roots=None, session_root=None):
+        """Chunked XXH64 + Merkle roots of `bufs` (pcs_fingerprint) into int64
+        device tensors: chunk_hashes (buffer-major, one per 4096-byte chunk),
+        roots (one per buffer), session_root (one value); each optional."""
         self._check(_L.pcs_fingerprint(self._h, _array(bufs), len(bufs), _dev_ptr(chunk_hashes),
                                          _dev_ptr(roots), _dev_ptr(session_root)))
 
     def classify(self, hashes, K: int, chunks_per_buf, bitmap, labels):
+        """Cross-replay classification (pcs_classify): hashes holds K x total
+        fingerprints (replay-major); bitmap gets one 64-bit word per 64-chunk
+        group (bit set: the K fingerprints differ), labels one byte per
+        buffer (1 = must snapshot, 0 = recomputable)."""
         n = len(chunks_per_buf)
         cpb = chunks_per_buf if isinstance(chunks_per_buf, ctypes.Array) else u64_array(chunks_per_buf)
         self._check(_L.pcs_classify(self._h, _dev_ptr(hashes), K, cpb, n, _dev_ptr(bitmap), _dev_ptr(labels)))
@@ -244,6 +255,10 @@ class Context:
     # -- contract ----------------------------------------------------------
     def checkpoint(self, plan, parent: int = 0, hash: bool = False, chunk_hashes=None, roots=None,
                    session_root=None) -> int:
+        """checkpoint(s) -> c (pcs_checkpoint): an immutable snapshot of the
+        plan's logical bytes, full (parent 0; fingerprinted while copied when
+        `hash`) or incremental against `parent` (only new or changed chunks
+        stored).  Returns the handle."""
         out = ctypes.c_uint64()
         self._check(_L.pcs_checkpoint(self._h, _array(plan), len(plan), parent, CKPT_HASH if hash else 0,
                                         _dev_ptr(chunk_hashes), _dev_ptr(roots), _dev_ptr(session_root),
@@ -266,6 +281,8 @@ class Context:
         return [int(out[i]) for i in range(len(counts))]
 
     def restore(self, snap: int, dsts):
+        """restore(c) -> s' (pcs_restore): writes the snapshot's logical bytes
+        into the destination descriptors (a ring may use a new head)."""
         self._check(_L.pcs_restore(self._h, snap, _array(dsts), len(dsts)))
 
     def restore_batch(self, snaps, dsts_per_snap, nbufs=None):
@@ -280,6 +297,9 @@ class Context:
         self._check(_L.pcs_restore_batch(self._h, s, len(snaps), arr, nb))
 
     def restore_verify(self, snap: int, dsts, bad_bitmap, bad_labels=None):
+        """Restore fused with verification (pcs_restore_verify): bad_bitmap
+        gets a bit per chunk whose restored bytes do not match the stored
+        fingerprint, bad_labels (optional) a byte per buffer."""
         self._check(_L.pcs_restore_verify(self._h, snap, _array(dsts), len(dsts), _dev_ptr(bad_bitmap),
                                           _dev_ptr(bad_labels)))
 
@@ -348,34 +368,46 @@ class Context:
                                        _dev_ptr(kept) if kept is not None else None))
 
     def fork(self, snap: int) -> int:
+        """fork(c) -> c' (pcs_fork): a second handle on the same immutable snapshot."""
         out = ctypes.c_uint64()
         self._check(_L.pcs_fork(self._h, snap, ctypes.byref(out)))
         return int(out.value)
 
     def delete(self, snap: int):
+        """delete(c) (pcs_delete): drops one handle; the bytes go when no handle
+        or incremental child refers to them."""
         self._check(_L.pcs_delete(self._h, snap))
 
     def info(self, snap: int) -> dict:
+        """Sizes and kind of a snapshot (pcs_snapshot_info)."""
         inf = PcsSnapInfo()
         self._check(_L.pcs_snapshot_info(self._h, snap, ctypes.byref(inf)))
         return {f: int(getattr(inf, f)) for f, _ in PcsSnapInfo._fields_ if f != "reserved"}
 
     def payload(self, snap: int, out: torch.Tensor):
+        """Copies the bytes the snapshot stores into the device tensor `out`
+        (pcs_snapshot_payload)."""
         self._check(_L.pcs_snapshot_payload(self._h, snap, _dev_ptr(out), out.numel() * out.element_size()))
 
     def stored_hashes(self, snap: int, out: torch.Tensor):
+        """Copies the snapshot's stored chunk fingerprints into the int64
+        device tensor `out` (pcs_snapshot_hashes)."""
         self._check(_L.pcs_snapshot_hashes(self._h, snap, _dev_ptr(out), out.numel()))
 
     def arena_stats(self) -> dict:
+        """Arena accounting: bytes used and free, largest free block, live handles."""
         v = [ctypes.c_uint64() for _ in range(4)]
         self._check(_L.pcs_arena_stats(self._h, *[ctypes.byref(x) for x in v]))
         return dict(zip(["used", "free", "largest_free", "live_handles"], [int(x.value) for x in v]))
 
     # -- kernel timing -----------------------------------------------------
     def set_timing(self, enable: bool):
+        """Brackets every kernel launch with HIP events while enabled (pcs_set_timing)."""
         self._check(_L.pcs_set_timing(self._h, 1 if enable else 0))
 
     def kernel_time(self, name: str):
+        """(launches, total ms) of the kernel family `name` since the last call
+        for it (pcs_kernel_time); waits for the stream."""
         n = ctypes.c_uint64()
         ms = ctypes.c_double()
         self._check(_L.pcs_kernel_time(self._h, name.encode(), ctypes.byref(n), ctypes.byref(ms)))
