@@ -479,6 +479,29 @@ def _timed(args, ctx, step, kernels):
     return elapsed / args.steps, {k: ctx.kernel_time(k) for k in kernels}
 
 
+def _oracle_leg(args, work, state_bytes, sample, gpu_value, reps=1):
+    """The oracle, as it stands, pinned to one host core, on one bounded
+    sample of a workload (`work`, on host copies of its inputs made before
+    timing): rate = state_bytes per call of `work` / time, in the unit of
+    the workload's own value (GB/s)."""
+    import oracle
+    oracle.build()
+    prev = os.sched_getaffinity(0)
+    core = min(prev)
+    os.sched_setaffinity(0, {core})
+    try:
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            work()
+        elapsed = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, prev)
+    v = reps * state_bytes / elapsed / 1e9
+    return {"value": round(v, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "%s; %.2f s of oracle compute on core %d" % (sample, elapsed, core),
+            "gpu_over_cpu": round(gpu_value / v, 1)}
+
+
 def run_kv_ring(args):
     """Windowed KV context: checkpoint + fingerprint of the 512 MiB window of a
     1 GiB ring (wrapping head), fork, two restores at new heads, delete."""
@@ -504,10 +527,27 @@ def run_kv_ring(args):
     W_ = g.window_bytes
     n, ms = kt["pack_hash"]
     nc, mc = kt["copy"]
-    return _line(args, 3 * W_ / t / 1e9, t * 1e3, "windowed KV ring: 32 layers x 2 x 8192 slots x 8 x 128 bf16 "
-                 "(1 GiB), 4096-token window at a wrapping head; checkpoint+fingerprint, fork, 2 restores",
-                 {"window_bytes": W_}, "k_hash<copy>", 2 * W_, ms / n,
-                 {"restore_ms": round(mc / nc, 4), "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
+    out = _line(args, 3 * W_ / t / 1e9, t * 1e3, "windowed KV ring: 32 layers x 2 x 8192 slots x 8 x 128 bf16 "
+                "(1 GiB), 4096-token window at a wrapping head; checkpoint+fingerprint, fork, 2 restores",
+                {"window_bytes": W_}, "k_hash<copy>", 2 * W_, ms / n,
+                {"restore_ms": round(mc / nc, 4), "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
+    if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
+        ring_h = ring.cpu().numpy()
+        dst_h = [np.empty_like(ring_h), np.empty_like(ring_h)]
+        geo = (g.outer, g.outer_stride, g.capacity, g.row_bytes)
+
+        def work():
+            st = oracle.Store()
+            snap = st.checkpoint([oracle.ring_window(ring_h, *geo, g.head, g.window)])
+            fork = st.fork(snap)
+            for h, d, head in ((snap, dst_h[0], h2), (fork, dst_h[1], (h2 + 1234) % g.capacity)):
+                (w,) = st.restore(h)
+                oracle.ring_place(w, d, *geo, head, g.window)
+        out["cpu_baseline"] = _oracle_leg(args, work, 3 * W_, "3 whole steps: checkpoint + fingerprint of the "
+                                          "512 MiB window, fork, 2 restores at new heads", out["value"], reps=3)
+    return out
 
 
 def run_verify(args):
@@ -540,12 +580,33 @@ def run_verify(args):
     nc, mc = kt["copy"]
     v_ms = mv / nv
     ctx.delete(snap)
-    return _line(args, 2 * W_ / t / 1e9, t * 1e3, "verify on restore, windowed KV ring: 32 layers x 2 x 8192 slots x 8 "
-                 "x 128 bf16 (1 GiB), 4096-token window; per step one restore with verification and one without",
-                 {"window_bytes": W_}, "k_hash<verify>", 2 * W_, v_ms,
-                 {"verify_ms": round(v_ms, 4), "restore_ms": round(mc / nc, 4),
-                  "verify_GBps_hbm": round(2 * W_ / (v_ms * 1e-3) / 1e9, 1),
-                  "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
+    out = _line(args, 2 * W_ / t / 1e9, t * 1e3, "verify on restore, windowed KV ring: 32 layers x 2 x 8192 slots x 8 "
+                "x 128 bf16 (1 GiB), 4096-token window; per step one restore with verification and one without",
+                {"window_bytes": W_}, "k_hash<verify>", 2 * W_, v_ms,
+                {"verify_ms": round(v_ms, 4), "restore_ms": round(mc / nc, 4),
+                 "verify_GBps_hbm": round(2 * W_ / (v_ms * 1e-3) / 1e9, 1),
+                 "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
+    if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
+        ring_h = ring.cpu().numpy()
+        dst_h = [np.empty_like(ring_h), np.empty_like(ring_h)]
+        geo = (g.outer, g.outer_stride, g.capacity, g.row_bytes)
+        st = oracle.Store()
+        osnap = st.checkpoint([oracle.ring_window(ring_h, *geo, g.head, g.window)])
+        stored = st.snapshot(osnap).hashes[0]
+
+        def work():
+            (w,) = st.restore(osnap)
+            oracle.ring_place(w, dst_h[0], *geo, h2, g.window)
+            _, labels = oracle.classify(np.stack([stored, oracle.chunk_hashes(w)]), [stored.size])
+            assert not labels.any()
+            (w2,) = st.restore(osnap)
+            oracle.ring_place(w2, dst_h[1], *geo, (h2 + 1234) % g.capacity, g.window)
+        out["cpu_baseline"] = _oracle_leg(args, work, 2 * W_, "4 whole steps: a restore verified against the "
+                                          "stored fingerprints and a plain restore of the 512 MiB window",
+                                          out["value"], reps=4)
+    return out
 
 
 def run_sweep(args):
@@ -572,10 +633,21 @@ def run_sweep(args):
     t, kt = _timed(args, ctx, step, ["hash", "classify", "map", "merkle"])
     nbytes = K * sum(plan.sizes)
     n, ms = kt["hash"]
-    return _line(args, nbytes / t / 1e9, t * 1e3, "classification sweep: 64 buffers, log-uniform 4 KiB-256 MiB, "
-                 "5 dtypes, K=8 replays (16 designated buffers with rewritten chunks); fingerprint + classify",
-                 {"bytes_per_step": nbytes, "replays": K}, "k_hash (fingerprint)", nbytes, ms / n,
-                 {"classify_ms": round(kt["classify"][1] / args.steps, 4)})
+    out = _line(args, nbytes / t / 1e9, t * 1e3, "classification sweep: 64 buffers, log-uniform 4 KiB-256 MiB, "
+                "5 dtypes, K=8 replays (16 designated buffers with rewritten chunks); fingerprint + classify",
+                {"bytes_per_step": nbytes, "replays": K}, "k_hash (fingerprint)", nbytes, ms / n,
+                {"classify_ms": round(kt["classify"][1] / args.steps, 4)})
+    if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
+        host = [[x.cpu().numpy() for x in reps[k]] for k in range(2)]
+
+        def work():
+            hs = [oracle.fingerprint(host[k])[0] for k in range(2)]
+            oracle.classify(np.stack(hs), cpb)
+        out["cpu_baseline"] = _oracle_leg(args, work, 2 * sum(plan.sizes), "2 of the 8 replays fingerprinted "
+                                          "(all 64 buffers each), then classified (K = 2), 3 times", out["value"], reps=3)
+    return out
 
 
 def run_bank(args):
@@ -617,11 +689,27 @@ def run_bank(args):
     # then read + write the dirty chunks (391 or 392 per step).
     hashed = state - 8 * (bank.latent_entry_bytes + bank.pose_entry_bytes)
     dirty = sum(391 + (1 if (224 * j) // 4096 != (224 * (j - 1)) // 4096 else 0) for j in range(2, 65)) * 4096
-    return _line(args, 2 * state / t / 1e9, t * 1e3, "growing memory bank: bf16 latents [16,60,104] + fp32 pose [7] "
-                 "per entry, 0->512 entries in steps of 8; 64 incremental checkpoints + 64 restores (random order)",
-                 {"state_bytes_checkpointed_and_restored": 2 * state}, "incremental (hash+diff, scan, compact, copy)",
-                 hashed + 2 * dirty, ms / args.steps, {"incremental_ms_per_run": round(ms / args.steps, 4),
-                              "restore_ms_per_run": round(kt["copy"][1] / args.steps, 4)})
+    out = _line(args, 2 * state / t / 1e9, t * 1e3, "growing memory bank: bf16 latents [16,60,104] + fp32 pose [7] "
+                "per entry, 0->512 entries in steps of 8; 64 incremental checkpoints + 64 restores (random order)",
+                {"state_bytes_checkpointed_and_restored": 2 * state}, "incremental (hash+diff, scan, compact, copy)",
+                hashed + 2 * dirty, ms / args.steps, {"incremental_ms_per_run": round(ms / args.steps, 4),
+                                                      "restore_ms_per_run": round(kt["copy"][1] / args.steps, 4)})
+    if not args.no_cpu_baseline:
+        import oracle
+        lat_h = np.ascontiguousarray(bank.latents).view(np.uint8).reshape(-1)
+        pos_h = np.ascontiguousarray(bank.poses).view(np.uint8).reshape(-1)
+        le, pe = bank.latent_entry_bytes, bank.pose_entry_bytes
+
+        def work():
+            st, hs, parent = oracle.Store(), [], 0
+            for j in range(1, 65):
+                parent = st.checkpoint([lat_h[:8 * j * le], pos_h[:8 * j * pe]], parent)
+                hs.append(parent)
+            for j in order:
+                st.restore(hs[j])
+        out["cpu_baseline"] = _oracle_leg(args, work, 2 * state, "one whole run: 64 chained incremental "
+                                          "checkpoints, 64 restores in the same random order", out["value"])
+    return out
 
 
 def run_markovian(args):
@@ -688,7 +776,7 @@ def run_markovian(args):
     fp_bytes = 2 * sum(x.numel() for x in r1)
     state = r1[0].numel() + r1[1].numel()
     n, ms = kt["hash"]
-    return _line(args, (fp_bytes + 2 * state) / t / 1e9, t * 1e3, "Markovian: obs uint8 [256,256,3], RNG 16 B, "
+    out = _line(args, (fp_bytes + 2 * state) / t / 1e9, t * 1e3, "Markovian: obs uint8 [256,256,3], RNG 16 B, "
                  "6 fp16 decoys; fingerprint 2 replays, classify, checkpoint+restore {obs, RNG} (latency-bound)",
                  {"fingerprinted_bytes": fp_bytes, "state_bytes": state}, "k_hash (fingerprint)", fp_bytes, ms / n,
                  {"step_us": round(t * 1e6, 1), "checkpoint_us_median": round(ck_us, 1),
@@ -697,6 +785,22 @@ def run_markovian(args):
                   "launch_sync_floor_us_median": round(floor_us, 1),
                   "pack_kernel_us": round(1e3 * kt["pack"][1] / max(1, kt["pack"][0]), 2),
                   "restore_kernel_us": round(1e3 * kt["copy"][1] / max(1, kt["copy"][0]), 2)})
+    if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
+        h1, h2 = [x.cpu().numpy() for x in r1], [x.cpu().numpy() for x in r2]
+
+        def work():
+            fp = [oracle.fingerprint(h)[0] for h in (h1, h2)]
+            oracle.classify(np.stack(fp), cpb)
+            st = oracle.Store()
+            snap = st.checkpoint([h1[0], h1[1]])
+            st.restore(snap)
+            st.delete(snap)
+        out["cpu_baseline"] = _oracle_leg(args, work, fp_bytes + 2 * state, "1000 whole steps: fingerprint of both "
+                                          "replays, classify, checkpoint + restore of {obs, RNG}", out["value"],
+                                          reps=1000)
+    return out
 
 
 def run_shrink(args):
@@ -728,13 +832,30 @@ def run_shrink(args):
     kept = keep * (le + pe)
     # In place: the kept entries are read and written twice (through scratch); scores read once.
     alg = 4 * kept + 4 * E
-    return _line(args, E * (le + pe) / t / 1e9, t * 1e3, "relevance-keyed shrink of the memory bank: 512 entries of "
-                 "bf16 latents [16,60,104] + fp32 pose [7], keep 12%% (%d) by pose distance to the anchor, in place; "
-                 "then an incremental checkpoint of the shrunk bank" % keep,
-                 {"entries": E, "kept": keep, "bank_bytes": E * (le + pe)}, "shrink (rank, scan, place, gather)", alg,
-                 ms / args.steps, {"shrink_ms": round(ms / args.steps, 4),
-                                   "incremental_checkpoint_ms": round(kt["incremental"][1] / args.steps, 4),
-                                   "restore_full_bank_ms": round(kt["copy"][1] / args.steps, 4)})
+    out = _line(args, E * (le + pe) / t / 1e9, t * 1e3, "relevance-keyed shrink of the memory bank: 512 entries of "
+                "bf16 latents [16,60,104] + fp32 pose [7], keep 12%% (%d) by pose distance to the anchor, in place; "
+                "then an incremental checkpoint of the shrunk bank" % keep,
+                {"entries": E, "kept": keep, "bank_bytes": E * (le + pe)}, "shrink (rank, scan, place, gather)", alg,
+                ms / args.steps, {"shrink_ms": round(ms / args.steps, 4),
+                                  "incremental_checkpoint_ms": round(kt["incremental"][1] / args.steps, 4),
+                                  "restore_full_bank_ms": round(kt["copy"][1] / args.steps, 4)})
+    if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
+        lat_h = np.ascontiguousarray(bank.latents).view(np.uint8).reshape(-1)
+        pos_h = np.ascontiguousarray(bank.poses).view(np.uint8).reshape(-1)
+        scores_h = W.pose_scores(bank, E, 0)
+        st = oracle.Store()
+        ofull = st.checkpoint([lat_h, pos_h])
+
+        def work():
+            lat_r, pos_r = st.restore(ofull)
+            _, (kl, kp) = oracle.bank_shrink([(lat_r, le), (pos_r, pe)], scores_h, keep)
+            st.delete(st.checkpoint([kl, kp], ofull))
+        out["cpu_baseline"] = _oracle_leg(args, work, E * (le + pe), "30 whole steps: restore of the full bank, "
+                                          "shrink to %d entries, incremental checkpoint" % keep, out["value"],
+                                          reps=30)
+    return out
 
 
 def run_discover(args):
@@ -839,14 +960,28 @@ def run_export(args):
     total = S * size
     state = g.window_bytes + plan.obs_bytes + plan.rng_bytes
     gbs = lambda t: round(total / t / 1e9, 2)
-    return _line(args, total / (t_exp_p + t_imp_p) / 1e9, (t_exp_p + t_imp_p) * 1e3,
-                 "durable images: export + import (with device re-verification) of %d sessions of %d B of state "
-                 "(KV window 4x2x2048x8x128 bf16 ring, obs 480x832x3 u8, RNG 16 B), pinned host memory" % (S, state),
-                 {"sessions": S, "image_bytes_per_session": size},
-                 "k_hash (import re-fingerprint, one session per launch)", state, ms / max(1, n),
-                 {"export_pinned_GBps": gbs(t_exp_p), "import_pinned_GBps": gbs(t_imp_p),
-                  "export_pageable_GBps": gbs(t_exp_g), "import_pageable_GBps": gbs(t_imp_g),
-                  "note": "host-link bound (PCIe); value counts image bytes moved per second"})
+    out = _line(args, total / (t_exp_p + t_imp_p) / 1e9, (t_exp_p + t_imp_p) * 1e3,
+                "durable images: export + import (with device re-verification) of %d sessions of %d B of state "
+                "(KV window 4x2x2048x8x128 bf16 ring, obs 480x832x3 u8, RNG 16 B), pinned host memory" % (S, state),
+                {"sessions": S, "image_bytes_per_session": size},
+                "k_hash (import re-fingerprint, one session per launch)", state, ms / max(1, n),
+                {"export_pinned_GBps": gbs(t_exp_p), "import_pinned_GBps": gbs(t_imp_p),
+                 "export_pageable_GBps": gbs(t_exp_g), "import_pageable_GBps": gbs(t_imp_g),
+                 "note": "host-link bound (PCIe); value counts image bytes moved per second"})
+    if not args.no_cpu_baseline:
+        import oracle
+        geo = (g.outer, g.outer_stride, g.capacity, g.row_bytes)
+        host = [(oracle.ring_window(rings[s].cpu().numpy(), *geo, plan.heads[s], g.window), obs[s].cpu().numpy(),
+                 rngs[s].cpu().numpy()) for s in range(2)]
+        lay = [(1, g.row_bytes, g.window, g.outer), (0, 0, 0, 0), (0, 0, 0, 0)]
+
+        def work():
+            for bufs in host:
+                assert len(oracle.export_image(bufs, lay)) == size
+        out["cpu_baseline"] = _oracle_leg(args, work, 2 * size, "images of 2 sessions written, 20 times "
+                                          "(export only: the oracle writes images and has no import)", out["value"],
+                                          reps=20)
+    return out
 
 
 OTHER = {"kv-ring": run_kv_ring, "verify": run_verify, "sweep": run_sweep, "bank": run_bank, "markovian": run_markovian,
