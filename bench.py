@@ -899,7 +899,7 @@ def run_discover(args):
     # Each probe's subset is checkpointed once (read + write) and restored once;
     # `moved` counted 2 x the subset per probe.
     per_launch = int(moved[0] / (args.steps + args.warmup) / max(1, result.get("probes", 1)))
-    return _line(args, moved[0] / (args.steps + args.warmup) / t / 1e9, t * 1e3,
+    out = _line(args, moved[0] / (args.steps + args.warmup) / t / 1e9, t * 1e3,
                  "discovering PCS by measurement on a mock world model: 8 components (obs 480x832x3 u8, RNG, "
                  "64-entry bank, pose, feature cache, scratch, an interchangeable context pair), 8-step away + "
                  "8-step return probe, eps 0, RNG control", {"components": 8, "state_bytes": state},
@@ -908,6 +908,21 @@ def run_discover(args):
                   "library_kernel_ms_per_discovery": round(lib_ms, 3),
                   "model_and_host_ms_per_discovery": round(t * 1e3 - lib_ms, 3),
                   "control_ok": result.get("control_ok")})
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import discover as OD
+        from oracle.mock_world import MockWorld
+        anchor = [x.cpu().numpy() for x in live.parts]
+        ref_o = oracle.fingerprint([MockWorld(spec, anchor).run(pa)])[0]
+        got = {}
+
+        def work():
+            got.update(OD.discover(OD.mock_probe(spec, anchor, pa, ref_o), 8, 0.0, control=1))
+        leg = _oracle_leg(args, work, moved[0] / (args.steps + args.warmup),
+                          "one whole discovery on the oracle's own mock model", out["value"])
+        leg["same_decisions"] = list(got.get("pcs", [])) == list(result.get("pcs", []))
+        out["cpu_baseline"] = leg
+    return out
 
 
 def run_export(args):
