@@ -450,17 +450,24 @@ def _line(args, metric_value, ms_per_step, workload, cfg, roof_kernel, alg_bytes
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None, "kernel": roof_kernel,
                      "avg_ms": round(avg_ms, 4), "algorithmic_bytes": alg_bytes},
     }
+    if _STEP_DIST is not None:
+        out["step_ms_device"] = _STEP_DIST
     if extra:
         out["breakdown"] = extra
     return out
 
 
+_STEP_DIST = None  # p10/p50/p90 of the device step times of the last _timed run
+
+
 def _timed(args, ctx, step, kernels):
     """Wall time per step from a pass without the library's per-launch timing
     events (which cost a few microseconds of host time per launch, enough to
-    slow workloads of many small launches), then kernel times from a second
-    pass of the same steps with them."""
+    slow workloads of many small launches), then the distribution of device
+    step times (p10/p50/p90) from a second pass, then kernel times from a
+    third pass of the same steps with the timing events on."""
     import torch
+    global _STEP_DIST
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -469,6 +476,16 @@ def _timed(args, ctx, step, kernels):
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    # Device time of each step: events recorded between steps on the
+    # context's stream, no synchronisation inside the pass.
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(ctx.stream)
+    for k in range(args.steps):
+        step()
+        evs[k + 1].record(ctx.stream)
+    torch.cuda.synchronize()
+    ms = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
+    _STEP_DIST = {"p10": round(_pct(ms, 10), 4), "p50": round(_pct(ms, 50), 4), "p90": round(_pct(ms, 90), 4)}
     for k in kernels:
         ctx.kernel_time(k)
     ctx.set_timing(True)
