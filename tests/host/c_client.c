@@ -6,9 +6,17 @@
  * snapshot, overwrites the session, restores the fork into it (the ring at
  * a new head) and exports the snapshot to a host image.
  *
+ * Then it rewrites chunk 1 of the flat buffer, takes an incremental
+ * checkpoint against the first snapshot, classifies the two fingerprint
+ * passes (K = 2), imports the exported image and restores from it, and
+ * restores the incremental snapshot.
+ *
  * Prints, one per line: "hash <i> <hex>" for every chunk fingerprint,
  * "root <b> <hex>", "session <hex>", "restored <0|1>" (1 when every logical
- * byte came back) and "image <bytes>"; exits 0 when every call succeeded.
+ * byte came back), "image <bytes>", "dirty <chunks stored by the
+ * incremental snapshot>", "bitmap <word> <hex>", "label <b> <0|1>",
+ * "imported_restored <0|1>" and "incremental_restored <0|1>"; exits 0 when
+ * every call succeeded.
  * tests/test_gpu_c_client.py builds it, runs it and checks the fingerprints
  * against the oracle.
  */
@@ -129,6 +137,67 @@ int main(void)
     void *image = malloc(image_bytes);
     if (!image) return 1;
     PCS_OK_(ctx, pcs_export(ctx, snap, image, image_bytes, &image_bytes));
+
+    /* Incremental checkpoint after rewriting chunk 1 of the flat buffer;
+     * classification of the two fingerprint passes (K = 2); import of the
+     * exported image and a restore from it; a restore of the incremental
+     * snapshot. */
+    uint8_t *h_flat2 = malloc(FLAT_BYTES), *h_chk = malloc(RING_BYTES);
+    void *d_k2 = NULL, *d_bitmap = NULL, *d_labels = NULL, *d_flat3 = NULL, *d_ring3 = NULL;
+    if (!h_flat2 || !h_chk) return 1;
+    memcpy(h_flat2, h_flat, FLAT_BYTES);
+    for (uint64_t i = 4096; i < 8192; ++i) h_flat2[i] ^= 0x5A;
+    HIP_OK(hipMemcpy(d_flat, h_flat2, FLAT_BYTES, hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(d_ring, h_ring, RING_BYTES, hipMemcpyHostToDevice));
+    HIP_OK(hipMalloc(&d_k2, 16 * total));
+    HIP_OK(hipMemcpy(d_k2, d_hashes, 8 * total, hipMemcpyDeviceToDevice));
+    pcs_snap inc = 0, imp = 0;
+    PCS_OK_(ctx, pcs_checkpoint(ctx, plan, 2, snap, 0, (uint64_t *)d_k2 + total, NULL, NULL, &inc));
+    pcs_snap_info inf;
+    PCS_OK_(ctx, pcs_snapshot_info(ctx, inc, &inf));
+    const uint64_t words = (chunks[0] + 63) / 64 + (chunks[1] + 63) / 64;
+    HIP_OK(hipMalloc(&d_bitmap, 8 * words));
+    HIP_OK(hipMalloc(&d_labels, 2));
+    PCS_OK_(ctx, pcs_classify(ctx, (const uint64_t *)d_k2, 2, chunks, 2, (uint64_t *)d_bitmap, (uint8_t *)d_labels));
+    PCS_OK_(ctx, pcs_import(ctx, image, image_bytes, &imp));
+    HIP_OK(hipMalloc(&d_flat3, FLAT_BYTES));
+    HIP_OK(hipMalloc(&d_ring3, RING_BYTES));
+    pcs_buf dst3[2] = {plan[0], ring_desc(d_ring3, NEW_HEAD)};
+    dst3[0].ptr = (uint64_t)(uintptr_t)d_flat3;
+    PCS_OK_(ctx, pcs_restore(ctx, imp, dst3, 2));
+    HIP_OK(hipDeviceSynchronize());
+    int imported_ok = 1;
+    HIP_OK(hipMemcpy(h_flat_back, d_flat3, FLAT_BYTES, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(h_chk, d_ring3, RING_BYTES, hipMemcpyDeviceToHost));
+    if (memcmp(h_flat_back, h_flat, FLAT_BYTES) != 0) imported_ok = 0;
+    for (uint32_t o = 0; o < OUTER; ++o)
+        for (uint32_t t = 0; t < WINDOW; ++t) {
+            const uint8_t *want = h_ring + o * CAPACITY * ROW + ((HEAD + t) % CAPACITY) * ROW;
+            const uint8_t *got = h_chk + o * CAPACITY * ROW + ((NEW_HEAD + t) % CAPACITY) * ROW;
+            if (memcmp(want, got, ROW) != 0) imported_ok = 0;
+        }
+    PCS_OK_(ctx, pcs_restore(ctx, inc, dst3, 2));
+    HIP_OK(hipDeviceSynchronize());
+    HIP_OK(hipMemcpy(h_flat_back, d_flat3, FLAT_BYTES, hipMemcpyDeviceToHost));
+    const int incremental_ok = memcmp(h_flat_back, h_flat2, FLAT_BYTES) == 0;
+    uint64_t h_bitmap[4] = {0, 0, 0, 0};
+    uint8_t h_labels[2] = {7, 7};
+    if (words > 4) return 1;
+    HIP_OK(hipMemcpy(h_bitmap, d_bitmap, 8 * words, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(h_labels, d_labels, 2, hipMemcpyDeviceToHost));
+    printf("dirty %llu\n", (unsigned long long)inf.dirty_chunks);
+    for (uint64_t w = 0; w < words; ++w) printf("bitmap %llu %016llx\n", (unsigned long long)w, (unsigned long long)h_bitmap[w]);
+    printf("label 0 %d\nlabel 1 %d\n", h_labels[0], h_labels[1]);
+    printf("imported_restored %d\nincremental_restored %d\n", imported_ok, incremental_ok);
+    PCS_OK_(ctx, pcs_delete(ctx, imp));
+    PCS_OK_(ctx, pcs_delete(ctx, inc));
+    (void)hipFree(d_k2);
+    (void)hipFree(d_bitmap);
+    (void)hipFree(d_labels);
+    (void)hipFree(d_flat3);
+    (void)hipFree(d_ring3);
+    free(h_flat2);
+    free(h_chk);
 
     uint64_t *h_hashes = malloc(8 * total), h_roots[2], h_sroot;
     if (!h_hashes) return 1;

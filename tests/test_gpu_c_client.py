@@ -1,9 +1,12 @@
 """The C ABI without Python: tests/host/c_client.c uses only include/pcs.h and
 the HIP runtime's allocation and copy calls (no torch) to fingerprint a
 session (a flat buffer of ragged size and a wrapped ring window), checkpoint
-it, fork it, restore the fork at a new ring head and export it.  Its printed
-fingerprints are compared with the oracle's, its restore check must pass,
-and its image size must equal the oracle image's."""
+it, fork it, restore the fork at a new ring head and export it; then it
+rewrites one chunk, takes an incremental checkpoint, classifies the two
+fingerprint passes, imports the exported image and restores from the
+import and from the incremental snapshot.  Its printed fingerprints, stored
+chunk count, bitmap and labels are compared with the oracle's, its restore
+checks must pass, and its image size must equal the oracle image's."""
 import os
 import subprocess
 
@@ -30,13 +33,17 @@ def test_c_client_matches_oracle():
     log("C client:", exe)
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr[-2000:]
-    hashes, roots, out = {}, {}, {}
+    hashes, roots, words, labels, out = {}, {}, {}, {}, {}
     for line in r.stdout.splitlines():
         f = line.split()
         if f[0] == "hash":
             hashes[int(f[1])] = int(f[2], 16)
         elif f[0] == "root":
             roots[int(f[1])] = int(f[2], 16)
+        elif f[0] == "bitmap":
+            words[int(f[1])] = int(f[2], 16)
+        elif f[0] == "label":
+            labels[int(f[1])] = int(f[2])
         else:
             out[f[0]] = f[1]
     flat = pattern(0, FLAT_BYTES)
@@ -49,3 +56,14 @@ def test_c_client_matches_oracle():
     assert out["restored"] == "1"
     image = oracle.export_image([flat, window], [(0, 0, 0, 0), (1, ROW, WINDOW, OUTER)])
     assert int(out["image"]) == len(image)
+    # Chunk 1 of the flat buffer rewritten, the ring unchanged.
+    flat2 = flat.copy()
+    flat2[4096:8192] ^= np.uint8(0x5A)
+    h2 = oracle.fingerprint([flat2, window])[0]
+    cpb = [oracle.chunk_count(flat.size), oracle.chunk_count(window.size)]
+    d, nd = oracle.dirty(h2, cpb, want_h, cpb)
+    assert int(out["dirty"]) == nd == 1
+    want_bm, want_lab = oracle.classify(np.stack([np.asarray(want_h, dtype=np.uint64), h2]), cpb)
+    assert [words[i] for i in range(len(words))] == [int(x) for x in want_bm]
+    assert [labels[0], labels[1]] == [int(x) for x in want_lab] == [1, 0]
+    assert out["imported_restored"] == "1" and out["incremental_restored"] == "1"
