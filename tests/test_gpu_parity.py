@@ -572,3 +572,32 @@ def test_incremental_chain_in_tight_arena(pcs):
         c.delete(h)
     assert c.arena_stats()["used"] == 0
     c.close()
+
+
+def test_kernel_timing_counts_and_resets(ctx, pcs):
+    """pcs_set_timing / pcs_kernel_time: while enabled, every launch of a
+    family is counted with a positive duration; a query resets the family;
+    launches made while disabled are not counted."""
+    rng = np.random.default_rng(40)
+    a = rng.integers(0, 256, size=300 * 4096 + 5, dtype=np.uint8)
+    d = dev(a)
+    out = torch.empty_like(d)
+    for fam in ("pack", "copy", "pack_hash", "merkle"):
+        ctx.kernel_time(fam)
+    s = ctx.checkpoint([pcs.flat(d)])            # not timed
+    ctx.set_timing(True)
+    for _ in range(3):
+        ctx.restore(s, [pcs.flat(out)])
+    s2 = ctx.checkpoint([pcs.flat(d)], hash=True)
+    ctx.set_timing(False)
+    ctx.restore(s, [pcs.flat(out)])              # not timed
+    n, ms = ctx.kernel_time("copy")
+    assert n == 3 and ms > 0
+    assert ctx.kernel_time("copy") == (0, 0.0)   # reset by the query
+    assert ctx.kernel_time("pack")[0] == 0       # the untimed plain checkpoint
+    n, ms = ctx.kernel_time("pack_hash")
+    assert n == 1 and ms > 0
+    assert ctx.kernel_time("merkle")[0] >= 1
+    assert np.array_equal(host(out), a)
+    ctx.delete(s)
+    ctx.delete(s2)
