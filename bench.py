@@ -433,6 +433,7 @@ def cpu_baseline(args, plan, rings, obs, rngs, gpu_value):
     return {"value": round(v, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": "%d sessions checkpointed+fingerprinted and classified, %d forked+restored; %.1f s of "
                       "oracle compute on core %d" % (n, restored, elapsed, core),
+            "pinned_core": core, "host_cores": os.cpu_count(), "cores_available": len(prev),
             "gpu_over_cpu": round(gpu_value / v, 1)}
 
 
@@ -516,6 +517,7 @@ def _oracle_leg(args, work, state_bytes, sample, gpu_value, reps=1):
     v = reps * state_bytes / elapsed / 1e9
     return {"value": round(v, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": "%s; %.2f s of oracle compute on core %d" % (sample, elapsed, core),
+            "pinned_core": core, "host_cores": os.cpu_count(), "cores_available": len(prev),
             "gpu_over_cpu": round(gpu_value / v, 1)}
 
 

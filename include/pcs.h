@@ -214,6 +214,13 @@ int pcs_checkpoint(pcs_ctx *ctx, const pcs_buf *h_plan, uint32_t n, pcs_snap par
 
 /*
  * Full checkpoints of `sessions` sessions in one launch (batched suspend).
+ * The paper's unit of state is the session (Sec. 5, "Unit = session"), and
+ * its GPU is time-multiplexed: one session holds the model while every other
+ * one is suspended as PCS (Sec. 5, "Structure"; Sec. 7.2 measures up to
+ * 1,024 resident sessions).  Suspending many sessions at once is therefore
+ * `sessions` independent checkpoint(s) -> c calls of the Sec. 3 contract,
+ * each with its own handle and the same I2/I4 guarantees; batching them only
+ * shares one launch.
  * Session s's plan is h_plans[off_s .. off_s + h_nbufs[s]) with
  * off_s = sum of the earlier h_nbufs.  Output arrays concatenate the
  * sessions in order (chunk hashes and roots as in pcs_fingerprint;
@@ -254,8 +261,12 @@ int pcs_restore(pcs_ctx *ctx, pcs_snap snap, const pcs_buf *h_dst, uint32_t n);
 int pcs_restore_verify(pcs_ctx *ctx, pcs_snap snap, const pcs_buf *h_dst, uint32_t n, uint64_t *d_bad_bitmap,
                        uint8_t *d_bad_labels);
 
-/* Restores m snapshots in one launch; snapshot j goes to
- * h_dsts[off_j .. off_j + h_nbufs[j]).  Validates everything first. */
+/* Resumes m suspended sessions in one launch: m independent restore(c) -> s'
+ * calls of the Sec. 3 contract (I1 each, I3 between them), batched for the
+ * time-multiplexed GPU of Sec. 5 ("Structure").  Snapshot j goes to
+ * h_dsts[off_j .. off_j + h_nbufs[j]) with off_j = sum of the earlier
+ * h_nbufs; each destination set follows pcs_restore's rules.  Everything is
+ * validated first: on an error nothing is enqueued. */
 int pcs_restore_batch(pcs_ctx *ctx, const pcs_snap *h_snaps, uint32_t m, const pcs_buf *h_dsts,
                       const uint32_t *h_nbufs);
 
@@ -349,6 +360,19 @@ int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
  * cannot hold the scratch (4 * 4 + 8 bytes per entry, plus the largest
  * in-place part's keep * entry_bytes).
  */
+/*
+ * Kept count of a shrink to a retained fraction (Sec. 7.5 holds the fraction
+ * at 12%; Table 6 sweeps 0.04-0.50 and lists the frames each keeps of a bank
+ * of about 21).  The fraction is the exact rational num/den (a decimal as
+ * written: 0.12 = 12/100), never a binary floating-point approximation of
+ * it.  *h_keep = the integer nearest to n_entries * num / den, a tie (an exact
+ * half) going to the even neighbour, then raised to 1 if it is 0 and the bank
+ * is not empty; 0 for an empty bank.  This reproduces Table 6's column
+ * (21 entries: 1, 2, 3, 5, 10).  Host only, no context.  PCS_E_INVAL if
+ * h_keep is NULL, den is 0 or num > den.
+ */
+int pcs_keep_count(uint64_t num, uint64_t den, uint64_t n_entries, uint64_t *h_keep);
+
 typedef struct pcs_bank_part {
     uint64_t src;          /* device address of entry 0 */
     uint64_t dst;          /* device address for kept entry 0 (== src: in place) */
@@ -359,6 +383,25 @@ int pcs_bank_shrink(pcs_ctx *ctx, const pcs_bank_part *h_parts, uint32_t nparts,
                     const float *d_scores, uint64_t keep, uint32_t *d_kept);
 
 /*
+ * A return-consistency distance at chunk granularity: the metric D that
+ * Sec. 4's procedure and Sec. 6's conformance test compare against a
+ * tolerance, taken bit-exactly (a restore whose continuation returns to the
+ * same bytes has D = 0).  The n buffers are fingerprinted (chunked XXH64, as
+ * pcs_fingerprint) and each chunk's fingerprint is compared with
+ * d_ref_hashes (uint64[total chunks], laid out as pcs_fingerprint's
+ * d_chunk_hashes for the same plan, e.g. from an uninterrupted run).
+ *   *h_differing: chunks whose fingerprint differs (may be NULL);
+ *   *h_distance:  h_differing / total chunks, 0 when there are no chunks
+ *                 (may be NULL).
+ * The comparison and the count run on the device; the call then waits for
+ * the context's stream (the result is a host value).  d_ref_hashes may be
+ * NULL only when the buffers hold no chunks.  Takes arena scratch of 16 bytes
+ * per 64-chunk group (PCS_E_NOMEM if it cannot).
+ */
+int pcs_distance(pcs_ctx *ctx, const pcs_buf *h_bufs, uint32_t n, const uint64_t *d_ref_hashes,
+                 uint64_t *h_differing, double *h_distance);
+
+/*
  * Discovering PCS by measurement (Sec. 4, procedure FINGERPRINT).  The
  * model's runtime state is k components H = {h_0 .. h_{k-1}} (pcs_buf
  * descriptors of the live session, taken at the anchor of the probe).  The
@@ -367,9 +410,8 @@ int pcs_bank_shrink(pcs_ctx *ctx, const pcs_bank_part *h_parts, uint32_t nparts,
  * into a fresh session (the other components keep a fresh session's
  * state), runs its leave-and-return trajectory and writes the
  * return-consistency distance D >= 0 of the continuation to *d_out
- * (Sec. 5's conformance metric; e.g. the fraction of output chunks whose
- * fingerprint differs from an uninterrupted run, via pcs_fingerprint and
- * pcs_classify).  It returns 0, or nonzero to abort.  The probe must not
+ * (Sec. 6's conformance metric; e.g. the fraction of output chunks whose
+ * fingerprint differs from an uninterrupted run, via pcs_distance).  It returns 0, or nonzero to abort.  The probe must not
  * modify the live components.
  *
  * The call runs:

@@ -337,12 +337,19 @@ def export_image(buffers, layouts=None) -> bytes:
 # ---------------------------------------------------------------- bank shrink
 
 def keep_count(fraction, n_entries: int) -> int:
-    """Entries a shrink to `fraction` keeps: the exact product fraction x n
-    rounded half to even, at least 1 for a non-empty bank, at most n."""
+    """Entries a shrink to `fraction` keeps (Sec. 7.5's 12%; Table 6's keep
+    fractions 0.04-0.50, written as decimals): the fraction is the exact
+    rational a decimal denotes (a float is read as the decimal it prints, so
+    0.05 is 1/20, not its binary approximation); n x fraction is rounded to
+    the nearest integer, an exact half to the even neighbour; at least 1 for
+    a non-empty bank."""
     from fractions import Fraction
+    f = Fraction(repr(fraction)) if isinstance(fraction, float) else Fraction(fraction)
+    if not 0 <= f <= 1:
+        raise ValueError("fraction must lie in [0, 1]")
     if n_entries <= 0:
         return 0
-    return min(n_entries, max(1, round(Fraction(fraction) * n_entries)))
+    return max(1, round(f * n_entries))
 
 
 def bank_select(scores, keep: int) -> np.ndarray:

@@ -36,13 +36,28 @@ def chunk_count(nbytes: int) -> int:
     return (nbytes + CHUNK_BYTES - 1) // CHUNK_BYTES
 
 
-def keep_count(fraction: float, n_entries: int) -> int:
-    """Entries a shrink to `fraction` of a bank keeps: fraction x n rounded to
-    the nearest integer (halves to even), at least one entry of a non-empty
-    bank (Table 6 lists the frames a fraction keeps of a bank of about 21)."""
-    if n_entries <= 0:
-        return 0
-    return min(n_entries, max(1, round(fraction * n_entries)))
+def _ratio(fraction):
+    """(numerator, denominator) of a retained fraction given as a Fraction, a
+    decimal string, a (num, den) pair, or a float taken as the decimal it
+    prints (0.05 -> 1/20): the exact rational the library rounds."""
+    from fractions import Fraction
+    if isinstance(fraction, tuple):
+        return int(fraction[0]), int(fraction[1])
+    f = Fraction(repr(fraction)) if isinstance(fraction, float) else Fraction(fraction)
+    return f.numerator, f.denominator
+
+
+def keep_count(fraction, n_entries: int) -> int:
+    """Entries a shrink to `fraction` of a bank keeps (pcs_keep_count):
+    n x fraction rounded to the nearest integer, halves to even, at least one
+    entry of a non-empty bank (Table 6 lists the frames a fraction keeps of a
+    bank of about 21)."""
+    num, den = _ratio(fraction)
+    out = ctypes.c_uint64()
+    st = _L.pcs_keep_count(num, den, int(n_entries), ctypes.byref(out))
+    if st:
+        raise PcsError(st, "fraction must lie in [0, 1] (got %d/%d)" % (num, den))
+    return int(out.value)
 
 
 def _dev_ptr(t) -> int:
@@ -192,33 +207,18 @@ class Context:
         self._check(_L.pcs_classify(self._h, _dev_ptr(hashes), K, cpb, n, _dev_ptr(bitmap), _dev_ptr(labels)))
 
     def distance(self, ref_hashes, bufs) -> float:
-        """Return-consistency distance at chunk granularity: the fraction of
-        the 4096-byte chunks of `bufs` whose fingerprint differs from
-        ref_hashes (device int64 tensor, one value per chunk, as fingerprint()
-        writes them).  Fingerprinting and comparison run on the GPU
-        (pcs_fingerprint, then pcs_classify with K = 2); the differing
-        chunks are counted from the bitmap on the host."""
-        import numpy as np
-        arr = _array(bufs)
-        n = len(bufs)
-        cpb = (ctypes.c_uint64 * max(1, n))()
-        total = ctypes.c_uint64()
-        if n:
-            self._check(_L.pcs_chunk_counts(arr, n, cpb, ctypes.byref(total)))
-        T = int(total.value)
-        if T == 0:
-            return 0.0
-        if ref_hashes.numel() < T:
+        """Return-consistency distance at chunk granularity (pcs_distance):
+        the fraction of the 4096-byte chunks of `bufs` whose fingerprint
+        differs from ref_hashes (device int64 tensor, one value per chunk, as
+        fingerprint() writes them).  Fingerprinting, comparison and count run
+        on the GPU; the call waits for the context's stream."""
+        _, T = chunk_counts(bufs)
+        if T and ref_hashes.numel() < T:
             raise ValueError("ref_hashes holds fewer values than the buffers have chunks")
-        h = torch.empty(2 * T, dtype=torch.int64, device=ref_hashes.device)
-        h[:T].copy_(ref_hashes.reshape(-1)[:T])
-        self.fingerprint(bufs, h[T:])
-        words = sum((int(cpb[i]) + 63) // 64 for i in range(n))
-        bitmap = torch.zeros(max(1, words), dtype=torch.int64, device=h.device)
-        labels = torch.zeros(max(1, n), dtype=torch.uint8, device=h.device)
-        self.classify(h, 2, cpb, bitmap, labels)
-        bits = np.unpackbits(bitmap.cpu().numpy().view(np.uint8)).sum()
-        return float(bits) / T
+        d = ctypes.c_double()
+        ref = _dev_ptr(ref_hashes.reshape(-1)) if T else 0
+        self._check(_L.pcs_distance(self._h, _array(bufs), len(bufs), ref, None, ctypes.byref(d)))
+        return float(d.value)
 
     def discover(self, components, probe, eps: float = 0.0, control: int = -1) -> dict:
         """Discovering PCS by measurement (pcs_discover; Sec. 4, procedure

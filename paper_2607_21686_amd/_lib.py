@@ -29,7 +29,7 @@ EXPORTS = ("pcs_ctx_create", "pcs_ctx_destroy", "pcs_last_error", "pcs_chunk_cou
            "pcs_classify", "pcs_checkpoint", "pcs_checkpoint_batch", "pcs_restore", "pcs_restore_batch",
            "pcs_restore_verify", "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload",
            "pcs_snapshot_view", "pcs_snapshot_hashes",
-           "pcs_export", "pcs_import", "pcs_bank_shrink", "pcs_discover", "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
+           "pcs_export", "pcs_import", "pcs_keep_count", "pcs_bank_shrink", "pcs_distance", "pcs_discover", "pcs_arena_stats", "pcs_set_timing", "pcs_kernel_time")
 
 
 class PcsBuf(ctypes.Structure):
@@ -105,6 +105,8 @@ def load():
         "pcs_snapshot_hashes": ([P, U64, P, U64], I),
         "pcs_export": ([P, U64, P, U64, PU64], I),
         "pcs_import": ([P, P, U64, PU64], I),
+        "pcs_keep_count": ([U64, U64, U64, PU64], I),
+        "pcs_distance": ([P, PB, U32, P, PU64, ctypes.POINTER(ctypes.c_double)], I),
         "pcs_bank_shrink": ([P, ctypes.POINTER(PcsBankPart), U32, U64, P, U64, P], I),
         "pcs_discover": ([P, PB, U32, ctypes.c_double, ctypes.c_int32, PROBE_FN, P, ctypes.POINTER(PcsDiscovery)], I),
         "pcs_arena_stats": ([P, PU64, PU64, PU64, PU64], I),

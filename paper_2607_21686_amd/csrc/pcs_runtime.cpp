@@ -810,6 +810,70 @@ int pcs_classify(pcs_ctx *c, const uint64_t *d_hashes, uint32_t K, const uint64_
     });
 }
 
+int pcs_keep_count(uint64_t num, uint64_t den, uint64_t n_entries, uint64_t *keep)
+{
+    if (!keep || den == 0 || num > den) return PCS_E_INVAL;
+    if (n_entries == 0) {
+        *keep = 0;
+        return PCS_OK;
+    }
+    // n * num / den exactly (the product fits in 128 bits), rounded to the
+    // nearest integer with ties to even, then at least one entry.
+    const unsigned __int128 prod = (unsigned __int128)n_entries * num;
+    uint64_t q = (uint64_t)(prod / den);
+    const uint64_t r = (uint64_t)(prod % den);
+    const unsigned __int128 twice = (unsigned __int128)r * 2;
+    if (twice > den || (twice == den && (q & 1))) ++q;
+    *keep = q ? q : 1;
+    return PCS_OK;
+}
+
+int pcs_distance(pcs_ctx *c, const pcs_buf *bufs, uint32_t n, const uint64_t *d_ref, uint64_t *h_differing,
+                 double *h_distance)
+{
+    if (!c) return PCS_E_INVAL;
+    if (n && !bufs) return fail(c, PCS_E_INVAL, "null buffer array");
+    if (n > (1u << 24)) return fail(c, PCS_E_INVAL, "too many buffers");
+    Job job;
+    if (int st = add_buffers(c, job, bufs, n, 0)) return st;
+    const uint64_t T = job.nchunks, G = job.ngroups;
+    if (T && !d_ref) return fail(c, PCS_E_INVAL, "null reference fingerprints");
+    uint64_t differing = 0;
+    if (T) {
+        // The diff tiles compare every chunk's fingerprint with the reference
+        // (a chunk the reference does not hold never occurs: same plan), one
+        // mask word per group; the scan's total is the number of set bits.
+        for (auto &jb : job.bufs) {
+            jb.parent_hash = (uint64_t)(d_ref + jb.chunk_begin);
+            jb.parent_chunks = jb.nchunks;
+        }
+        const uint32_t tiles = tile_split(G);
+        Carver cv;
+        uint64_t o_mask, o_offs, o_total;
+        cv.add(&o_mask, 8 * G);
+        cv.add(&o_offs, 8 * G);
+        cv.add(&o_total, 8);
+        Temp t(c);
+        Staged sg;
+        uint64_t xd, scr;
+        settle(c, false);
+        if (int st = stage(c, job, is_small(job), t, {}, cv.total, sg, xd, scr)) return st;
+        uint64_t *d_mask = (uint64_t *)(scr + o_mask), *d_offs = (uint64_t *)(scr + o_offs);
+        uint64_t *d_total = (uint64_t *)(scr + o_total);
+        hipStream_t s = c->stream;
+        int st = with_tables(sg, [&](const auto &tab) {
+            return launch(c, "hash", [&] { return launch_tile(tab, G, kModeDiff, nullptr, d_mask, 0, s, tiles); });
+        });
+        if (st) return st;
+        if ((st = launch(c, "classify", [&] { return launch_scan(d_mask, G, d_offs, d_total, s); }))) return st;
+        HIP_TRY(c, hipMemcpyAsync(&differing, d_total, 8, hipMemcpyDeviceToHost, s));
+        HIP_TRY(c, hipStreamSynchronize(s));
+    }
+    if (h_differing) *h_differing = differing;
+    if (h_distance) *h_distance = T ? (double)differing / (double)T : 0.0;
+    return PCS_OK;
+}
+
 int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uint64_t n_entries,
                     const float *d_scores, uint64_t keep, uint32_t *d_kept)
 {
@@ -1377,8 +1441,10 @@ int pcs_import(pcs_ctx *c, const void *h_src, uint64_t size, pcs_snap *out)
     if (int st = fingerprint_regions(c, addr, nb, (uint64_t *)h_dev, (uint64_t *)r_dev, (uint64_t *)(r_dev + 8 * n)))
         return drain(st);
     std::vector<uint64_t> got(T + n + 1);
-    HIP_TRY(c, hipMemcpyAsync(got.data(), (void *)h_dev, 8 * (T + n + 1), hipMemcpyDeviceToHost, s));
-    HIP_TRY(c, hipStreamSynchronize(s));
+    e = hipMemcpyAsync(got.data(), (void *)h_dev, 8 * (T + n + 1), hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return drain(hip_fail(c, e, "fingerprint download"));
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return drain(hip_fail(c, e, "hipStreamSynchronize"));
     for (uint64_t i = 0; i < T; ++i)
         if (got[i] != get64(img + L.hashes_off + 8 * i))
             return fail(c, PCS_E_CORRUPT, "chunk %llu does not match its fingerprint", (unsigned long long)i);

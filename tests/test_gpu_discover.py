@@ -181,3 +181,63 @@ def test_discover_errors(pcs):
     assert e.value.code == pcs.E_INVAL
     assert ctx.arena_stats() == before
     ctx.close()
+
+
+def _distance_abi(pcs, ctx, ref, bufs):
+    """pcs_distance through the C ABI: (differing chunks, distance)."""
+    import ctypes
+    from paper_2607_21686_amd import _lib
+    arr = pcs.BufArray(bufs)
+    cnt, d = ctypes.c_uint64(), ctypes.c_double()
+    st = _lib.lib().pcs_distance(ctx._h, arr.arr, len(bufs), ref.data_ptr() if ref is not None else None,
+                                 ctypes.byref(cnt), ctypes.byref(d))
+    assert st == 0, _lib.lib().pcs_last_error(ctx._h)
+    return int(cnt.value), float(d.value)
+
+
+@pytest.mark.parametrize("case", ["small", "large"])
+def test_distance_counts_differing_chunks(pcs, case):
+    """D = differing chunks / chunks, against the oracle's fingerprints of the
+    same bytes and of a reference copy with chosen chunks changed (Sec. 4's
+    metric, taken bit-exactly).  'small' carries its tables in the kernel
+    arguments and runs as sub-tiles; 'large' (more than 16 buffers, more than
+    128 groups) uploads them and runs whole-group tiles."""
+    rng = np.random.default_rng(91 if case == "small" else 92)
+    if case == "small":
+        sizes = [5000, 1, 3 * 4096 + 17, 64 * 4096 + 8, 0]
+    else:
+        sizes = [40 << 20] + [int(rng.integers(1, 3 * 4096)) for _ in range(20)]
+    log("distance:", case, "sizes", sizes[:4], "...")
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    total = sum(oracle.chunk_count(n) for n in sizes)
+    # The reference: the same bytes with a random set of chunks changed.
+    refb = [b.copy() for b in bufs]
+    changed = 0
+    for b in refb:
+        nch = oracle.chunk_count(b.size)
+        for c in range(nch):
+            if rng.random() < 0.3:
+                o = c * 4096 + int(rng.integers(0, min(4096, b.size - c * 4096)))
+                b[o] ^= 0x5A
+                changed += 1
+    ref_h = np.concatenate([oracle.fingerprint([b])[0] for b in refb])
+    got_h = np.concatenate([oracle.fingerprint([b])[0] for b in bufs])
+    want = int((ref_h != got_h).sum())
+    assert want == changed
+    ctx = pcs.Context(arena(64 << 20))
+    d = [dev(b) for b in bufs]
+    descs = [pcs.flat(t, n) for t, n in zip(d, sizes)]
+    ref = dev(ref_h.view(np.uint8)).view(torch.int64)
+    assert _distance_abi(pcs, ctx, ref, descs) == (want, want / total)
+    assert ctx.distance(ref, descs) == want / total
+    # Against itself: zero.
+    same = dev(got_h.view(np.uint8)).view(torch.int64)
+    assert _distance_abi(pcs, ctx, same, descs) == (0, 0.0)
+    # A second call with fewer buffers (scratch reuse).
+    n1 = oracle.chunk_count(sizes[0])
+    assert _distance_abi(pcs, ctx, ref[:max(n1, 1)].contiguous(), descs[:1]) == (
+        int((ref_h[:n1] != got_h[:n1]).sum()), float((ref_h[:n1] != got_h[:n1]).sum()) / n1)
+    # No chunks at all: D = 0 and no reference needed.
+    empty = [pcs.flat(d[0], 0)]
+    assert _distance_abi(pcs, ctx, None, empty) == (0, 0.0)
+    ctx.close()

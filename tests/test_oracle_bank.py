@@ -12,6 +12,8 @@ import itertools
 import math
 import os
 
+from fractions import Fraction
+
 import numpy as np
 import pytest
 
@@ -106,4 +108,37 @@ def test_keep_count_against_table6(orc):
     for _ in range(500):
         f, m = float(rng.random()), int(rng.integers(0, 5000))
         assert P.keep_count(f, m) == orc.keep_count(f, m)
+    for _ in range(500):  # exact decimals with two digits: many products land on a half
+        f, m = "0.%02d" % rng.integers(0, 100), int(rng.integers(0, 400))
+        assert P.keep_count(f, m) == orc.keep_count(f, m)
     assert orc.keep_count(0.5, 0) == 0 and orc.keep_count(0.0, 9) == 1 and orc.keep_count(1.0, 9) == 9
+    assert P.keep_count(0.5, 0) == 0 and P.keep_count(0.0, 9) == 1 and P.keep_count(1.0, 9) == 9
+
+
+# Products that land exactly on a half, computed by hand from the decimal
+# fraction (the binary float nearest 0.05 is slightly above it, so rounding
+# that value instead would give 3 for (0.05, 50)): a tie goes to the even
+# neighbour.
+EXACT_HALVES = [(0.05, 50, 2), (0.3, 5, 2), (0.5, 21, 10), (0.1, 25, 2), (0.7, 5, 4), (0.5, 1, 1),
+                (0.5, 3, 2), (0.5, 5, 2), (0.25, 10, 2), (0.25, 14, 4), (0.12, 25, 3), ("0.125", 4, 1),
+                ("0.125", 12, 2), ((1, 3), 3, 1), ((1, 2), 7, 4)]
+
+
+def test_keep_count_exact_halves(orc):
+    import paper_2607_21686_amd as P
+    for f, n, want in EXACT_HALVES:
+        assert orc.keep_count(f if not isinstance(f, tuple) else Fraction(*f), n) == want, (f, n)
+        assert P.keep_count(f, n) == want, (f, n)
+    # The decimal reading, not the binary one: a float and its decimal string agree.
+    for f in (0.05, 0.3, 0.1, 0.7, 0.12):
+        for n in range(0, 200):
+            assert P.keep_count(f, n) == P.keep_count(repr(f), n) == orc.keep_count(repr(f), n)
+
+
+def test_keep_count_rejects_bad_fractions(orc):
+    import paper_2607_21686_amd as P
+    for bad in ((3, 2), (1, 0)):
+        with pytest.raises(P.PcsError):
+            P.keep_count(bad, 10)
+    with pytest.raises(ValueError):
+        orc.keep_count(1.5, 10)
