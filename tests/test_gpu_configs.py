@@ -1,10 +1,11 @@
 """GPU parity at full size on the five seeded workload configurations, through
-the C ABI, against the CPU oracle.  Where the oracle cannot cover a whole
-output in seconds (the 1024-session batch), it checks sampled sessions one by
-one and the rest is checked through properties that hold at any size
-(restored bytes equal their sources; a restored ring fingerprints like the
-original).  Bit-exact throughout."""
+the C ABI, against the CPU oracle.  Every chunk fingerprint, buffer root and
+session root of every configuration is compared with the oracle (the
+1024-session batch one session at a time on a thread pool); snapshot bytes of
+the batch on sessions of every head class; restored bytes equal their sources
+and a restored ring fingerprints like the original.  Bit-exact throughout."""
 import gc
+import os
 
 import numpy as np
 import pytest
@@ -242,19 +243,50 @@ def test_config5_batched_suspend_resume(pcs):
     for s in snaps:
         assert ctx.info(s)["state_bytes"] == 34_752_528
     ghs, grt, gsr = u64(ch), u64(rt), u64(sr)
-    # Sampled sessions: full oracle fingerprints and snapshot bytes.
     per = sum(per_chunks)
-    for s in (0, 1, 511, S - 1):
-        log("config 5: oracle session", s)
+    # Every session: chunk fingerprints, buffer roots and session root against
+    # the oracle, from the session's raw ring bytes (the oracle takes the
+    # window itself).  Sessions are copied to the host one at a time; the
+    # oracle runs on a thread pool (its C calls release the interpreter lock).
+    from concurrent.futures import ThreadPoolExecutor
+
+    def check(s, r, o, q):
+        logical = [oracle.ring_window(r, g.outer, g.outer_stride, g.capacity, g.row_bytes, plan.heads[s], g.window),
+                   o, q]
+        oh, orr, osr = oracle.fingerprint(logical)
+        ok = (np.array_equal(ghs[s * per:(s + 1) * per], oh) and np.array_equal(grt[3 * s:3 * s + 3], orr)
+              and int(gsr[s]) == osr)
+        return s, ok
+
+    log("config 5: oracle fingerprints of all %d sessions" % S)
+    bad, pending = [], []
+    with ThreadPoolExecutor(max_workers=max(1, min(12, (os.cpu_count() or 2) - 1))) as ex:
+        for s in range(S):
+            pending.append(ex.submit(check, s, host(rings[s]), host(obs[s]), host(rngs[s])))
+            if len(pending) >= 24:
+                bad += [k for k, ok in (f.result() for f in pending[:12]) if not ok]
+                pending = pending[12:]
+            if s % 256 == 255:
+                log("config 5: %d sessions sent to the oracle" % (s + 1))
+        bad += [k for k, ok in (f.result() for f in pending) if not ok]
+    assert not bad, "sessions whose fingerprints differ from the oracle: %s" % bad[:20]
+    # Snapshot bytes against the oracle's canonical payload on sessions of
+    # every head class: a window that does not wrap, one that wraps between
+    # chunks, one that wraps inside a chunk (2048-byte rows, odd head).
+    C, Wn = g.capacity, g.window
+    classes = {"no wrap": [s for s in range(S) if plan.heads[s] + Wn <= C],
+               "wrap between chunks": [s for s in range(S) if plan.heads[s] + Wn > C and plan.heads[s] % 2 == 0],
+               "wrap inside a chunk": [s for s in range(S) if plan.heads[s] + Wn > C and plan.heads[s] % 2 == 1]}
+    sample = sorted(set([0, 1, 511, S - 1] + [x for v in classes.values() for x in v[:6]]))
+    assert all(len(v) >= 6 for v in classes.values()) and len(sample) >= 16
+    for s in sample:
+        log("config 5: snapshot bytes of session", s, "head", plan.heads[s])
         r = host(rings[s])
         logical = [oracle.ring_window(r, g.outer, g.outer_stride, g.capacity, g.row_bytes, plan.heads[s], g.window),
                    host(obs[s]), host(rngs[s])]
-        oh, orr, osr = oracle.fingerprint(logical)
-        assert np.array_equal(ghs[s * per:(s + 1) * per], oh)
-        assert np.array_equal(grt[3 * s:3 * s + 3], orr) and int(gsr[s]) == osr
         pay = torch.empty(ctx.info(snaps[s])["stored_bytes"], dtype=torch.uint8, device="cuda")
         ctx.payload(snaps[s], pay)
-        assert np.array_equal(host(pay), oracle.pack(logical))
+        assert np.array_equal(host(pay), oracle.pack(logical)), s
         del pay
     # Restore a random half in permuted order at new heads, in one launch.
     order, heads = plan.restore_order, plan.restore_heads
