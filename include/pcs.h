@@ -165,6 +165,31 @@ int pcs_fingerprint(pcs_ctx *ctx, const pcs_buf *h_bufs, uint32_t n, uint64_t *d
                     uint64_t *d_roots, uint64_t *d_session_root);
 
 /*
+ * pcs_fingerprint without allocation, for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * it).  Same arguments, outputs and stream ordering as pcs_fingerprint, and
+ * bit-identical results.  Its descriptor tables, group map and Merkle levels
+ * live in a static device array of 16 MiB that every GPU the library runs on
+ * holds until the process ends (its address is looked up once per device when
+ * the first context on that device is created); the tables of a job of more
+ * than 16 buffers or 64 physical runs reach it through a 2 MiB pinned host
+ * buffer made by pcs_ctx_create.  The call itself makes no device, pinned or
+ * HIP allocation, creates no HIP event (kernel timing skips it) and takes no
+ * arena space.
+ * Limits: at most 4096 buffers and 65536 physical runs (a ring window is at
+ * most two runs per ring), and at most 16 MiB of scratch: about 32 bytes per
+ * 64-chunk group (256 KiB of state) plus 160 bytes per buffer and 16 per run
+ * (about 120 GiB of state); beyond them PCS_E_INVAL, nothing enqueued.
+ * Every call on one GPU shares that GPU's array and it keeps the last call's
+ * contents (nothing in it needs clearing: each call writes what it reads):
+ * calls that overlap on one GPU (contexts on different streams not ordered
+ * against each other) race and give wrong results; calls ordered on one
+ * stream do not.
+ */
+int pcs_fingerprint_noalloc(pcs_ctx *ctx, const pcs_buf *h_bufs, uint32_t n, uint64_t *d_chunk_hashes,
+                            uint64_t *d_roots, uint64_t *d_session_root);
+
+/*
  * Cross-replay classification (derivability, Sec. 3 "The partition"; the
  * fingerprint stands in for the Sec. 4 ablation).
  *   d_hashes:  uint64[K][total], replay-major; each replay is laid out like

@@ -197,6 +197,13 @@ class Context:
         self._check(_L.pcs_fingerprint(self._h, _array(bufs), len(bufs), _dev_ptr(chunk_hashes),
                                          _dev_ptr(roots), _dev_ptr(session_root)))
 
+    def fingerprint_noalloc(self, bufs, chunk_hashes=None, roots=None, session_root=None):
+        """fingerprint() for callers that cannot allocate
+        (pcs_fingerprint_noalloc): same outputs, scratch in the library's
+        static per-GPU array; calls that overlap on one GPU race."""
+        self._check(_L.pcs_fingerprint_noalloc(self._h, _array(bufs), len(bufs), _dev_ptr(chunk_hashes),
+                                                 _dev_ptr(roots), _dev_ptr(session_root)))
+
     def classify(self, hashes, K: int, chunks_per_buf, bitmap, labels):
         """Cross-replay classification (pcs_classify): hashes holds K x total
         fingerprints (replay-major); bitmap gets one 64-bit word per 64-chunk

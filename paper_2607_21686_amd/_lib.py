@@ -26,6 +26,7 @@ _ERRNAMES = {E_INVAL: "PCS_E_INVAL", E_NOMEM: "PCS_E_NOMEM", E_HANDLE: "PCS_E_HA
 
 # Every symbol include/pcs.h declares.
 EXPORTS = ("pcs_ctx_create", "pcs_ctx_destroy", "pcs_last_error", "pcs_chunk_counts", "pcs_fingerprint",
+           "pcs_fingerprint_noalloc",
            "pcs_classify", "pcs_checkpoint", "pcs_checkpoint_batch", "pcs_restore", "pcs_restore_batch",
            "pcs_restore_verify", "pcs_fork", "pcs_delete", "pcs_snapshot_info", "pcs_snapshot_payload",
            "pcs_snapshot_view", "pcs_snapshot_hashes",
@@ -91,6 +92,7 @@ def load():
         "pcs_last_error": ([P], ctypes.c_char_p),
         "pcs_chunk_counts": ([PB, U32, PU64, PU64], I),
         "pcs_fingerprint": ([P, PB, U32, P, P, P], I),
+        "pcs_fingerprint_noalloc": ([P, PB, U32, P, P, P], I),
         "pcs_classify": ([P, P, U32, PU64, U32, P, P], I),
         "pcs_checkpoint": ([P, PB, U32, U64, U32, P, P, P, PU64], I),
         "pcs_checkpoint_batch": ([P, PB, ctypes.POINTER(U32), U32, U32, P, P, P, PU64], I),

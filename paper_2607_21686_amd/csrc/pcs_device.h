@@ -12,6 +12,12 @@
 
 namespace pcs {
 
+// Size of the per-device scratch array of the allocation-free fingerprint
+// entry point, and its device address on the current device (valid for the
+// life of the process; call once per device with that device current).
+constexpr uint64_t kStaticScratchBytes = 16ULL << 20;
+hipError_t static_scratch_address(uint64_t *addr);
+
 // Kernel launchers (pcs_kernels.hip).  All are asynchronous on `s`.
 enum TileMode : int {
     kModeHash = 0,    // fingerprint the buffer's runs

@@ -19,7 +19,23 @@
 // multiply work on the vector ALU.
 #include "pcs_device.h"
 
+// Device scratch of the allocation-free entry point (pcs_fingerprint_noalloc):
+// descriptor tables, the group map and the Merkle levels of one call.  Every
+// GPU the library runs on holds its own copy until the process ends.  In host
+// code this name is a host-side stand-in, never a device address: host code
+// uses only the per-device address that static_scratch_address returns.
+static __device__ __align__(256) uint8_t scratch[pcs::kStaticScratchBytes];
+
 namespace pcs {
+
+hipError_t static_scratch_address(uint64_t *addr)
+{
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    *addr = e == hipSuccess ? (uint64_t)p : 0;
+    return e;
+}
+
 namespace {
 
 // XXH64 primes (xxHash specification).

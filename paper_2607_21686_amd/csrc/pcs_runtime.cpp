@@ -12,6 +12,7 @@
 #include <cstring>
 #include <map>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -28,6 +29,11 @@ namespace {
 constexpr uint64_t kMaxGroups = (1ULL << 32) / 256 - 1;  // grid limit of the 256-lane kernels
 constexpr uint32_t kStagingSlots = 8;
 constexpr uint32_t kCountSlots = 4096;
+// Limits of pcs_fingerprint_noalloc: its descriptor tables pass through one
+// pinned host buffer of kNoAllocStagingBytes made at context creation.
+constexpr uint32_t kNoAllocMaxBufs = 4096, kNoAllocMaxRuns = 65536;
+constexpr uint64_t kNoAllocStagingBytes = 2ULL << 20;
+constexpr int kMaxDevices = 64;
 
 struct SnapNode;
 
@@ -56,7 +62,15 @@ struct pcs_ctx {
     std::vector<std::weak_ptr<pcs::SnapNode>> pending;
 
     bool timing = false;
+    bool no_events = false;  // set while a call that must create nothing runs (no timing events)
     std::map<std::string, std::vector<std::pair<hipEvent_t, hipEvent_t>>> timers;
+
+    // pcs_fingerprint_noalloc: the device's static scratch array (its address
+    // on the arena's device) and a fixed pinned staging buffer for tables.
+    uint64_t scratch_dev = 0;
+    void *na_host = nullptr;
+    hipEvent_t na_ev = nullptr;
+    bool na_pending = false;
 };
 
 namespace pcs {
@@ -220,7 +234,8 @@ int launch(pcs_ctx *c, const char *name, F &&f)
         if (a) (void)hipEventDestroy(a);
         if (b) (void)hipEventDestroy(b);
     };
-    if (c->timing) {
+    const bool timed = c->timing && !c->no_events;
+    if (timed) {
         hipError_t te = hipEventCreate(&a);
         if (te == hipSuccess) te = hipEventCreate(&b);
         if (te == hipSuccess) te = hipEventRecord(a, c->stream);
@@ -230,7 +245,7 @@ int launch(pcs_ctx *c, const char *name, F &&f)
         }
     }
     const hipError_t e = f();
-    if (c->timing) {
+    if (timed) {
         const hipError_t te = hipEventRecord(b, c->stream);
         if (te != hipSuccess) {
             drop();
@@ -680,6 +695,41 @@ int fingerprint_regions(pcs_ctx *c, const std::vector<uint64_t> &addr, const std
     return run_hash_job(c, job, false, {n}, rdst, sdst, true);
 }
 
+// The static scratch array's address on the device that holds `dev_ptr`,
+// looked up once per device (with that device current) and kept for the
+// life of the process: each GPU holds its own copy at its own address.
+hipError_t scratch_for(const void *dev_ptr, uint64_t *addr)
+{
+    static std::mutex mu;
+    static uint64_t cached[kMaxDevices];
+    hipPointerAttribute_t at;
+    hipError_t e = hipPointerGetAttributes(&at, dev_ptr);
+    if (e != hipSuccess) return e;
+    const int dev = at.device;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!cached[dev]) {
+        int cur = 0;
+        if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        uint64_t a = 0;
+        e = static_scratch_address(&a);
+        const hipError_t back = cur != dev ? hipSetDevice(cur) : hipSuccess;
+        if (e != hipSuccess) return e;
+        if (back != hipSuccess) return back;
+        cached[dev] = a;
+    }
+    *addr = cached[dev];
+    return hipSuccess;
+}
+
+// Clears c->no_events when the call that set it returns.
+struct NoEvents {
+    pcs_ctx *c;
+    explicit NoEvents(pcs_ctx *ctx) : c(ctx) { c->no_events = true; }
+    ~NoEvents() { c->no_events = false; }
+};
+
 }  // namespace
 }  // namespace pcs
 
@@ -711,6 +761,12 @@ int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ct
         return PCS_E_HIP;
     }
     for (uint32_t i = 0; i < kCountSlots; ++i) c->free_counts.push_back(kCountSlots - 1 - i);
+    if (hipHostMalloc(&c->na_host, kNoAllocStagingBytes, hipHostMallocDefault) != hipSuccess ||
+        hipEventCreateWithFlags(&c->na_ev, hipEventDisableTiming) != hipSuccess ||
+        scratch_for(d_arena, &c->scratch_dev) != hipSuccess) {
+        pcs_ctx_destroy(c);
+        return PCS_E_HIP;
+    }
     *out = c;
     return PCS_OK;
 }
@@ -731,6 +787,8 @@ int pcs_ctx_destroy(pcs_ctx *c)
         if (s.host) (void)hipHostFree(s.host);
     }
     if (c->counts) (void)hipHostFree(c->counts);
+    if (c->na_ev) (void)hipEventDestroy(c->na_ev);
+    if (c->na_host) (void)hipHostFree(c->na_host);
     delete c;
     return PCS_OK;
 }
@@ -768,6 +826,96 @@ int pcs_fingerprint(pcs_ctx *c, const pcs_buf *bufs, uint32_t n, uint64_t *d_has
     sdst[0].d[0] = (uint64_t)d_sroot;
     settle(c, false);
     return run_hash_job(c, job, false, {n}, rdst, sdst, d_roots || d_sroot);
+}
+
+int pcs_fingerprint_noalloc(pcs_ctx *c, const pcs_buf *bufs, uint32_t n, uint64_t *d_hashes, uint64_t *d_roots,
+                            uint64_t *d_sroot)
+{
+    if (!c) return PCS_E_INVAL;
+    if (n && !bufs) return fail(c, PCS_E_INVAL, "null buffer array");
+    if (n > kNoAllocMaxBufs) return fail(c, PCS_E_INVAL, "at most %u buffers without allocation (%u given)", kNoAllocMaxBufs, n);
+    if (!c->scratch_dev) return fail(c, PCS_E_HIP, "no static scratch on this device");
+    Job job;
+    if (int st = add_buffers(c, job, bufs, n, 0)) return st;
+    if (job.runs.size() > kNoAllocMaxRuns)
+        return fail(c, PCS_E_INVAL, "at most %u physical runs without allocation (%zu given)", kNoAllocMaxRuns,
+                    job.runs.size());
+    const uint64_t G = job.ngroups;
+    const bool want_roots = d_roots || d_sroot;
+    for (uint32_t b = 0; b < n; ++b) job.bufs[b].hash_dst[0] = d_hashes ? (uint64_t)(d_hashes + job.bufs[b].chunk_begin) : 0;
+    const bool small = is_small(job);
+    const uint32_t tiles = tile_split(G);
+    const uint64_t per_tile = kGroupChunks / tiles;
+
+    // Scratch layout: [job tables][Merkle lists] (uploaded; large jobs only),
+    // [group map (large jobs)][tile nodes][two Merkle levels][buffer roots].
+    std::vector<MerkleList> lists;
+    Carver cv;
+    uint64_t o_bufs = 0, o_runs = 0, o_lists = 0, o_map = 0, o_nodes, o_sa, o_sb, o_roots;
+    if (!small) {
+        cv.add(&o_bufs, sizeof(JobBuf) * n);
+        cv.add(&o_runs, sizeof(Run) * job.runs.size());
+        if (want_roots) cv.add(&o_lists, sizeof(MerkleList) * (n + 1));
+    }
+    const uint64_t hb = cv.total;
+    if (!small) cv.add(&o_map, sizeof(GroupRef) * G);
+    cv.add(&o_nodes, 8 * G * tiles);
+    cv.add(&o_sa, 8 * std::max<uint64_t>(G * tiles, n));
+    cv.add(&o_sb, 8 * std::max<uint64_t>(G * tiles, n));
+    cv.add(&o_roots, 8 * std::max<uint32_t>(n, 1));
+    if (cv.total > kStaticScratchBytes)
+        return fail(c, PCS_E_INVAL, "job needs %llu bytes of scratch, more than the %llu bytes available without "
+                    "allocation", (unsigned long long)cv.total, (unsigned long long)kStaticScratchBytes);
+    if (hb > kNoAllocStagingBytes)
+        return fail(c, PCS_E_INVAL, "job tables need %llu bytes, more than the %llu bytes of staging",
+                    (unsigned long long)hb, (unsigned long long)kNoAllocStagingBytes);
+    const uint64_t base = c->scratch_dev;
+    uint64_t *d_nodes = (uint64_t *)(base + o_nodes);
+    uint64_t *d_sa = (uint64_t *)(base + o_sa), *d_sb = (uint64_t *)(base + o_sb);
+    uint64_t *d_rt = (uint64_t *)(base + o_roots);
+    if (want_roots) {
+        for (uint32_t b = 0; b < n; ++b)
+            lists.push_back({job.bufs[b].group_begin * tiles, div_up(job.bufs[b].nchunks, per_tile),
+                             {d_roots ? (uint64_t)(d_roots + b) : 0, 0}});
+        lists.push_back({0, n, {(uint64_t)d_sroot, 0}});
+    }
+    NoEvents guard(c);
+    hipStream_t s = c->stream;
+    Staged sg;
+    sg.small = small;
+    if (small) {
+        memset(&sg.arg, 0, sizeof sg.arg);
+        sg.arg.nbuf = n;
+        if (n) memcpy(sg.arg.bufs, job.bufs.data(), sizeof(JobBuf) * n);
+        if (!job.runs.empty()) memcpy(sg.arg.runs, job.runs.data(), sizeof(Run) * job.runs.size());
+    } else {
+        sg.dev = DevTables{(const JobBuf *)(base + o_bufs), (const Run *)(base + o_runs),
+                           (const GroupRef *)(base + o_map), n, 0};
+        // The staging buffer is reused once the previous call's copy out of it has run.
+        if (c->na_pending) {
+            HIP_TRY(c, hipEventSynchronize(c->na_ev));
+            c->na_pending = false;
+        }
+        uint8_t *h = (uint8_t *)c->na_host;
+        memset(h, 0, hb);
+        if (n) memcpy(h + o_bufs, job.bufs.data(), sizeof(JobBuf) * n);
+        if (!job.runs.empty()) memcpy(h + o_runs, job.runs.data(), sizeof(Run) * job.runs.size());
+        if (want_roots) memcpy(h + o_lists, lists.data(), sizeof(MerkleList) * lists.size());
+        HIP_TRY(c, hipMemcpyAsync((void *)base, h, hb, hipMemcpyHostToDevice, s));
+        HIP_TRY(c, hipEventRecord(c->na_ev, s));
+        c->na_pending = true;
+        if (G) {
+            if (int st = launch(c, "map", [&] {
+                    return launch_group_map(sg.dev.bufs, sg.dev.runs, n, G, (GroupRef *)sg.dev.map, s);
+                }))
+                return st;
+        }
+    }
+    int st = with_tables(sg, [&](const auto &tab) {
+        return launch(c, "hash", [&] { return launch_tile(tab, G, kModeHash, d_nodes, nullptr, 0, s, tiles); });
+    });
+    if (st || !want_roots) return st;
+    return run_merkle(c, small, lists, n, base + o_lists, d_nodes, d_sa, d_sb, d_rt);
 }
 
 int pcs_classify(pcs_ctx *c, const uint64_t *d_hashes, uint32_t K, const uint64_t *h_chunks, uint32_t n,
