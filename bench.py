@@ -55,8 +55,11 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (for HBM counter scaling)")
     ap.add_argument("--traffic", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
-                    help="no GPU: write the scaled HBM traffic record of the fused pack+fingerprint and restore "
-                         "kernels from a FETCH_SIZE and a WRITE_SIZE run of this bench with --calibrate-copy")
+                    help="no GPU: write the scaled HBM traffic record of the workload's dominant kernels (batch, "
+                         "kv-ring or verify) from a FETCH_SIZE and a WRITE_SIZE run of this bench with "
+                         "--calibrate-copy and the same --workload")
+    ap.add_argument("--arena-mib", type=int, default=0,
+                    help="bank workload: arena size in MiB (default 1024)")
     ap.add_argument("--summarize", nargs="+", metavar="DB",
                     help="no GPU: print kernel statistics from rocprofv3 databases (trace or --pmc runs)")
     return ap.parse_args()
@@ -100,7 +103,26 @@ def summarize(dbs):
         print()
 
 
-TRAFFIC_JSON = os.path.join(ROOT, "profiles", "k_hash_copy_batch1024_traffic.json")
+# Per workload: the scaled-traffic record the bench line reads, and the
+# kernels it covers (name pattern in rocprofv3's kernel names, label).
+TRAFFIC = {
+    "batch": ("k_hash_copy_batch1024_traffic.json",
+              [("pack", "k_hash<pcs::DevTables, 1, 1024, 512, 64>",
+                "k_hash<DevTables, pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
+               ("copy", "k_copy<pcs::DevTables, false, 512, 1024, 64>",
+                "k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
+    "kv-ring": ("k_hash_copy_kv_ring_1gib_traffic.json",
+                [("pack", "k_hash<pcs::DevTables, 1, 1024, 512, 64>",
+                  "k_hash<DevTables, pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
+                 ("copy", "k_copy<pcs::DevTables, false, 512, 1024, 64>",
+                  "k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
+    "verify": ("k_hash_verify_kv_ring_1gib_traffic.json",
+               [("verify", "k_hash<pcs::DevTables, 3, 1024, 512, 64>",
+                 "k_hash<DevTables, verify, 1024 lanes, 512 B slices, 64 chunks> (restore + fingerprint + compare)"),
+                ("copy", "k_copy<pcs::DevTables, false, 512, 1024, 64>",
+                 "k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (plain restore)")]),
+}
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", TRAFFIC["batch"][0])
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_21686_amd", "csrc", f)
                   for f in ("pcs_kernels.hip", "pcs_device.h", "pcs_layout.h")]
 
@@ -113,68 +135,79 @@ def kernel_source_sha():
     return h.hexdigest()
 
 
-def traffic_record():
-    """Scaled HBM traffic of the fused pack+fingerprint kernel, measured with
+def traffic_record(workload="batch"):
+    """Scaled HBM traffic of the workload's dominant kernels, measured with
     rocprofv3 counters, if the kernel sources are unchanged since."""
     try:
-        rec = json.load(open(TRAFFIC_JSON))
-    except (OSError, ValueError):
+        rec = json.load(open(os.path.join(ROOT, "profiles", TRAFFIC[workload][0])))
+    except (OSError, ValueError, KeyError):
         return None
     return rec if rec.get("kernel_source_sha256") == kernel_source_sha() else None
 
 
-def traffic(fetch_db, write_db, sessions=1024, restored=512):
-    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB, as rocprofv3 reports them)
-    of the fused pack+fingerprint kernel and the restore copy kernel, each
-    scaled by what the same counter reads for the plain 1 GiB calibration copy
-    (true traffic 1 GiB read + 1 GiB written), against the algorithmic bytes of
-    one launch (state read once and written once)."""
-    import sqlite3
+def _state_bytes(workload, sessions):
+    """Algorithmic bytes of one launch of each kernel the traffic record
+    covers: the state read once and written once."""
     import workloads as W
+    if workload == "batch":
+        plan = W.config5_plan(4, sessions=sessions)
+        per = plan.ring.window_bytes + plan.obs_bytes + plan.rng_bytes
+        return {"pack": 2 * per * sessions, "copy": 2 * per * len(plan.restore_order)}
+    g, _ = W.kv_ring_geometry(32, 8192, 4096, 8, 128, 2)
+    return {"pack": 2 * g.window_bytes, "copy": 2 * g.window_bytes, "verify": 2 * g.window_bytes}
+
+
+def traffic(fetch_db, write_db, workload="batch", sessions=1024):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB, as rocprofv3 reports them)
+    of the workload's dominant kernels, each scaled by what the same counter
+    reads for the plain 1 GiB calibration copy (true traffic 1 GiB read +
+    1 GiB written), against the algorithmic bytes of one launch (state read
+    once and written once)."""
+    import sqlite3
+    fname, kernels = TRAFFIC[workload]
 
     def per_kernel(db, counter):
         cur = sqlite3.connect(db).cursor()
         q = "select kernel_name, value from counters_collection where counter_name = ?"
         rows = cur.execute(q, (counter,)).fetchall()
         pick = lambda pat: [v for n, v in rows if pat in n]
-        calib = max(pick("rocclr_copyBuffer"))
-        return {"pack": pick("k_hash<pcs::DevTables, 1, 1024, 512, 64>"),
-                "copy": pick("k_copy<pcs::DevTables, false, 512, 1024, 64>"),
-                "calib": calib}
+        out = {key: pick(pat) for key, pat, _ in kernels}
+        out["calib"] = max(pick("rocclr_copyBuffer"))
+        return out
 
     f, w = per_kernel(fetch_db, "FETCH_SIZE"), per_kernel(write_db, "WRITE_SIZE")
     gib_kib = (1 << 30) / 1024
     fs, ws = gib_kib / f["calib"], gib_kib / w["calib"]
-    plan = W.config5_plan(1, sessions=1)
-    state = plan.ring.window_bytes + plan.obs_bytes + plan.rng_bytes
+    alg = _state_bytes(workload, sessions)
     mean = lambda xs: sum(xs) / len(xs)
 
-    def one(kind, n_sessions):
-        fk, wk = mean(f[kind]), mean(w[kind])
+    def one(key):
+        fk, wk = mean(f[key]), mean(w[key])
         t = int(round((fk * fs + wk * ws) * 1024))
-        alg = 2 * state * n_sessions
         return {"fetch_KiB_per_dispatch": round(fk, 1), "write_KiB_per_dispatch": round(wk, 1),
-                "dispatches": [len(f[kind]), len(w[kind])], "traffic_bytes_per_launch": t,
-                "algorithmic_bytes_per_launch": alg, "traffic_over_algorithmic": round(t / alg, 5)}
+                "dispatches": [len(f[key]), len(w[key])], "traffic_bytes_per_launch": t,
+                "algorithmic_bytes_per_launch": alg[key], "traffic_over_algorithmic": round(t / alg[key], 5)}
 
-    rec = {"kernel": "k_hash<DevTables, pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)",
-           "workload": "batched suspend/resume, %d sessions x %d B of state" % (sessions, state),
-           "sessions": sessions,
-           "calibration_copy_bytes": 1 << 30, "calibration_fetch_KiB": round(f["calib"], 1),
-           "calibration_write_KiB": round(w["calib"], 1), "fetch_scale": round(fs, 6), "write_scale": round(ws, 6)}
-    rec.update(one("pack", sessions))
-    rec["restore_kernel"] = dict(kernel="k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (%d sessions)"
-                                 % restored, **one("copy", restored))
+    (k0, _, label0), (k1, _, label1) = kernels
+    rec = {"kernel": label0, "workload": workload, "calibration_copy_bytes": 1 << 30,
+           "calibration_fetch_KiB": round(f["calib"], 1), "calibration_write_KiB": round(w["calib"], 1),
+           "fetch_scale": round(fs, 6), "write_scale": round(ws, 6)}
+    if workload == "batch":
+        rec["sessions"] = sessions
+    rec.update(one(k0))
+    rec["second_kernel"] = dict(kernel=label1, **one(k1))
     rec["kernel_source_sha256"] = kernel_source_sha()
     # The commands that made the two databases (rocprofv3 writes <dir>/<name>_results.db).
+    wl = "" if workload == "batch" else " --workload %s" % workload
+
     def pmc_cmd(counter, db):
         rel = os.path.relpath(db)
         name = os.path.basename(rel)[:-len("_results.db")] if rel.endswith("_results.db") else "pmc"
-        return ("rocprofv3 --pmc %s -d %s -o %s -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline "
-                "--calibrate-copy" % (counter, os.path.dirname(rel) or ".", name))
+        return ("rocprofv3 --pmc %s -d %s -o %s -- python3 bench.py%s --steps 2 --warmup 1 --no-cpu-baseline "
+                "--calibrate-copy" % (counter, os.path.dirname(rel) or ".", name, wl))
     rec["commands"] = [pmc_cmd("FETCH_SIZE", fetch_db), pmc_cmd("WRITE_SIZE", write_db),
-                       "python3 bench.py --traffic %s %s" % (os.path.relpath(fetch_db), os.path.relpath(write_db))]
-    with open(TRAFFIC_JSON, "w") as fh:
+                       "python3 bench.py%s --traffic %s %s" % (wl, os.path.relpath(fetch_db), os.path.relpath(write_db))]
+    with open(os.path.join(ROOT, "profiles", fname), "w") as fh:
         json.dump(rec, fh, indent=1)
         fh.write("\n")
     print(json.dumps(rec, indent=1))
@@ -186,13 +219,22 @@ def main():
         summarize(args.summarize)
         return
     if args.traffic:
-        traffic(*args.traffic)
+        traffic(*args.traffic, workload=args.workload, sessions=args.sessions)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path.  Sessions are independent, so "
               "each GPU would run its own share of them with its own arena and stream, with no exchange "
               "between GPUs.", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        # One plain 1 GiB device-to-device copy: the reference dispatch that
+        # scales FETCH_SIZE / WRITE_SIZE to bytes.
+        import torch
+        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     if args.workload != "batch":
         out = OTHER[args.workload](args)
         print(json.dumps(out), flush=True)
@@ -262,13 +304,6 @@ def run_batch(args):
     nb_ckpt = [3] * S
     nb_rest = [3] * R
     order = plan.restore_order
-
-    if args.calibrate_copy:
-        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        b = torch.empty_like(a)
-        b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
 
     state = {"cur": 0}
 
@@ -344,7 +379,7 @@ def run_batch(args):
     avg_cp = ms_cp / max(1, n_cp)
     achieved_restore = 2 * rest_state / (avg_cp * 1e-3) / 1e9
 
-    rec = traffic_record()
+    rec = traffic_record("batch")
     traffic = rec["traffic_bytes_per_launch"] if rec and rec.get("sessions") == S else None
 
     out = {
@@ -441,6 +476,8 @@ def cpu_baseline(args, plan, rings, obs, rngs, gpu_value):
 
 def _line(args, metric_value, ms_per_step, workload, cfg, roof_kernel, alg_bytes, avg_ms, extra=None):
     achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
+    rec = traffic_record(args.workload)
+    traffic = rec["traffic_bytes_per_launch"] if rec and rec.get("algorithmic_bytes_per_launch") == alg_bytes else None
     out = {
         "metric": "checkpoint+restore GB/s and fingerprint GB/s at 1 MI355X; % of HBM peak",
         "value": round(metric_value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -448,7 +485,7 @@ def _line(args, metric_value, ms_per_step, workload, cfg, roof_kernel, alg_bytes
         "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic (seeded, generated on the GPU)",
         "config": dict({"workload": workload}, **cfg),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None, "kernel": roof_kernel,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, "kernel": roof_kernel,
                      "avg_ms": round(avg_ms, 4), "algorithmic_bytes": alg_bytes},
     }
     if _STEP_DIST is not None:
@@ -679,11 +716,11 @@ def run_bank(args):
     bank = W.config2(1)
     lat = torch.from_numpy(bank.latents.copy()).cuda()
     pos = torch.from_numpy(bank.poses.copy()).cuda()
-    # 4 GiB of arena: each incremental checkpoint reserves one slot per chunk
-    # until its stored-chunk count is known, and the reservations of the
-    # checkpoints in flight reach 3.3 GB; a tighter arena makes calls wait for
-    # the GPU (768 MiB: 3.1 instead of 2.5 ms of checkpoints per run).
-    ctx = P.Context(torch.empty(4 << 30, dtype=torch.uint8, device="cuda"))
+    # 1 GiB of arena by default (--arena-mib): the 64 snapshots keep about
+    # 130 MB; each incremental checkpoint in flight also reserves one slot per
+    # chunk of its prefix until the stream has produced its stored-chunk count.
+    arena_mib = args.arena_mib or 1024
+    ctx = P.Context(torch.empty(arena_mib << 20, dtype=torch.uint8, device="cuda"))
     plans = [P.BufArray([P.flat(lat, 8 * j * bank.latent_entry_bytes), P.flat(pos, 8 * j * bank.pose_entry_bytes)])
              for j in range(1, 65)]
     out_l, out_p = torch.empty_like(lat), torch.empty_like(pos)
@@ -702,17 +739,55 @@ def run_bank(args):
         for h in hs:
             ctx.delete(h)
     t, kt = _timed(args, ctx, step, ["pack_hash", "incremental", "copy", "merkle", "map"])
-    state = sum(8 * j * (bank.latent_entry_bytes + bank.pose_entry_bytes) for j in range(1, 65))
+    entry = bank.latent_entry_bytes + bank.pose_entry_bytes
+    state = sum(8 * j * entry for j in range(1, 65))
     n, ms = kt["incremental"]
-    # Incremental kernels per run: read every valid prefix once (j = 2..64),
-    # then read + write the dirty chunks (391 or 392 per step).
-    hashed = state - 8 * (bank.latent_entry_bytes + bank.pose_entry_bytes)
-    dirty = sum(391 + (1 if (224 * j) // 4096 != (224 * (j - 1)) // 4096 else 0) for j in range(2, 65)) * 4096
+
+    # Algorithmic bytes of incremental checkpoint j (parent j-1, j = 2..64):
+    # read the valid prefix once (V_j = 8j entries), read + write the dirty
+    # chunks (D_j: the 390 chunks of the 8 new latents, which fill whole
+    # chunks, and the pose buffer's last chunk, plus the one before it when
+    # the 224 new pose bytes cross a chunk boundary).
+    def dirty_chunks(j):
+        return 390 + 1 + (1 if (224 * j) // 4096 != (224 * (j - 1)) // 4096 and (224 * j) % 4096 else 0)
+
+    def alg_bytes(j):
+        return 8 * j * entry + 2 * 4096 * dirty_chunks(j)
+    whole = sum(alg_bytes(j) for j in range(2, 65))
+
+    # Late steps (j = 33..64, prefixes of 53-102 MB): a further pass whose
+    # kernel timing is on only for those checkpoints.
+    def late_run():
+        hs, parent = [], 0
+        for j in range(64):
+            if j == 32:
+                ctx.set_timing(True)
+            h = ctx.checkpoint(plans[j], parent=parent, hash=parent == 0)
+            hs.append(h)
+            parent = h
+        ctx.set_timing(False)
+        for h in hs:
+            ctx.delete(h)
+    for k in ("incremental", "pack_hash", "copy", "merkle", "map"):
+        ctx.kernel_time(k)
+    for _ in range(args.steps):
+        late_run()
+    torch.cuda.synchronize()
+    n_late, ms_late = ctx.kernel_time("incremental")
+    late_ms = ms_late / args.steps
+    late_bytes = sum(alg_bytes(j) for j in range(33, 65))
+    whole_GBps = whole / (ms / args.steps * 1e-3) / 1e9
     out = _line(args, 2 * state / t / 1e9, t * 1e3, "growing memory bank: bf16 latents [16,60,104] + fp32 pose [7] "
                 "per entry, 0->512 entries in steps of 8; 64 incremental checkpoints + 64 restores (random order)",
-                {"state_bytes_checkpointed_and_restored": 2 * state}, "incremental (hash+diff, scan, compact, copy)",
-                hashed + 2 * dirty, ms / args.steps, {"incremental_ms_per_run": round(ms / args.steps, 4),
-                                                      "restore_ms_per_run": round(kt["copy"][1] / args.steps, 4)})
+                {"state_bytes_checkpointed_and_restored": 2 * state, "arena_mib": arena_mib},
+                "incremental checkpoint kernels of steps 33-64 (fingerprint + diff, Merkle + scan, "
+                "slot assignment, dirty copy)", late_bytes, late_ms,
+                {"incremental_ms_per_run": round(ms / args.steps, 4),
+                 "incremental_GBps_hbm_whole_run": round(whole_GBps, 1),
+                 "incremental_frac_whole_run": round(whole_GBps / HBM_PEAK_GBPS, 4),
+                 "incremental_launches_per_run": round(n / args.steps, 1),
+                 "late_steps_ms": round(late_ms, 4), "late_steps_bytes": late_bytes,
+                 "restore_ms_per_run": round(kt["copy"][1] / args.steps, 4)})
     if not args.no_cpu_baseline:
         import oracle
         lat_h = np.ascontiguousarray(bank.latents).view(np.uint8).reshape(-1)

@@ -138,9 +138,9 @@ typedef struct pcs_snap_info {
  * every call of this context is enqueued.  The arena and the stream are
  * borrowed: the caller keeps them alive until pcs_ctx_destroy returns.
  * d_arena must be 16-byte aligned; the library uses the arena from its first
- * 4096-byte boundary on, in whole 4096-byte units, and PCS_E_INVAL results if
- * less than one unit remains.  Small pinned host buffers are allocated for
- * descriptor uploads.
+ * 4096-byte boundary on, in whole 4096-byte units, keeps the first unit for
+ * its own bookkeeping words, and PCS_E_INVAL results if fewer than two units
+ * remain.  Small pinned host buffers are allocated for descriptor uploads.
  */
 int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ctx **out);
 
@@ -380,10 +380,13 @@ int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
  * checkpoint of the shrunk bank (parent = the bank's last snapshot) stores
  * only the chunks the shrink changed.
  *
- * Limits and errors: n_entries <= 65536 and keep <= n_entries, else
+ * Selection takes O(n_entries) work (a radix select of the keep-th score,
+ * then index-ordered scans), in one workgroup.
+ *
+ * Limits and errors: n_entries <= 2^32 - 1 and keep <= n_entries, else
  * PCS_E_INVAL; nparts <= 64; entry_bytes > 0; PCS_E_NOMEM if the arena
- * cannot hold the scratch (4 * 4 + 8 bytes per entry, plus the largest
- * in-place part's keep * entry_bytes).
+ * cannot hold the scratch (4 bytes per kept entry when d_kept is NULL, plus
+ * the largest in-place part's keep * entry_bytes).
  */
 /*
  * Kept count of a shrink to a retained fraction (Sec. 7.5 holds the fraction
@@ -480,7 +483,10 @@ typedef struct pcs_discovery {
 int pcs_discover(pcs_ctx *ctx, const pcs_buf *h_components, uint32_t k, double eps, int32_t control,
                  pcs_probe_fn probe, void *user, pcs_discovery *out);
 
-/* Arena accounting: bytes in use, bytes free, largest free block, live handles. */
+/* Arena accounting: bytes in use (snapshots, the worst case of incremental
+ * checkpoints whose stored-chunk count has not come back yet, and scratch of
+ * calls in progress), bytes free (the rest of the arena less the unit the
+ * library keeps), largest free block, live handles.  Does not wait. */
 int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t *largest_free,
                     uint64_t *live_handles);
 

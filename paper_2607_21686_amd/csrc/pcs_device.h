@@ -36,12 +36,29 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
                        uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group = 1);
 template <class Tab>
 hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s);
-template <class Tab>
-hipError_t launch_compact(const Tab &tab, uint64_t ngroups, const uint64_t *dirty_mask, const uint64_t *offsets,
-                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s);
+// Where the stored chunks of an incremental checkpoint go.  Slot s is the
+// 4096 bytes ending s*4096 below the call's payload top (an arena offset).
+// The scan that totals the stored chunks takes the top from *bump (or from
+// `reset`, nonzero when the call starts a new segment of the arena), lowers
+// *bump by the slots it places, and writes the top to *top_out, which the
+// copy kernels read; with bump null it places nothing (the host writes
+// *top_out once it has allocated the slots).  host: two mapped pinned words
+// that receive the stored-chunk count and the top.
+struct SlotBump {
+    uint64_t *bump;
+    uint64_t reset;
+    uint64_t *top_out;
+    uint64_t *host;
+};
 template <class Tab>
 hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_t *total, uint64_t max_slots,
-                             uint64_t payload_top, hipStream_t s);
+                             const uint64_t *top_word, uint64_t arena_base, hipStream_t s);
+// Slot assignment + dirty copy of an incremental checkpoint in one launch
+// (from the scanned per-group offsets and the dirty masks); writes the whole
+// new manifest.
+template <class Tab>
+hipError_t launch_place_dirty(const Tab &tab, uint64_t ngroups, const uint64_t *dirty_mask, const uint64_t *offsets,
+                              const uint64_t *top_word, uint64_t arena_base, hipStream_t s);
 template <class Tab>
 hipError_t launch_classify(const Tab &tab, uint64_t ngroups, const uint64_t *hashes, uint32_t K, uint64_t total,
                            uint64_t *bitmap, hipStream_t s);
@@ -58,28 +75,27 @@ hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_
 hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64_t *scratch_a,
                                uint64_t *scratch_b, hipStream_t s);
 // Exclusive scan of the set-bit counts of per-group dirty masks (offsets
-// and total), the total also to a pinned host word when given.
-hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total, hipStream_t s,
-                       uint64_t *total_host = nullptr);
+// and total), then the placement of the slots (SlotBump).
+hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total,
+                       const SlotBump &bump, hipStream_t s);
 constexpr uint64_t kScanCompactMaxGroups = 4096;
 // Small incremental jobs (tables in the kernel arguments, at most
 // kScanCompactMaxGroups groups): one single-workgroup launch reduces the
 // Merkle lists and scans the dirty masks (total also to the pinned host
 // word); up to kScanCompactFusedGroups groups it also assigns the slots,
-// otherwise the offsets go to `offsets` and launch_compact follows.
+// otherwise the offsets go to `offsets` and launch_place_dirty follows.
 constexpr uint64_t kScanCompactFusedGroups = 64;
 hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
                                     uint64_t *scratch_b, const ArgTables &tab, uint64_t ngroups,
-                                    const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
-                                    uint64_t *offsets, uint64_t *total, uint64_t *total_host, hipStream_t s);
+                                    const uint64_t *dirty_mask, const SlotBump &bump, uint64_t *list,
+                                    uint64_t *offsets, uint64_t *total, hipStream_t s);
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
 // Flips the lowest bit of the byte at device address addr.
 hipError_t launch_flip_bit(uint64_t addr, hipStream_t s);
-// Bank shrink: flags[i] = entry i is among the `keep` best-ranked (score
-// order of pcs_bank_shrink), offsets = exclusive scan of flags, kept = the
-// kept indices in increasing order.
-hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *flags, uint64_t *offsets,
-                                uint64_t *total, uint32_t *kept, hipStream_t s);
+// Bank shrink: kept = the indices of the `keep` best-ranked entries (score
+// order of pcs_bank_shrink), in increasing order; one single-workgroup
+// launch (radix select, then index-ordered scans).
+hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept, hipStream_t s);
 // dst entry j <- src entry kept[j] (entry j when kept is null), count entries
 // of entry_bytes bytes.
 hipError_t launch_gather_entries(uint64_t src, uint64_t dst, uint64_t entry_bytes, const uint32_t *kept,

@@ -422,6 +422,13 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     const bool hasher = t < 4 * CPW && ci < nv;
     const uint32_t len = hasher ? cloc[ci].len : 0;
     const uint32_t nst = len >> 5;
+    // Incremental checkpoint: where the parent holds this chunk, fetched now
+    // and entered in the new manifest at the end if the chunk is clean (a
+    // dirty chunk's entry is its slot, written once the slots are placed).
+    uint64_t parent_loc = 0;
+    if (MODE == kModeDiff && hasher && q == 0 && jb.manifest && c0 + ci < jb.parent_chunks)
+        parent_loc = jb.parent_manifest ? ((const g_u64 *)jb.parent_manifest)[c0 + ci]
+                                        : jb.parent_slot0 + (c0 + ci) * kChunk;
     // Accumulator q with seed 0: P1 + P2, P2, 0, -P1.
     uint64_t va = q == 0 ? P1 + P2 : q == 1 ? P2 : q == 2 ? 0 : 0 - P1;
     uint64_t tw0 = 0, tw1 = 0, tw2 = 0, tw3 = 0;  // the chunk's tail (< 32 bytes), zero padded
@@ -511,6 +518,7 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
             if (MODE == kModeDiff) {
                 const bool d = i >= jb.parent_chunks || ((const g_u64 *)jb.parent_hash)[i] != h;
                 dflag[ci] = d ? 1u : 0u;
+                if (!d && jb.manifest) ((g_u64 *)jb.manifest)[i] = parent_loc;
             }
             if (MODE == kModeVerify) dflag[ci] = ((const g_u64 *)jb.parent_hash)[i] != h ? 1u : 0u;
         }
@@ -744,13 +752,8 @@ __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
 
 // ---------------------------------------------------------------- incremental
 
-// Where a scan takes entry j's count from: a count array (keep flags of a
-// bank shrink), or the number of set bits of a 64-bit dirty mask (one per
-// 64-chunk group of an incremental checkpoint).
-struct CountArray {
-    const uint32_t *p;
-    __device__ uint64_t operator()(uint64_t j) const { return p[j]; }
-};
+// A scan's entry j: the number of set bits of the 64-bit dirty mask of
+// group j of an incremental checkpoint.
 struct MaskBits {
     const uint64_t *p;
     __device__ uint64_t operator()(uint64_t j) const { return (uint64_t)__popcll(p[j]); }
@@ -786,51 +789,54 @@ __device__ void scan_counts(const Count counts, uint64_t n, uint64_t *offsets, u
     __syncthreads();
 }
 
-// Exclusive scan of counts; the total also goes to the caller's pinned host
-// word when one is given.
-template <class Count>
-__global__ __launch_bounds__(1024) void k_scan(const Count counts, uint64_t n, uint64_t *__restrict__ offsets,
-                                               uint64_t *__restrict__ total, uint64_t *total_host)
+// Thread 1023 of a scan of dirty masks, once the stored-chunk count is
+// known: takes this call's payload top from the bump word (bump_now, loaded
+// when the kernel started; or sb.reset) and
+// lowers the bump word by the count's slots, then publishes the count and
+// the top to the host words.  Returns the top (0 when sb.bump is null: the
+// host sets the top itself once it has read the count).
+__device__ uint64_t place_slots(const SlotBump &sb, uint64_t count, uint64_t bump_now)
 {
-    __shared__ uint64_t sums[2][1024];
-    scan_counts(counts, n, offsets, total, sums);
-    if (threadIdx.x == 1023 && total_host) {
-        *(volatile uint64_t *)total_host = *total;
+    uint64_t top = 0;
+    if (sb.bump) {
+        top = sb.reset ? sb.reset : bump_now;
+        *sb.bump = top - count * kChunk;
+        *sb.top_out = top;
+    }
+    if (sb.host) {
+        ((volatile uint64_t *)sb.host)[0] = count;
+        ((volatile uint64_t *)sb.host)[1] = top;
         __threadfence_system();
     }
+    return top;
+}
+
+// Exclusive scan of counts (offsets and total); for the dirty masks of an
+// incremental checkpoint also the placement of its slots (place_slots).
+template <class Count>
+__global__ __launch_bounds__(1024) void k_scan(const Count counts, uint64_t n, uint64_t *__restrict__ offsets,
+                                               uint64_t *__restrict__ total, const SlotBump sb)
+{
+    __shared__ uint64_t sums[2][1024];
+    const uint64_t bump_now = threadIdx.x == 1023 && sb.bump && !sb.reset ? *sb.bump : 0;
+    scan_counts(counts, n, offsets, total, sums);
+    if (threadIdx.x == 1023) place_slots(sb, *total, bump_now);
 }
 
 // Slot assignment for one chunk: dirty chunks get slots in (buffer, chunk)
-// order and are listed; the new manifest points a dirty chunk at its slot
-// (slot s is the 4096 bytes ending s*4096 below the top of the snapshot's
-// payload reservation: slots grow downwards, so the unused part of the
-// reservation is its low end) and a clean one at wherever the parent holds it.
+// order and are listed, and the new manifest points a dirty chunk at its
+// slot (slot s is the 4096 bytes ending s*4096 below the call's payload top,
+// an arena offset: slots grow downwards).  A clean chunk's entry (where the
+// parent holds it) was written by the diff tiles.
 __device__ __forceinline__ void compact_chunk(const JobBuf &jb, uint32_t b, uint64_t i, uint32_t lane, uint64_t mask,
                                               uint64_t off, uint64_t payload_arena_top, uint64_t *list)
 {
-    g_u64 *man = (g_u64 *)jb.manifest;
     if ((mask >> lane) & 1) {
         const uint64_t below = lane ? (mask & ((1ULL << lane) - 1)) : 0;
         const uint64_t slot = off + (uint64_t)__popcll(below);
         list[slot] = ((uint64_t)b << 40) | i;
-        man[i] = payload_arena_top - (slot + 1) * kChunk;
-    } else {
-        man[i] = jb.parent_manifest ? ((const g_u64 *)jb.parent_manifest)[i] : jb.parent_slot0 + i * kChunk;
+        ((g_u64 *)jb.manifest)[i] = payload_arena_top - (slot + 1) * kChunk;
     }
-}
-
-template <class Tab>
-__global__ __launch_bounds__(64) void k_compact(const Tab tab, const uint64_t *__restrict__ dirty_mask,
-                                                const uint64_t *__restrict__ offsets, uint64_t payload_arena_top,
-                                                uint64_t *__restrict__ list)
-{
-    const uint64_t G = blockIdx.x;
-    const uint32_t b = buf_index(tab, G);
-    const JobBuf &jb = tab.bufs[b];
-    const uint32_t lane = threadIdx.x;
-    const uint64_t i = (G - jb.group_begin) * kGroupChunks + lane;
-    if (i >= jb.nchunks) return;
-    compact_chunk(jb, b, i, lane, dirty_mask[G], offsets[G], payload_arena_top, list);
 }
 
 // Small incremental jobs (tables in the kernel arguments), after the
@@ -841,56 +847,102 @@ __global__ __launch_bounds__(64) void k_compact(const Tab tab, const uint64_t *_
 // kScanCompactFusedGroups groups): the offsets stay in LDS and the slot
 // assignment follows here, one thread per chunk (a chunk's slot depends only
 // on its group's mask and offset); otherwise the offsets go to `offsets` for
-// k_compact.
+// k_place_dirty.
 template <bool kCompact>
 __global__ __launch_bounds__(1024) void k_merkle_scan_small(const ArgLists L, const uint64_t *__restrict__ nodes,
                                                             uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
                                                             const ArgTables tab, uint64_t ngroups,
                                                             const uint64_t *__restrict__ dirty_mask,
-                                                            uint64_t payload_arena_top, uint64_t *__restrict__ list,
+                                                            const SlotBump bump, uint64_t *__restrict__ list,
                                                             uint64_t *__restrict__ offsets,
-                                                            uint64_t *__restrict__ total, uint64_t *total_host)
+                                                            uint64_t *__restrict__ total)
 {
     __shared__ uint64_t lds[4096];
     __shared__ uint64_t lds2[64];
     __shared__ uint64_t roots[kArgBufs];
     __shared__ uint64_t sums[2][1024];
     __shared__ uint64_t offs[kCompact ? kScanCompactFusedGroups : 1];
+    __shared__ uint64_t top_sh;
+    const uint64_t bump_now = threadIdx.x == 1023 && bump.bump && !bump.reset ? *bump.bump : 0;
     merkle_lists<1024>(L, nodes, sa, sb, lds, lds2, roots);
+    if constexpr (kCompact) scan_counts(MaskBits{dirty_mask}, ngroups, offs, total, sums);
+    else scan_counts(MaskBits{dirty_mask}, ngroups, offsets, total, sums);
+    if (threadIdx.x == 1023) top_sh = place_slots(bump, *total, bump_now);
     if constexpr (kCompact) {
-        scan_counts(MaskBits{dirty_mask}, ngroups, offs, total, sums);
+        __syncthreads();
+        const uint64_t top = top_sh;
         for (uint64_t e = threadIdx.x; e < ngroups * kGroupChunks; e += 1024) {
             const uint64_t g = e / kGroupChunks;
             const uint32_t lane = (uint32_t)(e % kGroupChunks);
             const uint32_t b = buf_index(tab, g);
             const JobBuf &jb = tab.bufs[b];
             const uint64_t i = (g - jb.group_begin) * kGroupChunks + lane;
-            if (i < jb.nchunks) compact_chunk(jb, b, i, lane, dirty_mask[g], offs[g], payload_arena_top, list);
+            if (i < jb.nchunks) compact_chunk(jb, b, i, lane, dirty_mask[g], offs[g], top, list);
         }
-    } else {
-        scan_counts(MaskBits{dirty_mask}, ngroups, offsets, total, sums);
-    }
-    if (threadIdx.x == 1023 && total_host) {
-        *(volatile uint64_t *)total_host = *total;
-        __threadfence_system();
     }
 }
 
-// Copies listed dirty chunks into their slots (slot s ends s*4096 below
-// `payload_top`): one wavefront per slot, each lane moving 64 bytes with
-// four 16-byte loads in flight, zero-padding partial chunks.
+// Copies listed dirty chunks into their slots (slot s ends s*4096 below the
+// payload top, the arena offset in *top_word): one wavefront per slot, each
+// lane moving 64 bytes with four 16-byte loads in flight, zero-padding
+// partial chunks.
 template <class Tab>
 __global__ __launch_bounds__(256) void k_pack_dirty(const Tab tab, const uint64_t *__restrict__ list,
-                                                    const uint64_t *__restrict__ total_ptr, uint64_t payload_top)
+                                                    const uint64_t *__restrict__ total_ptr,
+                                                    const uint64_t *__restrict__ top_word, uint64_t arena_base)
 {
     const uint64_t slot = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (slot >= *total_ptr) return;
+    const uint64_t payload_top = arena_base + *top_word;
     const uint32_t lane = threadIdx.x & 63;
     const uint64_t e = list[slot];
     const JobBuf &jb = tab.bufs[e >> 40];
     const uint64_t cb = (e & ((1ULL << 40) - 1)) * kChunk;
     const uint64_t len = umin(kChunk, jb.nbytes - cb);
     const uint64_t dst = payload_top - (slot + 1) * kChunk;
+    uint4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t x = (k * 64 + lane) * 16;
+        v[k] = make_uint4(0, 0, 0, 0);
+        if (x < len) {
+            const uint64_t a = phys_addr(tab.runs, jb.run_begin, jb.run_count, cb + x);
+            v[k] = x + 16 <= len ? load16(a) : load_partial(a, (uint32_t)(len - x));
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) store16(dst + (k * 64 + lane) * 16, v[k]);
+}
+
+// Slot assignment and dirty copy in one launch (jobs above
+// kScanCompactFusedGroups groups, after the scan of the dirty masks): one
+// wavefront per chunk, four per 256-lane workgroup.  The wavefront of a
+// dirty chunk takes its slot (below the payload top in *top_word) from its
+// group's scanned offset and the set bits of the mask below it, as
+// compact_chunk; lane 0 enters the slot in the manifest and all 64 lanes
+// copy the chunk into it, 64 bytes per lane, zero-padding a partial chunk.
+// A clean chunk's wavefront does nothing (the diff tiles entered it).
+template <class Tab>
+__global__ __launch_bounds__(256) void k_place_dirty(const Tab tab, const uint64_t *__restrict__ dirty_mask,
+                                                     const uint64_t *__restrict__ offsets,
+                                                     const uint64_t *__restrict__ top_word, uint64_t arena_base)
+{
+    const uint32_t lane = threadIdx.x & 63;
+    const uint64_t gc = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // the job's 64 x (group) + chunk slot
+    const uint64_t G = gc / kGroupChunks;
+    const uint32_t c = (uint32_t)(gc % kGroupChunks);
+    const JobBuf &jb = tab.bufs[buf_index(tab, G)];
+    const uint64_t i = (G - jb.group_begin) * kGroupChunks + c;
+    if (i >= jb.nchunks) return;
+    const uint64_t mask = dirty_mask[G];
+    if (!((mask >> c) & 1)) return;  // clean: the diff tiles entered it in the manifest
+    g_u64 *man = (g_u64 *)jb.manifest;
+    const uint64_t slot = offsets[G] + (uint64_t)__popcll(c ? mask & ((1ULL << c) - 1) : 0);
+    const uint64_t top = *top_word;  // arena offset
+    if (lane == 0) man[i] = top - (slot + 1) * kChunk;
+    const uint64_t cb = i * kChunk;
+    const uint64_t len = umin(kChunk, jb.nbytes - cb);
+    const uint64_t dst = arena_base + top - (slot + 1) * kChunk;
     uint4 v[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -1009,50 +1061,118 @@ __device__ __forceinline__ uint32_t score_key(uint32_t bits)
     return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
 }
 
-// Entry i is kept iff fewer than `keep` entries rank before it (a smaller
-// key, or an equal key at a lower index).  A lane quad per entry counts over
-// all keys, staged through LDS in tiles that the quads read in the same
-// order (broadcast reads, four keys per read).  A tile is padded to a
-// multiple of four with the largest key at indices past the end, which
-// never rank before anything.
-__global__ __launch_bounds__(256) void k_shrink_rank(const uint32_t *__restrict__ scores, uint32_t n, uint32_t keep,
-                                                     uint32_t *__restrict__ flags)
+// Inclusive prefix sum across the 64 lanes of a wavefront.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
 {
-    __shared__ __attribute__((aligned(16))) uint32_t tile[2048];
-    // Lane `part` of the quad compares against every fourth group of four
-    // keys of each tile; the quad sums its partial counts by shuffles.
-    const uint32_t gt = blockIdx.x * 256 + threadIdx.x;
-    const uint32_t i = gt >> 2, part = gt & 3;
-    const uint32_t ki = i < n ? score_key(scores[i]) : 0;
-    auto before = [&](uint32_t kj, uint32_t j) -> uint32_t { return (kj < ki || (kj == ki && j < i)) ? 1u : 0u; };
-    uint32_t rank = 0;
-    for (uint32_t base = 0; base < n; base += 2048) {
-        const uint32_t m = n - base < 2048 ? n - base : 2048;
-        const uint32_t m4 = (m + 3) & ~3u;
-        for (uint32_t j = threadIdx.x; j < m4; j += 256) tile[j] = j < m ? score_key(scores[base + j]) : 0xFFFFFFFFu;
-        __syncthreads();
-        const uint4 *t4 = reinterpret_cast<const uint4 *>(tile);
-#pragma unroll 4
-        for (uint32_t q = part; q < m4 / 4; q += 4) {
-            const uint4 v = t4[q];
-            const uint32_t j = base + 4 * q;
-            rank += before(v.x, j) + before(v.y, j + 1) + before(v.z, j + 2) + before(v.w, j + 3);
-        }
-        __syncthreads();
+    const uint32_t lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = (uint32_t)__shfl_up((int)x, d, 64);
+        if (lane >= (uint32_t)d) x += y;
     }
-    rank += (uint32_t)__shfl_xor((int)rank, 1, 64);
-    rank += (uint32_t)__shfl_xor((int)rank, 2, 64);
-    if (part == 0 && i < n) flags[i] = rank < keep ? 1u : 0u;
+    return x;
 }
 
-// Kept entry i goes to position offsets[i] (exclusive scan of the flags), so
-// the kept list is in increasing index order.
-__global__ __launch_bounds__(256) void k_shrink_place(const uint32_t *__restrict__ flags,
-                                                      const uint64_t *__restrict__ offsets, uint32_t n,
-                                                      uint32_t *__restrict__ kept)
+// Exclusive prefix sum of one value per thread over the 1024 threads of a
+// workgroup: wavefront scans, then one scan of the 16 wavefront totals.
+// Ends with a barrier.
+__device__ uint32_t block_excl_scan(uint32_t v, uint32_t *wsum)
 {
-    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-    if (i < n && flags[i]) kept[offsets[i]] = i;
+    const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    const uint32_t incl = wave_incl_scan(v);
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    if (wave == 0) {
+        const uint32_t w = lane < 16 ? wsum[lane] : 0;
+        const uint32_t wi = wave_incl_scan(w);
+        if (lane < 16) wsum[16 + lane] = wi - w;  // exclusive prefix of wavefront `lane`
+    }
+    __syncthreads();
+    const uint32_t out = incl - v + wsum[16 + wave];
+    __syncthreads();
+    return out;
+}
+
+// Selection of a bank shrink in one workgroup of 1024 lanes, O(n): the
+// `keep` best-ranked entries (a smaller key, or an equal key at a lower
+// index, ranks first) in increasing index order.
+//   1. Radix select, most significant byte first: four passes histogram the
+//      candidates' next byte (LDS atomics) and narrow to the bucket that holds
+//      the keep-th smallest key (wavefront 0 finds it with a prefix sum over
+//      the 256 buckets), which ends as K*, with `need` = how many entries
+//      with key K* are kept (those with the lowest indices).
+//   2. Each lane takes a contiguous segment of indices and counts its keys
+//      below K* and equal to K*; a scan of the equal counts gives each
+//      segment the rank of its first K* key, hence how many entries the
+//      segment keeps; a scan of those gives where its kept indices go.
+//   3. Each lane writes its segment's kept indices, in order.
+__global__ __launch_bounds__(1024) void k_shrink_select(const uint32_t *__restrict__ scores, uint32_t n, uint32_t keep,
+                                                        uint32_t *__restrict__ kept)
+{
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t wsum[32];
+    __shared__ uint32_t pick[2];
+    const uint32_t t = threadIdx.x, lane = t & 63;
+    uint32_t prefix = 0, pmask = 0, need = keep;  // need: 1-based rank of K* among the candidates
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t shift = 24 - 8 * p;
+        if (t < 256) hist[t] = 0;
+        __syncthreads();
+        for (uint32_t i = t; i < n; i += 1024) {
+            const uint32_t k = score_key(scores[i]);
+            if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (t < 64) {
+            // Lane l holds buckets 4l..4l+3; the bucket where the running
+            // count first reaches `need` is the one.
+            const uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2],
+                           h3 = hist[4 * lane + 3];
+            const uint32_t sum = h0 + h1 + h2 + h3;
+            const uint32_t incl = wave_incl_scan(sum);
+            uint32_t cum = incl - sum;
+            if (cum < need && incl >= need) {
+                uint32_t d = 4 * lane;
+                if (cum + h0 < need) {
+                    cum += h0;
+                    ++d;
+                    if (cum + h1 < need) {
+                        cum += h1;
+                        ++d;
+                        if (cum + h2 < need) {
+                            cum += h2;
+                            ++d;
+                        }
+                    }
+                }
+                pick[0] = d;
+                pick[1] = need - cum;
+            }
+        }
+        __syncthreads();
+        prefix |= pick[0] << shift;
+        pmask |= 255u << shift;
+        need = pick[1];
+        __syncthreads();
+    }
+    const uint32_t per = (n + 1023) / 1024;
+    const uint32_t s0 = t * per < n ? t * per : n, s1 = s0 + per < n ? s0 + per : n;
+    uint32_t lt = 0, eq = 0;
+    for (uint32_t i = s0; i < s1; ++i) {
+        const uint32_t k = score_key(scores[i]);
+        lt += k < prefix;
+        eq += k == prefix;
+    }
+    const uint32_t eq_before = block_excl_scan(eq, wsum);
+    const uint32_t eq_kept = need > eq_before ? (need - eq_before < eq ? need - eq_before : eq) : 0;
+    uint32_t pos = block_excl_scan(lt + eq_kept, wsum);
+    uint32_t rank = eq_before;
+    for (uint32_t i = s0; i < s1; ++i) {
+        const uint32_t k = score_key(scores[i]);
+        bool take = k < prefix;
+        if (k == prefix) take = rank++ < need;
+        if (take) kept[pos++] = i;
+    }
 }
 
 // Moves kept entries of one bank part: destination entry j <- source entry
@@ -1173,22 +1293,22 @@ hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t are
 }
 
 template <class Tab>
-hipError_t launch_compact(const Tab &tab, uint64_t ngroups, const uint64_t *dirty_mask, const uint64_t *offsets,
-                          uint64_t payload_arena_top, uint64_t *list, hipStream_t s)
+hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_t *total, uint64_t max_slots,
+                             const uint64_t *top_word, uint64_t arena_base, hipStream_t s)
 {
-    if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_compact<Tab>), dim3((uint32_t)ngroups), dim3(64), 0, s, tab, dirty_mask, offsets,
-                       payload_arena_top, list);
+    if (max_slots == 0) return hipSuccess;
+    const uint32_t blocks = (uint32_t)((max_slots + 3) / 4);
+    hipLaunchKernelGGL((k_pack_dirty<Tab>), dim3(blocks), dim3(256), 0, s, tab, list, total, top_word, arena_base);
     return hipGetLastError();
 }
 
 template <class Tab>
-hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_t *total, uint64_t max_slots,
-                             uint64_t payload_top, hipStream_t s)
+hipError_t launch_place_dirty(const Tab &tab, uint64_t ngroups, const uint64_t *dirty_mask, const uint64_t *offsets,
+                              const uint64_t *top_word, uint64_t arena_base, hipStream_t s)
 {
-    if (max_slots == 0) return hipSuccess;
-    const uint32_t blocks = (uint32_t)((max_slots + 3) / 4);
-    hipLaunchKernelGGL((k_pack_dirty<Tab>), dim3(blocks), dim3(256), 0, s, tab, list, total, payload_top);
+    if (ngroups == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_place_dirty<Tab>), dim3((uint32_t)(ngroups * (kGroupChunks / 4))), dim3(256), 0, s, tab,
+                       dirty_mask, offsets, top_word, arena_base);
     return hipGetLastError();
 }
 
@@ -1236,40 +1356,34 @@ hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64
 }
 
 hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total,
-                       hipStream_t s, uint64_t *total_host)
+                       const SlotBump &bump, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_scan<MaskBits>, dim3(1), dim3(1024), 0, s, MaskBits{dirty_mask}, n, offsets, total,
-                       total_host);
+    hipLaunchKernelGGL(k_scan<MaskBits>, dim3(1), dim3(1024), 0, s, MaskBits{dirty_mask}, n, offsets, total, bump);
     return hipGetLastError();
 }
 
 hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
                                     uint64_t *scratch_b, const ArgTables &tab, uint64_t ngroups,
-                                    const uint64_t *dirty_mask, uint64_t payload_arena_top, uint64_t *list,
-                                    uint64_t *offsets, uint64_t *total, uint64_t *total_host, hipStream_t s)
+                                    const uint64_t *dirty_mask, const SlotBump &bump, uint64_t *list,
+                                    uint64_t *offsets, uint64_t *total, hipStream_t s)
 {
     if (ngroups > kScanCompactMaxGroups) return hipErrorInvalidValue;
+    if (ngroups && ngroups <= kScanCompactFusedGroups && !bump.bump) return hipErrorInvalidValue;  // slots need a top
     if (ngroups <= kScanCompactFusedGroups)
         hipLaunchKernelGGL(k_merkle_scan_small<true>, dim3(1), dim3(1024), 0, s, lists, nodes, scratch_a, scratch_b,
-                           tab, ngroups, dirty_mask, payload_arena_top, list, offsets, total, total_host);
+                           tab, ngroups, dirty_mask, bump, list, offsets, total);
     else
         hipLaunchKernelGGL(k_merkle_scan_small<false>, dim3(1), dim3(1024), 0, s, lists, nodes, scratch_a, scratch_b,
-                           tab, ngroups, dirty_mask, payload_arena_top, list, offsets, total, total_host);
+                           tab, ngroups, dirty_mask, bump, list, offsets, total);
     return hipGetLastError();
 }
 
-hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *flags, uint64_t *offsets,
-                                uint64_t *total, uint32_t *kept, hipStream_t s)
+hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept, hipStream_t s)
 {
-    if (n == 0) return hipSuccess;
-    const uint32_t blocks = (n + 255) / 256;
-    hipLaunchKernelGGL(k_shrink_rank, dim3((n + 63) / 64), dim3(256), 0, s, reinterpret_cast<const uint32_t *>(scores),
-                       n, keep, flags);
-    if (hipError_t e = hipGetLastError()) return e;
-    hipLaunchKernelGGL(k_scan<CountArray>, dim3(1), dim3(1024), 0, s, CountArray{flags}, (uint64_t)n, offsets,
-                       total, nullptr);
-    if (hipError_t e = hipGetLastError()) return e;
-    hipLaunchKernelGGL(k_shrink_place, dim3(blocks), dim3(256), 0, s, flags, offsets, n, kept);
+    if (n == 0 || keep == 0) return hipSuccess;
+    if (keep > n) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_shrink_select, dim3(1), dim3(1024), 0, s, reinterpret_cast<const uint32_t *>(scores), n, keep,
+                       kept);
     return hipGetLastError();
 }
 
@@ -1308,10 +1422,10 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
     template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint64_t *, uint64_t, hipStream_t, \
                                          uint32_t);                                                               \
     template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t);                     \
-    template hipError_t launch_compact<Tab>(const Tab &, uint64_t, const uint64_t *, const uint64_t *, uint64_t,   \
-                                            uint64_t *, hipStream_t);                                             \
     template hipError_t launch_pack_dirty<Tab>(const Tab &, const uint64_t *, const uint64_t *, uint64_t,         \
-                                               uint64_t, hipStream_t);                                            \
+                                               const uint64_t *, uint64_t, hipStream_t);                          \
+    template hipError_t launch_place_dirty<Tab>(const Tab &, uint64_t, const uint64_t *, const uint64_t *,        \
+                                                const uint64_t *, uint64_t, hipStream_t);                         \
     template hipError_t launch_classify<Tab>(const Tab &, uint64_t, const uint64_t *, uint32_t, uint64_t,         \
                                              uint64_t *, hipStream_t);                                            \
     template hipError_t launch_labels<Tab>(const Tab &, const uint64_t *, uint8_t *, hipStream_t);

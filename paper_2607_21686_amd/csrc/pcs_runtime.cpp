@@ -10,6 +10,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -28,7 +29,10 @@ namespace {
 
 constexpr uint64_t kMaxGroups = (1ULL << 32) / 256 - 1;  // grid limit of the 256-lane kernels
 constexpr uint32_t kStagingSlots = 8;
-constexpr uint32_t kCountSlots = 4096;
+constexpr uint32_t kCountPairs = 2048;  // host word pairs (stored-chunk count, payload top), pair 0 for exact calls
+// A new segment for incremental payloads takes this share of the largest
+// free block (at least the call's worst case).
+constexpr uint64_t kSegmentShareNum = 1, kSegmentShareDen = 2;
 // Limits of pcs_fingerprint_noalloc: its descriptor tables pass through one
 // pinned host buffer of kNoAllocStagingBytes made at context creation.
 constexpr uint32_t kNoAllocMaxBufs = 4096, kNoAllocMaxRuns = 65536;
@@ -36,6 +40,34 @@ constexpr uint64_t kNoAllocStagingBytes = 2ULL << 20;
 constexpr int kMaxDevices = 64;
 
 struct SnapNode;
+
+// A block of the arena whose incremental payload slots the device places
+// downwards from `hi` (a bump word the scan kernels advance in stream
+// order), so the payloads of consecutive calls lie next to each other.  The
+// host claims each pending call's worst case (one slot per chunk) against it
+// and, once the call's stored-chunk count is read, only its actual slots.
+// The unused low part [lo, fill) goes back to the arena as soon as no call
+// placed here is pending; the segment is then closed.
+struct Segment {
+    uint64_t lo = 0, hi = 0;
+    uint64_t claim = 0;    // bytes below hi: settled calls' slots + pending calls' worst cases
+    uint64_t fill = 0;     // lowest slot placed by a settled call (hi before any)
+    uint32_t pending = 0;  // calls placed here whose count is not read yet
+    bool started = false;  // a call has set the bump word to hi
+    bool open = true;      // new calls may use it
+    bool retired = false;  // its unused part went back to the arena
+};
+
+// An incremental checkpoint enqueued on the stream whose stored-chunk count
+// the host has not read yet.  It outlives its snapshot if that is deleted
+// first (then the slots are released when the count arrives).
+struct PendingCall {
+    std::weak_ptr<SnapNode> node;
+    std::shared_ptr<Segment> seg;
+    uint64_t worst = 0;      // bytes claimed in the segment until settled
+    uint32_t pair = 0;       // host words 2*pair (count) and 2*pair+1 (top)
+    hipEvent_t ev = nullptr; // recorded after the call's last kernel
+};
 
 }  // namespace
 }  // namespace pcs
@@ -56,10 +88,16 @@ struct pcs_ctx {
     } staging[pcs::kStagingSlots];
     uint32_t next_slot = 0;
 
-    uint64_t *counts = nullptr;              // pinned, one per pending incremental snapshot
+    uint64_t *counts = nullptr;              // pinned word pairs, one per pending incremental checkpoint
     uint64_t *counts_dev = nullptr;          // the same words as the device addresses them
-    std::vector<uint32_t> free_counts;
-    std::vector<std::weak_ptr<pcs::SnapNode>> pending;
+    std::vector<uint32_t> free_pairs;
+    std::deque<pcs::PendingCall> pending;    // in stream order
+    std::shared_ptr<pcs::Segment> seg;       // the open segment, if any
+    hipEvent_t exact_ev = nullptr;           // an exact-size incremental call waits on it
+
+    // The arena's first unit, kept by the library: word 0 is the bump word of
+    // incremental slot placement, word 1 a call's payload top.
+    uint64_t bump_dev = 0, top_dev = 0;
 
     bool timing = false;
     bool no_events = false;  // set while a call that must create nothing runs (no timing events)
@@ -87,19 +125,16 @@ struct SnapNode {
     uint64_t total_chunks = 0, state_bytes = 0;
     uint64_t hashes_off = 0, manifest_off = 0, roots_off = 0, payload_off = 0;  // arena offsets
     uint64_t payload_bytes = 0;         // stored bytes (incremental: after settling)
-    uint64_t pay_off = 0, pay_bytes = 0;  // incremental: payload block (slots grow down from its top)
-    uint64_t pay_top = 0;               // incremental: arena offset of the top of the payload block
-    bool settled = true;
-    int count_slot = -1;
-    hipEvent_t ev = nullptr;
+    uint64_t pay_off = 0, pay_bytes = 0;  // incremental: its slots (known once settled)
+    uint64_t pay_top = 0;               // incremental: arena offset of the top of its slots
+    bool settled = true;                // incremental: stored-chunk count read
     std::shared_ptr<SnapNode> parent;   // chunks this snapshot's manifest points into
 
     ~SnapNode()
     {
-        if (ev) (void)hipEventDestroy(ev);
-        if (count_slot >= 0) ctx->free_counts.push_back((uint32_t)count_slot);
         if (block_bytes) ctx->arena.release(block_off, block_bytes);
-        if (pay_bytes) ctx->arena.release(pay_off, pay_bytes);
+        // An unsettled snapshot's slots are released by its pending call.
+        if (settled && pay_bytes) ctx->arena.release(pay_off, pay_bytes);
     }
 };
 
@@ -257,56 +292,74 @@ int launch(pcs_ctx *c, const char *name, F &&f)
     return PCS_OK;
 }
 
-// Incremental snapshots reserve worst-case payload space; once the stream
-// has produced the stored-chunk count, the unused tail goes back to the arena.
-void settle(pcs_ctx *c, bool wait)
+// Retires a segment no pending call uses any more: its unused low part goes
+// back to the arena, and it takes no new calls.
+void retire_if_idle(pcs_ctx *c, const std::shared_ptr<Segment> &g)
 {
-    std::vector<std::weak_ptr<SnapNode>> keep;
-    for (auto &w : c->pending) {
-        auto n = w.lock();
-        if (!n || n->settled) continue;
-        hipError_t q = wait ? hipEventSynchronize(n->ev) : hipEventQuery(n->ev);
-        if (q != hipSuccess) {
-            keep.push_back(w);
-            continue;
-        }
-        const uint64_t dirty = c->counts[n->count_slot];
-        c->free_counts.push_back((uint32_t)n->count_slot);
-        n->count_slot = -1;
-        n->payload_bytes = dirty * kChunk;
-        n->payload_off = n->pay_top - n->payload_bytes;
-        if (n->payload_bytes < n->pay_bytes) {
-            const uint64_t give = n->pay_bytes - n->payload_bytes;  // the low, unused end
-            c->arena.release(n->pay_off, give);
-            n->pay_off += give;
-            n->pay_bytes -= give;
-        }
-        n->settled = true;
-    }
-    c->pending.swap(keep);
+    if (g->pending || g->retired) return;
+    if (g->fill > g->lo) c->arena.release(g->lo, g->fill - g->lo);
+    g->retired = true;
+    g->open = false;
+    if (c->seg == g) c->seg.reset();
 }
 
-// Waits for the oldest incremental snapshot still pending (the stream
-// finishes them in order), then settles it and every other one that has
-// finished.  False if none is pending, or if the oldest one could not be
-// settled (a failed wait), so that callers never retry without progress.
+// Reads a finished call's stored-chunk count and payload top: the snapshot
+// learns where its slots are, the segment's claim drops to the actual slots.
+void finish_call(pcs_ctx *c, PendingCall &p)
+{
+    const uint64_t dirty = c->counts[2 * p.pair], top = c->counts[2 * p.pair + 1];
+    const uint64_t bytes = dirty * kChunk;
+    c->free_pairs.push_back(p.pair);
+    (void)hipEventDestroy(p.ev);
+    p.ev = nullptr;
+    Segment &g = *p.seg;
+    g.claim = g.claim - p.worst + bytes;
+    g.fill = top - bytes;
+    --g.pending;
+    if (auto n = p.node.lock()) {
+        n->pay_off = n->payload_off = top - bytes;
+        n->pay_bytes = n->payload_bytes = bytes;
+        n->pay_top = top;
+        n->settled = true;
+    } else if (bytes) {
+        c->arena.release(top - bytes, bytes);  // deleted before its count arrived
+    }
+    retire_if_idle(c, p.seg);
+}
+
+// Settles pending calls in stream order: those already finished, or (wait)
+// every one, waiting for each.  Stops at the first that has not finished or
+// whose wait failed.
+void settle(pcs_ctx *c, bool wait)
+{
+    while (!c->pending.empty()) {
+        PendingCall &p = c->pending.front();
+        const hipError_t q = wait ? hipEventSynchronize(p.ev) : hipEventQuery(p.ev);
+        if (q != hipSuccess) return;
+        finish_call(c, p);
+        c->pending.pop_front();
+    }
+}
+
+// Waits for the oldest pending call and settles it (and every other one
+// that has finished).  False if none is pending or the wait failed, so that
+// callers never retry without progress.
 bool settle_oldest(pcs_ctx *c)
 {
-    for (auto &w : c->pending) {
-        auto n = w.lock();
-        if (!n || n->settled) continue;
-        (void)hipEventSynchronize(n->ev);
-        settle(c, false);
-        return n->settled;
-    }
-    c->pending.clear();
-    return false;
+    if (c->pending.empty()) return false;
+    PendingCall &p = c->pending.front();
+    if (hipEventSynchronize(p.ev) != hipSuccess) return false;
+    finish_call(c, p);
+    c->pending.pop_front();
+    settle(c, false);
+    return true;
 }
 
 // Allocates a snapshot block (from the bottom, or the top of the arena),
-// first settling finished incremental snapshots, then waiting for pending
+// first settling finished incremental checkpoints, then waiting for pending
 // ones oldest first until the block fits: the wait ends as soon as enough
-// reserved payload space has been trimmed, not when the stream is idle.
+// space has come back (a segment closes when its last pending call is
+// settled), not when the stream is idle.
 bool alloc_settled(pcs_ctx *c, uint64_t bytes, uint64_t *off, bool top)
 {
     auto try_alloc = [&] { return top ? c->arena.alloc_top(bytes, off) : c->arena.alloc(bytes, off); };
@@ -315,6 +368,38 @@ bool alloc_settled(pcs_ctx *c, uint64_t bytes, uint64_t *off, bool top)
     while (settle_oldest(c))
         if (try_alloc()) return true;
     return false;
+}
+
+// The segment an incremental call of worst case `worst` bytes is placed in:
+// the open one if its unclaimed part holds the worst case, else a new one of
+// max(worst, half the largest free block) from the top of the arena (the old
+// one then closes once its pending calls settle), waiting for pending calls
+// oldest first while neither fits.  Null if nothing fits with no call
+// pending: the call then takes the exact path.
+std::shared_ptr<Segment> segment_for(pcs_ctx *c, uint64_t worst)
+{
+    settle(c, false);
+    for (;;) {
+        const auto &g = c->seg;
+        if (g && g->open && worst <= g->hi - g->lo - g->claim) return g;
+        const uint64_t share = c->arena.largest() / kSegmentShareDen * kSegmentShareNum / kAlign * kAlign;
+        const uint64_t size = std::max(worst, share);
+        uint64_t off = 0;
+        if (c->arena.largest() >= size && c->arena.alloc_top(size, &off)) {
+            auto ng = std::make_shared<Segment>();
+            ng->lo = off;
+            ng->hi = ng->fill = off + round_up(size, kAlign);
+            if (c->seg) {
+                auto old = c->seg;
+                old->open = false;
+                c->seg.reset();
+                retire_if_idle(c, old);  // now, or when its last pending call settles
+            }
+            c->seg = ng;
+            return ng;
+        }
+        if (!settle_oldest(c)) return nullptr;
+    }
 }
 
 bool alloc_block(pcs_ctx *c, uint64_t bytes, uint64_t *off) { return alloc_settled(c, bytes, off, false); }
@@ -744,7 +829,7 @@ int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ct
     if (!d_arena || (uint64_t)d_arena % 16) return PCS_E_INVAL;
     const uint64_t a = (uint64_t)d_arena;
     const uint64_t aligned = round_up(a, kAlign);
-    if (arena_bytes < aligned - a + kAlign) return PCS_E_INVAL;
+    if (arena_bytes < aligned - a + 2 * kAlign) return PCS_E_INVAL;  // one unit is the library's own
     auto *c = new pcs_ctx();
     c->arena_dev = aligned;
     c->arena.init((arena_bytes - (aligned - a)) / kAlign * kAlign);
@@ -755,12 +840,21 @@ int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ct
             return PCS_E_HIP;
         }
     }
-    if (hipHostMalloc((void **)&c->counts, 8 * kCountSlots, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
-        hipHostGetDevicePointer((void **)&c->counts_dev, c->counts, 0) != hipSuccess) {
+    if (hipHostMalloc((void **)&c->counts, 16 * kCountPairs, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
+        hipHostGetDevicePointer((void **)&c->counts_dev, c->counts, 0) != hipSuccess ||
+        hipEventCreateWithFlags(&c->exact_ev, hipEventDisableTiming) != hipSuccess) {
         pcs_ctx_destroy(c);
         return PCS_E_HIP;
     }
-    for (uint32_t i = 0; i < kCountSlots; ++i) c->free_counts.push_back(kCountSlots - 1 - i);
+    for (uint32_t i = kCountPairs - 1; i >= 1; --i) c->free_pairs.push_back(i);  // pair 0: exact calls
+    // The library's own unit: the first of the arena.
+    uint64_t own = 0;
+    if (!c->arena.alloc(kAlign, &own)) {
+        pcs_ctx_destroy(c);
+        return PCS_E_INVAL;
+    }
+    c->bump_dev = c->arena_dev + own;
+    c->top_dev = c->bump_dev + 8;
     if (hipHostMalloc(&c->na_host, kNoAllocStagingBytes, hipHostMallocDefault) != hipSuccess ||
         hipEventCreateWithFlags(&c->na_ev, hipEventDisableTiming) != hipSuccess ||
         scratch_for(d_arena, &c->scratch_dev) != hipSuccess) {
@@ -776,7 +870,11 @@ int pcs_ctx_destroy(pcs_ctx *c)
     if (!c) return PCS_E_INVAL;
     (void)hipStreamSynchronize(c->stream);
     c->handles.clear();
+    for (auto &p : c->pending)
+        if (p.ev) (void)hipEventDestroy(p.ev);
     c->pending.clear();
+    c->seg.reset();
+    if (c->exact_ev) (void)hipEventDestroy(c->exact_ev);
     for (auto &kv : c->timers)
         for (auto &ab : kv.second) {
             (void)hipEventDestroy(ab.first);
@@ -1013,7 +1111,8 @@ int pcs_distance(pcs_ctx *c, const pcs_buf *bufs, uint32_t n, const uint64_t *d_
             return launch(c, "hash", [&] { return launch_tile(tab, G, kModeDiff, nullptr, d_mask, 0, s, tiles); });
         });
         if (st) return st;
-        if ((st = launch(c, "classify", [&] { return launch_scan(d_mask, G, d_offs, d_total, s); }))) return st;
+        if ((st = launch(c, "classify", [&] { return launch_scan(d_mask, G, d_offs, d_total, SlotBump{}, s); })))
+            return st;
         HIP_TRY(c, hipMemcpyAsync(&differing, d_total, 8, hipMemcpyDeviceToHost, s));
         HIP_TRY(c, hipStreamSynchronize(s));
     }
@@ -1028,8 +1127,8 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
     if (!c) return PCS_E_INVAL;
     if (nparts > 64) return fail(c, PCS_E_INVAL, "at most 64 bank parts");
     if (nparts && !parts) return fail(c, PCS_E_INVAL, "null parts");
-    if (n_entries > 65536) return fail(c, PCS_E_INVAL, "at most 65536 bank entries (%llu given)",
-                                       (unsigned long long)n_entries);
+    if (n_entries > UINT32_MAX) return fail(c, PCS_E_INVAL, "at most 2^32 - 1 bank entries (%llu given)",
+                                            (unsigned long long)n_entries);
     if (keep > n_entries)
         return fail(c, PCS_E_INVAL, "keep %llu exceeds %llu entries", (unsigned long long)keep,
                     (unsigned long long)n_entries);
@@ -1049,24 +1148,22 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
         else if (db && q.dst < q.src + sb && q.src < q.dst + db)
             return fail(c, PCS_E_INVAL, "part %u: destination overlaps the source bank", p);
     }
-    if (n_entries == 0) return PCS_OK;
+    if (n_entries == 0 || keep == 0) return PCS_OK;
     Temp t(c);
     Carver cv;
-    uint64_t o_flags, o_offs, o_total, o_kept, o_stage;
-    cv.add(&o_flags, 4 * n_entries);
-    cv.add(&o_offs, 8 * n_entries);
-    cv.add(&o_total, 8);
-    cv.add(&o_kept, 4 * n_entries);
-    cv.add(&o_stage, stage_bytes);
-    if (int e = temp_alloc(c, t, cv.total)) return e;
-    const uint64_t base = c->arena_dev + t.off;
+    uint64_t o_kept = 0, o_stage = 0;
+    if (!d_kept) cv.add(&o_kept, 4 * keep);
+    if (stage_bytes) cv.add(&o_stage, stage_bytes);
+    uint64_t base = 0;
+    if (cv.total) {
+        if (int e = temp_alloc(c, t, cv.total)) return e;
+        base = c->arena_dev + t.off;
+    }
     uint32_t *kept = d_kept ? d_kept : (uint32_t *)(base + o_kept);
     if (int st = launch(c, "shrink", [&] {
-            return launch_shrink_select(d_scores, (uint32_t)n_entries, (uint32_t)keep, (uint32_t *)(base + o_flags),
-                                        (uint64_t *)(base + o_offs), (uint64_t *)(base + o_total), kept, c->stream);
+            return launch_shrink_select(d_scores, (uint32_t)n_entries, (uint32_t)keep, kept, c->stream);
         }))
         return st;
-    if (keep == 0) return PCS_OK;
     for (uint32_t p = 0; p < nparts; ++p) {
         const pcs_bank_part &q = parts[p];
         if (q.dst != q.src) {
@@ -1111,28 +1208,24 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     if (int st = add_buffers(c, job, plan, n, 0)) return st;
     const uint64_t T = job.nchunks, G = job.ngroups;
 
-    // Metadata block [hashes 8T][manifest 8T][roots 8(n+1)] from the bottom;
-    // payload reservation (one slot per chunk, trimmed once the stored count
-    // is known) from the top.
+    // Metadata block [hashes 8T][manifest 8T][roots 8(n+1)] from the bottom.
+    // The stored chunks go to slots the device places in a segment (see
+    // Segment): the host claims the worst case (one slot per chunk) until the
+    // stream has produced the count.  When no segment can hold the worst case
+    // even after every pending call has settled, the call takes the exact
+    // path: it waits for its own count, then allocates exactly that many slots.
     const uint64_t hashes_rel = 0, manifest_rel = 8 * T, roots_rel = 16 * T;
     const uint64_t meta = roots_rel + 8 * (n + 1);
-    if (c->free_counts.empty()) settle(c, true);
-    if (c->free_counts.empty()) return fail(c, PCS_E_NOMEM, "too many incremental snapshots in flight");
-    uint64_t boff, poff = 0;
+    if (c->free_pairs.empty()) settle(c, true);
+    if (c->free_pairs.empty()) return fail(c, PCS_E_NOMEM, "too many incremental snapshots in flight");
+    uint64_t boff;
     if (!alloc_block(c, meta, &boff))
         return fail(c, PCS_E_NOMEM, "arena cannot hold incremental snapshot metadata (%llu bytes)",
                     (unsigned long long)meta);
-    // Pipelined path: reserve one slot per chunk now and trim later.  When
-    // that does not fit (even after every pending trim), take the exact path:
-    // wait for the stored-chunk count, then allocate exactly that many slots.
-    const bool exact = T && !alloc_block_top(c, T * kChunk, &poff);
     auto node = std::make_shared<SnapNode>();
     node->ctx = c;
     node->block_off = boff;
     node->block_bytes = meta;
-    node->pay_off = poff;
-    node->pay_bytes = exact ? 0 : T * kChunk;
-    node->pay_top = poff + node->pay_bytes;
     node->nbufs = n;
     node->incremental = true;
     node->has_hashes = true;
@@ -1145,10 +1238,10 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     node->hashes_off = boff + hashes_rel;
     node->manifest_off = boff + manifest_rel;
     node->roots_off = boff + roots_rel;
-    node->payload_off = node->pay_top;
     node->parent = par;
-    if (hipEventCreateWithFlags(&node->ev, hipEventDisableTiming) != hipSuccess)
-        return fail(c, PCS_E_HIP, "hipEventCreate failed");
+    const uint64_t worst = T * kChunk;
+    std::shared_ptr<Segment> seg = T ? segment_for(c, worst) : nullptr;
+    const bool exact = T && !seg;
 
     // A small job fingerprints and diffs as sub-tiles; the Merkle lists then
     // reduce one node per sub-tile (an aligned 8-chunk subtree).
@@ -1172,11 +1265,44 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     }
     lists.push_back({0, n, {c->arena_dev + node->roots_off + 8 * n, (uint64_t)d_sroot}});
 
-    // A small job (tables in kernel arguments) that took the pipelined
-    // reservation runs as: fingerprint+diff, then one single-workgroup launch
-    // for the Merkle lists and the scan (+ the slot assignment up to 64
-    // groups; it also writes the stored-chunk count to pinned host memory),
-    // the slot assignment above 64 groups, the dirty copy.
+    // Where the scan places the slots: in the segment (pipelined), nowhere
+    // (exact: the host places them once it has read the count from pair 0),
+    // or no slots at all (no chunks).
+    uint32_t pair = 0;
+    SlotBump bump{nullptr, 0, nullptr, nullptr};
+    if (seg) {
+        pair = c->free_pairs.back();
+        c->free_pairs.pop_back();
+        bump = SlotBump{(uint64_t *)c->bump_dev, seg->started ? 0 : seg->hi, (uint64_t *)c->top_dev,
+                        &c->counts_dev[2 * pair]};
+        seg->started = true;
+        seg->claim += worst;
+        ++seg->pending;
+    } else if (exact) {
+        bump.host = &c->counts_dev[0];
+    }
+    // On an error before the call is recorded as pending, its claim goes back.
+    bool recorded = !seg;
+    struct Undo {
+        pcs_ctx *c;
+        std::shared_ptr<Segment> &seg;
+        uint64_t worst;
+        uint32_t pair;
+        bool &recorded;
+        ~Undo()
+        {
+            if (recorded) return;
+            seg->claim -= worst;
+            --seg->pending;
+            c->free_pairs.push_back(pair);
+            retire_if_idle(c, seg);
+        }
+    } undo{c, seg, worst, pair, recorded};
+
+    // A small job (tables in kernel arguments) on the pipelined path runs as:
+    // fingerprint+diff, then one single-workgroup launch for the Merkle lists,
+    // the scan and the slot placement (+ the slot assignment up to 64 groups),
+    // then the dirty copy (with the slot assignment above 64 groups).
     const bool small = is_small(job) && !exact && G <= kScanCompactMaxGroups;
     Carver cv;
     uint64_t o_nodes, o_sa, o_sb, o_roots, o_mask, o_offs, o_total, o_list;
@@ -1187,7 +1313,7 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     cv.add(&o_mask, 8 * G);
     cv.add(&o_offs, 8 * G);
     cv.add(&o_total, 8);
-    cv.add(&o_list, 8 * T);
+    cv.add(&o_list, small && G <= kScanCompactFusedGroups ? 8 * T : 8);
     Temp t(c);
     Staged sg;
     uint64_t lists_dev, scr;
@@ -1198,8 +1324,8 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     uint64_t *d_roots_tmp = (uint64_t *)(scr + o_roots);
     uint64_t *d_mask = (uint64_t *)(scr + o_mask), *d_offs = (uint64_t *)(scr + o_offs);
     uint64_t *d_total = (uint64_t *)(scr + o_total), *d_list = (uint64_t *)(scr + o_list);
+    const uint64_t *top_word = (const uint64_t *)c->top_dev;
     hipStream_t s = c->stream;
-    uint64_t payload_top_dev = c->arena_dev + node->pay_top;
     int st = with_tables(sg, [&](const auto &tab) {
         return launch(c, "incremental", [&] {
             return launch_tile(tab, G, kModeDiff, d_nodes, d_mask, 0, s, tiles);
@@ -1207,66 +1333,62 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     });
     if (st) return st;
     if (small) {
-        node->count_slot = (int)c->free_counts.back();
-        c->free_counts.pop_back();
-        uint64_t *host_word = &c->counts_dev[node->count_slot];
-        const uint64_t top = node->pay_top;
         const ArgLists al = arg_lists(lists, n);
         if ((st = launch(c, "incremental", [&] {
-                 return launch_merkle_scan_small(al, d_nodes, d_sa, d_sb, sg.arg, G, d_mask, top, d_list, d_offs,
-                                                 d_total, host_word, s);
+                 return launch_merkle_scan_small(al, d_nodes, d_sa, d_sb, sg.arg, G, d_mask, bump, d_list, d_offs,
+                                                 d_total, s);
              })))
             return st;
-        if (G > kScanCompactFusedGroups &&
-            (st = launch(c, "incremental", [&] { return launch_compact(sg.arg, G, d_mask, d_offs, top, d_list, s); })))
+        if (G > kScanCompactFusedGroups)
+            st = launch(c, "incremental", [&] {
+                return launch_place_dirty(sg.arg, G, d_mask, d_offs, top_word, c->arena_dev, s);
+            });
+        else
+            st = launch(c, "incremental", [&] {
+                return launch_pack_dirty(sg.arg, d_list, d_total, T, top_word, c->arena_dev, s);
+            });
+        if (st) return st;
+    } else {
+        if ((st = run_merkle(c, small, lists, n, lists_dev, d_nodes, d_sa, d_sb, d_roots_tmp))) return st;
+        if ((st = launch(c, "incremental", [&] { return launch_scan(d_mask, G, d_offs, d_total, bump, s); })))
             return st;
-        if ((st = launch(c, "incremental", [&] {
-                 return launch_pack_dirty(sg.arg, d_list, d_total, T, payload_top_dev, s);
-             })))
-            return st;
-        HIP_TRY(c, hipEventRecord(node->ev, s));
-        node->settled = false;
-        c->pending.push_back(node);
-        *out = new_handle(c, node);
-        return PCS_OK;
-    }
-    if ((st = run_merkle(c, small, lists, n, lists_dev, d_nodes, d_sa, d_sb, d_roots_tmp))) return st;
-    if ((st = launch(c, "incremental", [&] { return launch_scan(d_mask, G, d_offs, d_total, s); }))) return st;
-    if (exact) {
-        HIP_TRY(c, hipMemcpyAsync(&c->counts[c->free_counts.back()], d_total, 8, hipMemcpyDeviceToHost, s));
-        HIP_TRY(c, hipEventRecord(node->ev, s));
-        HIP_TRY(c, hipEventSynchronize(node->ev));
-        const uint64_t dirty = c->counts[c->free_counts.back()];
-        if (dirty && !alloc_block_top(c, dirty * kChunk, &poff))
-            return fail(c, PCS_E_NOMEM, "arena cannot hold %llu stored chunks of an incremental snapshot "
-                        "(its fingerprint outputs were written)", (unsigned long long)dirty);
-        node->pay_off = poff;
-        node->pay_bytes = dirty * kChunk;
-        node->pay_top = poff + node->pay_bytes;
-        node->payload_bytes = node->pay_bytes;
-        node->payload_off = poff;
-        payload_top_dev = c->arena_dev + node->pay_top;
-    }
-    st = with_tables(sg, [&](const auto &tab) {
-        if (int e = launch(c, "incremental", [&] {
-                return launch_compact(tab, G, d_mask, d_offs, node->pay_top, d_list, s);
-            }))
-            return e;
-        return launch(c, "incremental", [&] {
-            return launch_pack_dirty(tab, d_list, d_total, T, payload_top_dev, s);
+        if (exact) {
+            HIP_TRY(c, hipEventRecord(c->exact_ev, s));
+            HIP_TRY(c, hipEventSynchronize(c->exact_ev));
+            const uint64_t dirty = c->counts[0];
+            uint64_t poff = 0;
+            if (dirty && !alloc_block_top(c, dirty * kChunk, &poff))
+                return fail(c, PCS_E_NOMEM, "arena cannot hold %llu stored chunks of an incremental snapshot "
+                            "(its fingerprint outputs were written)", (unsigned long long)dirty);
+            node->pay_off = node->payload_off = poff;
+            node->pay_bytes = node->payload_bytes = dirty * kChunk;
+            node->pay_top = poff + dirty * kChunk;
+            c->counts[1] = node->pay_top;
+            HIP_TRY(c, hipMemcpyAsync((void *)c->top_dev, &c->counts[1], 8, hipMemcpyHostToDevice, s));
+        }
+        st = with_tables(sg, [&](const auto &tab) {
+            return launch(c, "incremental", [&] {
+                return launch_place_dirty(tab, G, d_mask, d_offs, top_word, c->arena_dev, s);
+            });
         });
-    });
-    if (st) return st;
-    if (exact) {
-        *out = new_handle(c, node);
-        return PCS_OK;
+        if (st) return st;
     }
-    node->count_slot = (int)c->free_counts.back();
-    c->free_counts.pop_back();
-    HIP_TRY(c, hipMemcpyAsync(&c->counts[node->count_slot], d_total, 8, hipMemcpyDeviceToHost, s));
-    HIP_TRY(c, hipEventRecord(node->ev, s));
-    node->settled = false;
-    c->pending.push_back(node);
+    if (seg) {
+        PendingCall pc;
+        pc.node = node;
+        pc.seg = seg;
+        pc.worst = worst;
+        pc.pair = pair;
+        HIP_TRY(c, hipEventCreateWithFlags(&pc.ev, hipEventDisableTiming));
+        const hipError_t e = hipEventRecord(pc.ev, s);
+        if (e != hipSuccess) {
+            (void)hipEventDestroy(pc.ev);
+            return hip_fail(c, e, "hipEventRecord");
+        }
+        node->settled = false;
+        c->pending.push_back(pc);
+        recorded = true;
+    }
     *out = new_handle(c, node);
     return PCS_OK;
 }
@@ -1424,8 +1546,21 @@ int pcs_arena_stats(pcs_ctx *c, uint64_t *used, uint64_t *free_bytes, uint64_t *
 {
     if (!c) return PCS_E_INVAL;
     settle(c, false);
-    if (used) *used = c->arena.used();
-    if (free_bytes) *free_bytes = c->arena.size() - c->arena.used();
+    // Not counted as used: the library's own unit, and the part of every
+    // live segment that neither a snapshot's slots nor a pending call's
+    // worst case claims.
+    uint64_t idle = 0;
+    std::vector<const Segment *> seen;
+    auto count = [&](const Segment *g) {
+        if (!g || g->retired || std::find(seen.begin(), seen.end(), g) != seen.end()) return;
+        seen.push_back(g);
+        idle += (g->hi - g->lo) - g->claim;
+    };
+    count(c->seg.get());
+    for (const auto &p : c->pending) count(p.seg.get());
+    const uint64_t in_use = c->arena.used() - kAlign - idle;
+    if (used) *used = in_use;
+    if (free_bytes) *free_bytes = c->arena.size() - kAlign - in_use;
     if (largest) *largest = c->arena.largest();
     if (live) *live = c->handles.size();
     return PCS_OK;

@@ -34,20 +34,28 @@ def test_percentiles():
     assert abs(b._pct([1.0, 2.0, 3.0, 4.0, 5.0], 90) - 4.6) < 1e-12
 
 
-def test_traffic_record_matches_the_kernel_sources():
+def test_traffic_records_match_the_kernel_sources():
+    """Every workload's record (the batch headline, the KV ring checkpoint,
+    the verified restore) belongs to the current kernel sources and its
+    numbers follow from its counters and the calibration factors."""
     b = bench_module()
-    rec = b.traffic_record()
-    assert rec is not None, "the committed traffic record was measured on other kernel sources"
-    assert rec["kernel_source_sha256"] == b.kernel_source_sha()
-    for part in (rec, rec["restore_kernel"]):
-        fetch = part["fetch_KiB_per_dispatch"] * 1024 * rec["fetch_scale"]
-        write = part["write_KiB_per_dispatch"] * 1024 * rec["write_scale"]
-        # traffic = scaled counters (rounded to 0.1 KiB per dispatch when stored)
-        assert abs(fetch + write - part["traffic_bytes_per_launch"]) <= 1e-6 * part["traffic_bytes_per_launch"] + 2048
-        assert abs(part["traffic_bytes_per_launch"] / part["algorithmic_bytes_per_launch"]
-                   - part["traffic_over_algorithmic"]) < 1e-4
-    # The algorithmic bytes are 2 x state for every session of the launch.
-    state = 34_752_528
-    assert rec["algorithmic_bytes_per_launch"] == 2 * state * rec["sessions"]
-    with open(b.TRAFFIC_JSON) as fh:
-        assert json.load(fh) == rec
+    for workload, (fname, kernels) in b.TRAFFIC.items():
+        rec = b.traffic_record(workload)
+        assert rec is not None, "%s: the committed traffic record was measured on other kernel sources" % workload
+        assert rec["kernel_source_sha256"] == b.kernel_source_sha()
+        assert rec["workload"] == workload
+        for part in (rec, rec["second_kernel"]):
+            fetch = part["fetch_KiB_per_dispatch"] * 1024 * rec["fetch_scale"]
+            write = part["write_KiB_per_dispatch"] * 1024 * rec["write_scale"]
+            # traffic = scaled counters (rounded to 0.1 KiB per dispatch when stored)
+            assert abs(fetch + write - part["traffic_bytes_per_launch"]) <= 1e-6 * part["traffic_bytes_per_launch"] + 2048
+            assert abs(part["traffic_bytes_per_launch"] / part["algorithmic_bytes_per_launch"]
+                       - part["traffic_over_algorithmic"]) < 1e-4
+        with open(os.path.join(ROOT, "profiles", fname)) as fh:
+            assert json.load(fh) == rec
+    # The algorithmic bytes are 2 x state of every session of the launch, and
+    # 2 x the 512 MiB window for the KV ring kernels.
+    rec = b.traffic_record("batch")
+    assert rec["algorithmic_bytes_per_launch"] == 2 * 34_752_528 * rec["sessions"]
+    for workload in ("kv-ring", "verify"):
+        assert b.traffic_record(workload)["algorithmic_bytes_per_launch"] == 2 * 512 * 2 ** 20

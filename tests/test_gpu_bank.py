@@ -29,7 +29,8 @@ CASES = [
     (37, [1, 28, 4096, 4100]),
     (513, [28, 16 * 60 * 104 * 2]),
     (4099, [4, 16, 60]),
-    (65536, [4, 28]),        # the largest bank the call accepts
+    (65536, [4, 28]),
+    (1 << 20, [4, 28]),      # a million entries: selection is linear, not pairwise
 ]
 
 
@@ -72,9 +73,18 @@ def test_shrink_rejects_bad_arguments(pcs):
         ("keep > n", lambda: ctx.bank_shrink([(a, None, 64)], s, 101)),
         ("entry_bytes 0", lambda: ctx.bank_shrink([(a, None, 0)], s, 3)),
         ("overlap", lambda: ctx.bank_shrink([(a, a[64:], 64)], s, 10)),
-        ("too many entries", lambda: ctx.bank_shrink([(torch.zeros(65537, dtype=torch.uint8, device="cuda"), None, 1)],
-                                                     scores_dev(np.zeros(65537, dtype=np.float32)), 1)),
+        ("too many entries", lambda: too_many()),
     ]
+
+    def too_many():
+        # 2^32 entries through the C ABI (checked before any part or score is
+        # read, so small buffers stand in for the bank).
+        import ctypes
+        from paper_2607_21686_amd import _lib
+        arr = (_lib.PcsBankPart * 1)(_lib.PcsBankPart(a.data_ptr(), a.data_ptr(), 1))
+        st = _lib.lib().pcs_bank_shrink(ctx._h, arr, 1, 1 << 32, s.data_ptr(), 1, None)
+        if st:
+            raise pcs.PcsError(st, _lib.lib().pcs_last_error(ctx._h).decode())
     for name, f in bad:
         log("bank shrink error case:", name)
         with pytest.raises(pcs.PcsError) as e:

@@ -546,8 +546,10 @@ def test_batch_checkpoint_is_all_or_nothing(pcs):
 
 def test_incremental_chain_in_tight_arena(pcs):
     # 64 growing incremental checkpoints whose final state is ~6.4 MiB must fit
-    # in a 16 MiB arena: worst-case reservations are given back without
-    # leaving holes the next (larger) reservation cannot use.
+    # in a 16 MiB arena: worst-case claims are given back without leaving
+    # holes the next (larger) call cannot use.  Once the stream is idle (every
+    # stored-chunk count read, every segment's unused part returned) the arena
+    # holds the snapshots and nothing else.
     bank = W.config2(1, capacity=512, latent_shape=(4, 15, 26), pose_dim=7, step_entries=8)
     lat, pos = dev(bank.latents), dev(bank.poses)
     final = 512 * (bank.latent_entry_bytes + bank.pose_entry_bytes)
@@ -560,6 +562,8 @@ def test_incremental_chain_in_tight_arena(pcs):
         h = c.checkpoint(plan, parent=parent, hash=parent == 0)
         handles.append(h)
         parent = h
+    assert c.arena_stats()["used"] <= 16 << 20
+    torch.cuda.synchronize()
     stats = c.arena_stats()
     assert stats["used"] < 2 * final + (1 << 20), stats
     for j in (0, 31, 63):
