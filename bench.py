@@ -107,20 +107,20 @@ def summarize(dbs):
 # kernels it covers (name pattern in rocprofv3's kernel names, label).
 TRAFFIC = {
     "batch": ("k_hash_copy_batch1024_traffic.json",
-              [("pack", "k_hash<pcs::DevTables, 1, 1024, 512, 64>",
-                "k_hash<DevTables, pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
-               ("copy", "k_copy<pcs::DevTables, false, 512, 1024, 64>",
-                "k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
+              [("pack", r"k_hash<pcs::\w+Tables, 1, 1024, 512, 64>",
+                "k_hash<pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
+               ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
+                "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
     "kv-ring": ("k_hash_copy_kv_ring_1gib_traffic.json",
-                [("pack", "k_hash<pcs::DevTables, 1, 1024, 512, 64>",
-                  "k_hash<DevTables, pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
-                 ("copy", "k_copy<pcs::DevTables, false, 512, 1024, 64>",
-                  "k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
+                [("pack", r"k_hash<pcs::\w+Tables, 1, 1024, 512, 64>",
+                  "k_hash<pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
+                 ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
+                  "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
     "verify": ("k_hash_verify_kv_ring_1gib_traffic.json",
-               [("verify", "k_hash<pcs::DevTables, 3, 1024, 512, 64>",
-                 "k_hash<DevTables, verify, 1024 lanes, 512 B slices, 64 chunks> (restore + fingerprint + compare)"),
-                ("copy", "k_copy<pcs::DevTables, false, 512, 1024, 64>",
-                 "k_copy<DevTables, unpack, 512 lanes, 1 KiB slices, 64 chunks> (plain restore)")]),
+               [("verify", r"k_hash<pcs::\w+Tables, 3, 1024, 512, 64>",
+                 "k_hash<verify, 1024 lanes, 512 B slices, 64 chunks> (restore + fingerprint + compare)"),
+                ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
+                 "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (plain restore)")]),
 }
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", TRAFFIC["batch"][0])
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_21686_amd", "csrc", f)
@@ -163,6 +163,7 @@ def traffic(fetch_db, write_db, workload="batch", sessions=1024):
     reads for the plain 1 GiB calibration copy (true traffic 1 GiB read +
     1 GiB written), against the algorithmic bytes of one launch (state read
     once and written once)."""
+    import re
     import sqlite3
     fname, kernels = TRAFFIC[workload]
 
@@ -170,7 +171,7 @@ def traffic(fetch_db, write_db, workload="batch", sessions=1024):
         cur = sqlite3.connect(db).cursor()
         q = "select kernel_name, value from counters_collection where counter_name = ?"
         rows = cur.execute(q, (counter,)).fetchall()
-        pick = lambda pat: [v for n, v in rows if pat in n]
+        pick = lambda pat: [v for n, v in rows if re.search(pat, n)]
         out = {key: pick(pat) for key, pat, _ in kernels}
         out["calib"] = max(pick("rocclr_copyBuffer"))
         return out
