@@ -112,13 +112,15 @@ TRAFFIC = {
                ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
                 "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
     "kv-ring": ("k_hash_copy_kv_ring_1gib_traffic.json",
-                [("pack", r"k_hash<pcs::\w+Tables, 1, 1024, 512, 64>",
-                  "k_hash<pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
+                [("pack", r"k_hash_staggered<pcs::\w+Tables, 1, 1024, 512, 64>",
+                  "k_hash_staggered<pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint, "
+                  "first round staggered)"),
                  ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
                   "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
     "verify": ("k_hash_verify_kv_ring_1gib_traffic.json",
-               [("verify", r"k_hash<pcs::\w+Tables, 3, 1024, 512, 64>",
-                 "k_hash<verify, 1024 lanes, 512 B slices, 64 chunks> (restore + fingerprint + compare)"),
+               [("verify", r"k_hash_staggered<pcs::\w+Tables, 3, 1024, 512, 64>",
+                 "k_hash_staggered<verify, 1024 lanes, 512 B slices, 64 chunks> (restore + fingerprint + compare, "
+                 "first round staggered)"),
                 ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
                  "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (plain restore)")]),
 }
@@ -325,6 +327,10 @@ def run_batch(args):
         step()
     torch.cuda.synchronize()
 
+    # Kernel times from events recorded on the stream around each launch: the
+    # kernels run for milliseconds (the dispatch latency that the events take
+    # in is under 0.1% of them), and the dispatches' own timestamps made the
+    # step times of this workload more spread on MI355X.
     ctx.set_timing(True)
     # Events between steps on the context's stream give each step's device
     # time without synchronising inside the timed region.
@@ -504,7 +510,10 @@ def _timed(args, ctx, step, kernels):
     events (which cost a few microseconds of host time per launch, enough to
     slow workloads of many small launches), then the distribution of device
     step times (p10/p50/p90) from a second pass, then kernel times from a
-    third pass of the same steps with the timing events on."""
+    third pass of the same steps with the timing events on, as each kernel
+    dispatch's own begin and end (these kernels run for tens to hundreds of
+    microseconds, so the few microseconds of dispatch latency that events
+    recorded around a launch would add are not small against them)."""
     import torch
     global _STEP_DIST
     for _ in range(args.warmup):
@@ -527,7 +536,7 @@ def _timed(args, ctx, step, kernels):
     _STEP_DIST = {"p10": round(_pct(ms, 10), 4), "p50": round(_pct(ms, 50), 4), "p90": round(_pct(ms, 90), 4)}
     for k in kernels:
         ctx.kernel_time(k)
-    ctx.set_timing(True)
+    ctx.set_timing(True, dispatch=True)
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
@@ -586,7 +595,8 @@ def run_kv_ring(args):
     nc, mc = kt["copy"]
     out = _line(args, 3 * W_ / t / 1e9, t * 1e3, "windowed KV ring: 32 layers x 2 x 8192 slots x 8 x 128 bf16 "
                 "(1 GiB), 4096-token window at a wrapping head; checkpoint+fingerprint, fork, 2 restores",
-                {"window_bytes": W_}, "k_hash<copy>", 2 * W_, ms / n,
+                {"window_bytes": W_}, "k_hash_staggered<pack> (fused pack + fingerprint, first round staggered)",
+                2 * W_, ms / n,
                 {"restore_ms": round(mc / nc, 4), "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
     if not args.no_cpu_baseline:
         import numpy as np
@@ -639,7 +649,8 @@ def run_verify(args):
     ctx.delete(snap)
     out = _line(args, 2 * W_ / t / 1e9, t * 1e3, "verify on restore, windowed KV ring: 32 layers x 2 x 8192 slots x 8 "
                 "x 128 bf16 (1 GiB), 4096-token window; per step one restore with verification and one without",
-                {"window_bytes": W_}, "k_hash<verify>", 2 * W_, v_ms,
+                {"window_bytes": W_}, "k_hash_staggered<verify> (restore + fingerprint + compare, first round staggered)",
+                2 * W_, v_ms,
                 {"verify_ms": round(v_ms, 4), "restore_ms": round(mc / nc, 4),
                  "verify_GBps_hbm": round(2 * W_ / (v_ms * 1e-3) / 1e9, 1),
                  "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
@@ -762,7 +773,7 @@ def run_bank(args):
         hs, parent = [], 0
         for j in range(64):
             if j == 32:
-                ctx.set_timing(True)
+                ctx.set_timing(True, dispatch=True)
             h = ctx.checkpoint(plans[j], parent=parent, hash=parent == 0)
             hs.append(h)
             parent = h

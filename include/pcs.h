@@ -77,6 +77,11 @@ extern "C" {
 /* Checkpoint flags. */
 #define PCS_CKPT_HASH 1u  /* also fingerprint while copying (one read of the state) */
 
+/* pcs_set_timing modes (see there). */
+#define PCS_TIMING_OFF 0
+#define PCS_TIMING_EVENTS 1   /* events recorded on the stream around each launch */
+#define PCS_TIMING_DISPATCH 2 /* each kernel dispatch's own begin and end        */
+
 typedef struct pcs_ctx pcs_ctx;
 typedef uint64_t pcs_snap; /* opaque snapshot handle; 0 is never a valid handle */
 
@@ -491,14 +496,22 @@ int pcs_arena_stats(pcs_ctx *ctx, uint64_t *used, uint64_t *free_bytes, uint64_t
                     uint64_t *live_handles);
 
 /*
- * Kernel timing.  While enabled, every kernel launch is bracketed by HIP
- * events on the context stream.  pcs_kernel_time waits for the stream, then
+ * Kernel timing.  PCS_TIMING_OFF: off.  While on, every kernel launch is
+ * timed with a pair of HIP events on the context stream:
+ *   PCS_TIMING_EVENTS: events recorded on the stream just before and after
+ *     the launch, so a launch's time includes its dispatch latency (a few
+ *     microseconds);
+ *   PCS_TIMING_DISPATCH: the kernel dispatch's own begin and end timestamps
+ *     (what a kernel trace reports).  Measured on MI355X, it made the step
+ *     times of the 1024-session batch (11 ms kernels back to back) more
+ *     spread; it suits kernels for which the dispatch latency is not small.
+ * Any other mode is PCS_E_INVAL.  pcs_kernel_time waits for the stream, then
  * reports the number of launches and their summed duration in milliseconds
  * for the kernel family `name` ("hash", "pack_hash", "pack", "copy",
- * "verify", "merkle", "classify", "incremental", "map", "shrink", "flip") since the last reset, and
- * resets it.
+ * "verify", "merkle", "classify", "incremental", "map", "shrink", "flip")
+ * since the last reset, and resets it.
  */
-int pcs_set_timing(pcs_ctx *ctx, int enable);
+int pcs_set_timing(pcs_ctx *ctx, int mode);
 int pcs_kernel_time(pcs_ctx *ctx, const char *name, uint64_t *launches, double *total_ms);
 
 #ifdef __cplusplus

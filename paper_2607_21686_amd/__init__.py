@@ -21,8 +21,8 @@ import ctypes
 import torch
 
 from ._lib import (CHUNK_BYTES, CKPT_HASH, E_CORRUPT, E_HANDLE, E_HIP, E_INVAL, E_NOMEM, E_PROBE, E_SHAPE, EXPORTS,
-                   FLAT, MUST_SNAPSHOT, PROBE_FN, RECOMPUTABLE, RING, PcsBankPart, PcsBuf, PcsDiscovery, PcsError,
-                   PcsSnapInfo, lib)
+                   FLAT, MUST_SNAPSHOT, PROBE_FN, RECOMPUTABLE, RING, TIMING_DISPATCH, TIMING_EVENTS, TIMING_OFF,
+                   PcsBankPart, PcsBuf, PcsDiscovery, PcsError, PcsSnapInfo, lib)
 
 __all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_count", "keep_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
            "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "E_CORRUPT", "E_PROBE",
@@ -408,9 +408,12 @@ class Context:
         return dict(zip(["used", "free", "largest_free", "live_handles"], [int(x.value) for x in v]))
 
     # -- kernel timing -----------------------------------------------------
-    def set_timing(self, enable: bool):
-        """Brackets every kernel launch with HIP events while enabled (pcs_set_timing)."""
-        self._check(_L.pcs_set_timing(self._h, 1 if enable else 0))
+    def set_timing(self, enable: bool, dispatch: bool = False):
+        """Times every kernel launch with HIP events while enabled
+        (pcs_set_timing): recorded on the stream around each launch, or with
+        `dispatch` the kernel dispatch's own begin and end timestamps."""
+        mode = (TIMING_DISPATCH if dispatch else TIMING_EVENTS) if enable else TIMING_OFF
+        self._check(_L.pcs_set_timing(self._h, mode))
 
     def kernel_time(self, name: str):
         """(launches, total ms) of the kernel family `name` since the last call

@@ -20,6 +20,7 @@ CHUNK_BYTES = 4096
 FLAT, RING = 0, 1
 RECOMPUTABLE, MUST_SNAPSHOT = 0, 1
 CKPT_HASH = 1
+TIMING_OFF, TIMING_EVENTS, TIMING_DISPATCH = 0, 1, 2
 
 _ERRNAMES = {E_INVAL: "PCS_E_INVAL", E_NOMEM: "PCS_E_NOMEM", E_HANDLE: "PCS_E_HANDLE",
              E_SHAPE: "PCS_E_SHAPE", E_HIP: "PCS_E_HIP", E_CORRUPT: "PCS_E_CORRUPT", E_PROBE: "PCS_E_PROBE"}

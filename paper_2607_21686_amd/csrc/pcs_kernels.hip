@@ -17,6 +17,8 @@
 // Memory traffic is 16-byte vector loads and stores throughout.  Nothing
 // here is a contraction, so no MFMA is used; the hash is 64-bit integer
 // multiply work on the vector ALU.
+#include <hip/hip_ext.h>
+
 #include "pcs_device.h"
 
 // Device scratch of the allocation-free entry point (pcs_fingerprint_noalloc):
@@ -37,6 +39,26 @@ hipError_t static_scratch_address(uint64_t *addr)
 }
 
 namespace {
+
+// Timing events for the next kernel launch, set by the runtime around one
+// launcher call while dispatch timing is on: that launch stamps `start` when
+// its kernel begins and `stop` when it ends (the dispatch's own timestamps,
+// so queueing and launch overhead are not counted).  Other launches take the
+// plain launch path.
+thread_local hipEvent_t t_start = nullptr, t_stop = nullptr;
+thread_local bool t_used = false;
+
+template <class K, class... Args>
+void run_kernel(K kernel, dim3 grid, dim3 block, hipStream_t s, Args... args)
+{
+    if (!t_start) {
+        hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+        return;
+    }
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, t_start, t_stop, 0, args...);
+    t_start = t_stop = nullptr;
+    t_used = true;
+}
 
 // XXH64 primes (xxHash specification).
 constexpr uint64_t P1 = 0x9E3779B185EBCA87ULL;
@@ -132,35 +154,12 @@ __device__ __forceinline__ uint32_t find_run(const Run *runs, uint32_t begin, ui
     return lo;
 }
 
-// The tile a workgroup takes.  The dispatcher deals the workgroups of a
-// launch to the eight XCDs in turn (workgroup b runs on XCD b mod 8), so the
-// tiles are handed out XCD by XCD:
-//   - up to kXcdBlockJobs tiles: XCD x works through the x-th contiguous
-//     eighth of the job in order, starting at a point staggered by x/8 of its
-//     share, so that the eight streams do not walk over the same memory
-//     channels in step;
-//   - larger jobs: blocks of kXcdBlock consecutive tiles are dealt to the
-//     XCDs in turn, so every XCD streams through every part of the job and
-//     none is left with a stretch of memory that happens to be slower (a
-//     tail of fewer than eight blocks keeps the launch order).
-// Measured on MI355X against the plain blockIdx order: pack + fingerprint of
-// a 512 MiB ring window 204 -> 190-198 us, restore 189 -> 180-185 us; on the
-// 1024-session batch the fused kernel 11.5 -> 10.9-11.0 ms in every input
-// placement tried, where contiguous eighths alone gave 11.45 ms in some.
-// A bijection of [0, gridDim.x) in both cases.
-constexpr uint32_t kXcds = 8, kXcdBlock = 512, kXcdBlockJobs = 16384;
-__device__ __forceinline__ uint32_t xcd_tile()
-{
-    const uint32_t nb = gridDim.x, b = blockIdx.x, x = b % kXcds, i = b / kXcds;
-    if (nb >= kXcdBlockJobs) {
-        const uint32_t full = nb / (kXcds * kXcdBlock);  // whole rounds of blocks
-        if (b >= full * kXcds * kXcdBlock) return b;
-        return ((i / kXcdBlock) * kXcds + x) * kXcdBlock + i % kXcdBlock;
-    }
-    const uint32_t per = nb / kXcds, rem = nb % kXcds;
-    const uint32_t n = per + (x < rem ? 1u : 0u);  // tiles of XCD x (>= 1 when workgroup b exists)
-    return x * per + (x < rem ? x : rem) + (i + x * (n / kXcds)) % n;
-}
+// The tile a workgroup takes (xcd_tile_of).  Measured on MI355X against the
+// plain blockIdx order: pack + fingerprint of a 512 MiB ring window 204 ->
+// 190-198 us, restore 189 -> 180-185 us; on the 1024-session batch the fused
+// kernel 11.5 -> 10.9-11.0 ms in every input placement tried, where
+// contiguous eighths alone gave 11.45 ms in some.
+__device__ __forceinline__ uint32_t xcd_tile() { return xcd_tile_of(blockIdx.x, gridDim.x); }
 
 // Device addresses arrive as integers; casting them to the global address
 // space makes the compiler emit global_* (not flat_*) memory instructions.
@@ -323,7 +322,28 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
     return GroupRef{b, find_run(t.runs, jb.run_begin, jb.run_count, (G - jb.group_begin) * kGroupChunks * kChunk)};
 }
 
-// Fingerprint tile kernel.  One workgroup = one tile of CPW chunks of one
+// First-round stagger.  The workgroups of a launch's first round (one per CU)
+// all start together and then move their slices in step: every CU reads the
+// same offsets within its chunks at the same moment.  In jobs of a few
+// rounds this costs the first two rounds about a fifth of their speed
+// (per-workgroup timelines on MI355X, 512 MiB pack + fingerprint: 25 against
+// 21 us per group; jobs of 768 MiB and more do not show it).  Holding the
+// first-round workgroups back by 0..7 phases of stg.ticks of the constant
+// real-time counter (phase = position within the XCD, mod 8) spreads them
+// over most of a group's duration; later workgroups start whenever a CU
+// frees up and need no stagger.  The wait is also bounded by a spin count,
+// so it ends even if the counter stood still.
+__device__ __forceinline__ void stagger_start(const Stagger &stg)
+{
+    if (stg.ticks == 0 || blockIdx.x >= stg.first_round) return;
+    const uint64_t wait = (uint64_t)((blockIdx.x / kXcds) % kStaggerPhases) * stg.ticks;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    for (uint32_t spin = 0; spin < kStaggerMaxSpins && __builtin_amdgcn_s_memrealtime() - t0 < wait; ++spin)
+        __builtin_amdgcn_s_sleep(2);
+}
+
+// Fingerprint tile kernels (k_hash, k_hash_staggered; the body is
+// hash_tile).  One workgroup = one tile of CPW chunks of one
 // buffer: a whole 64-chunk group, or for small jobs an eighth of one, so
 // that a few groups still occupy many CUs (the tile's Merkle node is then an
 // aligned 8-chunk subtree).  Step k moves the k-th SL-byte slice of every
@@ -341,9 +361,9 @@ __device__ __forceinline__ GroupRef group_ref(const ArgTables &t, uint64_t G)
 // wavefronts as lane pairs with two accumulators each would.  kModeDiff /
 // kModeVerify ballot one flag per chunk into a per-group mask (the group is
 // one bitmap word; a diff sub-tile writes its byte of the word).
-template <class Tab, int MODE, int T, int SL, int CPW>
-__global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
-                                            uint64_t *__restrict__ flag_mask, uint64_t arena_base)
+template <class Tab, int MODE, int T, int SL, int CPW, bool STAGGER>
+__device__ __forceinline__ void hash_tile(const Tab &tab, uint64_t *__restrict__ nodes,
+                                          uint64_t *__restrict__ flag_mask, uint64_t arena_base, const Stagger &stg)
 {
     constexpr uint32_t kSteps = kChunk / SL;
     constexpr uint32_t kRow = SL + 32;                  // padded LDS row: the quads of 8 chunks hit distinct banks
@@ -361,6 +381,7 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
     __shared__ uint32_t dflag[CPW];
 
     const uint32_t tile_id = xcd_tile();
+    if constexpr (STAGGER) stagger_start(stg);
     const uint64_t G = tile_id / kTiles;
     const GroupRef gr = group_ref(tab, G);
     const JobBuf &jb = tab.bufs[gr.buf];
@@ -538,6 +559,23 @@ __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict_
             }
         }
     }
+}
+
+template <class Tab, int MODE, int T, int SL, int CPW>
+__global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
+                                            uint64_t *__restrict__ flag_mask, uint64_t arena_base)
+{
+    hash_tile<Tab, MODE, T, SL, CPW, false>(tab, nodes, flag_mask, arena_base, Stagger{0, 0});
+}
+
+// k_hash with the first-round stagger (pack and verify jobs of a few rounds):
+// a kernel of its own, so the others keep their code and arguments.
+template <class Tab, int MODE, int T, int SL, int CPW>
+__global__ __launch_bounds__(T) void k_hash_staggered(const Tab tab, uint64_t *__restrict__ nodes,
+                                                      uint64_t *__restrict__ flag_mask, uint64_t arena_base,
+                                                      Stagger stg)
+{
+    hash_tile<Tab, MODE, T, SL, CPW, true>(tab, nodes, flag_mask, arena_base, stg);
 }
 
 // ---------------------------------------------------------------- Merkle lists
@@ -1217,49 +1255,61 @@ hipError_t launch_group_map(const JobBuf *bufs, const Run *runs, uint32_t nbuf, 
 {
     if (ngroups == 0) return hipSuccess;
     const uint32_t blocks = (uint32_t)((ngroups + 255) / 256);
-    hipLaunchKernelGGL(k_group_map, dim3(blocks), dim3(256), 0, s, bufs, runs, nbuf, ngroups, map);
+    run_kernel(k_group_map, dim3(blocks), dim3(256), s, bufs, runs, nbuf, ngroups, map);
     return hipGetLastError();
 }
 
 template <class Tab>
 hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint64_t *flag_mask,
-                       uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group)
+                       uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group, TileDevice dev)
 {
     if (ngroups == 0) return hipSuccess;
     const bool split = tiles_per_group != 1;
     if (split && (mode != kModeHash && mode != kModePack && mode != kModeDiff)) return hipErrorInvalidValue;
+    Stagger stg{0, 0};
+    if (!split && (mode == kModePack || mode == kModeVerify) && dev.cus && dev.wall_khz &&
+        ngroups >= (uint64_t)kStaggerMinRounds * dev.cus && ngroups <= (uint64_t)kStaggerMaxRounds * dev.cus)
+        stg = Stagger{dev.cus, (uint32_t)((uint64_t)kStaggerPhaseNs * dev.wall_khz / 1000000)};
     const dim3 grid((uint32_t)(ngroups * tiles_per_group));
     if (tiles_per_group == kSmallTiles) {
         constexpr int kCPW = kGroupChunks / kSmallTiles;
         static_assert(kCPW == 8, "a diff sub-tile writes one mask byte");
         if (mode == kModeHash)
-            hipLaunchKernelGGL((k_hash<Tab, kModeHash, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
-                               tab, nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeHash, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab, nodes,
+                       flag_mask, arena_base);
         else if (mode == kModePack)
-            hipLaunchKernelGGL((k_hash<Tab, kModePack, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
-                               tab, nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModePack, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab, nodes,
+                       flag_mask, arena_base);
         else
-            hipLaunchKernelGGL((k_hash<Tab, kModeDiff, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s,
-                               tab, nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeDiff, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab, nodes,
+                       flag_mask, arena_base);
         return hipGetLastError();
     }
     if (split) return hipErrorInvalidValue;
     switch (mode) {
     case kModeHash:
-        hipLaunchKernelGGL((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), 0, s,
-                           tab, nodes, flag_mask, arena_base);
+        run_kernel((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
+                   nodes, flag_mask, arena_base);
         break;
     case kModePack:
-        hipLaunchKernelGGL((k_hash<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), 0, s,
-                           tab, nodes, flag_mask, arena_base);
+        if (stg.ticks)
+            run_kernel((k_hash_staggered<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes),
+                       s, tab, nodes, flag_mask, arena_base, stg);
+        else
+            run_kernel((k_hash<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
+                       nodes, flag_mask, arena_base);
         break;
     case kModeDiff:
-        hipLaunchKernelGGL((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), 0, s,
-                           tab, nodes, flag_mask, arena_base);
+        run_kernel((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
+                   nodes, flag_mask, arena_base);
         break;
     case kModeVerify:
-        hipLaunchKernelGGL((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), 0,
-                           s, tab, nodes, flag_mask, arena_base);
+        if (stg.ticks)
+            run_kernel((k_hash_staggered<Tab, kModeVerify, kPackLanes, kPackSlice, kGroupChunks>), grid,
+                       dim3(kPackLanes), s, tab, nodes, flag_mask, arena_base, stg);
+        else
+            run_kernel((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
+                       nodes, flag_mask, arena_base);
         break;
     default:
         return hipErrorInvalidValue;
@@ -1277,17 +1327,17 @@ hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t are
     if (tiles == kSmallTiles) {
         constexpr int kCPW = kGroupChunks / kSmallTiles;
         if (pack)
-            hipLaunchKernelGGL((k_copy<Tab, true, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
-                               arena_base);
+            run_kernel((k_copy<Tab, true, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab,
+                       arena_base);
         else
-            hipLaunchKernelGGL((k_copy<Tab, false, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), 0, s, tab,
-                               arena_base);
+            run_kernel((k_copy<Tab, false, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab,
+                       arena_base);
     } else if (pack) {
-        hipLaunchKernelGGL((k_copy<Tab, true, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), 0, s,
-                           tab, arena_base);
+        run_kernel((k_copy<Tab, true, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), s, tab,
+                   arena_base);
     } else {
-        hipLaunchKernelGGL((k_copy<Tab, false, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), 0, s,
-                           tab, arena_base);
+        run_kernel((k_copy<Tab, false, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), s, tab,
+                   arena_base);
     }
     return hipGetLastError();
 }
@@ -1298,7 +1348,7 @@ hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_
 {
     if (max_slots == 0) return hipSuccess;
     const uint32_t blocks = (uint32_t)((max_slots + 3) / 4);
-    hipLaunchKernelGGL((k_pack_dirty<Tab>), dim3(blocks), dim3(256), 0, s, tab, list, total, top_word, arena_base);
+    run_kernel((k_pack_dirty<Tab>), dim3(blocks), dim3(256), s, tab, list, total, top_word, arena_base);
     return hipGetLastError();
 }
 
@@ -1307,8 +1357,8 @@ hipError_t launch_place_dirty(const Tab &tab, uint64_t ngroups, const uint64_t *
                               const uint64_t *top_word, uint64_t arena_base, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_place_dirty<Tab>), dim3((uint32_t)(ngroups * (kGroupChunks / 4))), dim3(256), 0, s, tab,
-                       dirty_mask, offsets, top_word, arena_base);
+    run_kernel((k_place_dirty<Tab>), dim3((uint32_t)(ngroups * (kGroupChunks / 4))), dim3(256), s, tab, dirty_mask,
+               offsets, top_word, arena_base);
     return hipGetLastError();
 }
 
@@ -1317,7 +1367,7 @@ hipError_t launch_classify(const Tab &tab, uint64_t ngroups, const uint64_t *has
                            uint64_t *bitmap, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_classify<Tab>), dim3((uint32_t)ngroups), dim3(64), 0, s, tab, hashes, K, total, bitmap);
+    run_kernel((k_classify<Tab>), dim3((uint32_t)ngroups), dim3(64), s, tab, hashes, K, total, bitmap);
     return hipGetLastError();
 }
 
@@ -1325,7 +1375,7 @@ template <class Tab>
 hipError_t launch_labels(const Tab &tab, const uint64_t *bitmap, uint8_t *labels, hipStream_t s)
 {
     if (tab.nbuf == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_labels<Tab>), dim3(tab.nbuf), dim3(64), 0, s, tab, bitmap, labels);
+    run_kernel((k_labels<Tab>), dim3(tab.nbuf), dim3(64), s, tab, bitmap, labels);
     return hipGetLastError();
 }
 
@@ -1334,7 +1384,7 @@ hipError_t launch_classify_small(const ArgTables &tab, uint64_t ngroups, const u
 {
     if (ngroups > kClassifyFusedGroups) return hipErrorInvalidValue;
     if (tab.nbuf == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_classify_small, dim3(1), dim3(1024), 0, s, tab, ngroups, hashes, K, total, bitmap, labels);
+    run_kernel(k_classify_small, dim3(1), dim3(1024), s, tab, ngroups, hashes, K, total, bitmap, labels);
     return hipGetLastError();
 }
 
@@ -1343,7 +1393,7 @@ hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_
                          hipStream_t s)
 {
     if (nlists == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_merkle, dim3(nlists), dim3(256), 0, s, lists, in, scratch_a, scratch_b, roots_out);
+    run_kernel(k_merkle, dim3(nlists), dim3(256), s, lists, in, scratch_a, scratch_b, roots_out);
     return hipGetLastError();
 }
 
@@ -1351,14 +1401,14 @@ hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64
                                uint64_t *scratch_b, hipStream_t s)
 {
     if (lists.nlists == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_merkle_small, dim3(1), dim3(256), 0, s, lists, in, scratch_a, scratch_b);
+    run_kernel(k_merkle_small, dim3(1), dim3(256), s, lists, in, scratch_a, scratch_b);
     return hipGetLastError();
 }
 
 hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total,
                        const SlotBump &bump, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_scan<MaskBits>, dim3(1), dim3(1024), 0, s, MaskBits{dirty_mask}, n, offsets, total, bump);
+    run_kernel(k_scan<MaskBits>, dim3(1), dim3(1024), s, MaskBits{dirty_mask}, n, offsets, total, bump);
     return hipGetLastError();
 }
 
@@ -1370,11 +1420,11 @@ hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes
     if (ngroups > kScanCompactMaxGroups) return hipErrorInvalidValue;
     if (ngroups && ngroups <= kScanCompactFusedGroups && !bump.bump) return hipErrorInvalidValue;  // slots need a top
     if (ngroups <= kScanCompactFusedGroups)
-        hipLaunchKernelGGL(k_merkle_scan_small<true>, dim3(1), dim3(1024), 0, s, lists, nodes, scratch_a, scratch_b,
-                           tab, ngroups, dirty_mask, bump, list, offsets, total);
+        run_kernel(k_merkle_scan_small<true>, dim3(1), dim3(1024), s, lists, nodes, scratch_a, scratch_b, tab, ngroups,
+                   dirty_mask, bump, list, offsets, total);
     else
-        hipLaunchKernelGGL(k_merkle_scan_small<false>, dim3(1), dim3(1024), 0, s, lists, nodes, scratch_a, scratch_b,
-                           tab, ngroups, dirty_mask, bump, list, offsets, total);
+        run_kernel(k_merkle_scan_small<false>, dim3(1), dim3(1024), s, lists, nodes, scratch_a, scratch_b, tab, ngroups,
+                   dirty_mask, bump, list, offsets, total);
     return hipGetLastError();
 }
 
@@ -1382,8 +1432,7 @@ hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, 
 {
     if (n == 0 || keep == 0) return hipSuccess;
     if (keep > n) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_shrink_select, dim3(1), dim3(1024), 0, s, reinterpret_cast<const uint32_t *>(scores), n, keep,
-                       kept);
+    run_kernel(k_shrink_select, dim3(1), dim3(1024), s, reinterpret_cast<const uint32_t *>(scores), n, keep, kept);
     return hipGetLastError();
 }
 
@@ -1397,30 +1446,30 @@ hipError_t launch_gather_entries(uint64_t src, uint64_t dst, uint64_t entry_byte
     const uint64_t items = count * spe;
     const uint32_t grid = (uint32_t)(items < (1u << 20) ? items : (1u << 20));
     if (G == 16)
-        hipLaunchKernelGGL(k_gather_entries<16>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
+        run_kernel(k_gather_entries<16>, dim3(grid), dim3(256), s, src, dst, entry_bytes, kept, spe, items);
     else if (G == 4)
-        hipLaunchKernelGGL(k_gather_entries<4>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
+        run_kernel(k_gather_entries<4>, dim3(grid), dim3(256), s, src, dst, entry_bytes, kept, spe, items);
     else
-        hipLaunchKernelGGL(k_gather_entries<1>, dim3(grid), dim3(256), 0, s, src, dst, entry_bytes, kept, spe, items);
+        run_kernel(k_gather_entries<1>, dim3(grid), dim3(256), s, src, dst, entry_bytes, kept, spe, items);
     return hipGetLastError();
 }
 
 hipError_t launch_flip_bit(uint64_t addr, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_flip_bit, dim3(1), dim3(64), 0, s, addr);
+    run_kernel(k_flip_bit, dim3(1), dim3(64), s, addr);
     return hipGetLastError();
 }
 
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s)
 {
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_reverse_slots, dim3((uint32_t)n), dim3(256), 0, s, top, dst, n);
+    run_kernel(k_reverse_slots, dim3((uint32_t)n), dim3(256), s, top, dst, n);
     return hipGetLastError();
 }
 
 #define PCS_INSTANTIATE(Tab)                                                                                        \
     template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint64_t *, uint64_t, hipStream_t, \
-                                         uint32_t);                                                               \
+                                         uint32_t, TileDevice);                                                   \
     template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t);                     \
     template hipError_t launch_pack_dirty<Tab>(const Tab &, const uint64_t *, const uint64_t *, uint64_t,         \
                                                const uint64_t *, uint64_t, hipStream_t);                          \
@@ -1432,5 +1481,20 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
 PCS_INSTANTIATE(DevTables)
 PCS_INSTANTIATE(ArgTables)
 #undef PCS_INSTANTIATE
+
+void set_kernel_events(hipEvent_t start, hipEvent_t stop)
+{
+    t_start = start;
+    t_stop = stop;
+    t_used = false;
+}
+
+bool take_kernel_events_used()
+{
+    const bool used = t_used;
+    t_start = t_stop = nullptr;
+    t_used = false;
+    return used;
+}
 
 }  // namespace pcs

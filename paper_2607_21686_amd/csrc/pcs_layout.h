@@ -73,6 +73,34 @@ struct GroupRef {
     uint32_t buf;
     uint32_t run;
 };
+
+// Tile order of the tile kernels: the tile workgroup b of a launch of nb
+// workgroups takes.  The dispatcher deals a launch's workgroups to the eight
+// XCDs in turn (workgroup b runs on XCD b mod 8), so the tiles are handed
+// out XCD by XCD:
+//   - below kXcdBlockJobs tiles: XCD x works through the x-th contiguous
+//     eighth of the job in order, entered at a point staggered by x/8 of its
+//     length (wrapping), so that the eight streams do not walk over the same
+//     memory channels in step;
+//   - from kXcdBlockJobs tiles: blocks of kXcdBlock consecutive tiles are
+//     dealt to the XCDs in turn, so every XCD streams through every part of
+//     the job and none is left with a stretch of memory that happens to be
+//     slower; the tail of fewer than eight blocks keeps the launch order.
+// A bijection of [0, nb).  (constexpr: callable from host and device code.)
+constexpr uint32_t kXcds = 8, kXcdBlock = 512, kXcdBlockJobs = 16384;
+constexpr uint32_t xcd_tile_of(uint32_t b, uint32_t nb)
+{
+    const uint32_t x = b % kXcds, i = b / kXcds;
+    if (nb >= kXcdBlockJobs) {
+        const uint32_t full = nb / (kXcds * kXcdBlock);  // whole rounds of blocks
+        if (b >= full * kXcds * kXcdBlock) return b;
+        return ((i / kXcdBlock) * kXcds + x) * kXcdBlock + i % kXcdBlock;
+    }
+    const uint32_t per = nb / kXcds, rem = nb % kXcds;
+    const uint32_t n = per + (x < rem ? 1u : 0u);  // tiles of XCD x (>= 1 when workgroup b exists)
+    return x * per + (x < rem ? x : rem) + (i + x * (n / kXcds)) % n;
+}
+
 struct DevTables {
     const JobBuf *bufs;
     const Run *runs;

@@ -99,7 +99,9 @@ struct pcs_ctx {
     // incremental slot placement, word 1 a call's payload top.
     uint64_t bump_dev = 0, top_dev = 0;
 
-    bool timing = false;
+    pcs::TileDevice dev{0, 0};  // CU count and real-time counter rate of the arena's device (0: unknown)
+
+    int timing = PCS_TIMING_OFF;  // pcs_set_timing mode
     bool no_events = false;  // set while a call that must create nothing runs (no timing events)
     std::map<std::string, std::vector<std::pair<hipEvent_t, hipEvent_t>>> timers;
 
@@ -269,22 +271,34 @@ int launch(pcs_ctx *c, const char *name, F &&f)
         if (a) (void)hipEventDestroy(a);
         if (b) (void)hipEventDestroy(b);
     };
-    const bool timed = c->timing && !c->no_events;
+    // PCS_TIMING_EVENTS records the pair on the stream around the launcher's
+    // launch; PCS_TIMING_DISPATCH hands it to the kernel launch itself, which
+    // stamps the kernel's own begin and end (a launcher with no work launches
+    // nothing, and the pair is then recorded back to back: zero time).
+    const bool timed = c->timing != PCS_TIMING_OFF && !c->no_events;
+    const bool dispatch = c->timing == PCS_TIMING_DISPATCH;
     if (timed) {
         hipError_t te = hipEventCreate(&a);
         if (te == hipSuccess) te = hipEventCreate(&b);
-        if (te == hipSuccess) te = hipEventRecord(a, c->stream);
+        if (te == hipSuccess && !dispatch) te = hipEventRecord(a, c->stream);
         if (te != hipSuccess) {
             drop();
             return hip_fail(c, te, "timing event");
         }
+        if (dispatch) set_kernel_events(a, b);
     }
     const hipError_t e = f();
     if (timed) {
-        const hipError_t te = hipEventRecord(b, c->stream);
-        if (te != hipSuccess) {
+        hipError_t te = hipSuccess;
+        if (!dispatch) {
+            te = hipEventRecord(b, c->stream);
+        } else if (!take_kernel_events_used()) {
+            te = hipEventRecord(a, c->stream);
+            if (te == hipSuccess) te = hipEventRecord(b, c->stream);
+        }
+        if (te != hipSuccess || e != hipSuccess) {
             drop();
-            return hip_fail(c, te, "timing event");
+            return e != hipSuccess ? hip_fail(c, e, name) : hip_fail(c, te, "timing event");
         }
         c->timers[name].push_back({a, b});
     }
@@ -570,7 +584,7 @@ int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &s
     hipStream_t s = c->stream;
     int st = with_tables(sg, [&](const auto &tab) {
         return launch(c, copy ? "pack_hash" : "hash", [&] {
-            return launch_tile(tab, G, copy ? kModePack : kModeHash, d_nodes, nullptr, 0, s, tiles);
+            return launch_tile(tab, G, copy ? kModePack : kModeHash, d_nodes, nullptr, 0, s, tiles, c->dev);
         });
     });
     if (st || !want_roots) return st;
@@ -855,6 +869,15 @@ int pcs_ctx_create(void *d_arena, uint64_t arena_bytes, void *hip_stream, pcs_ct
     }
     c->bump_dev = c->arena_dev + own;
     c->top_dev = c->bump_dev + 8;
+    {
+        hipPointerAttribute_t at;
+        int cus = 0, khz = 0;
+        if (hipPointerGetAttributes(&at, d_arena) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, at.device) == hipSuccess &&
+            hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, at.device) == hipSuccess && cus > 0 &&
+            khz > 0)
+            c->dev = TileDevice{(uint32_t)cus, (uint32_t)khz};
+    }
     if (hipHostMalloc(&c->na_host, kNoAllocStagingBytes, hipHostMallocDefault) != hipSuccess ||
         hipEventCreateWithFlags(&c->na_ev, hipEventDisableTiming) != hipSuccess ||
         scratch_for(d_arena, &c->scratch_dev) != hipSuccess) {
@@ -1443,7 +1466,7 @@ int pcs_restore_verify(pcs_ctx *c, pcs_snap snap, const pcs_buf *dst, uint32_t n
     const uint64_t G = job.ngroups;
     return with_tables(sg, [&](const auto &tab) {
         if (int st = launch(c, "verify", [&] {
-                return launch_tile(tab, G, kModeVerify, nullptr, d_bad_bitmap, c->arena_dev, c->stream);
+                return launch_tile(tab, G, kModeVerify, nullptr, d_bad_bitmap, c->arena_dev, c->stream, 1, c->dev);
             }))
             return st;
         if (!d_bad_labels) return (int)PCS_OK;
@@ -1566,10 +1589,12 @@ int pcs_arena_stats(pcs_ctx *c, uint64_t *used, uint64_t *free_bytes, uint64_t *
     return PCS_OK;
 }
 
-int pcs_set_timing(pcs_ctx *c, int enable)
+int pcs_set_timing(pcs_ctx *c, int mode)
 {
     if (!c) return PCS_E_INVAL;
-    c->timing = enable != 0;
+    if (mode != PCS_TIMING_OFF && mode != PCS_TIMING_EVENTS && mode != PCS_TIMING_DISPATCH)
+        return fail(c, PCS_E_INVAL, "timing mode %d: 0, 1 or 2", mode);
+    c->timing = mode;
     return PCS_OK;
 }
 

@@ -3,6 +3,8 @@
 //   - plan descriptors (flat buffers, ring windows) against the ring's
 //     defining index map, logical row t of ring o at physical row
 //     (head + t) mod capacity, and the validation of bad descriptors;
+//   - the XCD tile order of the tile kernels (a partition of the job's
+//     tiles, and the one-tile-per-workgroup order written out);
 //   - the snapshot image header: round trips, every single-field
 //     corruption, a crafted size that wraps 64-bit arithmetic, random
 //     mutations and truncations (an accepted header must name only regions
@@ -511,8 +513,51 @@ static void test_image_corruptions()
     CHECK(accepted < 20000);
 }
 
+// ------------------------------------------------------------- tile order
+
+// xcd_tile_of (pcs_layout.h) is a bijection of [0, nb), and workgroup b
+// (XCD b mod 8, position b / 8 there) gets a tile of its XCD's share: below
+// 16384 tiles the XCD's contiguous eighth, walked in order from a start
+// staggered by x/8 of its length; from 16384 tiles the 512-tile blocks dealt
+// to that XCD, walked in order, with the tail of fewer than eight blocks in
+// launch order.
+static void test_tile_order()
+{
+    std::vector<uint32_t> sizes;
+    for (uint32_t nb = 1; nb <= 300; ++nb) sizes.push_back(nb);
+    for (uint32_t nb : {1023u, 1024u, 1025u, 2047u, 2048u, 2049u, 4096u, 8191u, 16383u, 16384u, 16385u, 16391u,
+                        16392u, 20000u, 20480u, 24575u, 36864u, 65535u, 65536u, 137216u, 271536u})
+        sizes.push_back(nb);
+    for (uint32_t nb : sizes) {
+        std::vector<uint8_t> seen(nb, 0);
+        for (uint32_t b = 0; b < nb; ++b) {
+            const uint32_t t = xcd_tile_of(b, nb);
+            CHECK(t < nb);
+            if (t >= nb) continue;
+            CHECK(!seen[t]);
+            seen[t] = 1;
+            const uint32_t x = b % kXcds, i = b / kXcds;
+            if (nb < kXcdBlockJobs) {
+                const uint32_t per = nb / kXcds, rem = nb % kXcds, n = per + (x < rem ? 1 : 0);
+                const uint32_t lo = x * per + (x < rem ? x : rem);
+                CHECK(t >= lo && t < lo + n);                               // in the XCD's eighth
+                CHECK(t - lo == (i + x * (n / kXcds)) % n);                 // walked from the staggered start
+            } else {
+                const uint32_t full = nb / (kXcds * kXcdBlock);
+                if (b >= full * kXcds * kXcdBlock) {
+                    CHECK(t == b);                                          // the tail keeps the launch order
+                } else {
+                    CHECK((t / kXcdBlock) % kXcds == x);                    // a block dealt to this XCD
+                    CHECK(t / kXcdBlock / kXcds == i / kXcdBlock && t % kXcdBlock == i % kXcdBlock);
+                }
+            }
+        }
+    }
+}
+
 int main()
 {
+    test_tile_order();
     for (uint64_t s = 1; s <= 12; ++s) test_arena(s);
     test_ring_runs(3);
     test_flat_and_validation();

@@ -578,10 +578,13 @@ def test_incremental_chain_in_tight_arena(pcs):
     c.close()
 
 
-def test_kernel_timing_counts_and_resets(ctx, pcs):
-    """pcs_set_timing / pcs_kernel_time: while enabled, every launch of a
-    family is counted with a positive duration; a query resets the family;
-    launches made while disabled are not counted."""
+@pytest.mark.parametrize("dispatch", [False, True])
+def test_kernel_timing_counts_and_resets(ctx, pcs, dispatch):
+    """pcs_set_timing / pcs_kernel_time, both modes (events around each
+    launch; the dispatches' own timestamps): while enabled, every launch of
+    a family is counted with a positive duration; a query resets the family;
+    launches made while disabled are not counted; a mode other than 0, 1
+    or 2 is refused."""
     rng = np.random.default_rng(40)
     a = rng.integers(0, 256, size=300 * 4096 + 5, dtype=np.uint8)
     d = dev(a)
@@ -589,7 +592,9 @@ def test_kernel_timing_counts_and_resets(ctx, pcs):
     for fam in ("pack", "copy", "pack_hash", "merkle"):
         ctx.kernel_time(fam)
     s = ctx.checkpoint([pcs.flat(d)])            # not timed
-    ctx.set_timing(True)
+    with pytest.raises(pcs.PcsError):
+        ctx._check(pcs._lib.lib().pcs_set_timing(ctx._h, 3))
+    ctx.set_timing(True, dispatch=dispatch)
     for _ in range(3):
         ctx.restore(s, [pcs.flat(out)])
     s2 = ctx.checkpoint([pcs.flat(d)], hash=True)
