@@ -1304,7 +1304,10 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     } else if (exact) {
         bump.host = &c->counts_dev[0];
     }
-    // On an error before the call is recorded as pending, its claim goes back.
+    // On an error before the call is recorded as pending, its claim goes back
+    // and the segment closes: a scan this call had already enqueued moves the
+    // device's bump word below the slots the host counts, so no later call
+    // may be placed after it in this segment (a new segment resets the word).
     bool recorded = !seg;
     struct Undo {
         pcs_ctx *c;
@@ -1317,6 +1320,8 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
             if (recorded) return;
             seg->claim -= worst;
             --seg->pending;
+            seg->open = false;
+            if (c->seg == seg) c->seg.reset();
             c->free_pairs.push_back(pair);
             retire_if_idle(c, seg);
         }
