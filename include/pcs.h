@@ -372,24 +372,28 @@ int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
  * A bank is n_entries entries held as nparts component arrays (struct of
  * arrays, e.g. latents and poses); part p's entry i is entry_bytes bytes at
  * src + i * entry_bytes.  d_scores holds n_entries float32 relevance scores
- * on the device, supplied by the caller (e.g. pose distance to the anchor);
+ * on the device (4-byte aligned), supplied by the caller (e.g. pose distance to the anchor);
  * LOWER is more relevant.  Scores are ordered totally by their bit pattern:
  * -inf < ... < -0.0 < +0.0 < ... < +inf < every NaN; equal scores rank the
  * lower index first.  The call keeps the `keep` best-ranked entries and
  * writes them, in increasing original index order (a stable compaction), to
  * dst + j * entry_bytes, j = 0..keep-1, for every part.  dst == src shrinks
  * in place (through arena scratch); otherwise the keep * entry_bytes bytes
- * at dst must not overlap the n_entries * entry_bytes bytes at src.  If
+ * at dst must not overlap the n_entries * entry_bytes bytes at src.  No
+ * part's destination may overlap another part's source or destination.  If
  * d_kept is not NULL it receives the kept indices (keep uint32 values,
  * increasing).  Asynchronous on the context stream; a following incremental
  * checkpoint of the shrunk bank (parent = the bank's last snapshot) stores
  * only the chunks the shrink changed.
  *
  * Selection takes O(n_entries) work (a radix select of the keep-th score,
- * then index-ordered scans), in one workgroup.
+ * then index-ordered scans), in one workgroup: six streams over the scores
+ * at one CU's bandwidth.
  *
  * Limits and errors: n_entries <= 2^32 - 1 and keep <= n_entries, else
- * PCS_E_INVAL; nparts <= 64; entry_bytes > 0; PCS_E_NOMEM if the arena
+ * PCS_E_INVAL; nparts <= 64; entry_bytes > 0; misaligned scores and
+ * overlapping ranges as above
+ * are PCS_E_INVAL (nothing is moved); PCS_E_NOMEM if the arena
  * cannot hold the scratch (4 bytes per kept entry when d_kept is NULL, plus
  * the largest in-place part's keep * entry_bytes).
  */

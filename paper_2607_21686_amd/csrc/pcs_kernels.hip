@@ -1099,37 +1099,96 @@ __device__ __forceinline__ uint32_t score_key(uint32_t bits)
     return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
 }
 
-// Inclusive prefix sum across the 64 lanes of a wavefront.
+// Inclusive prefix sum across the 64 lanes of a wavefront, in DPP moves (no
+// LDS round trips): shifts by 1, 2, 4 and 8 lanes within each row of 16
+// lanes, then row 0's total (lane 15) into row 1 and row 2's into row 3
+// (row_bcast:15), then rows 0-1's total (lane 31) into rows 2 and 3
+// (row_bcast:31).  A lane whose source lies outside its row, or a row the
+// row mask leaves out, adds 0 (the `old` operand).
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
 {
-    const uint32_t lane = threadIdx.x & 63;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t y = (uint32_t)__shfl_up((int)x, d, 64);
-        if (lane >= (uint32_t)d) x += y;
-    }
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
     return x;
 }
 
-// Exclusive prefix sum of one value per thread over the 1024 threads of a
-// workgroup: wavefront scans, then one scan of the 16 wavefront totals.
-// Ends with a barrier.
-__device__ uint32_t block_excl_scan(uint32_t v, uint32_t *wsum)
+// hist[b] += 1 for every lane of the wavefront with m set.  AGG: lanes that
+// share the first such lane's bucket are added with one atomic (ties, the
+// common conflict, cost one LDS atomic per wavefront, not 64 serialised
+// ones); worth its extra steps on long streams only.
+template <bool AGG>
+__device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t b, bool m)
 {
-    const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
-    const uint32_t incl = wave_incl_scan(v);
-    if (lane == 63) wsum[wave] = incl;
-    __syncthreads();
-    if (wave == 0) {
-        const uint32_t w = lane < 16 ? wsum[lane] : 0;
-        const uint32_t wi = wave_incl_scan(w);
-        if (lane < 16) wsum[16 + lane] = wi - w;  // exclusive prefix of wavefront `lane`
+    if constexpr (!AGG) {
+        if (m) atomicAdd(&hist[b], 1u);
+        return;
     }
-    __syncthreads();
-    const uint32_t out = incl - v + wsum[16 + wave];
-    __syncthreads();
-    return out;
+    const uint64_t act = __ballot(m);
+    if (!act) return;
+    const int leader = __builtin_ctzll(act);
+    const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)b, leader);
+    const bool same = m && b == lb;
+    const uint64_t sm = __ballot(same);
+    if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[lb], (uint32_t)__popcll(sm));
+    else if (m && !same) atomicAdd(&hist[b], 1u);
 }
+
+// Set bits of a wavefront mask in the lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// How a selection reads its n scores.  The array starts head = (address mod
+// 16) / 4 scores past a 16-byte boundary; in the aligned view that starts
+// there (group g = scores 4g - head .. 4g - head + 3), the whole groups
+// [gf0, gf1) are read 16 bytes at a time, and the at most three scores before
+// them, [0, e_lo), and after them, [e_hi, n), one at a time.
+struct SelView {
+    uint64_t base;  // address of score -head (16-byte aligned)
+    uint64_t gf0, gf1, e_lo, e_hi;
+    uint32_t head;
+};
+__device__ __forceinline__ SelView sel_view(uint64_t scores, uint32_t n)
+{
+    SelView v;
+    v.head = (uint32_t)(scores & 15) / 4;
+    v.base = scores - 4 * v.head;
+    v.gf0 = v.head ? 1 : 0;
+    const uint64_t g1 = ((uint64_t)n + v.head) / 4;
+    v.gf1 = g1 > v.gf0 ? g1 : v.gf0;
+    v.e_lo = umin(n, 4 * v.gf0 - v.head);
+    const uint64_t hi = umin(n, 4 * v.gf1 - v.head);
+    v.e_hi = hi > v.e_lo ? hi : v.e_lo;
+    return v;
+}
+// Keys of U groups: group g0 + stride * u for u < U, or group `last` where
+// that lies at or past `end` (ok[u] false).  All U loads are issued before
+// any key is formed (a scheduling barrier keeps the compiler from moving each
+// load down to its first use, which would wait on them one at a time).
+template <int U>
+__device__ __forceinline__ void load_keys(const SelView &v, uint64_t g0, uint64_t stride, uint64_t end,
+                                          uint32_t (&k)[U][4], bool (&ok)[U])
+{
+    v4u32 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint64_t g = g0 + stride * u;
+        ok[u] = g < end;
+        x[u] = *(const g_v4u32 *)(v.base + 16 * (ok[u] ? g : end - 1));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) k[u][j] = score_key(x[u][j]);
+}
+// Key of score i, read alone.
+__device__ __forceinline__ uint32_t key_at(uint64_t scores, uint64_t i) { return score_key(((const g_u32 *)scores)[i]); }
 
 // Selection of a bank shrink in one workgroup of 1024 lanes, O(n): the
 // `keep` best-ranked entries (a smaller key, or an equal key at a lower
@@ -1139,27 +1198,70 @@ __device__ uint32_t block_excl_scan(uint32_t v, uint32_t *wsum)
 //      the keep-th smallest key (wavefront 0 finds it with a prefix sum over
 //      the 256 buckets), which ends as K*, with `need` = how many entries
 //      with key K* are kept (those with the lowest indices).
-//   2. Each lane takes a contiguous segment of indices and counts its keys
-//      below K* and equal to K*; a scan of the equal counts gives each
-//      segment the rank of its first K* key, hence how many entries the
-//      segment keeps; a scan of those gives where its kept indices go.
-//   3. Each lane writes its segment's kept indices, in order.
-__global__ __launch_bounds__(1024) void k_shrink_select(const uint32_t *__restrict__ scores, uint32_t n, uint32_t keep,
+//   2. The whole groups are cut into sixteen ranges of a multiple of 64
+//      groups, one per wavefront, which counts its keys below K* and equal to
+//      K*; the counts of the ranges before a range give the rank of its first
+//      K* key, hence how many entries it keeps, and where its kept indices
+//      go.  The single scores before and after the whole groups are ranges of
+//      their own, first and last.
+//   3. Each wavefront streams its range again, in index order, and compacts
+//      its kept indices with wavefront ballots; it stops once all of them
+//      are written.
+// Reads: U groups per lane in flight (8 for large banks, so that one CU keeps
+// enough loads in flight to stream the scores); a small bank (U = 1, at most
+// 1024 whole groups) is read once, each lane holding the one group it owns,
+// and every pass reuses it.  Wavefront 0 holds the single scores throughout,
+// one per lane.
+constexpr uint32_t kSelectWideEntries = 65536;  // larger banks take the 8-group selection
+template <int U>
+__global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_t n, uint32_t keep,
                                                         uint32_t *__restrict__ kept)
 {
+    // Per range: keys below K* (cnt[r]) and equal to K* (cnt[18 + r]); range 0
+    // = the single scores before the whole groups, 1 + w = wavefront w's
+    // groups, 17 = the single scores after.
     __shared__ uint32_t hist[256];
-    __shared__ uint32_t wsum[32];
+    __shared__ uint32_t cnt[36];
     __shared__ uint32_t pick[2];
-    const uint32_t t = threadIdx.x, lane = t & 63;
+    const uint32_t t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const SelView v = sel_view(scores, n);
+    const uint64_t nfull = v.gf1 - v.gf0, per = (nfull + 1023) / 1024 * 64;
+    const uint64_t w0 = v.gf0 + umin(wave * per, nfull), w1 = v.gf0 + umin(wave * per + per, nfull);
+    const bool resident = U == 1 && nfull <= 1024;
+
+    // Single score `lane` of [0, e_lo) ++ [e_hi, n), in wavefront 0.
+    const uint64_t ei = lane < v.e_lo ? lane : v.e_hi + (lane - v.e_lo);
+    const bool ein = wave == 0 && lane < 8 && ei < n && (lane < v.e_lo || ei >= v.e_hi);
+    const bool ehead = ein && lane < v.e_lo, etail = ein && lane >= v.e_lo;
+    uint32_t eraw = 0;
+    if (ein) eraw = ((const g_u32 *)scores)[ei];
+    uint32_t rk[1][4] = {{0, 0, 0, 0}};
+    bool rok[1] = {false};
+    if (resident && w0 < w1) load_keys<1>(v, w0 + lane, 64, w1, rk, rok);
+    const uint32_t ek = score_key(eraw);
+
     uint32_t prefix = 0, pmask = 0, need = keep;  // need: 1-based rank of K* among the candidates
     for (int p = 0; p < 4; ++p) {
         const uint32_t shift = 24 - 8 * p;
         if (t < 256) hist[t] = 0;
         __syncthreads();
-        for (uint32_t i = t; i < n; i += 1024) {
-            const uint32_t k = score_key(scores[i]);
-            if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+        if (resident) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                hist_add<(U > 1)>(hist, (rk[0][j] >> shift) & 255u, rok[0] && (rk[0][j] & pmask) == prefix);
+        } else {
+            for (uint64_t g0 = v.gf0; g0 < v.gf1; g0 += 1024ull * U) {
+                uint32_t k[U][4];
+                bool ok[U];
+                load_keys<U>(v, g0 + t, 1024, v.gf1, k, ok);
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        hist_add<(U > 1)>(hist, (k[u][j] >> shift) & 255u, ok[u] && (k[u][j] & pmask) == prefix);
+            }
         }
+        if (wave == 0) hist_add<(U > 1)>(hist, (ek >> shift) & 255u, ein && (ek & pmask) == prefix);
         __syncthreads();
         if (t < 64) {
             // Lane l holds buckets 4l..4l+3; the bucket where the running
@@ -1193,23 +1295,112 @@ __global__ __launch_bounds__(1024) void k_shrink_select(const uint32_t *__restri
         need = pick[1];
         __syncthreads();
     }
-    const uint32_t per = (n + 1023) / 1024;
-    const uint32_t s0 = t * per < n ? t * per : n, s1 = s0 + per < n ? s0 + per : n;
+
+    // 2. Counts per range (wavefront totals, the same in every lane).
     uint32_t lt = 0, eq = 0;
-    for (uint32_t i = s0; i < s1; ++i) {
-        const uint32_t k = score_key(scores[i]);
-        lt += k < prefix;
-        eq += k == prefix;
+    const auto count = [&](const uint32_t(&k)[4], bool ok) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            lt += (uint32_t)__popcll(__ballot(ok && k[j] < prefix));
+            eq += (uint32_t)__popcll(__ballot(ok && k[j] == prefix));
+        }
+    };
+    if (resident) {
+        count(rk[0], rok[0]);
+    } else {
+        for (uint64_t g0 = w0; g0 < w1; g0 += 64ull * U) {
+            uint32_t k[U][4];
+            bool ok[U];
+            load_keys<U>(v, g0 + lane, 64, w1, k, ok);
+#pragma unroll
+            for (int u = 0; u < U; ++u) count(k[u], ok[u]);
+        }
     }
-    const uint32_t eq_before = block_excl_scan(eq, wsum);
-    const uint32_t eq_kept = need > eq_before ? (need - eq_before < eq ? need - eq_before : eq) : 0;
-    uint32_t pos = block_excl_scan(lt + eq_kept, wsum);
-    uint32_t rank = eq_before;
-    for (uint32_t i = s0; i < s1; ++i) {
-        const uint32_t k = score_key(scores[i]);
-        bool take = k < prefix;
-        if (k == prefix) take = rank++ < need;
-        if (take) kept[pos++] = i;
+    if (lane == 0) {
+        cnt[1 + wave] = lt;
+        cnt[19 + wave] = eq;
+    }
+    if (wave == 0) {
+        const uint32_t a = (uint32_t)__popcll(__ballot(ehead && ek < prefix));
+        const uint32_t b = (uint32_t)__popcll(__ballot(ehead && ek == prefix));
+        const uint32_t c = (uint32_t)__popcll(__ballot(etail && ek < prefix));
+        const uint32_t d = (uint32_t)__popcll(__ballot(etail && ek == prefix));
+        if (lane == 0) {
+            cnt[0] = a;
+            cnt[18] = b;
+            cnt[17] = c;
+            cnt[35] = d;
+        }
+    }
+    __syncthreads();
+
+    // 3. Placement.  Kept entries (pos) and K* keys (rank) in the ranges
+    // before range r:
+    const auto range_start = [&](uint32_t r, uint32_t &pos, uint32_t &rank) {
+        pos = rank = 0;
+        for (uint32_t x = 0; x < r; ++x) {
+            const uint32_t e = cnt[18 + x];
+            pos += cnt[x] + (need > rank ? min(need - rank, e) : 0u);
+            rank += e;
+        }
+    };
+    if (wave == 0) {
+        // The single scores: lane order is index order within each range.
+        uint32_t ph, rh, pt, rt;
+        range_start(0, ph, rh);
+        range_start(17, pt, rt);
+        const uint64_t eqh = __ballot(ehead && ek == prefix), eqt = __ballot(etail && ek == prefix);
+        const uint32_t r = ehead ? rh + lanes_below(eqh) : rt + lanes_below(eqt);
+        const bool take = ein && (ek < prefix || (ek == prefix && r < need));
+        const uint64_t th = __ballot(ehead && take), tt = __ballot(etail && take);
+        if (take) kept[ehead ? ph + lanes_below(th) : pt + lanes_below(tt)] = (uint32_t)ei;
+    }
+    uint32_t pos, rank;
+    range_start(1 + wave, pos, rank);
+    const uint32_t pos_end = pos + lt + (need > rank ? min(need - rank, eq) : 0u);
+    // One group per lane, in index order (lane by lane, score by score);
+    // every lane of the wavefront takes part (ballots).  The K* keys and the
+    // kept entries before score j of this lane: those of the lanes below,
+    // then this lane's before j.
+    const auto place = [&](const uint32_t(&k)[4], bool ok, uint64_t g) {
+        uint64_t em[4], tm[4];
+        uint32_t r = rank, take = 0, o = pos;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            em[j] = __ballot(ok && k[j] == prefix);
+            r += lanes_below(em[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (!ok) continue;
+            if (k[j] < prefix) take |= 1u << j;
+            else if (k[j] == prefix && r++ < need) take |= 1u << j;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            tm[j] = __ballot((take >> j) & 1);
+            o += lanes_below(tm[j]);
+        }
+        const uint64_t e0 = 4 * g - v.head;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if ((take >> j) & 1) kept[o++] = (uint32_t)(e0 + j);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            rank += (uint32_t)__popcll(em[j]);
+            pos += (uint32_t)__popcll(tm[j]);
+        }
+    };
+    if (resident) {
+        if (pos < pos_end) place(rk[0], rok[0], w0 + lane);
+    } else {
+        for (uint64_t g0 = w0; g0 < w1 && pos < pos_end; g0 += 64ull * U) {
+            uint32_t k[U][4];
+            bool ok[U];
+            load_keys<U>(v, g0 + lane, 64, w1, k, ok);
+#pragma unroll
+            for (int u = 0; u < U; ++u) place(k[u], ok[u], g0 + 64ull * u + lane);
+        }
     }
 }
 
@@ -1432,7 +1623,11 @@ hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, 
 {
     if (n == 0 || keep == 0) return hipSuccess;
     if (keep > n) return hipErrorInvalidValue;
-    run_kernel(k_shrink_select, dim3(1), dim3(1024), s, reinterpret_cast<const uint32_t *>(scores), n, keep, kept);
+    if ((uint64_t)scores & 3) return hipErrorInvalidValue;
+    if (n > kSelectWideEntries)
+        run_kernel(k_shrink_select<8>, dim3(1), dim3(1024), s, (uint64_t)scores, n, keep, kept);
+    else
+        run_kernel(k_shrink_select<1>, dim3(1), dim3(1024), s, (uint64_t)scores, n, keep, kept);
     return hipGetLastError();
 }
 

@@ -1156,6 +1156,7 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
         return fail(c, PCS_E_INVAL, "keep %llu exceeds %llu entries", (unsigned long long)keep,
                     (unsigned long long)n_entries);
     if (n_entries && !d_scores) return fail(c, PCS_E_INVAL, "null scores");
+    if ((uint64_t)d_scores & 3) return fail(c, PCS_E_INVAL, "scores must be 4-byte aligned");
     uint64_t stage_bytes = 0;
     for (uint32_t p = 0; p < nparts; ++p) {
         const pcs_bank_part &q = parts[p];
@@ -1171,6 +1172,19 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
         else if (db && q.dst < q.src + sb && q.src < q.dst + db)
             return fail(c, PCS_E_INVAL, "part %u: destination overlaps the source bank", p);
     }
+    // The parts move one after another, so no part may write where another
+    // part reads or writes.
+    const auto overlap = [](uint64_t a, uint64_t na, uint64_t b, uint64_t nb) {
+        return na && nb && a < b + nb && b < a + na;
+    };
+    for (uint32_t p = 0; p < nparts && n_entries; ++p)
+        for (uint32_t q = 0; q < nparts; ++q) {
+            if (p == q) continue;
+            const pcs_bank_part &a = parts[p], &b = parts[q];
+            if (overlap(a.dst, keep * a.entry_bytes, b.src, n_entries * b.entry_bytes) ||
+                overlap(a.dst, keep * a.entry_bytes, b.dst, keep * b.entry_bytes))
+                return fail(c, PCS_E_INVAL, "part %u: destination overlaps part %u", p, q);
+        }
     if (n_entries == 0 || keep == 0) return PCS_OK;
     Temp t(c);
     Carver cv;

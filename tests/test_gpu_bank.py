@@ -68,11 +68,17 @@ def test_shrink_rejects_bad_arguments(pcs):
     ctx = pcs.Context(arena(16 << 20))
     before = ctx.arena_stats()
     a = torch.zeros(64 * 200, dtype=torch.uint8, device="cuda")   # room for 200 entries: the C checks decide
+    b = torch.zeros(64 * 200, dtype=torch.uint8, device="cuda")
+    y = torch.zeros(64 * 200, dtype=torch.uint8, device="cuda")
     s = scores_dev(np.arange(100, dtype=np.float32))
     bad = [
         ("keep > n", lambda: ctx.bank_shrink([(a, None, 64)], s, 101)),
         ("entry_bytes 0", lambda: ctx.bank_shrink([(a, None, 0)], s, 3)),
         ("overlap", lambda: ctx.bank_shrink([(a, a[64:], 64)], s, 10)),
+        # One part writes where another reads (in place on y), or two parts
+        # write the same bytes.
+        ("part dst over part src", lambda: ctx.bank_shrink([(b, y, 64), (y, None, 64)], s, 10)),
+        ("part dst over part dst", lambda: ctx.bank_shrink([(a, y, 64), (b, y[320:], 64)], s, 10)),
         ("too many entries", lambda: too_many()),
     ]
 
@@ -92,6 +98,70 @@ def test_shrink_rejects_bad_arguments(pcs):
         assert e.value.code == pcs.E_INVAL, name
         assert ctx.arena_stats() == before, name
     ctx.bank_shrink([(a, None, 64)], scores_dev(np.zeros(0, dtype=np.float32)), 0)   # empty bank: nothing to do
+    ctx.bank_shrink([(a, y, 64), (b, y[640:], 64)], s, 10)   # disjoint destinations in one buffer are fine
+    ctx.close()
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 4099, 70001])
+def test_shrink_selection_unaligned_scores(pcs, n):
+    """Scores that start 4, 8 or 12 bytes past a 16-byte boundary (the
+    selection reads 16-byte groups and takes the ragged head and tail one
+    score at a time): the kept indices match the oracle's."""
+    rng = np.random.default_rng(90 + n)
+    ctx = pcs.Context(arena(16 << 20))
+    s = tricky_scores(rng, n)
+    for off in (1, 2, 3):
+        big = torch.zeros(n + 4, dtype=torch.float32, device="cuda")
+        view = big[off:off + n]
+        view.copy_(torch.from_numpy(np.ascontiguousarray(s, dtype=np.float32)))
+        assert view.data_ptr() % 16 == 4 * off
+        for keep in sorted({1, (n + 1) // 2, n}):
+            log("bank shrink unaligned scores n", n, "offset", 4 * off, "keep", keep)
+            want_kept, _ = oracle.bank_shrink([], s, keep)
+            kept = torch.full((keep,), -1, dtype=torch.int32, device="cuda")
+            ctx.bank_shrink([], view, keep, kept)
+            assert host(kept).view(np.uint32).tolist() == want_kept.tolist()
+    ctx.close()
+
+
+def test_shrink_rejects_misaligned_scores(pcs):
+    import ctypes
+    from paper_2607_21686_amd import _lib
+    ctx = pcs.Context(arena(16 << 20))
+    s = scores_dev(np.arange(16, dtype=np.float32))
+    kept = torch.zeros(4, dtype=torch.int32, device="cuda")
+    st = _lib.lib().pcs_bank_shrink(ctx._h, None, 0, 8, s.data_ptr() + 2, 4, kept.data_ptr())
+    assert st == pcs.E_INVAL
+    assert b"aligned" in _lib.lib().pcs_last_error(ctx._h)
+    ctx.close()
+
+
+def test_shrink_selection_at_the_entry_limit(pcs):
+    """Selection alone (no parts) over 2^32 - 1 scores, the most the call
+    takes: every score 1.0 but a few planted lower ones, placed at both ends
+    and in the last segments of the selection's lanes, so that the strided
+    histogram loops and the last segment's bounds run up to 2^32.  The kept
+    indices are the planted ones plus the lowest-indexed ties."""
+    n = (1 << 32) - 1
+    log("bank shrink selection n", n)
+    ctx = pcs.Context(arena(16 << 20))
+    s = torch.full((n,), 1.0, dtype=torch.float32, device="cuda")
+    per = -(-n // 1024)
+    planted = {n - 1: -2.0, n - 2: 0.5, (1 << 32) - 1024: 0.0, 1022 * per + 5: -1.0, 1023 * per: 0.25, 7: 0.75,
+               per - 1: 0.5}
+    for i, v in planted.items():
+        s[i] = v
+    for keep in (len(planted), len(planted) + 3):
+        kept = torch.full((keep,), -1, dtype=torch.int32, device="cuda")
+        ctx.bank_shrink([], s, keep, kept)
+        ties = [i for i in range(10) if i not in planted][:keep - len(planted)]
+        assert host(kept).view(np.uint32).tolist() == sorted(list(planted) + ties)
+    # Only the two lowest: the last two lanes' segments hold them.
+    kept = torch.full((2,), -1, dtype=torch.int32, device="cuda")
+    ctx.bank_shrink([], s, 2, kept)
+    assert host(kept).view(np.uint32).tolist() == sorted([n - 1, 1022 * per + 5])
+    del s
+    torch.cuda.empty_cache()
     ctx.close()
 
 
