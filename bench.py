@@ -941,7 +941,7 @@ def run_shrink(args):
     out = _line(args, E * (le + pe) / t / 1e9, t * 1e3, "relevance-keyed shrink of the memory bank: 512 entries of "
                 "bf16 latents [16,60,104] + fp32 pose [7], keep 12%% (%d) by pose distance to the anchor, in place; "
                 "then an incremental checkpoint of the shrunk bank" % keep,
-                {"entries": E, "kept": keep, "bank_bytes": E * (le + pe)}, "shrink (rank, scan, place, gather)", alg,
+                {"entries": E, "kept": keep, "bank_bytes": E * (le + pe)}, "shrink (select, gather)", alg,
                 ms / args.steps, {"shrink_ms": round(ms / args.steps, 4),
                                   "incremental_checkpoint_ms": round(kt["incremental"][1] / args.steps, 4),
                                   "restore_full_bank_ms": round(kt["copy"][1] / args.steps, 4)})
