@@ -19,6 +19,8 @@
 // multiply work on the vector ALU.
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "pcs_device.h"
 
 // Device scratch of the allocation-free entry point (pcs_fingerprint_noalloc):
@@ -1083,6 +1085,20 @@ __global__ __launch_bounds__(1024) void k_classify_small(const ArgTables tab, ui
 constexpr int kPackLanes = 1024, kPackSlice = 512;
 constexpr int kHashLanes = 256, kHashSlice = 512;
 constexpr int kCopyLanes = 512, kCopySlice = 1024;
+// Fingerprint and diff tiles of jobs whose tables travel in the kernel
+// arguments take 1024 lanes up to a few rounds of groups: one workgroup per
+// CU then keeps the whole CU's loads in flight, where 256-lane tiles leave
+// part of a round's CUs with one tile and others with two (measured:
+// incremental checkpoints of flat 64-512 MiB 4-9% faster, the growing bank's
+// late steps 8%; fingerprints of flat 64-256 MiB 8-15%).  With device tables
+// a tile's first access is a dependent load of its group-map entry, which
+// four 256-lane tiles per CU hide and one 1024-lane tile does not (a wrapping
+// KV ring window: diff 115 -> 131 us, fingerprint 89 -> 106 us), so those
+// keep 256 lanes.  Above the bounds the wide tiles stop paying: a diff of
+// 4096 groups is even and one of 8192 groups 19% slower; a fingerprint of
+// 2048 groups is 5% faster on a flat buffer and 1.5% slower on a 64-run KV
+// ring window.
+constexpr uint64_t kWideDiffGroups = 2048, kWideHashGroups = 1024;
 constexpr int kSmallLanes = 256;  // sub-tiles of small jobs: 8 chunks per workgroup
 // A sub-tile moves whole chunks in one step (8 granules per lane): a small
 // job's time is a tile's latency, one load round trip per step.
@@ -1477,10 +1493,15 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
         return hipGetLastError();
     }
     if (split) return hipErrorInvalidValue;
+    constexpr bool kArgTab = std::is_same<Tab, ArgTables>::value;
     switch (mode) {
     case kModeHash:
-        run_kernel((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
-                   nodes, flag_mask, arena_base);
+        if (kArgTab && ngroups <= kWideHashGroups)
+            run_kernel((k_hash<Tab, kModeHash, kPackLanes, kHashSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
+                       nodes, flag_mask, arena_base);
+        else
+            run_kernel((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
+                       nodes, flag_mask, arena_base);
         break;
     case kModePack:
         if (stg.ticks)
@@ -1491,8 +1512,12 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
                        nodes, flag_mask, arena_base);
         break;
     case kModeDiff:
-        run_kernel((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
-                   nodes, flag_mask, arena_base);
+        if (kArgTab && ngroups <= kWideDiffGroups)
+            run_kernel((k_hash<Tab, kModeDiff, kPackLanes, kHashSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
+                       nodes, flag_mask, arena_base);
+        else
+            run_kernel((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
+                       nodes, flag_mask, arena_base);
         break;
     case kModeVerify:
         if (stg.ticks)

@@ -1,0 +1,94 @@
+"""GPU parity on both sides of the job sizes where fingerprint and diff
+tiles of argument-table jobs widen from 256 to 1024 lanes (fingerprints up
+to 1024 groups, incremental checkpoints up to 2048 groups): chunk
+fingerprints, buffer and session roots, the stored bytes of incremental
+checkpoints and their restores, against the oracle.  Three ragged buffers,
+so the tables travel in the kernel arguments."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_util import arena, dev, host, log, u64, zeros_u64
+
+pytestmark = pytest.mark.gpu
+
+GROUP = 64 * 4096
+
+
+@pytest.fixture(scope="module")
+def pcs():
+    import paper_2607_21686_amd as P
+    return P
+
+
+def sizes_for(groups):
+    # Buffers of groups - 2, 1 and 1 groups, the first and second ragged.
+    s = [(groups - 3) * GROUP + 5 * 4096 + 77, 37 * 4096 + 100, 3]
+    assert sum(-(-oracle.chunk_count(n) // 64) for n in s) == groups
+    return s
+
+
+@pytest.mark.parametrize("groups", [1024, 1025])
+def test_fingerprint_width_boundary(pcs, groups):
+    rng = np.random.default_rng([41, groups])
+    sizes = sizes_for(groups)
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    log("fingerprint width boundary:", groups, "groups")
+    h, r, s = oracle.fingerprint(bufs)
+    d = [dev(b) for b in bufs]
+    ctx = pcs.Context(arena(64 << 20))
+    try:
+        ch, rt, sr = zeros_u64(h.size), zeros_u64(len(sizes)), zeros_u64(1)
+        ctx.fingerprint([pcs.flat(t, n) for t, n in zip(d, sizes)], ch, rt, sr)
+        assert np.array_equal(u64(ch)[:h.size], h)
+        assert np.array_equal(u64(rt)[:len(sizes)], r)
+        assert int(u64(sr)[0]) == s
+    finally:
+        ctx.close()
+
+
+@pytest.mark.parametrize("groups", [2048, 2049])
+def test_incremental_width_boundary(pcs, groups):
+    rng = np.random.default_rng([43, groups])
+    sizes = sizes_for(groups)
+    cur = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    d = [dev(b) for b in cur]
+    log("incremental width boundary:", groups, "groups")
+    ctx = pcs.Context(arena(sum(sizes) + (160 << 20)))
+    try:
+        st = oracle.Store()
+        chain = [(ctx.checkpoint([pcs.flat(t, n) for t, n in zip(d, sizes)], hash=True), st.checkpoint(cur),
+                  [b.copy() for b in cur])]
+        total = sum(oracle.chunk_count(n) for n in sizes)
+        for step in range(2):
+            # Rewrite chunks spread over every buffer, the last (partial) ones included.
+            for b in cur:
+                nch = oracle.chunk_count(b.size)
+                for c in list(rng.integers(0, nch, size=40)) + [nch - 1]:
+                    a = int(c) * 4096
+                    b[a:min(b.size, a + 4096)] = rng.integers(0, 256, size=min(4096, b.size - a), dtype=np.uint8)
+            for t, b in zip(d, cur):
+                t.copy_(torch.from_numpy(b))
+            ch, rt, sr = zeros_u64(total), zeros_u64(len(sizes)), zeros_u64(1)
+            s = ctx.checkpoint([pcs.flat(t, n) for t, n in zip(d, sizes)], parent=chain[-1][0], chunk_hashes=ch,
+                               roots=rt, session_root=sr)
+            o = st.checkpoint(cur, chain[-1][1])
+            want_h, want_r, want_s = oracle.fingerprint(cur)
+            assert np.array_equal(u64(ch)[:total], want_h)
+            assert np.array_equal(u64(rt)[:len(sizes)], want_r) and int(u64(sr)[0]) == int(want_s)
+            inf = ctx.info(s)
+            assert inf["stored_bytes"] == st.payload(o).size
+            pay = torch.empty(max(1, inf["stored_bytes"]), dtype=torch.uint8, device="cuda")
+            ctx.payload(s, pay)
+            assert np.array_equal(host(pay)[:inf["stored_bytes"]], st.payload(o))
+            del pay
+            chain.append((s, o, [b.copy() for b in cur]))
+        for s, _, want in chain[1:]:
+            outs = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in sizes]
+            ctx.restore(s, [pcs.flat(t, n) for t, n in zip(outs, sizes)])
+            assert all(np.array_equal(host(t), w) for t, w in zip(outs, want))
+        for s, _, _ in reversed(chain):
+            ctx.delete(s)
+    finally:
+        ctx.close()
