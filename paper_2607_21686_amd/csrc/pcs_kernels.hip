@@ -19,6 +19,7 @@
 // multiply work on the vector ALU.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "pcs_device.h"
@@ -652,16 +653,62 @@ __global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ l
     }
 }
 
+// Promote-odd Merkle root of ls[0, m) already in LDS (m <= 4096), computed
+// by the workgroup (NT lanes); valid in thread 0.  Ends with a barrier.
+template <int NT>
+__device__ uint64_t reduce_lds(const uint64_t *ls, uint64_t m, uint64_t *lds2)
+{
+    constexpr uint32_t NW = NT / 64;
+    const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    uint64_t root = 0;
+    if (m == 0) {
+        root = empty_hash();
+    } else {
+        if (m > 64) {
+            const uint64_t nb = (m + 63) / 64;
+            for (uint64_t blk = wave; blk < nb; blk += NW) {
+                const uint32_t cnt = (uint32_t)umin(64, m - 64 * blk);
+                const uint64_t v = lane < cnt ? ls[64 * blk + lane] : 0;
+                const uint64_t r = wave_merkle(v, cnt);
+                if (lane == 0) lds2[blk] = r;
+            }
+            __syncthreads();
+            ls = lds2;
+            m = nb;
+        }
+        if (wave == 0) root = wave_merkle(lane < m ? ls[lane] : 0, (uint32_t)m);
+    }
+    __syncthreads();
+    return root;
+}
+
 // The lists of a small job, reduced by one workgroup of NT lanes: every
 // buffer list, then every session list over the buffer roots just computed
-// (kept in LDS).  Ends with a barrier.
+// (kept in LDS).  Buffer lists that follow each other in `in` and hold at
+// most 4096 values together (a job's buffers, the usual case) are loaded
+// into LDS in one pass, so the lists wait on one round trip to memory, not
+// one each.  Ends with a barrier.
 template <int NT>
 __device__ void merkle_lists(const ArgLists &L, const uint64_t *in, uint64_t *sa, uint64_t *sb, uint64_t *lds,
                              uint64_t *lds2, uint64_t *roots)
 {
+    bool one_pass = L.nbuf_lists > 0;
+    const uint64_t lo = one_pass ? L.lists[0].begin : 0;
+    uint64_t hi = lo;
+    for (uint32_t j = 0; j < L.nbuf_lists; ++j) {
+        one_pass = one_pass && L.lists[j].begin == hi;
+        hi = L.lists[j].begin + L.lists[j].count;
+    }
+    one_pass = one_pass && hi - lo <= 4096;
+    if (one_pass) {
+        for (uint64_t j = threadIdx.x; j < hi - lo; j += NT) lds[j] = in[lo + j];
+        __syncthreads();
+    }
     for (uint32_t j = 0; j < L.nbuf_lists; ++j) {
         const MerkleList &Lst = L.lists[j];
-        const uint64_t root = reduce_list<NT>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
+        const uint64_t root =
+            one_pass ? reduce_lds<NT>(lds + (Lst.begin - lo), Lst.count, lds2)
+                     : reduce_list<NT>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
         if (threadIdx.x == 0) {
             roots[j] = root;
             if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
@@ -792,6 +839,23 @@ __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
 
 // ---------------------------------------------------------------- incremental
 
+// Inclusive prefix sum across the 64 lanes of a wavefront, in DPP moves (no
+// LDS round trips): shifts by 1, 2, 4 and 8 lanes within each row of 16
+// lanes, then row 0's total (lane 15) into row 1 and row 2's into row 3
+// (row_bcast:15), then rows 0-1's total (lane 31) into rows 2 and 3
+// (row_bcast:31).  A lane whose source lies outside its row, or a row the
+// row mask leaves out, adds 0 (the `old` operand).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
+{
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    return x;
+}
+
 // A scan's entry j: the number of set bits of the 64-bit dirty mask of
 // group j of an incremental checkpoint.
 struct MaskBits {
@@ -879,6 +943,42 @@ __device__ __forceinline__ void compact_chunk(const JobBuf &jb, uint32_t b, uint
     }
 }
 
+// Exclusive scan of the dirty masks' set bits of a small incremental job
+// (at most kScanCompactMaxGroups groups): thread t holds the masks of groups
+// 4t .. 4t+3 (0 past the job), loaded when the kernel started; DPP
+// wavefront scans, then one over the 16 wavefront totals (counts stay below
+// 2^32).  Writes offsets[] (LDS or global) and returns the total in every
+// thread.  Ends with a barrier.
+__device__ uint64_t scan_masks_small(const uint64_t (&mk)[4], uint64_t ngroups, uint64_t *offsets, uint32_t *wsum)
+{
+    const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    uint32_t c[4], sum = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        c[k] = (uint32_t)__popcll(mk[k]);
+        sum += c[k];
+    }
+    const uint32_t incl = wave_incl_scan(sum);
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    if (wave == 0) {
+        const uint32_t w = lane < 16 ? wsum[lane] : 0;
+        const uint32_t wi = wave_incl_scan(w);
+        if (lane < 16) wsum[16 + lane] = wi - w;
+        if (lane == 15) wsum[32] = wi;
+    }
+    __syncthreads();
+    uint64_t run = incl - sum + wsum[16 + wave];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (4 * t + k < ngroups) offsets[4 * t + k] = run;
+        run += c[k];
+    }
+    const uint64_t total = wsum[32];
+    __syncthreads();
+    return total;
+}
+
 // Small incremental jobs (tables in the kernel arguments), after the
 // fingerprint + diff tiles, in one workgroup and one launch: the Merkle
 // lists (buffer and session roots), then the exclusive scan of the dirty
@@ -900,14 +1000,21 @@ __global__ __launch_bounds__(1024) void k_merkle_scan_small(const ArgLists L, co
     __shared__ uint64_t lds[4096];
     __shared__ uint64_t lds2[64];
     __shared__ uint64_t roots[kArgBufs];
-    __shared__ uint64_t sums[2][1024];
     __shared__ uint64_t offs[kCompact ? kScanCompactFusedGroups : 1];
     __shared__ uint64_t top_sh;
-    const uint64_t bump_now = threadIdx.x == 1023 && bump.bump && !bump.reset ? *bump.bump : 0;
+    __shared__ uint32_t wsum[33];
+    static_assert(kScanCompactMaxGroups <= 4 * 1024, "four dirty masks per thread");
+    // The masks are loaded first, so that their round trip to memory
+    // overlaps the Merkle reduction.
+    const uint32_t t = threadIdx.x;
+    uint64_t mk[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mk[k] = 4 * t + k < ngroups ? dirty_mask[4 * t + k] : 0;
+    const uint64_t bump_now = t == 1023 && bump.bump && !bump.reset ? *bump.bump : 0;
     merkle_lists<1024>(L, nodes, sa, sb, lds, lds2, roots);
-    if constexpr (kCompact) scan_counts(MaskBits{dirty_mask}, ngroups, offs, total, sums);
-    else scan_counts(MaskBits{dirty_mask}, ngroups, offsets, total, sums);
-    if (threadIdx.x == 1023) top_sh = place_slots(bump, *total, bump_now);
+    const uint64_t count = scan_masks_small(mk, ngroups, kCompact ? offs : offsets, wsum);
+    if (t == 0) *total = count;
+    if (t == 1023) top_sh = place_slots(bump, count, bump_now);
     if constexpr (kCompact) {
         __syncthreads();
         const uint64_t top = top_sh;
@@ -956,45 +1063,50 @@ __global__ __launch_bounds__(256) void k_pack_dirty(const Tab tab, const uint64_
 
 // Slot assignment and dirty copy in one launch (jobs above
 // kScanCompactFusedGroups groups, after the scan of the dirty masks): one
-// wavefront per chunk, four per 256-lane workgroup.  The wavefront of a
-// dirty chunk takes its slot (below the payload top in *top_word) from its
-// group's scanned offset and the set bits of the mask below it, as
-// compact_chunk; lane 0 enters the slot in the manifest and all 64 lanes
-// copy the chunk into it, 64 bytes per lane, zero-padding a partial chunk.
-// A clean chunk's wavefront does nothing (the diff tiles entered it).
+// wavefront per chunk, four per 256-lane workgroup, striding over the job's
+// chunk positions (64 per group) so that a large job launches no more than
+// kPlaceBlocks workgroups.  The wavefront of a dirty chunk takes its slot
+// (below the payload top in *top_word) from its group's scanned offset and
+// the set bits of the mask below it, as compact_chunk; lane 0 enters the
+// slot in the manifest and all 64 lanes copy the chunk into it, 64 bytes per
+// lane, zero-padding a partial chunk.  A clean chunk costs its wavefront one
+// (cached) mask load: the diff tiles entered it in the manifest.
+constexpr uint64_t kPlaceBlocks = 2048;  // 8192 wavefronts: eight workgroups per CU
 template <class Tab>
-__global__ __launch_bounds__(256) void k_place_dirty(const Tab tab, const uint64_t *__restrict__ dirty_mask,
+__global__ __launch_bounds__(256) void k_place_dirty(const Tab tab, uint64_t npos, const uint64_t *__restrict__ dirty_mask,
                                                      const uint64_t *__restrict__ offsets,
                                                      const uint64_t *__restrict__ top_word, uint64_t arena_base)
 {
     const uint32_t lane = threadIdx.x & 63;
-    const uint64_t gc = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // the job's 64 x (group) + chunk slot
-    const uint64_t G = gc / kGroupChunks;
-    const uint32_t c = (uint32_t)(gc % kGroupChunks);
-    const JobBuf &jb = tab.bufs[buf_index(tab, G)];
-    const uint64_t i = (G - jb.group_begin) * kGroupChunks + c;
-    if (i >= jb.nchunks) return;
-    const uint64_t mask = dirty_mask[G];
-    if (!((mask >> c) & 1)) return;  // clean: the diff tiles entered it in the manifest
-    g_u64 *man = (g_u64 *)jb.manifest;
-    const uint64_t slot = offsets[G] + (uint64_t)__popcll(c ? mask & ((1ULL << c) - 1) : 0);
-    const uint64_t top = *top_word;  // arena offset
-    if (lane == 0) man[i] = top - (slot + 1) * kChunk;
-    const uint64_t cb = i * kChunk;
-    const uint64_t len = umin(kChunk, jb.nbytes - cb);
-    const uint64_t dst = arena_base + top - (slot + 1) * kChunk;
-    uint4 v[4];
+    const uint64_t stride = (uint64_t)gridDim.x * 4;
+    for (uint64_t gc = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6); gc < npos; gc += stride) {
+        const uint64_t G = gc / kGroupChunks;
+        const uint32_t c = (uint32_t)(gc % kGroupChunks);
+        const uint64_t mask = dirty_mask[G];
+        if (!((mask >> c) & 1)) continue;
+        const JobBuf &jb = tab.bufs[buf_index(tab, G)];
+        const uint64_t i = (G - jb.group_begin) * kGroupChunks + c;
+        if (i >= jb.nchunks) continue;  // (a mask never sets such a bit)
+        g_u64 *man = (g_u64 *)jb.manifest;
+        const uint64_t slot = offsets[G] + (uint64_t)__popcll(c ? mask & ((1ULL << c) - 1) : 0);
+        const uint64_t top = *top_word;  // arena offset
+        if (lane == 0) man[i] = top - (slot + 1) * kChunk;
+        const uint64_t cb = i * kChunk;
+        const uint64_t len = umin(kChunk, jb.nbytes - cb);
+        const uint64_t dst = arena_base + top - (slot + 1) * kChunk;
+        uint4 v[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const uint32_t x = (k * 64 + lane) * 16;
-        v[k] = make_uint4(0, 0, 0, 0);
-        if (x < len) {
-            const uint64_t a = phys_addr(tab.runs, jb.run_begin, jb.run_count, cb + x);
-            v[k] = x + 16 <= len ? load16(a) : load_partial(a, (uint32_t)(len - x));
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t x = (k * 64 + lane) * 16;
+            v[k] = make_uint4(0, 0, 0, 0);
+            if (x < len) {
+                const uint64_t a = phys_addr(tab.runs, jb.run_begin, jb.run_count, cb + x);
+                v[k] = x + 16 <= len ? load16(a) : load_partial(a, (uint32_t)(len - x));
+            }
         }
-    }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) store16(dst + (k * 64 + lane) * 16, v[k]);
+        for (int k = 0; k < 4; ++k) store16(dst + (k * 64 + lane) * 16, v[k]);
+    }
 }
 
 // Copies n slots stored downwards from `top` into increasing order at dst
@@ -1113,23 +1225,6 @@ __device__ __forceinline__ uint32_t score_key(uint32_t bits)
 {
     if ((bits & 0x7F800000u) == 0x7F800000u && (bits & 0x007FFFFFu)) return 0xFFFFFFFFu;
     return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
-}
-
-// Inclusive prefix sum across the 64 lanes of a wavefront, in DPP moves (no
-// LDS round trips): shifts by 1, 2, 4 and 8 lanes within each row of 16
-// lanes, then row 0's total (lane 15) into row 1 and row 2's into row 3
-// (row_bcast:15), then rows 0-1's total (lane 31) into rows 2 and 3
-// (row_bcast:31).  A lane whose source lies outside its row, or a row the
-// row mask leaves out, adds 0 (the `old` operand).
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
-{
-    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
-    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
-    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
-    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
-    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
-    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
-    return x;
 }
 
 // hist[b] += 1 for every lane of the wavefront with m set.  AGG: lanes that
@@ -1573,8 +1668,9 @@ hipError_t launch_place_dirty(const Tab &tab, uint64_t ngroups, const uint64_t *
                               const uint64_t *top_word, uint64_t arena_base, hipStream_t s)
 {
     if (ngroups == 0) return hipSuccess;
-    run_kernel((k_place_dirty<Tab>), dim3((uint32_t)(ngroups * (kGroupChunks / 4))), dim3(256), s, tab, dirty_mask,
-               offsets, top_word, arena_base);
+    const uint64_t npos = ngroups * kGroupChunks;
+    const uint32_t blocks = (uint32_t)std::min<uint64_t>((npos + 3) / 4, kPlaceBlocks);
+    run_kernel((k_place_dirty<Tab>), dim3(blocks), dim3(256), s, tab, npos, dirty_mask, offsets, top_word, arena_base);
     return hipGetLastError();
 }
 

@@ -2,8 +2,9 @@
 tiles of argument-table jobs widen from 256 to 1024 lanes (fingerprints up
 to 1024 groups, incremental checkpoints up to 2048 groups): chunk
 fingerprints, buffer and session roots, the stored bytes of incremental
-checkpoints and their restores, against the oracle.  Three ragged buffers,
-so the tables travel in the kernel arguments."""
+checkpoints and their restores, against the oracle; and on both sides of
+the node count up to which a small job's Merkle lists load into LDS in one
+pass.  Three ragged buffers, so the tables travel in the kernel arguments."""
 import numpy as np
 import pytest
 import torch
@@ -90,5 +91,31 @@ def test_incremental_width_boundary(pcs, groups):
             assert all(np.array_equal(host(t), w) for t, w in zip(outs, want))
         for s, _, _ in reversed(chain):
             ctx.delete(s)
+    finally:
+        ctx.close()
+
+
+@pytest.mark.parametrize("groups", [4096, 4100])
+def test_merkle_lists_past_one_lds_pass(pcs, groups):
+    """Argument-table jobs whose buffer lists hold more than 4096 Merkle
+    nodes together reduce them list by list through memory instead of in
+    one LDS pass: both sides of that bound, fingerprints and the fused
+    checkpoint's roots against the oracle."""
+    rng = np.random.default_rng([47, groups])
+    sizes = sizes_for(groups)
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    log("merkle lists past one LDS pass:", groups, "groups")
+    h, r, s = oracle.fingerprint(bufs)
+    d = [dev(b) for b in bufs]
+    ctx = pcs.Context(arena(sum(sizes) + (64 << 20)))
+    try:
+        ch, rt, sr = zeros_u64(h.size), zeros_u64(len(sizes)), zeros_u64(1)
+        ctx.fingerprint([pcs.flat(t, n) for t, n in zip(d, sizes)], ch, rt, sr)
+        assert np.array_equal(u64(ch)[:h.size], h)
+        assert np.array_equal(u64(rt)[:len(sizes)], r) and int(u64(sr)[0]) == s
+        rt2, sr2 = zeros_u64(len(sizes)), zeros_u64(1)
+        snap = ctx.checkpoint([pcs.flat(t, n) for t, n in zip(d, sizes)], hash=True, roots=rt2, session_root=sr2)
+        assert np.array_equal(u64(rt2)[:len(sizes)], r) and int(u64(sr2)[0]) == s
+        ctx.delete(snap)
     finally:
         ctx.close()
