@@ -936,8 +936,10 @@ def run_shrink(args):
     t, kt = _timed(args, ctx, step, ["shrink", "incremental", "copy"])
     n, ms = kt["shrink"]
     kept = keep * (le + pe)
-    # In place: the kept entries are read and written twice (through scratch); scores read once.
-    alg = 4 * kept + 4 * E
+    # The kept entries read and written once, the scores read once.  (In place,
+    # a kept entry whose source is itself a destination also goes through a
+    # staging area: overhead, not counted.)
+    alg = 2 * kept + 4 * E
     out = _line(args, E * (le + pe) / t / 1e9, t * 1e3, "relevance-keyed shrink of the memory bank: 512 entries of "
                 "bf16 latents [16,60,104] + fp32 pose [7], keep 12%% (%d) by pose distance to the anchor, in place; "
                 "then an incremental checkpoint of the shrunk bank" % keep,

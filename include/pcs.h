@@ -378,7 +378,8 @@ int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
  * lower index first.  The call keeps the `keep` best-ranked entries and
  * writes them, in increasing original index order (a stable compaction), to
  * dst + j * entry_bytes, j = 0..keep-1, for every part.  dst == src shrinks
- * in place (through arena scratch); otherwise the keep * entry_bytes bytes
+ * in place (a kept entry whose source is itself a destination goes through
+ * arena scratch, the others move directly); otherwise the keep * entry_bytes bytes
  * at dst must not overlap the n_entries * entry_bytes bytes at src.  No
  * part's destination may overlap another part's source or destination.  If
  * d_kept is not NULL it receives the kept indices (keep uint32 values,
@@ -388,14 +389,14 @@ int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
  *
  * Selection takes O(n_entries) work (a radix select of the keep-th score,
  * then index-ordered scans), in one workgroup: six streams over the scores
- * at one CU's bandwidth.
+ * at one CU's bandwidth.  The moves of all parts share two launches (the
+ * staging of in-place sources, then the placement).
  *
  * Limits and errors: n_entries <= 2^32 - 1 and keep <= n_entries, else
  * PCS_E_INVAL; nparts <= 64; entry_bytes > 0; misaligned scores and
- * overlapping ranges as above
- * are PCS_E_INVAL (nothing is moved); PCS_E_NOMEM if the arena
- * cannot hold the scratch (4 bytes per kept entry when d_kept is NULL, plus
- * the largest in-place part's keep * entry_bytes).
+ * overlapping ranges as above are PCS_E_INVAL (nothing is moved);
+ * PCS_E_NOMEM if the arena cannot hold the scratch (4 bytes per kept entry
+ * when d_kept is NULL, plus keep * entry_bytes for every in-place part).
  */
 /*
  * Kept count of a shrink to a retained fraction (Sec. 7.5 holds the fraction

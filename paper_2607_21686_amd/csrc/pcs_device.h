@@ -125,9 +125,12 @@ hipError_t launch_flip_bit(uint64_t addr, hipStream_t s);
 // order of pcs_bank_shrink), in increasing order; one single-workgroup
 // launch (radix select, then index-ordered scans).
 hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept, hipStream_t s);
-// dst entry j <- src entry kept[j] (entry j when kept is null), count entries
-// of entry_bytes bytes.
-hipError_t launch_gather_entries(uint64_t src, uint64_t dst, uint64_t entry_bytes, const uint32_t *kept,
-                                 uint64_t count, hipStream_t s);
+// Bank shrink moves, all parts: dst entry j <- src entry kept[j], j < keep.
+// stage: the pass that copies, for in-place parts (stage != 0), the entries
+// a compaction would overwrite before reading them to their staging areas;
+// it must run before the place pass (stage false), which writes every
+// destination.
+hipError_t launch_move_entries(const ShrinkParts &parts, const uint32_t *kept, uint64_t keep, bool stage,
+                               hipStream_t s);
 
 }  // namespace pcs

@@ -1515,28 +1515,40 @@ __global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_
     }
 }
 
-// Moves kept entries of one bank part: destination entry j <- source entry
-// kept[j] (entry j itself when kept is null), eb bytes each, in G-byte
-// granules (eb and both bases are multiples of G).  Work item w is slice
-// w % spe of entry w / spe, 256 granules per slice; workgroups stride over
-// the items.
-template <int G>
-__global__ __launch_bounds__(256) void k_gather_entries(uint64_t src, uint64_t dst, uint64_t eb,
-                                                        const uint32_t *__restrict__ kept, uint64_t spe,
-                                                        uint64_t items)
+// Moves of a bank shrink, every part in one launch; work item w is slice sl
+// of kept entry j of the part whose items hold w (the part is the same for
+// all lanes of a workgroup).  Kept indices increase, so kept[j] >= j, and in
+// place the entries overwritten are the destinations j < keep.  A source
+// kept[j] < keep (other than j itself) is such a destination, written by
+// another item of the same pass: STAGE copies those sources to the part's
+// staging area (slot j) first.  The place pass then writes destination j
+// from the staging area, or straight from a source kept[j] >= keep, which no
+// destination overwrites, and in place skips kept[j] == j (already there).
+// Out-of-place parts gather straight from the source and do nothing in the
+// stage pass.
+__device__ __forceinline__ void move_granule(uint64_t a, uint64_t d, uint64_t g)
 {
-    for (uint64_t w = blockIdx.x; w < items; w += gridDim.x) {
-        const uint64_t j = w / spe, sl = w % spe;
-        const uint64_t x = (sl * 256 + threadIdx.x) * G;
-        if (x >= eb) continue;
-        const uint64_t si = kept ? kept[j] : j;
-        const uint64_t a = src + si * eb + x, d = dst + j * eb + x;
-        if constexpr (G == 16) {
-            store16_nt(d, load16_nt(a));
-        } else if constexpr (G == 4) {
-            *(g_u32 *)d = *(const g_u32 *)a;
-        } else {
-            *(g_u8 *)d = *(const g_u8 *)a;
+    if (g == 16) store16_nt(d, load16_nt(a));
+    else if (g == 4) *(g_u32 *)d = *(const g_u32 *)a;
+    else *(g_u8 *)d = *(const g_u8 *)a;
+}
+template <bool STAGE>
+__global__ __launch_bounds__(256) void k_move_entries(const ShrinkParts P, const uint32_t *__restrict__ kept,
+                                                      uint64_t keep)
+{
+    for (uint64_t w = blockIdx.x; w < P.items; w += gridDim.x) {
+        uint32_t p = 0;
+        while (p + 1 < P.n && P.p[p + 1].item_begin <= w) ++p;
+        const ShrinkPart &q = P.p[p];
+        const uint64_t r = w - q.item_begin, j = r / q.spe, x = ((r % q.spe) * 256 + threadIdx.x) * q.g;
+        if (x >= q.eb) continue;
+        const uint64_t e = kept[j];
+        const bool in_place = q.stage != 0;
+        if (STAGE) {
+            if (in_place && e < keep && e != j) move_granule(q.src + e * q.eb + x, q.stage + j * q.eb + x, q.g);
+        } else if (!(in_place && e == j)) {
+            const uint64_t a = in_place && e < keep ? q.stage + j * q.eb : q.src + e * q.eb;
+            move_granule(a + x, q.dst + j * q.eb + x, q.g);
         }
     }
 }
@@ -1752,21 +1764,14 @@ hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, 
     return hipGetLastError();
 }
 
-hipError_t launch_gather_entries(uint64_t src, uint64_t dst, uint64_t entry_bytes, const uint32_t *kept,
-                                 uint64_t count, hipStream_t s)
+hipError_t launch_move_entries(const ShrinkParts &parts, const uint32_t *kept, uint64_t keep, bool stage,
+                               hipStream_t s)
 {
-    if (count == 0 || entry_bytes == 0) return hipSuccess;
-    const auto aligned = [&](uint64_t g) { return entry_bytes % g == 0 && src % g == 0 && dst % g == 0; };
-    const int G = aligned(16) ? 16 : aligned(4) ? 4 : 1;
-    const uint64_t spe = (entry_bytes / G + 255) / 256;
-    const uint64_t items = count * spe;
-    const uint32_t grid = (uint32_t)(items < (1u << 20) ? items : (1u << 20));
-    if (G == 16)
-        run_kernel(k_gather_entries<16>, dim3(grid), dim3(256), s, src, dst, entry_bytes, kept, spe, items);
-    else if (G == 4)
-        run_kernel(k_gather_entries<4>, dim3(grid), dim3(256), s, src, dst, entry_bytes, kept, spe, items);
-    else
-        run_kernel(k_gather_entries<1>, dim3(grid), dim3(256), s, src, dst, entry_bytes, kept, spe, items);
+    if (parts.n > kShrinkParts) return hipErrorInvalidValue;
+    if (parts.items == 0) return hipSuccess;
+    const uint32_t grid = (uint32_t)std::min<uint64_t>(parts.items, 1u << 20);
+    if (stage) run_kernel(k_move_entries<true>, dim3(grid), dim3(256), s, parts, kept, keep);
+    else run_kernel(k_move_entries<false>, dim3(grid), dim3(256), s, parts, kept, keep);
     return hipGetLastError();
 }
 

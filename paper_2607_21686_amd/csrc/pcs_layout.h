@@ -129,4 +129,25 @@ static_assert(sizeof(ArgLists) + 256 <= 4096, "Merkle lists must fit in the kern
 // The small incremental launch passes both, with a few pointers and sizes.
 static_assert(sizeof(ArgLists) + sizeof(ArgTables) + 128 <= 4096, "Merkle lists and tables must fit together");
 
+// The entry moves of a bank shrink, every part in one launch.  Part p moves
+// the kept entries of entry_bytes eb from src to dst (stage: in place, the
+// staging area for entries the compaction would overwrite before reading
+// them; 0 out of place) in g-byte granules (16, 4 or 1, what the addresses
+// and eb allow), spe slices of 256 granules per entry; its work items are
+// [item_begin, item_begin + keep * spe).
+struct ShrinkPart {
+    uint64_t src, dst, stage;
+    uint64_t eb;
+    uint64_t item_begin;
+    uint64_t g, spe;
+};
+constexpr uint32_t kShrinkParts = 64;
+struct ShrinkParts {
+    uint32_t n;
+    uint32_t pad;
+    uint64_t items;
+    ShrinkPart p[kShrinkParts];
+};
+static_assert(sizeof(ShrinkParts) + 64 <= 4096, "shrink parts must fit in the kernel arguments");
+
 }  // namespace pcs

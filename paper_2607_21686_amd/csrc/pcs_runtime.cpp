@@ -1157,7 +1157,6 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
                     (unsigned long long)n_entries);
     if (n_entries && !d_scores) return fail(c, PCS_E_INVAL, "null scores");
     if ((uint64_t)d_scores & 3) return fail(c, PCS_E_INVAL, "scores must be 4-byte aligned");
-    uint64_t stage_bytes = 0;
     for (uint32_t p = 0; p < nparts; ++p) {
         const pcs_bank_part &q = parts[p];
         if (q.entry_bytes == 0) return fail(c, PCS_E_INVAL, "part %u: entry_bytes must be > 0", p);
@@ -1167,12 +1166,10 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
         const uint64_t sb = n_entries * q.entry_bytes, db = keep * q.entry_bytes;
         if (q.src > UINT64_MAX - sb || q.dst > UINT64_MAX - db)
             return fail(c, PCS_E_INVAL, "part %u: address range wraps", p);
-        if (q.dst == q.src)
-            stage_bytes = std::max(stage_bytes, db);
-        else if (db && q.dst < q.src + sb && q.src < q.dst + db)
+        if (q.dst != q.src && db && q.dst < q.src + sb && q.src < q.dst + db)
             return fail(c, PCS_E_INVAL, "part %u: destination overlaps the source bank", p);
     }
-    // The parts move one after another, so no part may write where another
+    // The parts move in the same launches, so no part may write where another
     // part reads or writes.
     const auto overlap = [](uint64_t a, uint64_t na, uint64_t b, uint64_t nb) {
         return na && nb && a < b + nb && b < a + na;
@@ -1186,42 +1183,49 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
                 return fail(c, PCS_E_INVAL, "part %u: destination overlaps part %u", p, q);
         }
     if (n_entries == 0 || keep == 0) return PCS_OK;
+    // Scratch: the kept indices (when the caller takes none) and, per
+    // in-place part, a staging area of keep entries (slot j holds the source
+    // of destination j when that source is itself a destination).
     Temp t(c);
     Carver cv;
-    uint64_t o_kept = 0, o_stage = 0;
+    uint64_t o_kept = 0;
+    std::vector<uint64_t> o_stage(nparts, 0);
     if (!d_kept) cv.add(&o_kept, 4 * keep);
-    if (stage_bytes) cv.add(&o_stage, stage_bytes);
+    for (uint32_t p = 0; p < nparts; ++p)
+        if (parts[p].dst == parts[p].src) cv.add(&o_stage[p], keep * parts[p].entry_bytes);
     uint64_t base = 0;
     if (cv.total) {
         if (int e = temp_alloc(c, t, cv.total)) return e;
         base = c->arena_dev + t.off;
     }
     uint32_t *kept = d_kept ? d_kept : (uint32_t *)(base + o_kept);
+    ShrinkParts P{};
+    P.n = nparts;
+    bool any_in_place = false;
+    for (uint32_t p = 0; p < nparts; ++p) {
+        const pcs_bank_part &q = parts[p];
+        ShrinkPart &sp = P.p[p];
+        sp.src = q.src;
+        sp.dst = q.dst;
+        sp.stage = q.dst == q.src ? base + o_stage[p] : 0;
+        sp.eb = q.entry_bytes;
+        const auto aligned = [&](uint64_t g) {
+            return q.entry_bytes % g == 0 && q.src % g == 0 && q.dst % g == 0 && sp.stage % g == 0;
+        };
+        sp.g = aligned(16) ? 16 : aligned(4) ? 4 : 1;
+        sp.spe = (q.entry_bytes / sp.g + 255) / 256;
+        sp.item_begin = P.items;
+        P.items += keep * sp.spe;
+        any_in_place = any_in_place || sp.stage != 0;
+    }
     if (int st = launch(c, "shrink", [&] {
             return launch_shrink_select(d_scores, (uint32_t)n_entries, (uint32_t)keep, kept, c->stream);
         }))
         return st;
-    for (uint32_t p = 0; p < nparts; ++p) {
-        const pcs_bank_part &q = parts[p];
-        if (q.dst != q.src) {
-            if (int st = launch(c, "shrink", [&] {
-                    return launch_gather_entries(q.src, q.dst, q.entry_bytes, kept, keep, c->stream);
-                }))
-                return st;
-            continue;
-        }
-        // In place: gather into scratch, then copy the kept prefix back.
-        const uint64_t stage = base + o_stage;
-        if (int st = launch(c, "shrink", [&] {
-                return launch_gather_entries(q.src, stage, q.entry_bytes, kept, keep, c->stream);
-            }))
+    if (any_in_place)
+        if (int st = launch(c, "shrink", [&] { return launch_move_entries(P, kept, keep, true, c->stream); }))
             return st;
-        if (int st = launch(c, "shrink", [&] {
-                return launch_gather_entries(stage, q.dst, q.entry_bytes, nullptr, keep, c->stream);
-            }))
-            return st;
-    }
-    return PCS_OK;
+    return launch(c, "shrink", [&] { return launch_move_entries(P, kept, keep, false, c->stream); });
 }
 
 int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent, uint32_t flags,

@@ -64,6 +64,38 @@ def test_shrink_matches_oracle(pcs, case):
     ctx.close()
 
 
+@pytest.mark.parametrize("n", [5, 300, 4099])
+def test_shrink_mixed_parts_in_one_call(pcs, n):
+    """Parts in place and out of place, with 16-, 4- and 1-byte granules, in
+    one call (the moves of every part share two launches): kept entries
+    against the oracle, for keep from 1 to n, so that kept sources inside and
+    outside the destination range, and entries already in place, all occur."""
+    rng = np.random.default_rng(80 + n)
+    ctx = pcs.Context(arena(64 << 20))
+    s = tricky_scores(rng, n)
+    sd = scores_dev(s)
+    sizes = [64, 28, 3, 200]
+    in_place = [True, False, True, False]
+    parts = [rng.integers(0, 256, size=n * eb, dtype=np.uint8) for eb in sizes]
+    for keep in sorted({1, 2, n // 2, n - 1, n}):
+        want_kept, want = oracle.bank_shrink(list(zip(parts, sizes)), s, keep)
+        log("bank shrink mixed parts n", n, "keep", keep)
+        srcs = [dev(p) for p in parts]
+        dsts = [None if ip else torch.full((max(1, keep * eb),), 0xA5, dtype=torch.uint8, device="cuda")
+                for eb, ip in zip(sizes, in_place)]
+        kept = torch.full((max(1, keep),), -1, dtype=torch.int32, device="cuda")
+        ctx.bank_shrink([(a, d, eb) for a, d, eb in zip(srcs, dsts, sizes)], sd, keep, kept)
+        assert host(kept).view(np.uint32)[:keep].tolist() == want_kept.tolist()
+        for p, a, d, eb, w, ip in zip(parts, srcs, dsts, sizes, want, in_place):
+            got = host(a if ip else d)
+            assert np.array_equal(got[:keep * eb], w)
+            if ip:
+                assert np.array_equal(got[keep * eb:], p[keep * eb:])
+            else:
+                assert np.array_equal(host(a), p)
+    ctx.close()
+
+
 def test_shrink_rejects_bad_arguments(pcs):
     ctx = pcs.Context(arena(16 << 20))
     before = ctx.arena_stats()
