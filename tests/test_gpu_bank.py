@@ -134,6 +134,30 @@ def test_shrink_rejects_bad_arguments(pcs):
     ctx.close()
 
 
+def test_shrink_refuses_when_scratch_does_not_fit(pcs):
+    """In place, each part needs keep entries of staging scratch in the arena:
+    an arena too small for it refuses the call with PCS_E_NOMEM before any
+    launch, and neither the bank nor the arena changes."""
+    ctx = pcs.Context(arena(2 << 20))
+    before = ctx.arena_stats()
+    rng = np.random.default_rng(5)
+    n, eb = 200, 64 << 10
+    bank = rng.integers(0, 256, size=n * eb, dtype=np.uint8)
+    a = dev(bank)
+    s = scores_dev(rng.random(n).astype(np.float32))
+    with pytest.raises(pcs.PcsError) as e:
+        ctx.bank_shrink([(a, None, eb)], s, 100)
+    assert e.value.code == pcs.E_NOMEM
+    assert np.array_equal(host(a), bank)
+    assert ctx.arena_stats() == before
+    # Out of place needs no staging: the same shrink into another buffer goes through.
+    out = torch.empty(100 * eb, dtype=torch.uint8, device="cuda")
+    ctx.bank_shrink([(a, out, eb)], s, 100)
+    want_kept, (want,) = oracle.bank_shrink([(bank, eb)], s.cpu().numpy(), 100)
+    assert np.array_equal(host(out), want)
+    ctx.close()
+
+
 @pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 4099, 70001])
 def test_shrink_selection_unaligned_scores(pcs, n):
     """Scores that start 4, 8 or 12 bytes past a 16-byte boundary (the
