@@ -118,8 +118,8 @@ TRAFFIC = {
                  ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
                   "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
     "verify": ("k_hash_verify_kv_ring_1gib_traffic.json",
-               [("verify", r"k_hash_staggered<pcs::\w+Tables, 3, 1024, 512, 64>",
-                 "k_hash_staggered<verify, 1024 lanes, 512 B slices, 64 chunks> (restore + fingerprint + compare, "
+               [("verify", r"k_hash_staggered<pcs::\w+Tables, 3, 1024, 1024, 64>",
+                 "k_hash_staggered<verify, 1024 lanes, 1 KiB slices, 64 chunks> (restore + fingerprint + compare, "
                  "first round staggered)"),
                 ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
                  "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (plain restore)")]),
