@@ -1185,14 +1185,16 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
     if (n_entries == 0 || keep == 0) return PCS_OK;
     // Scratch: the kept indices (when the caller takes none) and, per
     // in-place part, a staging area of keep entries (slot j holds the source
-    // of destination j when that source is itself a destination).
+    // of destination j when that source is itself a destination).  Keeping
+    // every entry leaves an in-place part as it is: it moves nothing.
+    const auto moves = [&](const pcs_bank_part &q) { return q.dst != q.src || keep < n_entries; };
     Temp t(c);
     Carver cv;
     uint64_t o_kept = 0;
     std::vector<uint64_t> o_stage(nparts, 0);
     if (!d_kept) cv.add(&o_kept, 4 * keep);
     for (uint32_t p = 0; p < nparts; ++p)
-        if (parts[p].dst == parts[p].src) cv.add(&o_stage[p], keep * parts[p].entry_bytes);
+        if (parts[p].dst == parts[p].src && moves(parts[p])) cv.add(&o_stage[p], keep * parts[p].entry_bytes);
     uint64_t base = 0;
     if (cv.total) {
         if (int e = temp_alloc(c, t, cv.total)) return e;
@@ -1207,7 +1209,7 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
         ShrinkPart &sp = P.p[p];
         sp.src = q.src;
         sp.dst = q.dst;
-        sp.stage = q.dst == q.src ? base + o_stage[p] : 0;
+        sp.stage = q.dst == q.src && moves(q) ? base + o_stage[p] : 0;
         sp.eb = q.entry_bytes;
         const auto aligned = [&](uint64_t g) {
             return q.entry_bytes % g == 0 && q.src % g == 0 && q.dst % g == 0 && sp.stage % g == 0;
@@ -1215,7 +1217,7 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
         sp.g = aligned(16) ? 16 : aligned(4) ? 4 : 1;
         sp.spe = (q.entry_bytes / sp.g + 255) / 256;
         sp.item_begin = P.items;
-        P.items += keep * sp.spe;
+        if (moves(q)) P.items += keep * sp.spe;  // else the part has no items
         any_in_place = any_in_place || sp.stage != 0;
     }
     if (int st = launch(c, "shrink", [&] {

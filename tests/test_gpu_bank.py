@@ -150,6 +150,11 @@ def test_shrink_refuses_when_scratch_does_not_fit(pcs):
     assert e.value.code == pcs.E_NOMEM
     assert np.array_equal(host(a), bank)
     assert ctx.arena_stats() == before
+    # Keeping every entry in place moves nothing and needs no staging.
+    kept = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    ctx.bank_shrink([(a, None, eb)], s, n, kept)
+    assert host(kept).view(np.uint32).tolist() == list(range(n))
+    assert np.array_equal(host(a), bank)
     # Out of place needs no staging: the same shrink into another buffer goes through.
     out = torch.empty(100 * eb, dtype=torch.uint8, device="cuda")
     ctx.bank_shrink([(a, out, eb)], s, 100)
