@@ -388,15 +388,17 @@ int pcs_import(pcs_ctx *ctx, const void *h_src, uint64_t size, pcs_snap *out);
  * only the chunks the shrink changed.
  *
  * Selection takes O(n_entries) work (a radix select of the keep-th score,
- * then index-ordered scans), in one workgroup: six streams over the scores
- * at one CU's bandwidth.  The moves of all parts share two launches (the
- * staging of in-place sources, then the placement).
+ * then index-ordered scans): one workgroup up to 32768 entries, else every
+ * CU in twelve launches (six streams over the scores).  The moves of all
+ * parts share two launches (the staging of in-place sources, then the
+ * placement).
  *
  * Limits and errors: n_entries <= 2^32 - 1 and keep <= n_entries, else
  * PCS_E_INVAL; nparts <= 64; entry_bytes > 0; misaligned scores and
  * overlapping ranges as above are PCS_E_INVAL (nothing is moved);
  * PCS_E_NOMEM if the arena cannot hold the scratch (4 bytes per kept entry
- * when d_kept is NULL, plus keep * entry_bytes for every in-place part).
+ * when d_kept is NULL, up to 530 KB of selection state above 32768 entries,
+ * plus keep * entry_bytes for every in-place part that moves).
  */
 /*
  * Kept count of a shrink to a retained fraction (Sec. 7.5 holds the fraction

@@ -122,9 +122,15 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
 // Flips the lowest bit of the byte at device address addr.
 hipError_t launch_flip_bit(uint64_t addr, hipStream_t s);
 // Bank shrink: kept = the indices of the `keep` best-ranked entries (score
-// order of pcs_bank_shrink), in increasing order; one single-workgroup
-// launch (radix select, then index-ordered scans).
-hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept, hipStream_t s);
+// order of pcs_bank_shrink), in increasing order: a radix select, then
+// index-ordered scans.  select_steps(n) launches, step 0 first: one
+// single-workgroup launch for small banks, else twelve (scratch: device
+// memory of select_scratch_bytes(n) bytes, 256-byte aligned, nothing to
+// clear).
+uint32_t select_steps(uint32_t n);
+uint64_t select_scratch_bytes(uint32_t n);
+hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept, uint64_t scratch,
+                                uint32_t step, hipStream_t s);
 // Bank shrink moves, all parts: dst entry j <- src entry kept[j], j < keep.
 // stage: the pass that copies, for in-place parts (stage != 0), the entries
 // a compaction would overwrite before reading them to their staging areas;

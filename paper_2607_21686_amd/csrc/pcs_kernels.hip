@@ -1282,8 +1282,8 @@ __device__ __forceinline__ SelView sel_view(uint64_t scores, uint32_t n)
     v.e_hi = hi > v.e_lo ? hi : v.e_lo;
     return v;
 }
-// Keys of U groups: group g0 + stride * u for u < U, or group `last` where
-// that lies at or past `end` (ok[u] false).  All U loads are issued before
+// Keys of U groups: group g0 + stride * u for u < U, or group end - 1 where
+// that lies at or past `end` (ok[u] false; a valid address, its keys unused).  All U loads are issued before
 // any key is formed (a scheduling barrier keeps the compiler from moving each
 // load down to its first use, which would wait on them one at a time).
 template <int U>
@@ -1306,30 +1306,141 @@ __device__ __forceinline__ void load_keys(const SelView &v, uint64_t g0, uint64_
 // Key of score i, read alone.
 __device__ __forceinline__ uint32_t key_at(uint64_t scores, uint64_t i) { return score_key(((const g_u32 *)scores)[i]); }
 
-// Selection of a bank shrink in one workgroup of 1024 lanes, O(n): the
-// `keep` best-ranked entries (a smaller key, or an equal key at a lower
-// index, ranks first) in increasing index order.
+// The single scores a selection reads one at a time (before and after the
+// whole groups), one per lane of wavefront 0: lane l < 8 holds score l of
+// [0, e_lo) ++ [e_hi, n).  `raw` is loaded at once; its key is formed later,
+// so that the load overlaps others.
+struct SelSingle {
+    uint64_t i;
+    bool in, head, tail;
+    uint32_t raw;
+};
+__device__ __forceinline__ SelSingle sel_single(const SelView &v, uint64_t scores, uint32_t n, uint32_t lane,
+                                                bool wave0)
+{
+    SelSingle s;
+    s.i = lane < v.e_lo ? lane : v.e_hi + (lane - v.e_lo);
+    s.in = wave0 && lane < 8 && s.i < n && (lane < v.e_lo || s.i >= v.e_hi);
+    s.head = s.in && lane < v.e_lo;
+    s.tail = s.in && lane >= v.e_lo;
+    s.raw = 0;
+    if (s.in) s.raw = ((const g_u32 *)scores)[s.i];
+    return s;
+}
+
+// One radix-select pass's choice, in wavefront 0: lane l holds buckets
+// 4l..4l+3 of the histogram, and the bucket where the running count first
+// reaches `need` is the one.  True in the one lane that finds it, with the
+// bucket and the rank of the keep-th key among that bucket's keys.
+__device__ __forceinline__ bool pick_bucket(const uint32_t *hist, uint32_t need, uint32_t lane, uint32_t &bucket,
+                                            uint32_t &rest)
+{
+    const uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2], h3 = hist[4 * lane + 3];
+    const uint32_t sum = h0 + h1 + h2 + h3;
+    const uint32_t incl = wave_incl_scan(sum);
+    uint32_t cum = incl - sum;
+    if (!(cum < need && incl >= need)) return false;
+    uint32_t d = 4 * lane;
+    if (cum + h0 < need) {
+        cum += h0;
+        ++d;
+        if (cum + h1 < need) {
+            cum += h1;
+            ++d;
+            if (cum + h2 < need) {
+                cum += h2;
+                ++d;
+            }
+        }
+    }
+    bucket = d;
+    rest = need - cum;
+    return true;
+}
+
+// Counts of keys below and equal to K* among the single scores (head pair,
+// tail pair); every lane of wavefront 0 gets them.
+__device__ __forceinline__ void count_singles(const SelSingle &s, uint32_t key, uint32_t prefix, uint32_t (&c)[4])
+{
+    c[0] = (uint32_t)__popcll(__ballot(s.head && key < prefix));
+    c[1] = (uint32_t)__popcll(__ballot(s.head && key == prefix));
+    c[2] = (uint32_t)__popcll(__ballot(s.tail && key < prefix));
+    c[3] = (uint32_t)__popcll(__ballot(s.tail && key == prefix));
+}
+
+// Writes the kept single scores, wavefront 0: lane order is index order
+// within the head and the tail; (ph, rh) and (pt, rt) are the kept entries
+// and K* keys before each.
+__device__ __forceinline__ void place_singles(const SelSingle &s, uint32_t key, uint32_t prefix, uint32_t need,
+                                              uint32_t ph, uint32_t rh, uint32_t pt, uint32_t rt,
+                                              uint32_t *__restrict__ kept)
+{
+    const uint64_t eqh = __ballot(s.head && key == prefix), eqt = __ballot(s.tail && key == prefix);
+    const uint32_t r = s.head ? rh + lanes_below(eqh) : rt + lanes_below(eqt);
+    const bool take = s.in && (key < prefix || (key == prefix && r < need));
+    const uint64_t th = __ballot(s.head && take), tt = __ballot(s.tail && take);
+    if (take) kept[s.head ? ph + lanes_below(th) : pt + lanes_below(tt)] = (uint32_t)s.i;
+}
+
+// Writes the kept indices of one whole group per lane of a wavefront, in
+// index order (lane by lane, score by score); every lane takes part
+// (ballots).  The K* keys and kept entries before score j of a lane: those
+// of the lanes below, then its own before j.  pos and rank (kept entries and
+// K* keys before this wavefront's groups) advance, the same in every lane.
+__device__ __forceinline__ void place_group(const uint32_t (&k)[4], bool ok, uint64_t g, uint32_t head,
+                                            uint32_t prefix, uint32_t need, uint32_t &pos, uint32_t &rank,
+                                            uint32_t *__restrict__ kept)
+{
+    uint64_t em[4], tm[4];
+    uint32_t r = rank, take = 0, o = pos;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        em[j] = __ballot(ok && k[j] == prefix);
+        r += lanes_below(em[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (!ok) continue;
+        if (k[j] < prefix) take |= 1u << j;
+        else if (k[j] == prefix && r++ < need) take |= 1u << j;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        tm[j] = __ballot((take >> j) & 1);
+        o += lanes_below(tm[j]);
+    }
+    const uint64_t e0 = 4 * g - head;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if ((take >> j) & 1) kept[o++] = (uint32_t)(e0 + j);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        rank += (uint32_t)__popcll(em[j]);
+        pos += (uint32_t)__popcll(tm[j]);
+    }
+}
+
+// Selection of a bank of at most kSelectOneWorkgroupEntries scores in one
+// workgroup of 1024 lanes: the `keep` best-ranked entries (a smaller key, or
+// an equal key at a lower index, ranks first) in increasing index order.
 //   1. Radix select, most significant byte first: four passes histogram the
 //      candidates' next byte (LDS atomics) and narrow to the bucket that holds
 //      the keep-th smallest key (wavefront 0 finds it with a prefix sum over
 //      the 256 buckets), which ends as K*, with `need` = how many entries
 //      with key K* are kept (those with the lowest indices).
-//   2. The whole groups are cut into sixteen ranges of a multiple of 64
-//      groups, one per wavefront, which counts its keys below K* and equal to
-//      K*; the counts of the ranges before a range give the rank of its first
-//      K* key, hence how many entries it keeps, and where its kept indices
-//      go.  The single scores before and after the whole groups are ranges of
-//      their own, first and last.
-//   3. Each wavefront streams its range again, in index order, and compacts
-//      its kept indices with wavefront ballots; it stops once all of them
-//      are written.
-// Reads: U groups per lane in flight (8 for large banks, so that one CU keeps
-// enough loads in flight to stream the scores); a small bank (U = 1, at most
-// 1024 whole groups) is read once, each lane holding the one group it owns,
-// and every pass reuses it.  Wavefront 0 holds the single scores throughout,
-// one per lane.
-constexpr uint32_t kSelectWideEntries = 65536;  // larger banks take the 8-group selection
-template <int U>
+//   2. Sixteen ranges of a multiple of 64 whole groups, one per wavefront
+//      (up to 1024 groups each lane holds its one group, read once for every
+//      pass), count their keys below K* and equal to K*; the counts of the ranges before a range give the rank
+//      of its first K* key, hence how many entries it keeps, and where its
+//      kept indices go.  The single scores before and after the whole groups
+//      are ranges of their own, first and last, held by wavefront 0.
+//   3. Each wavefront compacts its kept indices with ballots.
+// Larger banks take the multi-workgroup selection (k_sel_*), which follows
+// the same steps with a launch per pass.
+// Up to here one workgroup is faster (26 us at 16384 scores, 45 us at 32768)
+// than the twelve launches of the multi-workgroup selection (55 us at 16385
+// to 65536, 69 us at 2^20, 1.7 ms at 2^28 where one workgroup took 330 ms).
+constexpr uint32_t kSelectOneWorkgroupEntries = 32768;
 __global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_t n, uint32_t keep,
                                                         uint32_t *__restrict__ kept)
 {
@@ -1343,18 +1454,12 @@ __global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_
     const SelView v = sel_view(scores, n);
     const uint64_t nfull = v.gf1 - v.gf0, per = (nfull + 1023) / 1024 * 64;
     const uint64_t w0 = v.gf0 + umin(wave * per, nfull), w1 = v.gf0 + umin(wave * per + per, nfull);
-    const bool resident = U == 1 && nfull <= 1024;
-
-    // Single score `lane` of [0, e_lo) ++ [e_hi, n), in wavefront 0.
-    const uint64_t ei = lane < v.e_lo ? lane : v.e_hi + (lane - v.e_lo);
-    const bool ein = wave == 0 && lane < 8 && ei < n && (lane < v.e_lo || ei >= v.e_hi);
-    const bool ehead = ein && lane < v.e_lo, etail = ein && lane >= v.e_lo;
-    uint32_t eraw = 0;
-    if (ein) eraw = ((const g_u32 *)scores)[ei];
+    const bool resident = nfull <= 1024;  // each lane holds its one group for every pass
+    const SelSingle es = sel_single(v, scores, n, lane, wave == 0);
     uint32_t rk[1][4] = {{0, 0, 0, 0}};
     bool rok[1] = {false};
     if (resident && w0 < w1) load_keys<1>(v, w0 + lane, 64, w1, rk, rok);
-    const uint32_t ek = score_key(eraw);
+    const uint32_t ek = score_key(es.raw);
 
     uint32_t prefix = 0, pmask = 0, need = keep;  // need: 1-based rank of K* among the candidates
     for (int p = 0; p < 4; ++p) {
@@ -1364,46 +1469,23 @@ __global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_
         if (resident) {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                hist_add<(U > 1)>(hist, (rk[0][j] >> shift) & 255u, rok[0] && (rk[0][j] & pmask) == prefix);
+                hist_add<false>(hist, (rk[0][j] >> shift) & 255u, rok[0] && (rk[0][j] & pmask) == prefix);
         } else {
-            for (uint64_t g0 = v.gf0; g0 < v.gf1; g0 += 1024ull * U) {
-                uint32_t k[U][4];
-                bool ok[U];
-                load_keys<U>(v, g0 + t, 1024, v.gf1, k, ok);
+            for (uint64_t g0 = w0; g0 < w1; g0 += 64) {
+                uint32_t k[1][4];
+                bool ok[1];
+                load_keys<1>(v, g0 + lane, 64, w1, k, ok);
 #pragma unroll
-                for (int u = 0; u < U; ++u)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        hist_add<(U > 1)>(hist, (k[u][j] >> shift) & 255u, ok[u] && (k[u][j] & pmask) == prefix);
+                for (int j = 0; j < 4; ++j)
+                    hist_add<false>(hist, (k[0][j] >> shift) & 255u, ok[0] && (k[0][j] & pmask) == prefix);
             }
         }
-        if (wave == 0) hist_add<(U > 1)>(hist, (ek >> shift) & 255u, ein && (ek & pmask) == prefix);
+        if (wave == 0) hist_add<false>(hist, (ek >> shift) & 255u, es.in && (ek & pmask) == prefix);
         __syncthreads();
-        if (t < 64) {
-            // Lane l holds buckets 4l..4l+3; the bucket where the running
-            // count first reaches `need` is the one.
-            const uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1], h2 = hist[4 * lane + 2],
-                           h3 = hist[4 * lane + 3];
-            const uint32_t sum = h0 + h1 + h2 + h3;
-            const uint32_t incl = wave_incl_scan(sum);
-            uint32_t cum = incl - sum;
-            if (cum < need && incl >= need) {
-                uint32_t d = 4 * lane;
-                if (cum + h0 < need) {
-                    cum += h0;
-                    ++d;
-                    if (cum + h1 < need) {
-                        cum += h1;
-                        ++d;
-                        if (cum + h2 < need) {
-                            cum += h2;
-                            ++d;
-                        }
-                    }
-                }
-                pick[0] = d;
-                pick[1] = need - cum;
-            }
+        uint32_t bucket, rest;
+        if (t < 64 && pick_bucket(hist, need, lane, bucket, rest)) {
+            pick[0] = bucket;
+            pick[1] = rest;
         }
         __syncthreads();
         prefix |= pick[0] << shift;
@@ -1424,12 +1506,11 @@ __global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_
     if (resident) {
         count(rk[0], rok[0]);
     } else {
-        for (uint64_t g0 = w0; g0 < w1; g0 += 64ull * U) {
-            uint32_t k[U][4];
-            bool ok[U];
-            load_keys<U>(v, g0 + lane, 64, w1, k, ok);
-#pragma unroll
-            for (int u = 0; u < U; ++u) count(k[u], ok[u]);
+        for (uint64_t g0 = w0; g0 < w1; g0 += 64) {
+            uint32_t k[1][4];
+            bool ok[1];
+            load_keys<1>(v, g0 + lane, 64, w1, k, ok);
+            count(k[0], ok[0]);
         }
     }
     if (lane == 0) {
@@ -1437,15 +1518,13 @@ __global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_
         cnt[19 + wave] = eq;
     }
     if (wave == 0) {
-        const uint32_t a = (uint32_t)__popcll(__ballot(ehead && ek < prefix));
-        const uint32_t b = (uint32_t)__popcll(__ballot(ehead && ek == prefix));
-        const uint32_t c = (uint32_t)__popcll(__ballot(etail && ek < prefix));
-        const uint32_t d = (uint32_t)__popcll(__ballot(etail && ek == prefix));
+        uint32_t c[4];
+        count_singles(es, ek, prefix, c);
         if (lane == 0) {
-            cnt[0] = a;
-            cnt[18] = b;
-            cnt[17] = c;
-            cnt[35] = d;
+            cnt[0] = c[0];
+            cnt[18] = c[1];
+            cnt[17] = c[2];
+            cnt[35] = c[3];
         }
     }
     __syncthreads();
@@ -1461,62 +1540,205 @@ __global__ __launch_bounds__(1024) void k_shrink_select(uint64_t scores, uint32_
         }
     };
     if (wave == 0) {
-        // The single scores: lane order is index order within each range.
         uint32_t ph, rh, pt, rt;
         range_start(0, ph, rh);
         range_start(17, pt, rt);
-        const uint64_t eqh = __ballot(ehead && ek == prefix), eqt = __ballot(etail && ek == prefix);
-        const uint32_t r = ehead ? rh + lanes_below(eqh) : rt + lanes_below(eqt);
-        const bool take = ein && (ek < prefix || (ek == prefix && r < need));
-        const uint64_t th = __ballot(ehead && take), tt = __ballot(etail && take);
-        if (take) kept[ehead ? ph + lanes_below(th) : pt + lanes_below(tt)] = (uint32_t)ei;
+        place_singles(es, ek, prefix, need, ph, rh, pt, rt, kept);
     }
     uint32_t pos, rank;
     range_start(1 + wave, pos, rank);
     const uint32_t pos_end = pos + lt + (need > rank ? min(need - rank, eq) : 0u);
-    // One group per lane, in index order (lane by lane, score by score);
-    // every lane of the wavefront takes part (ballots).  The K* keys and the
-    // kept entries before score j of this lane: those of the lanes below,
-    // then this lane's before j.
-    const auto place = [&](const uint32_t(&k)[4], bool ok, uint64_t g) {
-        uint64_t em[4], tm[4];
-        uint32_t r = rank, take = 0, o = pos;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            em[j] = __ballot(ok && k[j] == prefix);
-            r += lanes_below(em[j]);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (!ok) continue;
-            if (k[j] < prefix) take |= 1u << j;
-            else if (k[j] == prefix && r++ < need) take |= 1u << j;
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            tm[j] = __ballot((take >> j) & 1);
-            o += lanes_below(tm[j]);
-        }
-        const uint64_t e0 = 4 * g - v.head;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if ((take >> j) & 1) kept[o++] = (uint32_t)(e0 + j);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            rank += (uint32_t)__popcll(em[j]);
-            pos += (uint32_t)__popcll(tm[j]);
-        }
-    };
     if (resident) {
-        if (pos < pos_end) place(rk[0], rok[0], w0 + lane);
+        if (pos < pos_end) place_group(rk[0], rok[0], w0 + lane, v.head, prefix, need, pos, rank, kept);
     } else {
-        for (uint64_t g0 = w0; g0 < w1 && pos < pos_end; g0 += 64ull * U) {
-            uint32_t k[U][4];
-            bool ok[U];
-            load_keys<U>(v, g0 + lane, 64, w1, k, ok);
-#pragma unroll
-            for (int u = 0; u < U; ++u) place(k[u], ok[u], g0 + 64ull * u + lane);
+        for (uint64_t g0 = w0; g0 < w1 && pos < pos_end; g0 += 64) {
+            uint32_t k[1][4];
+            bool ok[1];
+            load_keys<1>(v, g0 + lane, 64, w1, k, ok);
+            place_group(k[0], ok[0], g0 + lane, v.head, prefix, need, pos, rank, kept);
         }
+    }
+}
+
+// ---- multi-workgroup selection (banks of more than kSelectOneWorkgroupEntries
+// scores).  The same steps as k_shrink_select, a launch each: k_sel_init,
+// then per radix pass k_sel_hist (every workgroup adds its LDS histogram
+// into the pass's device histogram) and k_sel_pick (one wavefront narrows the
+// prefix), then k_sel_count (keys below / equal to K* per wavefront range),
+// k_sel_scan (where each range's kept indices go) and k_sel_place.  The
+// whole groups are cut into one range of a multiple of 64 groups per
+// wavefront of the grid, read with 8 groups per lane in flight; range 0 and
+// range R - 1 are the single scores, held by wavefront 0 of workgroup 0.
+struct SelState {
+    uint32_t prefix, pmask, need, pad;
+    uint32_t hist[2][256];  // pass p adds into hist[p % 2]; pick p clears the other
+};
+constexpr int kSelU = 8;
+__device__ __forceinline__ void sel_wave_range(const SelView &v, uint64_t gw, uint64_t nwaves, uint64_t &w0,
+                                               uint64_t &w1)
+{
+    const uint64_t nfull = v.gf1 - v.gf0;
+    const uint64_t per = (nfull + 64 * nwaves - 1) / (64 * nwaves) * 64;
+    w0 = v.gf0 + umin(gw * per, nfull);
+    w1 = v.gf0 + umin(gw * per + per, nfull);
+}
+
+__global__ __launch_bounds__(256) void k_sel_init(SelState *__restrict__ st, uint32_t keep)
+{
+    if (threadIdx.x == 0) {
+        st->prefix = 0;
+        st->pmask = 0;
+        st->need = keep;
+    }
+    st->hist[0][threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(1024) void k_sel_hist(uint64_t scores, uint32_t n, SelState *__restrict__ st, int p)
+{
+    __shared__ uint32_t hist[256];
+    const uint32_t t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const SelView v = sel_view(scores, n);
+    const uint32_t shift = 24 - 8 * p, prefix = st->prefix, pmask = st->pmask;
+    if (t < 256) hist[t] = 0;
+    __syncthreads();
+    uint64_t w0, w1;
+    sel_wave_range(v, (uint64_t)blockIdx.x * 16 + wave, (uint64_t)gridDim.x * 16, w0, w1);
+    for (uint64_t g0 = w0; g0 < w1; g0 += 64ull * kSelU) {
+        uint32_t k[kSelU][4];
+        bool ok[kSelU];
+        load_keys<kSelU>(v, g0 + lane, 64, w1, k, ok);
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                hist_add<true>(hist, (k[u][j] >> shift) & 255u, ok[u] && (k[u][j] & pmask) == prefix);
+    }
+    if (blockIdx.x == 0 && wave == 0) {
+        const SelSingle es = sel_single(v, scores, n, lane, true);
+        const uint32_t ek = score_key(es.raw);
+        hist_add<true>(hist, (ek >> shift) & 255u, es.in && (ek & pmask) == prefix);
+    }
+    __syncthreads();
+    if (t < 256 && hist[t]) atomicAdd(&st->hist[p & 1][t], hist[t]);
+}
+
+__global__ __launch_bounds__(64) void k_sel_pick(SelState *__restrict__ st, int p)
+{
+    const uint32_t lane = threadIdx.x, shift = 24 - 8 * p;
+    uint32_t bucket, rest;
+    if (pick_bucket(st->hist[p & 1], st->need, lane, bucket, rest)) {
+        st->prefix |= bucket << shift;
+        st->pmask |= 255u << shift;
+        st->need = rest;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) st->hist[(p + 1) & 1][4 * lane + i] = 0;
+}
+
+// Range r's keys below K* (lt[r]) and equal to K* (eq[r]).
+__global__ __launch_bounds__(1024) void k_sel_count(uint64_t scores, uint32_t n, const SelState *__restrict__ st,
+                                                    uint32_t *__restrict__ lt_out, uint32_t *__restrict__ eq_out)
+{
+    const uint32_t t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const SelView v = sel_view(scores, n);
+    const uint32_t prefix = st->prefix;
+    const uint64_t gw = (uint64_t)blockIdx.x * 16 + wave, nwaves = (uint64_t)gridDim.x * 16;
+    uint64_t w0, w1;
+    sel_wave_range(v, gw, nwaves, w0, w1);
+    uint32_t lt = 0, eq = 0;
+    for (uint64_t g0 = w0; g0 < w1; g0 += 64ull * kSelU) {
+        uint32_t k[kSelU][4];
+        bool ok[kSelU];
+        load_keys<kSelU>(v, g0 + lane, 64, w1, k, ok);
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                lt += (uint32_t)__popcll(__ballot(ok[u] && k[u][j] < prefix));
+                eq += (uint32_t)__popcll(__ballot(ok[u] && k[u][j] == prefix));
+            }
+    }
+    if (lane == 0) {
+        lt_out[1 + gw] = lt;
+        eq_out[1 + gw] = eq;
+    }
+    if (blockIdx.x == 0 && wave == 0) {
+        const SelSingle es = sel_single(v, scores, n, lane, true);
+        uint32_t c[4];
+        count_singles(es, score_key(es.raw), prefix, c);
+        if (lane == 0) {
+            lt_out[0] = c[0];
+            eq_out[0] = c[1];
+            lt_out[nwaves + 1] = c[2];
+            eq_out[nwaves + 1] = c[3];
+        }
+    }
+}
+
+// Where each of the R ranges starts: the kept entries before it (pos) are
+// the keys below K* before it plus the first `need` K* keys, so pos =
+// LT + min(need, EQ) and rank = EQ for the exclusive prefix sums LT and EQ of
+// the counts.  One workgroup; every thread scans a contiguous segment.
+__global__ __launch_bounds__(1024) void k_sel_scan(const SelState *__restrict__ st, const uint32_t *__restrict__ lt,
+                                                   const uint32_t *__restrict__ eq, uint32_t R,
+                                                   uint32_t *__restrict__ pos_out, uint32_t *__restrict__ rank_out)
+{
+    __shared__ uint32_t wsum[2][33];
+    const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    const uint32_t per = (R + 1023) / 1024, s0 = min(t * per, R), s1 = min(s0 + per, R);
+    uint32_t a = 0, b = 0;
+    for (uint32_t r = s0; r < s1; ++r) {
+        a += lt[r];
+        b += eq[r];
+    }
+    const uint32_t ia = wave_incl_scan(a), ib = wave_incl_scan(b);
+    if (lane == 63) {
+        wsum[0][wave] = ia;
+        wsum[1][wave] = ib;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        const uint32_t x = lane < 16 ? wsum[0][lane] : 0, y = lane < 16 ? wsum[1][lane] : 0;
+        const uint32_t xi = wave_incl_scan(x), yi = wave_incl_scan(y);
+        if (lane < 16) {
+            wsum[0][16 + lane] = xi - x;
+            wsum[1][16 + lane] = yi - y;
+        }
+    }
+    __syncthreads();
+    const uint32_t need = st->need;
+    uint32_t LT = ia - a + wsum[0][16 + wave], EQ = ib - b + wsum[1][16 + wave];
+    for (uint32_t r = s0; r < s1; ++r) {
+        pos_out[r] = LT + min(need, EQ);
+        rank_out[r] = EQ;
+        LT += lt[r];
+        EQ += eq[r];
+    }
+}
+
+__global__ __launch_bounds__(1024) void k_sel_place(uint64_t scores, uint32_t n, const SelState *__restrict__ st,
+                                                    const uint32_t *__restrict__ pos_in,
+                                                    const uint32_t *__restrict__ rank_in, uint32_t *__restrict__ kept)
+{
+    const uint32_t t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const SelView v = sel_view(scores, n);
+    const uint32_t prefix = st->prefix, need = st->need;
+    const uint64_t gw = (uint64_t)blockIdx.x * 16 + wave, nwaves = (uint64_t)gridDim.x * 16;
+    if (blockIdx.x == 0 && wave == 0) {
+        const SelSingle es = sel_single(v, scores, n, lane, true);
+        place_singles(es, score_key(es.raw), prefix, need, pos_in[0], rank_in[0], pos_in[nwaves + 1],
+                      rank_in[nwaves + 1], kept);
+    }
+    uint64_t w0, w1;
+    sel_wave_range(v, gw, nwaves, w0, w1);
+    uint32_t pos = pos_in[1 + gw], rank = rank_in[1 + gw];
+    const uint32_t pos_end = pos_in[2 + gw];  // the next range's start
+    for (uint64_t g0 = w0; g0 < w1 && pos < pos_end; g0 += 64ull * kSelU) {
+        uint32_t k[kSelU][4];
+        bool ok[kSelU];
+        load_keys<kSelU>(v, g0 + lane, 64, w1, k, ok);
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u) place_group(k[u], ok[u], g0 + 64ull * u + lane, v.head, prefix, need, pos, rank, kept);
     }
 }
 
@@ -1757,15 +1979,54 @@ hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes
     return hipGetLastError();
 }
 
-hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept, hipStream_t s)
+// Scratch of a multi-workgroup selection: SelState, then lt, eq, pos and
+// rank arrays of R = 16 x workgroups + 2 ranges.
+constexpr uint32_t kSelBlocks = 2048;
+static uint32_t select_blocks(uint32_t n) { return std::max<uint32_t>(1, std::min<uint32_t>((n + 4095) / 4096, kSelBlocks)); }
+static uint64_t sel_array_bytes(uint32_t R) { return ((uint64_t)R * 4 + 255) / 256 * 256; }
+static uint64_t sel_state_bytes() { return (sizeof(SelState) + 255) / 256 * 256; }
+
+uint32_t select_steps(uint32_t n) { return n > kSelectOneWorkgroupEntries ? 12 : 1; }
+
+uint64_t select_scratch_bytes(uint32_t n)
+{
+    if (n <= kSelectOneWorkgroupEntries) return 0;
+    return sel_state_bytes() + 4 * sel_array_bytes(select_blocks(n) * 16 + 2);
+}
+
+hipError_t launch_shrink_select(const float *scores, uint32_t n, uint32_t keep, uint32_t *kept, uint64_t scratch,
+                                uint32_t step, hipStream_t s)
 {
     if (n == 0 || keep == 0) return hipSuccess;
-    if (keep > n) return hipErrorInvalidValue;
+    if (keep > n || step >= select_steps(n)) return hipErrorInvalidValue;
     if ((uint64_t)scores & 3) return hipErrorInvalidValue;
-    if (n > kSelectWideEntries)
-        run_kernel(k_shrink_select<8>, dim3(1), dim3(1024), s, (uint64_t)scores, n, keep, kept);
-    else
-        run_kernel(k_shrink_select<1>, dim3(1), dim3(1024), s, (uint64_t)scores, n, keep, kept);
+    const uint64_t sc = (uint64_t)scores;
+    if (n <= kSelectOneWorkgroupEntries) {
+        run_kernel(k_shrink_select, dim3(1), dim3(1024), s, sc, n, keep, kept);
+        return hipGetLastError();
+    }
+    if (!scratch || (scratch & 255)) return hipErrorInvalidValue;
+    const uint32_t B = select_blocks(n), R = B * 16 + 2;
+    SelState *st = (SelState *)scratch;
+    uint32_t *lt = (uint32_t *)(scratch + sel_state_bytes());
+    uint32_t *eq = (uint32_t *)((uint64_t)lt + sel_array_bytes(R));
+    uint32_t *pos = (uint32_t *)((uint64_t)eq + sel_array_bytes(R));
+    uint32_t *rank = (uint32_t *)((uint64_t)pos + sel_array_bytes(R));
+    if (step == 0) {
+        run_kernel(k_sel_init, dim3(1), dim3(256), s, st, keep);
+    } else if (step <= 8) {
+        const int p = (int)(step - 1) / 2;
+        if (step % 2) run_kernel(k_sel_hist, dim3(B), dim3(1024), s, sc, n, st, p);
+        else run_kernel(k_sel_pick, dim3(1), dim3(64), s, st, p);
+    } else if (step == 9) {
+        run_kernel(k_sel_count, dim3(B), dim3(1024), s, sc, n, (const SelState *)st, lt, eq);
+    } else if (step == 10) {
+        run_kernel(k_sel_scan, dim3(1), dim3(1024), s, (const SelState *)st, (const uint32_t *)lt,
+                   (const uint32_t *)eq, R, pos, rank);
+    } else {
+        run_kernel(k_sel_place, dim3(B), dim3(1024), s, sc, n, (const SelState *)st, (const uint32_t *)pos,
+                   (const uint32_t *)rank, kept);
+    }
     return hipGetLastError();
 }
 

@@ -1183,16 +1183,19 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
                 return fail(c, PCS_E_INVAL, "part %u: destination overlaps part %u", p, q);
         }
     if (n_entries == 0 || keep == 0) return PCS_OK;
-    // Scratch: the kept indices (when the caller takes none) and, per
-    // in-place part, a staging area of keep entries (slot j holds the source
-    // of destination j when that source is itself a destination).  Keeping
-    // every entry leaves an in-place part as it is: it moves nothing.
+    // Scratch: the kept indices (when the caller takes none), the state of a
+    // large bank's selection, and, per in-place part, a staging area of keep
+    // entries (slot j holds the source of destination j when that source is
+    // itself a destination).  Keeping every entry leaves an in-place part as
+    // it is: it moves nothing.
     const auto moves = [&](const pcs_bank_part &q) { return q.dst != q.src || keep < n_entries; };
     Temp t(c);
     Carver cv;
-    uint64_t o_kept = 0;
+    uint64_t o_kept = 0, o_sel = 0;
     std::vector<uint64_t> o_stage(nparts, 0);
     if (!d_kept) cv.add(&o_kept, 4 * keep);
+    const uint64_t sel_bytes = select_scratch_bytes((uint32_t)n_entries);
+    if (sel_bytes) cv.add(&o_sel, sel_bytes);
     for (uint32_t p = 0; p < nparts; ++p)
         if (parts[p].dst == parts[p].src && moves(parts[p])) cv.add(&o_stage[p], keep * parts[p].entry_bytes);
     uint64_t base = 0;
@@ -1220,10 +1223,13 @@ int pcs_bank_shrink(pcs_ctx *c, const pcs_bank_part *parts, uint32_t nparts, uin
         if (moves(q)) P.items += keep * sp.spe;  // else the part has no items
         any_in_place = any_in_place || sp.stage != 0;
     }
-    if (int st = launch(c, "shrink", [&] {
-            return launch_shrink_select(d_scores, (uint32_t)n_entries, (uint32_t)keep, kept, c->stream);
-        }))
-        return st;
+    for (uint32_t step = 0; step < select_steps((uint32_t)n_entries); ++step)
+        if (int st = launch(c, "shrink", [&] {
+                return launch_shrink_select(d_scores, (uint32_t)n_entries, (uint32_t)keep, kept,
+                                            sel_bytes ? base + o_sel : 0, step, c->stream);
+            }))
+            return st;
+    if (P.items == 0) return PCS_OK;  // no part moves (none given, or in place keeping every entry)
     if (any_in_place)
         if (int st = launch(c, "shrink", [&] { return launch_move_entries(P, kept, keep, true, c->stream); }))
             return st;
