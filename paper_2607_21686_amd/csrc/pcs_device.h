@@ -98,11 +98,16 @@ hipError_t launch_labels(const Tab &tab, const uint64_t *bitmap, uint8_t *labels
 constexpr uint64_t kClassifyFusedGroups = 1024;
 hipError_t launch_classify_small(const ArgTables &tab, uint64_t ngroups, const uint64_t *hashes, uint32_t K,
                                  uint64_t total, uint64_t *bitmap, uint8_t *labels, hipStream_t s);
+// Per-list Merkle reductions (one workgroup per list, or one for all the
+// lists of a small job).  pre: every buffer list of more than
+// kMerkleLdsValues values had its first level reduced by
+// launch_merkle_blocks (into scratch_a at the list's offset).
 hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_t *in,
                          uint64_t *scratch_a, uint64_t *scratch_b, uint64_t *roots_out,
-                         hipStream_t s);
+                         uint64_t max_count, bool pre, hipStream_t s);
 hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64_t *scratch_a,
-                               uint64_t *scratch_b, hipStream_t s);
+                               uint64_t *scratch_b, bool pre, hipStream_t s);
+hipError_t launch_merkle_blocks(const LongLists &lists, const uint64_t *in, uint64_t *scratch_a, hipStream_t s);
 // Exclusive scan of the set-bit counts of per-group dirty masks (offsets
 // and total), then the placement of the slots (SlotBump).
 hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets, uint64_t *total,

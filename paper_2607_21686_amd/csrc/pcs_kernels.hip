@@ -584,14 +584,15 @@ __global__ __launch_bounds__(T) void k_hash_staggered(const Tab tab, uint64_t *_
 // ---------------------------------------------------------------- Merkle lists
 
 // Promote-odd Merkle root of src[0, m), computed by the whole workgroup
-// (NT lanes); the result is valid in thread 0.  Aligned 64-value blocks
+// (NT lanes; pre: the first level of a list of more than 4096 values is
+// already in sa); the result is valid in thread 0.  Aligned 64-value blocks
 // reduce independently (one wavefront each); up to two passes through global
 // scratch sa/sb (each read only after it is fully written) bring the list to
 // <= 4096 values, then the rest happens in LDS.  Ends with a barrier so the
 // LDS buffers can be reused.
 template <int NT>
 __device__ uint64_t reduce_list(const uint64_t *src, uint64_t m, uint64_t *sa, uint64_t *sb, uint64_t *lds,
-                                uint64_t *lds2)
+                                uint64_t *lds2, bool pre)
 {
     constexpr uint32_t NW = NT / 64;  // wavefronts
     const uint32_t t = threadIdx.x, wave = t >> 6, lane = t & 63;
@@ -601,12 +602,26 @@ __device__ uint64_t reduce_list(const uint64_t *src, uint64_t m, uint64_t *sa, u
     } else {
         uint64_t *scratch[2] = {sa, sb};
         for (int k = 0; k < 2 && m > 4096; ++k) {
+            // Four blocks per wavefront in flight: their loads issue before
+            // the first reduction (a scheduling barrier keeps them there).
+            // pre: the first level is already in sa (k_merkle_blocks).
             const uint64_t nb = (m + 63) / 64;
-            for (uint64_t blk = wave; blk < nb; blk += NW) {
-                const uint32_t cnt = (uint32_t)umin(64, m - 64 * blk);
-                const uint64_t v = lane < cnt ? src[64 * blk + lane] : 0;
-                const uint64_t r = wave_merkle(v, cnt);
-                if (lane == 0) scratch[k][blk] = r;
+            for (uint64_t blk0 = wave; blk0 < nb && !(pre && k == 0); blk0 += 4 * NW) {
+                uint64_t v[4];
+                uint32_t cnt[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const uint64_t blk = blk0 + u * NW;
+                    cnt[u] = blk < nb ? (uint32_t)umin(64, m - 64 * blk) : 0;
+                    v[u] = lane < cnt[u] ? src[64 * blk + lane] : 0;
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (!cnt[u]) continue;
+                    const uint64_t r = wave_merkle(v[u], cnt[u]);
+                    if (lane == 0) scratch[k][blk0 + u * NW] = r;
+                }
             }
             __syncthreads();
             src = scratch[k];
@@ -636,16 +651,19 @@ __device__ uint64_t reduce_list(const uint64_t *src, uint64_t m, uint64_t *sa, u
     return root;
 }
 
-// One workgroup per list (device-memory list table).
-__global__ __launch_bounds__(256) void k_merkle(const MerkleList *__restrict__ lists,
-                                                const uint64_t *__restrict__ in,
-                                                uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
-                                                uint64_t *__restrict__ roots_out)
+// One workgroup per list (device-memory list table); NT lanes (1024 when a
+// list is long enough to need passes through memory, else 256).
+template <int NT>
+__global__ __launch_bounds__(NT) void k_merkle(const MerkleList *__restrict__ lists,
+                                               const uint64_t *__restrict__ in,
+                                               uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
+                                               uint64_t *__restrict__ roots_out, bool pre)
 {
     __shared__ uint64_t lds[4096];
     __shared__ uint64_t lds2[64];
     const MerkleList Lst = lists[blockIdx.x];
-    const uint64_t root = reduce_list<256>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
+    const uint64_t root =
+        reduce_list<NT>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2, pre);
     if (threadIdx.x == 0) {
         if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
         if (Lst.dst[1]) *(g_u64 *)Lst.dst[1] = root;
@@ -690,7 +708,7 @@ __device__ uint64_t reduce_lds(const uint64_t *ls, uint64_t m, uint64_t *lds2)
 // one each.  Ends with a barrier.
 template <int NT>
 __device__ void merkle_lists(const ArgLists &L, const uint64_t *in, uint64_t *sa, uint64_t *sb, uint64_t *lds,
-                             uint64_t *lds2, uint64_t *roots)
+                             uint64_t *lds2, uint64_t *roots, bool pre = false)
 {
     bool one_pass = L.nbuf_lists > 0;
     const uint64_t lo = one_pass ? L.lists[0].begin : 0;
@@ -708,7 +726,7 @@ __device__ void merkle_lists(const ArgLists &L, const uint64_t *in, uint64_t *sa
         const MerkleList &Lst = L.lists[j];
         const uint64_t root =
             one_pass ? reduce_lds<NT>(lds + (Lst.begin - lo), Lst.count, lds2)
-                     : reduce_list<NT>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2);
+                     : reduce_list<NT>(in + Lst.begin, Lst.count, sa + Lst.begin, sb + Lst.begin, lds, lds2, pre);
         if (threadIdx.x == 0) {
             roots[j] = root;
             if (Lst.dst[0]) *(g_u64 *)Lst.dst[0] = root;
@@ -733,13 +751,31 @@ __device__ void merkle_lists(const ArgLists &L, const uint64_t *in, uint64_t *sa
 }
 
 // One workgroup for a small job's Merkle lists.
-__global__ __launch_bounds__(256) void k_merkle_small(const ArgLists L, const uint64_t *__restrict__ in,
-                                                      uint64_t *__restrict__ sa, uint64_t *__restrict__ sb)
+__global__ __launch_bounds__(1024) void k_merkle_small(const ArgLists L, const uint64_t *__restrict__ in,
+                                                       uint64_t *__restrict__ sa, uint64_t *__restrict__ sb, bool pre)
 {
     __shared__ uint64_t lds[4096];
     __shared__ uint64_t lds2[64];
     __shared__ uint64_t roots[kArgBufs];
-    merkle_lists<256>(L, in, sa, sb, lds, lds2, roots);
+    merkle_lists<1024>(L, in, sa, sb, lds, lds2, roots, pre);
+}
+
+// Grid-wide first level of long Merkle lists (LongLists): wavefront w
+// reduces aligned 64-value block w - block_begin[j] of list j into
+// sa[begin[j] + block], where the list's own reduction would have put it.
+__global__ __launch_bounds__(256) void k_merkle_blocks(const LongLists L, const uint64_t *__restrict__ in,
+                                                       uint64_t *__restrict__ sa)
+{
+    const uint64_t w = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63;
+    if (w >= L.block_begin[L.n]) return;
+    uint32_t j = 0;
+    while (j + 1 < L.n && L.block_begin[j + 1] <= w) ++j;
+    const uint64_t blk = w - L.block_begin[j];
+    const uint32_t cnt = (uint32_t)umin(64, L.count[j] - 64 * blk);
+    const uint64_t v = lane < cnt ? in[L.begin[j] + 64 * blk + lane] : 0;
+    const uint64_t r = wave_merkle(v, cnt);
+    if (lane == 0) sa[L.begin[j] + blk] = r;
 }
 
 // ---------------------------------------------------------------- copies
@@ -1941,18 +1977,30 @@ hipError_t launch_classify_small(const ArgTables &tab, uint64_t ngroups, const u
 
 hipError_t launch_merkle(const MerkleList *lists, uint32_t nlists, const uint64_t *in,
                          uint64_t *scratch_a, uint64_t *scratch_b, uint64_t *roots_out,
-                         hipStream_t s)
+                         uint64_t max_count, bool pre, hipStream_t s)
 {
     if (nlists == 0) return hipSuccess;
-    run_kernel(k_merkle, dim3(nlists), dim3(256), s, lists, in, scratch_a, scratch_b, roots_out);
+    if (max_count > kMerkleLdsValues)
+        run_kernel(k_merkle<1024>, dim3(nlists), dim3(1024), s, lists, in, scratch_a, scratch_b, roots_out, pre);
+    else
+        run_kernel(k_merkle<256>, dim3(nlists), dim3(256), s, lists, in, scratch_a, scratch_b, roots_out, pre);
+    return hipGetLastError();
+}
+
+hipError_t launch_merkle_blocks(const LongLists &lists, const uint64_t *in, uint64_t *scratch_a, hipStream_t s)
+{
+    if (lists.n == 0 || lists.n > kLongLists) return lists.n ? hipErrorInvalidValue : hipSuccess;
+    const uint64_t waves = lists.block_begin[lists.n];
+    if (waves == 0) return hipSuccess;
+    run_kernel(k_merkle_blocks, dim3((uint32_t)((waves + 3) / 4)), dim3(256), s, lists, in, scratch_a);
     return hipGetLastError();
 }
 
 hipError_t launch_merkle_small(const ArgLists &lists, const uint64_t *in, uint64_t *scratch_a,
-                               uint64_t *scratch_b, hipStream_t s)
+                               uint64_t *scratch_b, bool pre, hipStream_t s)
 {
     if (lists.nlists == 0) return hipSuccess;
-    run_kernel(k_merkle_small, dim3(1), dim3(256), s, lists, in, scratch_a, scratch_b);
+    run_kernel(k_merkle_small, dim3(1), dim3(1024), s, lists, in, scratch_a, scratch_b, pre);
     return hipGetLastError();
 }
 

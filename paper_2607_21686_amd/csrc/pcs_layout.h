@@ -129,6 +129,22 @@ static_assert(sizeof(ArgLists) + 256 <= 4096, "Merkle lists must fit in the kern
 // The small incremental launch passes both, with a few pointers and sizes.
 static_assert(sizeof(ArgLists) + sizeof(ArgTables) + 128 <= 4096, "Merkle lists and tables must fit together");
 
+// Buffer lists of a Merkle launch that hold more than kMerkleLdsValues
+// values (a buffer of more than 1 GiB): when at most kLongLists of them, a
+// grid-wide pass reduces their aligned 64-value blocks first,
+// one wavefront each, into the list's first scratch level (at the list's own
+// offset), and the per-list reduction starts from there.  Block b of the
+// pass belongs to list j when block_begin[j] <= b < block_begin[j + 1].
+constexpr uint64_t kMerkleLdsValues = 4096;
+constexpr uint32_t kLongLists = 4;  // more long lists reduce in parallel, one workgroup each, anyway
+struct LongLists {
+    uint32_t n;
+    uint32_t pad;
+    uint64_t begin[kLongLists];
+    uint64_t count[kLongLists];
+    uint64_t block_begin[kLongLists + 1];
+};
+
 // The entry moves of a bank shrink, every part in one launch.  Part p moves
 // the kept entries of entry_bytes eb from src to dst (stage: in place, the
 // staging area for entries the compaction would overwrite before reading

@@ -528,20 +528,48 @@ ArgLists arg_lists(const std::vector<MerkleList> &lists, uint32_t nbuf_lists)
 }
 
 // Buffer roots then session roots: one single-workgroup launch for a small
-// job, else one workgroup per list in two launches.
+// job, else one workgroup per list in two launches.  Buffer lists of more
+// than kMerkleLdsValues values (up to kLongLists of them) first have their
+// 64-value blocks reduced by every CU (one more launch), which a single
+// workgroup would otherwise do a block per wavefront at a time.
 int run_merkle(pcs_ctx *c, bool small, const std::vector<MerkleList> &lists, uint32_t nbuf_lists,
                uint64_t lists_dev, uint64_t *d_nodes, uint64_t *d_sa, uint64_t *d_sb, uint64_t *d_roots)
 {
     hipStream_t s = c->stream;
+    LongLists ll{};
+    uint32_t nlong = 0;
+    for (uint32_t j = 0; j < nbuf_lists; ++j)
+        if (lists[j].count > kMerkleLdsValues) {
+            if (nlong < kLongLists) {
+                ll.begin[nlong] = lists[j].begin;
+                ll.count[nlong] = lists[j].count;
+                ll.block_begin[nlong + 1] = ll.block_begin[nlong] + (lists[j].count + 63) / 64;
+            }
+            ++nlong;
+        }
+    const bool pre = nlong > 0 && nlong <= kLongLists;
+    if (pre) {
+        ll.n = nlong;
+        if (int st = launch(c, "merkle", [&] { return launch_merkle_blocks(ll, d_nodes, d_sa, s); })) return st;
+    }
     if (small) {
         const ArgLists al = arg_lists(lists, nbuf_lists);
-        return launch(c, "merkle", [&] { return launch_merkle_small(al, d_nodes, d_sa, d_sb, s); });
+        return launch(c, "merkle", [&] { return launch_merkle_small(al, d_nodes, d_sa, d_sb, pre, s); });
     }
     const MerkleList *d_lists = (const MerkleList *)lists_dev;
     const uint32_t nsess = (uint32_t)lists.size() - nbuf_lists;
-    if (int st = launch(c, "merkle", [&] { return launch_merkle(d_lists, nbuf_lists, d_nodes, d_sa, d_sb, d_roots, s); }))
+    uint64_t max_buf = 0, max_sess = 0;  // the longest list of each launch picks its workgroup size
+    for (size_t j = 0; j < lists.size(); ++j) {
+        uint64_t &m = j < nbuf_lists ? max_buf : max_sess;
+        m = std::max(m, lists[j].count);
+    }
+    if (int st = launch(c, "merkle", [&] {
+            return launch_merkle(d_lists, nbuf_lists, d_nodes, d_sa, d_sb, d_roots, max_buf, pre, s);
+        }))
         return st;
-    return launch(c, "merkle", [&] { return launch_merkle(d_lists + nbuf_lists, nsess, d_roots, d_sa, d_sb, nullptr, s); });
+    return launch(c, "merkle", [&] {
+        return launch_merkle(d_lists + nbuf_lists, nsess, d_roots, d_sa, d_sb, nullptr, max_sess, false, s);
+    });
 }
 
 int run_hash_job(pcs_ctx *c, Job &job, bool copy, const std::vector<uint32_t> &sess_nbufs,

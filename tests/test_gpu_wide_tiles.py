@@ -119,3 +119,36 @@ def test_merkle_lists_past_one_lds_pass(pcs, groups):
         ctx.delete(snap)
     finally:
         ctx.close()
+
+
+@pytest.mark.parametrize("case", ["2 long, argument tables", "1 long + 16 short, device tables",
+                                  "5 long, in-workgroup passes"])
+def test_merkle_long_lists(pcs, case):
+    """Buffers of more than 4096 groups: up to four such lists first have their
+    64-value blocks reduced by a grid-wide launch (argument and device
+    tables); with more, each list's workgroup does it.  Fingerprints, buffer
+    and session roots, and the fused checkpoint's roots against the oracle."""
+    rng = np.random.default_rng([53, len(case)])
+    if case.startswith("2 long"):
+        sizes = [4100 * GROUP - 3, 4097 * GROUP + 11, 5]
+    elif case.startswith("1 long"):
+        sizes = [4099 * GROUP + 7] + [int(rng.integers(1, 3 * 4096)) for _ in range(16)]
+    else:
+        sizes = [4097 * GROUP + k for k in range(5)]
+    log("merkle long lists:", case)
+    bufs = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    h, r, s = oracle.fingerprint(bufs)
+    d = [dev(b) for b in bufs]
+    ctx = pcs.Context(arena(sum(sizes) + (256 << 20)))
+    try:
+        descs = [pcs.flat(t, n) for t, n in zip(d, sizes)]
+        ch, rt, sr = zeros_u64(h.size), zeros_u64(len(sizes)), zeros_u64(1)
+        ctx.fingerprint(descs, ch, rt, sr)
+        assert np.array_equal(u64(ch)[:h.size], h)
+        assert np.array_equal(u64(rt)[:len(sizes)], r) and int(u64(sr)[0]) == s
+        rt2, sr2 = zeros_u64(len(sizes)), zeros_u64(1)
+        snap = ctx.checkpoint(descs, hash=True, roots=rt2, session_root=sr2)
+        assert np.array_equal(u64(rt2)[:len(sizes)], r) and int(u64(sr2)[0]) == s
+        ctx.delete(snap)
+    finally:
+        ctx.close()
