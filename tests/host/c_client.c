@@ -189,6 +189,57 @@ int main(void)
     for (uint64_t w = 0; w < words; ++w) printf("bitmap %llu %016llx\n", (unsigned long long)w, (unsigned long long)h_bitmap[w]);
     printf("label 0 %d\nlabel 1 %d\n", h_labels[0], h_labels[1]);
     printf("imported_restored %d\nincremental_restored %d\n", imported_ok, incremental_ok);
+
+    /* Return-consistency distance of the current bytes (chunk 1 of the flat
+     * buffer rewritten) against the first fingerprints. */
+    uint64_t differing = 0;
+    double distance = -1.0;
+    PCS_OK_(ctx, pcs_distance(ctx, plan, 2, (const uint64_t *)d_hashes, &differing, &distance));
+    printf("differing %llu\ndistance %.17g\n", (unsigned long long)differing, distance);
+
+    /* Relevance-keyed shrink of a 21-entry bank to 12%: latents in place,
+     * poses into another buffer. */
+    enum { BANK = 21, LAT = 40, POSE = 12 };
+    uint64_t keep = 0;
+    if (pcs_keep_count(12, 100, BANK, &keep) != PCS_OK || keep == 0 || keep > BANK) return 1;
+    uint8_t h_lat[BANK * LAT], h_pose[BANK * POSE];
+    float h_scores[BANK];
+    for (int i = 0; i < BANK; ++i) {
+        for (int j = 0; j < LAT; ++j) h_lat[i * LAT + j] = (uint8_t)(i * 13 + j * 7);
+        for (int j = 0; j < POSE; ++j) h_pose[i * POSE + j] = (uint8_t)(i * 29 + j * 3 + 5);
+        h_scores[i] = (float)((i * 37) % 11) - 5.0f;
+    }
+    void *d_lat, *d_pose, *d_pose_out, *d_scores, *d_kept;
+    HIP_OK(hipMalloc(&d_lat, sizeof h_lat));
+    HIP_OK(hipMalloc(&d_pose, sizeof h_pose));
+    HIP_OK(hipMalloc(&d_pose_out, keep * POSE));
+    HIP_OK(hipMalloc(&d_scores, sizeof h_scores));
+    HIP_OK(hipMalloc(&d_kept, 4 * keep));
+    HIP_OK(hipMemcpy(d_lat, h_lat, sizeof h_lat, hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(d_pose, h_pose, sizeof h_pose, hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(d_scores, h_scores, sizeof h_scores, hipMemcpyHostToDevice));
+    const pcs_bank_part parts[2] = {
+        {.src = (uint64_t)(uintptr_t)d_lat, .dst = (uint64_t)(uintptr_t)d_lat, .entry_bytes = LAT},
+        {.src = (uint64_t)(uintptr_t)d_pose, .dst = (uint64_t)(uintptr_t)d_pose_out, .entry_bytes = POSE},
+    };
+    PCS_OK_(ctx, pcs_bank_shrink(ctx, parts, 2, BANK, (const float *)d_scores, keep, (uint32_t *)d_kept));
+    HIP_OK(hipDeviceSynchronize());
+    uint32_t h_kept[BANK];
+    HIP_OK(hipMemcpy(h_kept, d_kept, 4 * keep, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(h_lat, d_lat, keep * LAT, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(h_pose, d_pose_out, keep * POSE, hipMemcpyDeviceToHost));
+    printf("keep %llu\n", (unsigned long long)keep);
+    for (uint64_t j = 0; j < keep; ++j) printf("kept %llu %u\n", (unsigned long long)j, h_kept[j]);
+    printf("shrunk_lat ");
+    for (uint64_t b = 0; b < keep * LAT; ++b) printf("%02x", h_lat[b]);
+    printf("\nshrunk_pose ");
+    for (uint64_t b = 0; b < keep * POSE; ++b) printf("%02x", h_pose[b]);
+    printf("\n");
+    (void)hipFree(d_lat);
+    (void)hipFree(d_pose);
+    (void)hipFree(d_pose_out);
+    (void)hipFree(d_scores);
+    (void)hipFree(d_kept);
     PCS_OK_(ctx, pcs_delete(ctx, imp));
     PCS_OK_(ctx, pcs_delete(ctx, inc));
     (void)hipFree(d_k2);

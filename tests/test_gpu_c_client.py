@@ -4,7 +4,9 @@ session (a flat buffer of ragged size and a wrapped ring window), checkpoint
 it, fork it, restore the fork at a new ring head and export it; then it
 rewrites one chunk, takes an incremental checkpoint, classifies the two
 fingerprint passes, imports the exported image and restores from the
-import and from the incremental snapshot.  Its printed fingerprints, stored
+import and from the incremental snapshot; then it takes the chunk distance
+of the rewritten bytes from the first fingerprints and shrinks a small
+bank to 12% (one part in place, one out of place).  Its printed fingerprints, stored
 chunk count, bitmap and labels are compared with the oracle's, its restore
 checks must pass, and its image size must equal the oracle image's."""
 import os
@@ -33,7 +35,7 @@ def test_c_client_matches_oracle():
     log("C client:", exe)
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr[-2000:]
-    hashes, roots, words, labels, out = {}, {}, {}, {}, {}
+    hashes, roots, words, labels, kept, out = {}, {}, {}, {}, {}, {}
     for line in r.stdout.splitlines():
         f = line.split()
         if f[0] == "hash":
@@ -44,6 +46,8 @@ def test_c_client_matches_oracle():
             words[int(f[1])] = int(f[2], 16)
         elif f[0] == "label":
             labels[int(f[1])] = int(f[2])
+        elif f[0] == "kept":
+            kept[int(f[1])] = int(f[2])
         else:
             out[f[0]] = f[1]
     flat = pattern(0, FLAT_BYTES)
@@ -67,3 +71,18 @@ def test_c_client_matches_oracle():
     assert [words[i] for i in range(len(words))] == [int(x) for x in want_bm]
     assert [labels[0], labels[1]] == [int(x) for x in want_lab] == [1, 0]
     assert out["imported_restored"] == "1" and out["incremental_restored"] == "1"
+    # Distance of the rewritten bytes from the first fingerprints: one chunk of all.
+    total = sum(cpb)
+    assert int(out["differing"]) == 1 and float(out["distance"]) == 1 / total
+    # The 21-entry bank shrunk to 12% (Table 6: 3 frames), latents in place, poses out of place.
+    bank, lat_b, pose_b = 21, 40, 12
+    i = np.arange(bank)
+    lat = ((i[:, None] * 13 + np.arange(lat_b)[None, :] * 7) & 0xFF).astype(np.uint8).reshape(-1)
+    pose = ((i[:, None] * 29 + np.arange(pose_b)[None, :] * 3 + 5) & 0xFF).astype(np.uint8).reshape(-1)
+    scores = ((i * 37) % 11 - 5).astype(np.float32)
+    keep = oracle.keep_count(0.12, bank)
+    assert int(out["keep"]) == keep == 3
+    want_kept, (want_lat, want_pose) = oracle.bank_shrink([(lat, lat_b), (pose, pose_b)], scores, keep)
+    assert [kept[j] for j in range(keep)] == want_kept.tolist()
+    assert bytes.fromhex(out["shrunk_lat"]) == want_lat.tobytes()
+    assert bytes.fromhex(out["shrunk_pose"]) == want_pose.tobytes()
