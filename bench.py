@@ -107,14 +107,14 @@ def summarize(dbs):
 # kernels it covers (name pattern in rocprofv3's kernel names, label).
 TRAFFIC = {
     "batch": ("k_hash_copy_batch1024_traffic.json",
-              [("pack", r"k_hash<pcs::\w+Tables, 1, 1024, 512, 64>",
-                "k_hash<pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint)"),
+              [("pack", r"k_hash<pcs::\w+Tables, 1, 1024, 512, 64, false>",
+                "k_hash<pack, 1024 lanes, 512 B slices, 64 chunks, nontemporal stores> (fused pack + fingerprint)"),
                ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
                 "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
     "kv-ring": ("k_hash_copy_kv_ring_1gib_traffic.json",
                 [("pack", r"k_hash_staggered<pcs::\w+Tables, 1, 1024, 512, 64>",
                   "k_hash_staggered<pack, 1024 lanes, 512 B slices, 64 chunks> (fused pack + fingerprint, "
-                  "first round staggered)"),
+                  "first round staggered, write-back stores)"),
                  ("copy", r"k_copy<pcs::\w+Tables, false, 512, 1024, 64>",
                   "k_copy<unpack, 512 lanes, 1 KiB slices, 64 chunks> (restore scatter)")]),
     "verify": ("k_hash_verify_kv_ring_1gib_traffic.json",
@@ -595,7 +595,7 @@ def run_kv_ring(args):
     nc, mc = kt["copy"]
     out = _line(args, 3 * W_ / t / 1e9, t * 1e3, "windowed KV ring: 32 layers x 2 x 8192 slots x 8 x 128 bf16 "
                 "(1 GiB), 4096-token window at a wrapping head; checkpoint+fingerprint, fork, 2 restores",
-                {"window_bytes": W_}, "k_hash_staggered<pack> (fused pack + fingerprint, first round staggered)",
+                {"window_bytes": W_}, "k_hash_staggered<pack> (fused pack + fingerprint, first round staggered, write-back stores)",
                 2 * W_, ms / n,
                 {"restore_ms": round(mc / nc, 4), "restore_GBps_hbm": round(2 * W_ / (mc / nc * 1e-3) / 1e9, 1)})
     if not args.no_cpu_baseline:

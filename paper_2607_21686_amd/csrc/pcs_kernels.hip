@@ -363,8 +363,10 @@ __device__ __forceinline__ void stagger_start(const Stagger &stg)
 // chain costs each wavefront and spreads the hashing over twice as many
 // wavefronts as lane pairs with two accumulators each would.  kModeDiff /
 // kModeVerify ballot one flag per chunk into a per-group mask (the group is
-// one bitmap word; a diff sub-tile writes its byte of the word).
-template <class Tab, int MODE, int T, int SL, int CPW, bool STAGGER>
+// one bitmap word; a diff sub-tile writes its byte of the word).  WB: the
+// pack stores go through the caches (write-back) instead of streaming past
+// them; see kPackWriteBackMaxRounds.
+template <class Tab, int MODE, int T, int SL, int CPW, bool STAGGER, bool WB>
 __device__ __forceinline__ void hash_tile(const Tab &tab, uint64_t *__restrict__ nodes,
                                           uint64_t *__restrict__ flag_mask, uint64_t arena_base, const Stagger &stg)
 {
@@ -463,7 +465,10 @@ __device__ __forceinline__ void hash_tile(const Tab &tab, uint64_t *__restrict__
             const uint32_t c = (k * T + t) / LPS;
             if (c < nv) {
                 const uint32_t x = step * SL + slot;
-                if (MODE == kModePack) store16_nt(sa[k] + x, r[k]);
+                if (MODE == kModePack) {
+                    if (WB) store16(sa[k] + x, r[k]);
+                    else store16_nt(sa[k] + x, r[k]);
+                }
                 if (kFromSlots && x < gl[k]) {
                     if (x + 16 <= gl[k]) store16_nt(runs_addr(k, x), r[k]);
                     else store_partial(runs_addr(k, x), r[k], gl[k] - x);
@@ -564,21 +569,22 @@ __device__ __forceinline__ void hash_tile(const Tab &tab, uint64_t *__restrict__
     }
 }
 
-template <class Tab, int MODE, int T, int SL, int CPW>
+template <class Tab, int MODE, int T, int SL, int CPW, bool WB>
 __global__ __launch_bounds__(T) void k_hash(const Tab tab, uint64_t *__restrict__ nodes,
                                             uint64_t *__restrict__ flag_mask, uint64_t arena_base)
 {
-    hash_tile<Tab, MODE, T, SL, CPW, false>(tab, nodes, flag_mask, arena_base, Stagger{0, 0});
+    hash_tile<Tab, MODE, T, SL, CPW, false, WB>(tab, nodes, flag_mask, arena_base, Stagger{0, 0});
 }
 
 // k_hash with the first-round stagger (pack and verify jobs of a few rounds):
-// a kernel of its own, so the others keep their code and arguments.
+// a kernel of its own, so the others keep their code and arguments.  Its
+// jobs are all within the write-back bound, so a pack stores write-back.
 template <class Tab, int MODE, int T, int SL, int CPW>
 __global__ __launch_bounds__(T) void k_hash_staggered(const Tab tab, uint64_t *__restrict__ nodes,
                                                       uint64_t *__restrict__ flag_mask, uint64_t arena_base,
                                                       Stagger stg)
 {
-    hash_tile<Tab, MODE, T, SL, CPW, true>(tab, nodes, flag_mask, arena_base, stg);
+    hash_tile<Tab, MODE, T, SL, CPW, true, MODE == kModePack>(tab, nodes, flag_mask, arena_base, stg);
 }
 
 // ---------------------------------------------------------------- Merkle lists
@@ -1236,6 +1242,19 @@ constexpr int kPackLanes = 1024, kPackSlice = 512;
 // 128-576 MiB within -4% .. +2%), while the staggered pack is 1-3% slower
 // with them and keeps 512 B.
 constexpr int kVerifyStaggerSlice = 1024;
+// The fused pack of a job of at most this many rounds (one workgroup per CU)
+// stores the snapshot through the caches (plain stores), a larger job past
+// them (nontemporal stores).  Measured on MI355X in one process, alternating,
+// with the loads nontemporal in both: pack + fingerprint of flat 64-127 MiB
+// 15-21% faster, 128-576 MiB 3-10%, KV ring windows of 64-576 MiB 4-20%, and
+// a checkpoint followed by a restore of it 3-17% faster per step (the
+// restore also finds part of the snapshot still in the caches); the 512 MiB
+// KV ring step (checkpoint, fork, two restores) 564 -> 551 us.  Above the
+// bound write-back stops paying: the 1024-session batch 10.84 -> 11.40 ms
+// and flat 1-4 GiB 3-4% slower in the same process.  Restores keep
+// nontemporal stores whatever the size (plain ones: the KV ring restore 177
+// -> 196 us, its verified restore 181 -> 196 us).
+constexpr uint32_t kPackWriteBackMaxRounds = kStaggerMaxRounds;
 constexpr int kHashLanes = 256, kHashSlice = 512;
 constexpr int kCopyLanes = 512, kCopySlice = 1024;
 // Fingerprint and diff tiles of jobs whose tables travel in the kernel
@@ -1852,14 +1871,14 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
         constexpr int kCPW = kGroupChunks / kSmallTiles;
         static_assert(kCPW == 8, "a diff sub-tile writes one mask byte");
         if (mode == kModeHash)
-            run_kernel((k_hash<Tab, kModeHash, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab, nodes,
-                       flag_mask, arena_base);
-        else if (mode == kModePack)
-            run_kernel((k_hash<Tab, kModePack, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab, nodes,
-                       flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeHash, kSmallLanes, kSmallSlice, kCPW, false>), grid, dim3(kSmallLanes), s,
+                       tab, nodes, flag_mask, arena_base);
+        else if (mode == kModePack)  // sub-tile jobs are far within the write-back bound
+            run_kernel((k_hash<Tab, kModePack, kSmallLanes, kSmallSlice, kCPW, true>), grid, dim3(kSmallLanes), s, tab,
+                       nodes, flag_mask, arena_base);
         else
-            run_kernel((k_hash<Tab, kModeDiff, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab, nodes,
-                       flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeDiff, kSmallLanes, kSmallSlice, kCPW, false>), grid, dim3(kSmallLanes), s,
+                       tab, nodes, flag_mask, arena_base);
         return hipGetLastError();
     }
     if (split) return hipErrorInvalidValue;
@@ -1867,35 +1886,38 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
     switch (mode) {
     case kModeHash:
         if (kArgTab && ngroups <= kWideHashGroups)
-            run_kernel((k_hash<Tab, kModeHash, kPackLanes, kHashSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
-                       nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeHash, kPackLanes, kHashSlice, kGroupChunks, false>), grid, dim3(kPackLanes), s,
+                       tab, nodes, flag_mask, arena_base);
         else
-            run_kernel((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
-                       nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeHash, kHashLanes, kHashSlice, kGroupChunks, false>), grid, dim3(kHashLanes), s,
+                       tab, nodes, flag_mask, arena_base);
         break;
     case kModePack:
         if (stg.ticks)
             run_kernel((k_hash_staggered<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes),
                        s, tab, nodes, flag_mask, arena_base, stg);
+        else if (ngroups <= (uint64_t)kPackWriteBackMaxRounds * std::max<uint32_t>(dev.cus, 1))
+            run_kernel((k_hash<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks, true>), grid, dim3(kPackLanes), s,
+                       tab, nodes, flag_mask, arena_base);
         else
-            run_kernel((k_hash<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
-                       nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModePack, kPackLanes, kPackSlice, kGroupChunks, false>), grid, dim3(kPackLanes), s,
+                       tab, nodes, flag_mask, arena_base);
         break;
     case kModeDiff:
         if (kArgTab && ngroups <= kWideDiffGroups)
-            run_kernel((k_hash<Tab, kModeDiff, kPackLanes, kHashSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
-                       nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeDiff, kPackLanes, kHashSlice, kGroupChunks, false>), grid, dim3(kPackLanes), s,
+                       tab, nodes, flag_mask, arena_base);
         else
-            run_kernel((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks>), grid, dim3(kHashLanes), s, tab,
-                       nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeDiff, kHashLanes, kHashSlice, kGroupChunks, false>), grid, dim3(kHashLanes), s,
+                       tab, nodes, flag_mask, arena_base);
         break;
     case kModeVerify:
         if (stg.ticks)
             run_kernel((k_hash_staggered<Tab, kModeVerify, kPackLanes, kVerifyStaggerSlice, kGroupChunks>), grid,
                        dim3(kPackLanes), s, tab, nodes, flag_mask, arena_base, stg);
         else
-            run_kernel((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice, kGroupChunks>), grid, dim3(kPackLanes), s, tab,
-                       nodes, flag_mask, arena_base);
+            run_kernel((k_hash<Tab, kModeVerify, kPackLanes, kPackSlice, kGroupChunks, false>), grid,
+                       dim3(kPackLanes), s, tab, nodes, flag_mask, arena_base);
         break;
     default:
         return hipErrorInvalidValue;

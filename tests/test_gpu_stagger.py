@@ -1,13 +1,14 @@
 """GPU parity on both sides of the first-round stagger's job-size bounds.
 
 Whole-group pack + fingerprint and verified-restore jobs of 2 to 9 rounds
-(one workgroup per CU) hold their first-round workgroups back by phase; the
-bytes and fingerprints must not depend on it.  Jobs of 2 rounds - 1, 2
-rounds, 9 rounds and 9 rounds + 1 groups (from the device's CU count), made
-of ragged buffers, are checked against the oracle: chunk fingerprints,
-buffer and session roots, the stored payload, the restored bytes and a
-clean verification bitmap; and at 2 and 9 rounds a corrupted snapshot's
-verification bitmap and labels."""
+(one workgroup per CU) hold their first-round workgroups back by phase, and
+pack jobs of at most 9 rounds store the snapshot write-back (larger ones
+nontemporal); the bytes and fingerprints must not depend on either.  Jobs
+of 1 round, 2 rounds - 1, 2 rounds, 9 rounds and 9 rounds + 1 groups (from
+the device's CU count), made of ragged buffers, are checked against the
+oracle: chunk fingerprints, buffer and session roots, the stored payload,
+the restored bytes and a clean verification bitmap; and at 2 and 9 rounds a
+corrupted snapshot's verification bitmap and labels."""
 import numpy as np
 import pytest
 import torch
@@ -30,7 +31,7 @@ def cus():
     return torch.cuda.get_device_properties(0).multi_processor_count
 
 
-@pytest.mark.parametrize("rounds,extra", [(2, -1), (2, 0), (9, 0), (9, 1)])
+@pytest.mark.parametrize("rounds,extra", [(1, 0), (2, -1), (2, 0), (9, 0), (9, 1)])
 def test_stagger_bounds_parity(pcs, rounds, extra):
     G = rounds * cus() + extra
     # Buffers of G - 3, 2 and 1 groups with ragged tails.
