@@ -63,8 +63,12 @@ template <class Tab>
 hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nodes, uint64_t *flag_mask,
                        uint64_t arena_base, hipStream_t s, uint32_t tiles_per_group = 1,
                        TileDevice dev = TileDevice{0, 0});
+// A plain pack of a job within the write-back bound (kPackWriteBackMaxRounds
+// rounds of `cus` workgroups) stores write-back, other copies nontemporal
+// (cus 0: nontemporal).
 template <class Tab>
-hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s);
+hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s,
+                       uint32_t cus = 0);
 // Where the stored chunks of an incremental checkpoint go.  Slot s is the
 // 4096 bytes ending s*4096 below the call's payload top (an arena offset).
 // The scan that totals the stored chunks takes the top from *bump (or from

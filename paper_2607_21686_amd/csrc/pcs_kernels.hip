@@ -798,7 +798,7 @@ __global__ __launch_bounds__(256) void k_merkle_blocks(const LongLists L, const 
 //            arena offsets) -> the destination buffer's runs; only logical
 //            bytes are written.
 template <class Tab, bool PACK, int T, int SL, int CPW>
-__global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
+__global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base, bool wb)
 {
     constexpr uint32_t kSteps = kChunk / SL, LPS = SL / 16;
     constexpr int U = CPW * SL / 16 / T;
@@ -866,8 +866,11 @@ __global__ __launch_bounds__(T) void k_copy(const Tab tab, uint64_t arena_base)
 #pragma unroll
         for (int k = 0; k < U; ++k) {
             const uint32_t x = off(k, step);
-            if (PACK) {
-                if (sa[k]) store16_nt(sa[k] + x, v[k]);
+            if (PACK) {  // wb: write-back stores (jobs within kPackWriteBackMaxRounds)
+                if (sa[k]) {
+                    if (wb) store16(sa[k] + x, v[k]);
+                    else store16_nt(sa[k] + x, v[k]);
+                }
             } else if (x < gl[k]) {
                 if (x + 16 <= gl[k]) store16_nt(runs_addr(k, x), v[k]);
                 else store_partial(runs_addr(k, x), v[k], gl[k] - x);
@@ -1927,25 +1930,26 @@ hipError_t launch_tile(const Tab &tab, uint64_t ngroups, int mode, uint64_t *nod
 
 // Copies need no per-group output, so a small job is cut into sub-tiles here.
 template <class Tab>
-hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s)
+hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t arena_base, hipStream_t s, uint32_t cus)
 {
     if (ngroups == 0) return hipSuccess;
     const uint32_t tiles = tile_split(ngroups);
     const dim3 grid((uint32_t)(ngroups * tiles));
+    const bool wb = pack && ngroups <= (uint64_t)kPackWriteBackMaxRounds * cus;
     if (tiles == kSmallTiles) {
         constexpr int kCPW = kGroupChunks / kSmallTiles;
         if (pack)
             run_kernel((k_copy<Tab, true, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab,
-                       arena_base);
+                       arena_base, wb);
         else
             run_kernel((k_copy<Tab, false, kSmallLanes, kSmallSlice, kCPW>), grid, dim3(kSmallLanes), s, tab,
-                       arena_base);
+                       arena_base, false);
     } else if (pack) {
         run_kernel((k_copy<Tab, true, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), s, tab,
-                   arena_base);
+                   arena_base, wb);
     } else {
         run_kernel((k_copy<Tab, false, kCopyLanes, kCopySlice, kGroupChunks>), grid, dim3(kCopyLanes), s, tab,
-                   arena_base);
+                   arena_base, false);
     }
     return hipGetLastError();
 }
@@ -2127,7 +2131,7 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
 #define PCS_INSTANTIATE(Tab)                                                                                        \
     template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint64_t *, uint64_t, hipStream_t, \
                                          uint32_t, TileDevice);                                                   \
-    template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t);                     \
+    template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t, uint32_t);           \
     template hipError_t launch_pack_dirty<Tab>(const Tab &, const uint64_t *, const uint64_t *, uint64_t,         \
                                                const uint64_t *, uint64_t, hipStream_t);                          \
     template hipError_t launch_place_dirty<Tab>(const Tab &, uint64_t, const uint64_t *, const uint64_t *,        \

@@ -738,7 +738,7 @@ int checkpoint_full(pcs_ctx *c, const pcs_buf *plans, const uint32_t *nbufs, uin
         const uint64_t G = job.ngroups;
         if (!st)
             st = with_tables(sg, [&](const auto &tab) {
-                return launch(c, "pack", [&] { return launch_copy(tab, G, true, 0, c->stream); });
+                return launch(c, "pack", [&] { return launch_copy(tab, G, true, 0, c->stream, c->dev.cus); });
             });
     }
     if (st) return st;  // nodes (and their blocks) are released here
