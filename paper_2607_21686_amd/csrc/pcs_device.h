@@ -72,20 +72,20 @@ hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t are
 // Where the stored chunks of an incremental checkpoint go.  Slot s is the
 // 4096 bytes ending s*4096 below the call's payload top (an arena offset).
 // The scan that totals the stored chunks takes the top from *bump (or from
-// `reset`, nonzero when the call starts a new segment of the arena), lowers
-// *bump by the slots it places, and writes the top to *top_out, which the
-// copy kernels read; with bump null it places nothing (the host writes
-// *top_out once it has allocated the slots).  host: two mapped pinned words
-// that receive the stored-chunk count and the top.
+// `reset`, nonzero when the call starts a new segment of the arena), writes
+// the top lowered by the slots it places to *bump_out (the other of two
+// words, so that every workgroup of the launch may still read *bump; the
+// next call reads *bump_out), and the top to *top_out, which the copy
+// kernels of separate launches read; with bump null it places nothing (the
+// host writes *top_out once it has allocated the slots).  host: two mapped
+// pinned words that receive the stored-chunk count and the top.
 struct SlotBump {
     uint64_t *bump;
+    uint64_t *bump_out;
     uint64_t reset;
     uint64_t *top_out;
     uint64_t *host;
 };
-template <class Tab>
-hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_t *total, uint64_t max_slots,
-                             const uint64_t *top_word, uint64_t arena_base, hipStream_t s);
 // Slot assignment + dirty copy of an incremental checkpoint in one launch
 // (from the scanned per-group offsets and the dirty masks); writes the whole
 // new manifest.
@@ -118,15 +118,14 @@ hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets
                        const SlotBump &bump, hipStream_t s);
 constexpr uint64_t kScanCompactMaxGroups = 4096;
 // Small incremental jobs (tables in the kernel arguments, at most
-// kScanCompactMaxGroups groups): one single-workgroup launch reduces the
-// Merkle lists and scans the dirty masks (total also to the pinned host
-// word); up to kScanCompactFusedGroups groups it also assigns the slots,
-// otherwise the offsets go to `offsets` and launch_place_dirty follows.
-constexpr uint64_t kScanCompactFusedGroups = 64;
-hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
+// kScanCompactMaxGroups groups), after the fingerprint + diff tiles: one
+// launch reduces the Merkle lists, scans the dirty masks (total also to
+// *total and the pinned host words), places the slots and copies the dirty
+// chunks.  bump.bump and bump.bump_out must differ.
+hipError_t launch_merkle_scan_place(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
                                     uint64_t *scratch_b, const ArgTables &tab, uint64_t ngroups,
-                                    const uint64_t *dirty_mask, const SlotBump &bump, uint64_t *list,
-                                    uint64_t *offsets, uint64_t *total, hipStream_t s);
+                                    const uint64_t *dirty_mask, const SlotBump &bump, uint64_t *total,
+                                    uint64_t arena_base, hipStream_t s);
 hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStream_t s);
 // Flips the lowest bit of the byte at device address addr.
 hipError_t launch_flip_bit(uint64_t addr, hipStream_t s);

@@ -940,16 +940,16 @@ __device__ void scan_counts(const Count counts, uint64_t n, uint64_t *offsets, u
 
 // Thread 1023 of a scan of dirty masks, once the stored-chunk count is
 // known: takes this call's payload top from the bump word (bump_now, loaded
-// when the kernel started; or sb.reset) and
-// lowers the bump word by the count's slots, then publishes the count and
-// the top to the host words.  Returns the top (0 when sb.bump is null: the
-// host sets the top itself once it has read the count).
+// when the kernel started; or sb.reset), writes it lowered by the count's
+// slots to the next call's bump word, then publishes the count and the top
+// to the host words.  Returns the top (0 when sb.bump is null: the host
+// sets the top itself once it has read the count).
 __device__ uint64_t place_slots(const SlotBump &sb, uint64_t count, uint64_t bump_now)
 {
     uint64_t top = 0;
     if (sb.bump) {
         top = sb.reset ? sb.reset : bump_now;
-        *sb.bump = top - count * kChunk;
+        *sb.bump_out = top - count * kChunk;
         *sb.top_out = top;
     }
     if (sb.host) {
@@ -970,22 +970,6 @@ __global__ __launch_bounds__(1024) void k_scan(const Count counts, uint64_t n, u
     const uint64_t bump_now = threadIdx.x == 1023 && sb.bump && !sb.reset ? *sb.bump : 0;
     scan_counts(counts, n, offsets, total, sums);
     if (threadIdx.x == 1023) place_slots(sb, *total, bump_now);
-}
-
-// Slot assignment for one chunk: dirty chunks get slots in (buffer, chunk)
-// order and are listed, and the new manifest points a dirty chunk at its
-// slot (slot s is the 4096 bytes ending s*4096 below the call's payload top,
-// an arena offset: slots grow downwards).  A clean chunk's entry (where the
-// parent holds it) was written by the diff tiles.
-__device__ __forceinline__ void compact_chunk(const JobBuf &jb, uint32_t b, uint64_t i, uint32_t lane, uint64_t mask,
-                                              uint64_t off, uint64_t payload_arena_top, uint64_t *list)
-{
-    if ((mask >> lane) & 1) {
-        const uint64_t below = lane ? (mask & ((1ULL << lane) - 1)) : 0;
-        const uint64_t slot = off + (uint64_t)__popcll(below);
-        list[slot] = ((uint64_t)b << 40) | i;
-        ((g_u64 *)jb.manifest)[i] = payload_arena_top - (slot + 1) * kChunk;
-    }
 }
 
 // Exclusive scan of the dirty masks' set bits of a small incremental job
@@ -1024,74 +1008,14 @@ __device__ uint64_t scan_masks_small(const uint64_t (&mk)[4], uint64_t ngroups, 
     return total;
 }
 
-// Small incremental jobs (tables in the kernel arguments), after the
-// fingerprint + diff tiles, in one workgroup and one launch: the Merkle
-// lists (buffer and session roots), then the exclusive scan of the dirty
-// masks' set bits, with the stored-chunk count written to device memory and
-// to the caller's pinned host word.  kCompact (at most
-// kScanCompactFusedGroups groups): the offsets stay in LDS and the slot
-// assignment follows here, one thread per chunk (a chunk's slot depends only
-// on its group's mask and offset); otherwise the offsets go to `offsets` for
-// k_place_dirty.
-template <bool kCompact>
-__global__ __launch_bounds__(1024) void k_merkle_scan_small(const ArgLists L, const uint64_t *__restrict__ nodes,
-                                                            uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
-                                                            const ArgTables tab, uint64_t ngroups,
-                                                            const uint64_t *__restrict__ dirty_mask,
-                                                            const SlotBump bump, uint64_t *__restrict__ list,
-                                                            uint64_t *__restrict__ offsets,
-                                                            uint64_t *__restrict__ total)
-{
-    __shared__ uint64_t lds[4096];
-    __shared__ uint64_t lds2[64];
-    __shared__ uint64_t roots[kArgBufs];
-    __shared__ uint64_t offs[kCompact ? kScanCompactFusedGroups : 1];
-    __shared__ uint64_t top_sh;
-    __shared__ uint32_t wsum[33];
-    static_assert(kScanCompactMaxGroups <= 4 * 1024, "four dirty masks per thread");
-    // The masks are loaded first, so that their round trip to memory
-    // overlaps the Merkle reduction.
-    const uint32_t t = threadIdx.x;
-    uint64_t mk[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) mk[k] = 4 * t + k < ngroups ? dirty_mask[4 * t + k] : 0;
-    const uint64_t bump_now = t == 1023 && bump.bump && !bump.reset ? *bump.bump : 0;
-    merkle_lists<1024>(L, nodes, sa, sb, lds, lds2, roots);
-    const uint64_t count = scan_masks_small(mk, ngroups, kCompact ? offs : offsets, wsum);
-    if (t == 0) *total = count;
-    if (t == 1023) top_sh = place_slots(bump, count, bump_now);
-    if constexpr (kCompact) {
-        __syncthreads();
-        const uint64_t top = top_sh;
-        for (uint64_t e = threadIdx.x; e < ngroups * kGroupChunks; e += 1024) {
-            const uint64_t g = e / kGroupChunks;
-            const uint32_t lane = (uint32_t)(e % kGroupChunks);
-            const uint32_t b = buf_index(tab, g);
-            const JobBuf &jb = tab.bufs[b];
-            const uint64_t i = (g - jb.group_begin) * kGroupChunks + lane;
-            if (i < jb.nchunks) compact_chunk(jb, b, i, lane, dirty_mask[g], offs[g], top, list);
-        }
-    }
-}
-
-// Copies listed dirty chunks into their slots (slot s ends s*4096 below the
-// payload top, the arena offset in *top_word): one wavefront per slot, each
-// lane moving 64 bytes with four 16-byte loads in flight, zero-padding
-// partial chunks.
+// Moves chunk i of buffer jb (its logical bytes, zero-padded to 4096) to
+// device address dst: the 64 lanes of a wavefront, 64 bytes each, four
+// 16-byte loads in flight per lane.
 template <class Tab>
-__global__ __launch_bounds__(256) void k_pack_dirty(const Tab tab, const uint64_t *__restrict__ list,
-                                                    const uint64_t *__restrict__ total_ptr,
-                                                    const uint64_t *__restrict__ top_word, uint64_t arena_base)
+__device__ __forceinline__ void copy_chunk(const Tab &tab, const JobBuf &jb, uint64_t i, uint64_t dst, uint32_t lane)
 {
-    const uint64_t slot = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (slot >= *total_ptr) return;
-    const uint64_t payload_top = arena_base + *top_word;
-    const uint32_t lane = threadIdx.x & 63;
-    const uint64_t e = list[slot];
-    const JobBuf &jb = tab.bufs[e >> 40];
-    const uint64_t cb = (e & ((1ULL << 40) - 1)) * kChunk;
+    const uint64_t cb = i * kChunk;
     const uint64_t len = umin(kChunk, jb.nbytes - cb);
-    const uint64_t dst = payload_top - (slot + 1) * kChunk;
     uint4 v[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -1106,13 +1030,80 @@ __global__ __launch_bounds__(256) void k_pack_dirty(const Tab tab, const uint64_
     for (int k = 0; k < 4; ++k) store16(dst + (k * 64 + lane) * 16, v[k]);
 }
 
-// Slot assignment and dirty copy in one launch (jobs above
-// kScanCompactFusedGroups groups, after the scan of the dirty masks): one
+// Small incremental jobs (tables in the kernel arguments, at most
+// kScanCompactMaxGroups groups), after the fingerprint + diff tiles, in one
+// launch of 1024-lane workgroups that need nothing from one another.
+// Workgroup 0 reduces the Merkle lists (buffer and session roots), scans
+// the dirty masks' set bits and publishes the stored-chunk count and the
+// payload top (place_slots: *total, the next call's bump word, the host
+// words).  Every other workgroup scans the masks itself (at most 4096
+// words, the same for all, so mostly from L2) into LDS and takes the top
+// from *bump.bump, which only an earlier launch wrote; its wavefront w
+// then stores slots w, w + stride, ...: slot s belongs to the last group
+// whose exclusive offset is at most s (a group with no dirty chunk shares
+// its offset with the next group, so the last such group holds s), and
+// within it to the dirty chunk with s - offset dirty chunks below it.
+// Slots therefore follow (buffer, chunk) order, as k_place_dirty assigns
+// them.  Lane 0 enters the slot in the manifest (clean chunks' entries
+// were written by the diff tiles) and the wavefront copies the chunk.
+__global__ __launch_bounds__(1024) void k_merkle_scan_place(const ArgLists L, const uint64_t *__restrict__ nodes,
+                                                            uint64_t *__restrict__ sa, uint64_t *__restrict__ sb,
+                                                            const ArgTables tab, uint64_t ngroups,
+                                                            const uint64_t *__restrict__ dirty_mask,
+                                                            const SlotBump bump, uint64_t *__restrict__ total,
+                                                            uint64_t arena_base)
+{
+    __shared__ uint64_t lds[4096];  // Merkle values (workgroup 0), then the groups' offsets
+    __shared__ uint64_t msk[kScanCompactMaxGroups];
+    __shared__ uint64_t lds2[64];
+    __shared__ uint64_t roots[kArgBufs];
+    __shared__ uint32_t wsum[33];
+    static_assert(kScanCompactMaxGroups <= 4 * 1024 && kScanCompactMaxGroups <= 4096,
+                  "four dirty masks per thread, offsets in the Merkle LDS array");
+    const uint32_t t = threadIdx.x;
+    uint64_t mk[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mk[k] = 4 * t + k < ngroups ? dirty_mask[4 * t + k] : 0;
+    const uint64_t top = !bump.bump ? 0 : bump.reset ? bump.reset : *bump.bump;
+    if (blockIdx.x == 0) {
+        // The masks' round trip to memory overlaps the Merkle reduction.
+        merkle_lists<1024>(L, nodes, sa, sb, lds, lds2, roots);
+        const uint64_t count = scan_masks_small(mk, ngroups, lds, wsum);
+        if (t == 0) *total = count;
+        if (t == 1023) place_slots(bump, count, top);
+        return;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        if (4 * t + k < ngroups) msk[4 * t + k] = mk[k];
+    const uint64_t count = scan_masks_small(mk, ngroups, lds, wsum);  // ends with a barrier: msk is visible
+    const uint32_t lane = t & 63;
+    const uint64_t stride = (uint64_t)(gridDim.x - 1) * 16;
+    for (uint64_t s = (uint64_t)(blockIdx.x - 1) * 16 + (t >> 6); s < count; s += stride) {
+        uint32_t lo = 0, hi = (uint32_t)ngroups;  // lds[lo] <= s (lds[0] = 0)
+        while (hi - lo > 1) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (lds[mid] <= s) lo = mid; else hi = mid;
+        }
+        const uint64_t m = msk[lo];
+        const uint32_t k = (uint32_t)(s - lds[lo]);
+        const uint32_t below = (uint32_t)__popcll(lane ? m & ((1ULL << lane) - 1) : 0);
+        const uint32_t c = (uint32_t)__ffsll((unsigned long long)__ballot(((m >> lane) & 1) && below == k)) - 1;
+        const JobBuf &jb = tab.bufs[buf_index(tab, lo)];
+        const uint64_t i = (lo - jb.group_begin) * kGroupChunks + c;
+        const uint64_t slot_off = top - (s + 1) * kChunk;  // arena offset
+        if (lane == 0) ((g_u64 *)jb.manifest)[i] = slot_off;
+        copy_chunk(tab, jb, i, arena_base + slot_off, lane);
+    }
+}
+
+// Slot assignment and dirty copy in one launch (jobs with device tables,
+// or whose slots the host placed, after the scan of the dirty masks): one
 // wavefront per chunk, four per 256-lane workgroup, striding over the job's
 // chunk positions (64 per group) so that a large job launches no more than
 // kPlaceBlocks workgroups.  The wavefront of a dirty chunk takes its slot
 // (below the payload top in *top_word) from its group's scanned offset and
-// the set bits of the mask below it, as compact_chunk; lane 0 enters the
+// the set bits of the mask below it, as k_merkle_scan_place; lane 0 enters the
 // slot in the manifest and all 64 lanes copy the chunk into it, 64 bytes per
 // lane, zero-padding a partial chunk.  A clean chunk costs its wavefront one
 // (cached) mask load: the diff tiles entered it in the manifest.
@@ -1136,21 +1127,7 @@ __global__ __launch_bounds__(256) void k_place_dirty(const Tab tab, uint64_t npo
         const uint64_t slot = offsets[G] + (uint64_t)__popcll(c ? mask & ((1ULL << c) - 1) : 0);
         const uint64_t top = *top_word;  // arena offset
         if (lane == 0) man[i] = top - (slot + 1) * kChunk;
-        const uint64_t cb = i * kChunk;
-        const uint64_t len = umin(kChunk, jb.nbytes - cb);
-        const uint64_t dst = arena_base + top - (slot + 1) * kChunk;
-        uint4 v[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const uint32_t x = (k * 64 + lane) * 16;
-            v[k] = make_uint4(0, 0, 0, 0);
-            if (x < len) {
-                const uint64_t a = phys_addr(tab.runs, jb.run_begin, jb.run_count, cb + x);
-                v[k] = x + 16 <= len ? load16(a) : load_partial(a, (uint32_t)(len - x));
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) store16(dst + (k * 64 + lane) * 16, v[k]);
+        copy_chunk(tab, jb, i, arena_base + top - (slot + 1) * kChunk, lane);
     }
 }
 
@@ -1955,16 +1932,6 @@ hipError_t launch_copy(const Tab &tab, uint64_t ngroups, bool pack, uint64_t are
 }
 
 template <class Tab>
-hipError_t launch_pack_dirty(const Tab &tab, const uint64_t *list, const uint64_t *total, uint64_t max_slots,
-                             const uint64_t *top_word, uint64_t arena_base, hipStream_t s)
-{
-    if (max_slots == 0) return hipSuccess;
-    const uint32_t blocks = (uint32_t)((max_slots + 3) / 4);
-    run_kernel((k_pack_dirty<Tab>), dim3(blocks), dim3(256), s, tab, list, total, top_word, arena_base);
-    return hipGetLastError();
-}
-
-template <class Tab>
 hipError_t launch_place_dirty(const Tab &tab, uint64_t ngroups, const uint64_t *dirty_mask, const uint64_t *offsets,
                               const uint64_t *top_word, uint64_t arena_base, hipStream_t s)
 {
@@ -2037,19 +2004,19 @@ hipError_t launch_scan(const uint64_t *dirty_mask, uint64_t n, uint64_t *offsets
     return hipGetLastError();
 }
 
-hipError_t launch_merkle_scan_small(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
+hipError_t launch_merkle_scan_place(const ArgLists &lists, const uint64_t *nodes, uint64_t *scratch_a,
                                     uint64_t *scratch_b, const ArgTables &tab, uint64_t ngroups,
-                                    const uint64_t *dirty_mask, const SlotBump &bump, uint64_t *list,
-                                    uint64_t *offsets, uint64_t *total, hipStream_t s)
+                                    const uint64_t *dirty_mask, const SlotBump &bump, uint64_t *total,
+                                    uint64_t arena_base, hipStream_t s)
 {
     if (ngroups > kScanCompactMaxGroups) return hipErrorInvalidValue;
-    if (ngroups && ngroups <= kScanCompactFusedGroups && !bump.bump) return hipErrorInvalidValue;  // slots need a top
-    if (ngroups <= kScanCompactFusedGroups)
-        run_kernel(k_merkle_scan_small<true>, dim3(1), dim3(1024), s, lists, nodes, scratch_a, scratch_b, tab, ngroups,
-                   dirty_mask, bump, list, offsets, total);
-    else
-        run_kernel(k_merkle_scan_small<false>, dim3(1), dim3(1024), s, lists, nodes, scratch_a, scratch_b, tab, ngroups,
-                   dirty_mask, bump, list, offsets, total);
+    if (ngroups && (!bump.bump || !bump.bump_out || bump.bump == bump.bump_out)) return hipErrorInvalidValue;
+    // Workgroup 0, then enough 16-wavefront workgroups for one stored chunk
+    // per wavefront if every chunk is stored (at most kPlaceBlocks / 4).
+    const uint64_t npos = ngroups * kGroupChunks;
+    const uint32_t blocks = 1 + (uint32_t)std::min<uint64_t>((npos + 15) / 16, kPlaceBlocks / 4);
+    run_kernel(k_merkle_scan_place, dim3(blocks), dim3(1024), s, lists, nodes, scratch_a, scratch_b, tab, ngroups,
+               dirty_mask, bump, total, arena_base);
     return hipGetLastError();
 }
 
@@ -2132,8 +2099,6 @@ hipError_t launch_reverse_slots(uint64_t top, uint64_t dst, uint64_t n, hipStrea
     template hipError_t launch_tile<Tab>(const Tab &, uint64_t, int, uint64_t *, uint64_t *, uint64_t, hipStream_t, \
                                          uint32_t, TileDevice);                                                   \
     template hipError_t launch_copy<Tab>(const Tab &, uint64_t, bool, uint64_t, hipStream_t, uint32_t);           \
-    template hipError_t launch_pack_dirty<Tab>(const Tab &, const uint64_t *, const uint64_t *, uint64_t,         \
-                                               const uint64_t *, uint64_t, hipStream_t);                          \
     template hipError_t launch_place_dirty<Tab>(const Tab &, uint64_t, const uint64_t *, const uint64_t *,        \
                                                 const uint64_t *, uint64_t, hipStream_t);                         \
     template hipError_t launch_classify<Tab>(const Tab &, uint64_t, const uint64_t *, uint32_t, uint64_t,         \

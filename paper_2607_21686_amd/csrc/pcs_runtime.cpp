@@ -95,9 +95,12 @@ struct pcs_ctx {
     std::shared_ptr<pcs::Segment> seg;       // the open segment, if any
     hipEvent_t exact_ev = nullptr;           // an exact-size incremental call waits on it
 
-    // The arena's first unit, kept by the library: word 0 is the bump word of
-    // incremental slot placement, word 1 a call's payload top.
+    // The arena's first unit, kept by the library: words 0 and 2 are the bump
+    // words of incremental slot placement (a call reads word bump_par and
+    // writes the other, which the next call reads), word 1 a call's payload
+    // top.
     uint64_t bump_dev = 0, top_dev = 0;
+    uint32_t bump_par = 0;
 
     pcs::TileDevice dev{0, 0};  // CU count and real-time counter rate of the arena's device (0: unknown)
 
@@ -1346,12 +1349,14 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     // (exact: the host places them once it has read the count from pair 0),
     // or no slots at all (no chunks).
     uint32_t pair = 0;
-    SlotBump bump{nullptr, 0, nullptr, nullptr};
+    SlotBump bump{nullptr, nullptr, 0, nullptr, nullptr};
     if (seg) {
         pair = c->free_pairs.back();
         c->free_pairs.pop_back();
-        bump = SlotBump{(uint64_t *)c->bump_dev, seg->started ? 0 : seg->hi, (uint64_t *)c->top_dev,
-                        &c->counts_dev[2 * pair]};
+        uint64_t *words = (uint64_t *)c->bump_dev;
+        bump = SlotBump{words + 2 * c->bump_par, words + 2 * (c->bump_par ^ 1), seg->started ? 0 : seg->hi,
+                        (uint64_t *)c->top_dev, &c->counts_dev[2 * pair]};
+        c->bump_par ^= 1;
         seg->started = true;
         seg->claim += worst;
         ++seg->pending;
@@ -1381,13 +1386,12 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
         }
     } undo{c, seg, worst, pair, recorded};
 
-    // A small job (tables in kernel arguments) on the pipelined path runs as:
-    // fingerprint+diff, then one single-workgroup launch for the Merkle lists,
-    // the scan and the slot placement (+ the slot assignment up to 64 groups),
-    // then the dirty copy (with the slot assignment above 64 groups).
+    // A small job (tables in kernel arguments) on the pipelined path runs as
+    // two launches: fingerprint+diff, then the Merkle lists, the scan, the
+    // slot placement and the dirty copy.
     const bool small = is_small(job) && !exact && G <= kScanCompactMaxGroups;
     Carver cv;
-    uint64_t o_nodes, o_sa, o_sb, o_roots, o_mask, o_offs, o_total, o_list;
+    uint64_t o_nodes, o_sa, o_sb, o_roots, o_mask, o_offs, o_total;
     cv.add(&o_nodes, 8 * G * tiles);
     cv.add(&o_sa, 8 * std::max<uint64_t>(G * tiles, n));
     cv.add(&o_sb, 8 * std::max<uint64_t>(G * tiles, n));
@@ -1395,7 +1399,6 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     cv.add(&o_mask, 8 * G);
     cv.add(&o_offs, 8 * G);
     cv.add(&o_total, 8);
-    cv.add(&o_list, small && G <= kScanCompactFusedGroups ? 8 * T : 8);
     Temp t(c);
     Staged sg;
     uint64_t lists_dev, scr;
@@ -1405,7 +1408,7 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     uint64_t *d_sa = (uint64_t *)(scr + o_sa), *d_sb = (uint64_t *)(scr + o_sb);
     uint64_t *d_roots_tmp = (uint64_t *)(scr + o_roots);
     uint64_t *d_mask = (uint64_t *)(scr + o_mask), *d_offs = (uint64_t *)(scr + o_offs);
-    uint64_t *d_total = (uint64_t *)(scr + o_total), *d_list = (uint64_t *)(scr + o_list);
+    uint64_t *d_total = (uint64_t *)(scr + o_total);
     const uint64_t *top_word = (const uint64_t *)c->top_dev;
     hipStream_t s = c->stream;
     int st = with_tables(sg, [&](const auto &tab) {
@@ -1417,19 +1420,10 @@ int pcs_checkpoint(pcs_ctx *c, const pcs_buf *plan, uint32_t n, pcs_snap parent,
     if (small) {
         const ArgLists al = arg_lists(lists, n);
         if ((st = launch(c, "incremental", [&] {
-                 return launch_merkle_scan_small(al, d_nodes, d_sa, d_sb, sg.arg, G, d_mask, bump, d_list, d_offs,
-                                                 d_total, s);
+                 return launch_merkle_scan_place(al, d_nodes, d_sa, d_sb, sg.arg, G, d_mask, bump, d_total,
+                                                 c->arena_dev, s);
              })))
             return st;
-        if (G > kScanCompactFusedGroups)
-            st = launch(c, "incremental", [&] {
-                return launch_place_dirty(sg.arg, G, d_mask, d_offs, top_word, c->arena_dev, s);
-            });
-        else
-            st = launch(c, "incremental", [&] {
-                return launch_pack_dirty(sg.arg, d_list, d_total, T, top_word, c->arena_dev, s);
-            });
-        if (st) return st;
     } else {
         if ((st = run_merkle(c, small, lists, n, lists_dev, d_nodes, d_sa, d_sb, d_roots_tmp))) return st;
         if ((st = launch(c, "incremental", [&] { return launch_scan(d_mask, G, d_offs, d_total, bump, s); })))
