@@ -152,3 +152,59 @@ def test_merkle_long_lists(pcs, case):
         ctx.delete(snap)
     finally:
         ctx.close()
+
+
+@pytest.mark.parametrize("groups", [3, 65, 4096])
+def test_incremental_every_chunk_then_none_then_one(pcs, groups):
+    """Incremental checkpoints of argument-table jobs whose stored-chunk count
+    spans its whole range: every chunk rewritten (at 4096 groups, 262,000
+    stored chunks, several per wavefront of the slot placement), then none,
+    then only the last chunk of the last buffer.  Chunk fingerprints, roots,
+    stored bytes and restores against the oracle."""
+    rng = np.random.default_rng([59, groups])
+    sizes = sizes_for(groups)
+    cur = [rng.integers(0, 256, size=n, dtype=np.uint8) for n in sizes]
+    d = [dev(b) for b in cur]
+    log("incremental every chunk / none / one:", groups, "groups")
+    ctx = pcs.Context(arena(2 * sum(sizes) + (256 << 20)))
+    try:
+        st = oracle.Store()
+        chain = [(ctx.checkpoint([pcs.flat(t, n) for t, n in zip(d, sizes)], hash=True), st.checkpoint(cur),
+                  [b.copy() for b in cur])]
+        total = sum(oracle.chunk_count(n) for n in sizes)
+
+        def every(bufs):
+            for b in bufs:
+                b ^= 0x5A
+
+        def none(bufs):
+            pass
+
+        def last(bufs):
+            bufs[-1][-1] ^= 1
+        for change, stored in ((every, total), (none, 0), (last, 1)):
+            change(cur)
+            for t, b in zip(d, cur):
+                t.copy_(torch.from_numpy(b))
+            ch, rt, sr = zeros_u64(total), zeros_u64(len(sizes)), zeros_u64(1)
+            s = ctx.checkpoint([pcs.flat(t, n) for t, n in zip(d, sizes)], parent=chain[-1][0], chunk_hashes=ch,
+                               roots=rt, session_root=sr)
+            o = st.checkpoint(cur, chain[-1][1])
+            want_h, want_r, want_s = oracle.fingerprint(cur)
+            assert np.array_equal(u64(ch)[:total], want_h)
+            assert np.array_equal(u64(rt)[:len(sizes)], want_r) and int(u64(sr)[0]) == int(want_s)
+            inf = ctx.info(s)
+            assert inf["stored_bytes"] == st.payload(o).size == stored * 4096
+            pay = torch.empty(max(1, inf["stored_bytes"]), dtype=torch.uint8, device="cuda")
+            ctx.payload(s, pay)
+            assert np.array_equal(host(pay)[:inf["stored_bytes"]], st.payload(o))
+            del pay
+            chain.append((s, o, [b.copy() for b in cur]))
+        for s, _, want in chain[1:]:
+            outs = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in sizes]
+            ctx.restore(s, [pcs.flat(t, n) for t, n in zip(outs, sizes)])
+            assert all(np.array_equal(host(t), w) for t, w in zip(outs, want))
+        for s, _, _ in reversed(chain):
+            ctx.delete(s)
+    finally:
+        ctx.close()
