@@ -288,7 +288,7 @@ def run_batch(args):
     dsts = P.BufArray([b for k in range(R) for b in (
         P.ring(dst_rings[k], g.outer, g.capacity, g.row_bytes, plan.restore_heads[k], g.window),
         P.flat(dst_obs[k]), P.flat(dst_rngs[k]))])
-    per_session_chunks = [P.chunk_count(g.window_bytes), P.chunk_count(plan.obs_bytes), P.chunk_count(plan.rng_bytes)]
+    per_session_chunks = P.chunk_counts(plans.bufs[:3])[0]
     cpb_list = per_session_chunks * S
     cpb = P.u64_array(cpb_list)
     total_chunks = sum(cpb_list)
@@ -686,8 +686,7 @@ def run_sweep(args):
     plan = W.config4_plan(3)
     reps = W.config4_device(plan, 3)
     K = plan.replays
-    cpb = [P.chunk_count(n) for n in plan.sizes]
-    total = sum(cpb)
+    cpb, total = P.chunk_counts([P.flat(t) for t in reps[0]])
     ctx = P.Context(torch.empty(256 << 20, dtype=torch.uint8, device="cuda"))
     bufs = P.BufArray([P.flat(t) for rep in reps for t in rep])
     H = torch.zeros(K * total, dtype=torch.int64, device="cuda")
@@ -829,7 +828,7 @@ def run_markovian(args):
     r2 = [torch.from_numpy(b.copy()).cuda() for b in c.buffers(2)]
     ctx = P.Context(torch.empty(64 << 20, dtype=torch.uint8, device="cuda"))
     both = P.BufArray([P.flat(t) for t in r1 + r2])
-    cpb = [P.chunk_count(t.numel()) for t in r1]
+    cpb = P.chunk_counts([P.flat(t) for t in r1])[0]
     total = sum(cpb)
     H = torch.zeros(2 * total, dtype=torch.int64, device="cuda")
     bm = torch.zeros(sum((x + 63) // 64 for x in cpb), dtype=torch.int64, device="cuda")
@@ -984,7 +983,7 @@ def run_discover(args):
     ctx = P.Context(torch.empty(512 << 20, dtype=torch.uint8, device="cuda"))
     descs = P.BufArray([P.flat(t) for t in live.parts])
     ref = MockWorldGPU(spec, [t.clone() for t in live.parts]).run(pa)
-    ref_h = torch.zeros(P.chunk_count(ref.numel()), dtype=torch.int64, device="cuda")
+    ref_h = torch.zeros(P.chunk_counts([P.flat(ref)])[1], dtype=torch.int64, device="cuda")
     ctx.fingerprint([P.flat(ref)], ref_h)
     moved = [0]
 

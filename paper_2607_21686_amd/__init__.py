@@ -24,16 +24,11 @@ from ._lib import (CHUNK_BYTES, CKPT_HASH, E_CORRUPT, E_HANDLE, E_HIP, E_INVAL, 
                    FLAT, MUST_SNAPSHOT, PROBE_FN, RECOMPUTABLE, RING, TIMING_DISPATCH, TIMING_EVENTS, TIMING_OFF,
                    PcsBankPart, PcsBuf, PcsDiscovery, PcsError, PcsSnapInfo, lib)
 
-__all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_count", "keep_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
+__all__ = ["Context", "PcsError", "BufArray", "u64_array", "flat", "ring", "chunk_counts", "keep_count", "CHUNK_BYTES", "CKPT_HASH", "FLAT", "RING",
            "RECOMPUTABLE", "MUST_SNAPSHOT", "E_INVAL", "E_NOMEM", "E_HANDLE", "E_SHAPE", "E_HIP", "E_CORRUPT", "E_PROBE",
            "EXPORTS"]
 
 _L = lib()  # fails loudly if the HIP library is missing
-
-
-def chunk_count(nbytes: int) -> int:
-    """Number of 4096-byte chunks of a buffer of nbytes logical bytes."""
-    return (nbytes + CHUNK_BYTES - 1) // CHUNK_BYTES
 
 
 def _ratio(fraction):

@@ -130,7 +130,7 @@ def test_discover_mock_world_matches_oracle(pcs):
     # Reference: an uninterrupted continuation from the anchor (on a copy).
     ref_world = MockWorldGPU(spec, [t.clone() for t in g.parts])
     ref_frames = ref_world.run(pa)
-    nref = pcs.chunk_count(ref_frames.numel())
+    nref = pcs.chunk_counts([pcs.flat(ref_frames)])[1]
     ref_h = torch.zeros(nref, dtype=torch.int64, device="cuda")
     ctx.fingerprint([pcs.flat(ref_frames)], ref_h)
 
