@@ -578,6 +578,64 @@ def test_incremental_chain_in_tight_arena(pcs):
     c.close()
 
 
+def test_incremental_exact_placement_then_pipelined(pcs):
+    """An incremental checkpoint whose worst case (a slot for every chunk of
+    the prefix) does not fit the arena beside its parent: the host reads the
+    stored-chunk count and places exactly that many slots (diff, scan, slot
+    copy: three incremental launches).  Then, on the same context, one of a
+    1 MiB prefix against the same parent, which fits and takes the pipelined
+    small path (two launches, a new arena segment).  Stored bytes,
+    fingerprints and restores against the oracle."""
+    rng = np.random.default_rng(77)
+    n = 16 << 20
+    cur = [rng.integers(0, 256, size=n, dtype=np.uint8), rng.integers(0, 256, size=5000, dtype=np.uint8)]
+    d = [dev(b) for b in cur]
+    log("incremental exact placement")
+    c = pcs.Context(arena(n + (2 << 20)))
+    try:
+        st = oracle.Store()
+        base = (c.checkpoint([pcs.flat(t) for t in d], hash=True), st.checkpoint(cur))
+        flipped = rng.choice(oracle.chunk_count(n), size=40, replace=False)
+        fresh = [k for k in range(256) if k not in set(int(x) for x in flipped)][:3]
+        made = []
+        for flips, prefix, launches in ((flipped, n, 3), (fresh, 1 << 20, 2)):
+            for k in flips:
+                cur[0][int(k) * 4096] ^= 0xFF
+            cur[1][-1] = (int(cur[1][-1]) + 1) % 256
+            for t, b in zip(d, cur):
+                t.copy_(torch.from_numpy(b))
+            logical = [cur[0][:prefix].copy(), cur[1].copy()]
+            total = sum(oracle.chunk_count(b.size) for b in logical)
+            c.kernel_time("incremental")
+            c.set_timing(True)
+            ch, rt, sr = zeros_u64(total), zeros_u64(2), zeros_u64(1)
+            s = c.checkpoint([pcs.flat(d[0], prefix), pcs.flat(d[1])], parent=base[0], chunk_hashes=ch, roots=rt,
+                             session_root=sr)
+            c.set_timing(False)
+            assert c.kernel_time("incremental")[0] == launches
+            o = st.checkpoint(logical, base[1])
+            want_h, want_r, want_s = oracle.fingerprint(logical)
+            assert np.array_equal(u64(ch)[:total], want_h)
+            assert np.array_equal(u64(rt)[:2], want_r) and int(u64(sr)[0]) == int(want_s)
+            inf = c.info(s)
+            assert inf["stored_bytes"] == st.payload(o).size > 0
+            if launches == 3:
+                assert inf["stored_bytes"] == 41 * 4096
+            pay = torch.empty(inf["stored_bytes"], dtype=torch.uint8, device="cuda")
+            c.payload(s, pay)
+            assert np.array_equal(host(pay), st.payload(o))
+            del pay
+            outs = [torch.empty(b.size, dtype=torch.uint8, device="cuda") for b in logical]
+            c.restore(s, [pcs.flat(t) for t in outs])
+            assert all(np.array_equal(host(t), b) for t, b in zip(outs, logical))
+            del outs
+            made.append(s)
+        for s in made + [base[0]]:
+            c.delete(s)
+    finally:
+        c.close()
+
+
 @pytest.mark.parametrize("dispatch", [False, True])
 def test_kernel_timing_counts_and_resets(ctx, pcs, dispatch):
     """pcs_set_timing / pcs_kernel_time, both modes (events around each
