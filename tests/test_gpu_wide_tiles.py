@@ -208,3 +208,49 @@ def test_incremental_every_chunk_then_none_then_one(pcs, groups):
             ctx.delete(s)
     finally:
         ctx.close()
+
+
+def test_buffer_past_4_gib(pcs):
+    """One flat buffer of 2^32 + 12,365 bytes (chunk indices past 2^20, byte
+    offsets past 2^32, a partial last chunk): fingerprinted full checkpoint,
+    then an incremental one (device tables, slots placed in an arena
+    segment) storing the chunks changed below 64 KiB, just past 4 GiB and
+    at the end; chunk fingerprints, roots, stored bytes and the restore
+    against the oracle."""
+    n = (1 << 32) + 3 * 4096 + 77
+    log("buffer past 4 GiB:", n, "bytes")
+    a = np.frombuffer(np.random.default_rng(61).bytes(n), dtype=np.uint8).copy()
+    d = torch.from_numpy(a).cuda()
+    total = oracle.chunk_count(n)
+    ctx = pcs.Context(arena(2 * n + (512 << 20)))
+    try:
+        st = oracle.Store()
+        ch, rt, sr = zeros_u64(total), zeros_u64(1), zeros_u64(1)
+        base = ctx.checkpoint([pcs.flat(d)], hash=True, chunk_hashes=ch, roots=rt, session_root=sr)
+        want_h, want_r, want_s = oracle.fingerprint([a])
+        assert np.array_equal(u64(ch)[:total], want_h)
+        assert int(u64(rt)[0]) == int(want_r[0]) and int(u64(sr)[0]) == int(want_s)
+        o_base = st.checkpoint([a])
+        for i in (12345, (1 << 32) + 5, n - 1):
+            a[i] ^= 1
+            d[i] = int(a[i])
+        ch2, rt2, sr2 = zeros_u64(total), zeros_u64(1), zeros_u64(1)
+        inc = ctx.checkpoint([pcs.flat(d)], parent=base, chunk_hashes=ch2, roots=rt2, session_root=sr2)
+        want_h, want_r, want_s = oracle.fingerprint([a])
+        assert np.array_equal(u64(ch2)[:total], want_h)
+        assert int(u64(rt2)[0]) == int(want_r[0]) and int(u64(sr2)[0]) == int(want_s)
+        o_inc = st.checkpoint([a], o_base)
+        inf = ctx.info(inc)
+        assert inf["stored_bytes"] == st.payload(o_inc).size == 3 * 4096
+        pay = torch.empty(inf["stored_bytes"], dtype=torch.uint8, device="cuda")
+        ctx.payload(inc, pay)
+        assert np.array_equal(host(pay), st.payload(o_inc))
+        del st, o_base, o_inc
+        out = torch.empty_like(d)
+        ctx.restore(inc, [pcs.flat(out)])
+        assert np.array_equal(host(out), a)
+        del out
+        ctx.delete(inc)
+        ctx.delete(base)
+    finally:
+        ctx.close()
